@@ -1,0 +1,238 @@
+"""Routing plan: correspondence, de-duplication, balance, wire format.
+
+Follows WeightBridge Sec. 3.1 (correspondence is the overlap of two workers'
+source maps in the checkpoint index space) and Sec. 3.2 ("Generating an
+efficient routing plan": a tensor replicated on the trainer side is split into
+distinct slices, one per replica, so the trainers together send one copy and
+no replica becomes a single-source bottleneck). The receive stage is planned
+directly: each rollout rank receives everything it needs from the trainers.
+The canonical choices below are this build's reading; the paper fixes none of
+them:
+
+1. Trainer *groups*: placements of one checkpoint tensor with identical
+   rectangles form one group whose owner set is the sorted list of ranks that
+   hold it. Distinct groups of a tensor must be disjoint.
+2. Visit rollout rank d ascending, then d's placements Q in layout order, then
+   the groups of Q's tensor ordered by (r0, c0, r1, c1). Each non-empty
+   X = Q.rect & g.rect is a *region*; together the regions of Q must cover Q.
+3. A region with one owner is one segment. Otherwise it is split into k equal
+   parts (k = number of owners): by rows when it has at least k rows, else by
+   columns; part j spans [floor(j n / k), floor((j+1) n / k)) of that axis.
+   Empty parts are dropped. Parts are handed out per owner set by deficit:
+   each owner q of the set keeps E_q = k * (bytes assigned to q) - (bytes of
+   all regions of the set so far); the region's bytes are first added to the
+   total, then its parts, largest first (ties: lower part index), each go to
+   the owner with the smallest E_q (ties: lower rank). Since the E_q of a set
+   sum to zero after every region and a part always goes to a negative E_q,
+   no owner ever exceeds its even share of the set by more than one part.
+4. Wire format (Sec. 3.2, the packing kernel coalesces the tensors for one
+   receiver into one contiguous buffer): the payloads of sender s for receiver
+   d follow the canonical order, each a row-major copy of its rectangle in the
+   sender's dtype, each starting at a multiple of 256 bytes of its region. A
+   sender's buffer holds its regions by ascending receiver; a receiver's
+   buffer holds the regions by ascending sender; every region starts at a
+   multiple of 4096 bytes.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+from .layout import DTYPE_BYTES, Layout
+
+PAYLOAD_ALIGN = 256
+REGION_ALIGN = 4096
+
+
+@dataclass(frozen=True)
+class Rect:
+    r0: int
+    r1: int
+    c0: int
+    c1: int
+
+    @property
+    def numel(self) -> int:
+        return (self.r1 - self.r0) * (self.c1 - self.c0)
+
+    def intersect(self, o: "Rect"):
+        r0, r1, c0, c1 = max(self.r0, o.r0), min(self.r1, o.r1), max(self.c0, o.c0), min(self.c1, o.c1)
+        return Rect(r0, r1, c0, c1) if r0 < r1 and c0 < c1 else None
+
+
+@dataclass
+class Segment:
+    s: int          # sender (trainer rank)
+    d: int          # receiver (rollout rank)
+    t: int          # checkpoint tensor
+    rect: Rect
+    src_pl: int     # placement index in the sender's layout
+    dst_pl: int     # placement index in the receiver's layout
+    nbytes: int     # payload bytes (sender dtype)
+    region: int = -1  # index of the region the segment was cut from
+    send_off: int = 0
+    recv_off: int = 0
+
+
+@dataclass
+class Region:
+    owners: tuple
+    nbytes: int     # bytes of the whole region (sender dtype)
+
+
+@dataclass
+class Plan:
+    trainer: Layout
+    rollout: Layout
+    segments: list[Segment]
+    regions: list[Region]
+    send_bytes: list[int]
+    recv_bytes: list[int]
+
+
+def _align(x: int, a: int) -> int:
+    return -(-x // a) * a
+
+
+class PlanError(ValueError):
+    pass
+
+
+def build_plan(trainer: Layout, rollout: Layout) -> Plan:
+    cat = trainer.catalog
+    if [(t.name, t.rows, t.cols) for t in cat] != [(t.name, t.rows, t.cols) for t in rollout.catalog]:
+        raise PlanError("trainer and rollout catalogs differ")
+
+    # 1. trainer groups: rect -> owners (ascending rank) and their placement index
+    by_rect: dict[tuple, dict] = {}
+    for s, rk in enumerate(trainer.ranks):
+        for pi, p in enumerate(rk.placements):
+            key = (p.t, p.r0, p.r1, p.c0, p.c1)
+            owners = by_rect.setdefault(key, {})
+            if s in owners:
+                raise PlanError("a trainer rank holds the same rectangle twice")
+            owners[s] = pi
+    groups: dict[int, list] = {}
+    for (t, r0, r1, c0, c1), owners in by_rect.items():
+        groups.setdefault(t, []).append((Rect(r0, r1, c0, c1), tuple(sorted(owners)), owners))
+    for t, gl in groups.items():
+        gl.sort(key=lambda g: (g[0].r0, g[0].c0, g[0].r1, g[0].c1))
+        for a in range(len(gl)):
+            for b in range(a + 1, len(gl)):
+                if gl[a][0].intersect(gl[b][0]) is not None:
+                    raise PlanError(f"overlapping, non-identical trainer rectangles in tensor {t}")
+
+    # 2./3. regions and segments in canonical order
+    deficit: dict[tuple, dict[int, int]] = {}
+    segments: list[Segment] = []
+    regions: list[Region] = []
+    for d, rk in enumerate(rollout.ranks):
+        for qi, q in enumerate(rk.placements):
+            qrect = Rect(q.r0, q.r1, q.c0, q.c1)
+            covered = 0
+            for grect, owners, pl_of in groups.get(q.t, []):
+                x = qrect.intersect(grect)
+                if x is None:
+                    continue
+                covered += x.numel
+                esizes = {DTYPE_BYTES[trainer.ranks[s].locals[trainer.ranks[s].placements[pl_of[s]].u].dtype]
+                          for s in owners}
+                if len(esizes) != 1:
+                    raise PlanError("replicas of one rectangle hold different dtypes")
+                esize = esizes.pop()
+                k = len(owners)
+                if k == 1:
+                    parts = [(x, owners[0])]
+                else:
+                    by_rows = (x.r1 - x.r0) >= k
+                    n = (x.r1 - x.r0) if by_rows else (x.c1 - x.c0)
+                    pieces = []
+                    for j in range(k):
+                        a, b = j * n // k, (j + 1) * n // k
+                        if a < b:
+                            pieces.append(Rect(x.r0 + a, x.r0 + b, x.c0, x.c1) if by_rows
+                                          else Rect(x.r0, x.r1, x.c0 + a, x.c0 + b))
+                    e = deficit.setdefault(owners, {s: 0 for s in owners})
+                    for s in owners:
+                        e[s] -= x.numel * esize
+                    who = [None] * len(pieces)
+                    for j in sorted(range(len(pieces)), key=lambda j: (-pieces[j].numel, j)):
+                        s = min(owners, key=lambda s: (e[s], s))
+                        e[s] += k * pieces[j].numel * esize
+                        who[j] = s
+                    parts = list(zip(pieces, who))
+                for part, s in parts:
+                    segments.append(Segment(s, d, q.t, part, pl_of[s], qi, part.numel * esize, len(regions)))
+                regions.append(Region(owners, x.numel * esize))
+            if covered != q.numel:
+                raise PlanError(f"rollout rank {d} placement {qi} is not fully held by the trainers")
+
+    # 4. wire offsets
+    ns, nd = trainer.nranks, rollout.nranks
+    payload_end: dict[tuple, int] = {}
+    for sg in segments:
+        off = _align(payload_end.get((sg.s, sg.d), 0), PAYLOAD_ALIGN)
+        sg.send_off = off
+        sg.recv_off = off
+        payload_end[(sg.s, sg.d)] = off + sg.nbytes
+    send_region = {}
+    send_bytes = []
+    for s in range(ns):
+        pos = 0
+        for d in range(nd):
+            if (s, d) in payload_end:
+                pos = _align(pos, REGION_ALIGN)
+                send_region[(s, d)] = pos
+                pos += payload_end[(s, d)]
+        send_bytes.append(pos)
+    recv_region = {}
+    recv_bytes = []
+    for d in range(nd):
+        pos = 0
+        for s in range(ns):
+            if (s, d) in payload_end:
+                pos = _align(pos, REGION_ALIGN)
+                recv_region[(s, d)] = pos
+                pos += payload_end[(s, d)]
+        recv_bytes.append(pos)
+    for sg in segments:
+        sg.send_off += send_region[(sg.s, sg.d)]
+        sg.recv_off += recv_region[(sg.s, sg.d)]
+    return Plan(trainer, rollout, segments, regions, send_bytes, recv_bytes)
+
+
+def dump(plan: Plan) -> str:
+    """Canonical text form of a plan, one line per segment."""
+    out = [f"plan trainer_ranks={plan.trainer.nranks} rollout_ranks={plan.rollout.nranks} segments={len(plan.segments)}"]
+    out += [f"send {s} {b}" for s, b in enumerate(plan.send_bytes)]
+    out += [f"recv {d} {b}" for d, b in enumerate(plan.recv_bytes)]
+    for g in plan.segments:
+        r = g.rect
+        out.append(f"seg {g.s} {g.d} {g.t} {r.r0} {r.r1} {r.c0} {r.c1} {g.src_pl} {g.dst_pl} {g.send_off} {g.recv_off} {g.nbytes}")
+    return "\n".join(out) + "\n"
+
+
+def dump_layout(layout: Layout) -> str:
+    """Canonical text form of a layout."""
+    out = [f"layout ranks={layout.nranks} tensors={len(layout.catalog)}"]
+    for r, rk in enumerate(layout.ranks):
+        out.append(f"rank {r} locals={len(rk.locals)} placements={len(rk.placements)}")
+        for u, lc in enumerate(rk.locals):
+            out.append(f"local {u} {lc.name} {lc.dtype} {lc.batch} {lc.rows} {lc.cols} {lc.block} {lc.scale} {lc.scales}")
+        for p in rk.placements:
+            out.append(f"pl {p.t} {p.r0} {p.r1} {p.c0} {p.c1} {p.u} {p.base} {p.ld} {p.tr}")
+    return "\n".join(out) + "\n"
+
+
+def sender_loads(plan: Plan):
+    """(load, ideal) bytes per sender: ideal counts each region's bytes split
+    evenly over its owners."""
+    ns = plan.trainer.nranks
+    load = [0] * ns
+    ideal = [0.0] * ns
+    for g in plan.segments:
+        load[g.s] += g.nbytes
+    for reg in plan.regions:
+        for s in reg.owners:
+            ideal[s] += reg.nbytes / len(reg.owners)
+    return load, ideal

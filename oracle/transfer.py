@@ -1,0 +1,156 @@
+"""Pack, the network stand-in, unpack, and the plan-independent expectation.
+
+WeightBridge Sec. 3.2: on the trainer side a packing kernel transforms the
+tensors planned for a round into checkpoint format and coalesces them into one
+contiguous buffer per receiver; on the rollout side an assembly kernel gathers
+the shards from different senders, transforms them into inference format and
+writes them into the model parameters. Here each step is spelled out element
+by element with explicit index arithmetic (placement semantics from
+``layout``), one segment at a time.
+
+Tensors are numpy arrays of raw codes: uint32 for f32, uint16 for bf16, uint8
+for f8e4m3 (fp32 values for scale tensors are uint32 codes too).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from . import casts
+from .layout import DTYPE_BYTES, Layout, Placement
+from .plan import Plan
+
+CODE_DTYPE = {"f32": np.uint32, "bf16": np.uint16, "f8e4m3": np.uint8}
+
+
+def local_index(p: Placement, i, j):
+    """Flat local index of checkpoint element (i, j) under placement p."""
+    if p.tr:
+        return p.base + (j - p.c0) * p.ld + (i - p.r0)
+    return p.base + (i - p.r0) * p.ld + (j - p.c0)
+
+
+def _grid(r0, r1, c0, c1):
+    return np.arange(r0, r1, dtype=np.int64)[:, None], np.arange(c0, c1, dtype=np.int64)[None, :]
+
+
+def materialize(layout: Layout, rank: int, values, dtype=None) -> list[np.ndarray]:
+    """Local tensors of one rank filled from the checkpoint (what a weight
+    loader does). ``values(t)`` returns checkpoint tensor t as a [rows, cols]
+    array of codes in the local dtype (or of ``dtype`` when given, e.g. element
+    identifiers). Unplaced elements are zero."""
+    rk = layout.ranks[rank]
+    out = [np.zeros(lc.numel, dtype=dtype or CODE_DTYPE[lc.dtype]) for lc in rk.locals]
+    for p in rk.placements:
+        i, j = _grid(p.r0, p.r1, p.c0, p.c1)
+        out[p.u][local_index(p, i, j)] = values(p.t)[p.r0:p.r1, p.c0:p.c1]
+    return out
+
+
+def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray]) -> np.ndarray:
+    """Send buffer of trainer rank s: every segment's rectangle, read through
+    the sender's placement, written row-major at its send offset."""
+    buf = np.zeros(plan.send_bytes[s], dtype=np.uint8)
+    rk = plan.trainer.ranks[s]
+    for g in plan.segments:
+        if g.s != s:
+            continue
+        p = rk.placements[g.src_pl]
+        lc = rk.locals[p.u]
+        r = g.rect
+        i, j = _grid(r.r0, r.r1, r.c0, r.c1)
+        vals = trainer_locals[p.u][local_index(p, i, j)]          # [rows, cols] codes
+        buf[g.send_off:g.send_off + g.nbytes] = np.ascontiguousarray(vals).view(np.uint8).ravel()
+        assert vals.dtype == CODE_DTYPE[lc.dtype]
+    return buf
+
+
+def network(plan: Plan, d: int, send_bufs: dict[int, np.ndarray]) -> np.ndarray:
+    """Receive buffer of rollout rank d: each sender's region for d, copied."""
+    buf = np.zeros(plan.recv_bytes[d], dtype=np.uint8)
+    for g in plan.segments:
+        if g.d == d:
+            buf[g.recv_off:g.recv_off + g.nbytes] = send_bufs[g.s][g.send_off:g.send_off + g.nbytes]
+    return buf
+
+
+def _convert(codes: np.ndarray, src: str, dst: str) -> np.ndarray:
+    if src == dst:
+        return codes
+    if src == "f32" and dst == "bf16":
+        return casts.f32_to_bf16(codes)
+    if src == "bf16" and dst == "f32":
+        return casts.bf16_to_f32(codes)
+    raise ValueError(f"unsupported cast {src} -> {dst}")
+
+
+def _to_f32(codes: np.ndarray, src: str) -> np.ndarray:
+    return codes.astype(np.uint32) if src == "f32" else casts.bf16_to_f32(codes)
+
+
+def _quantize_local(lc, staged_f32_codes: np.ndarray):
+    """Blockwise quantisation of one staged local tensor (per batch matrix)."""
+    x = staged_f32_codes.view(np.float32).reshape(lc.batch, lc.rows, lc.cols)
+    codes = np.empty((lc.batch, lc.rows, lc.cols), dtype=np.uint8)
+    nbr, nbc = -(-lc.rows // lc.block), -(-lc.cols // lc.block)
+    scales = np.empty((lc.batch, nbr, nbc), dtype=np.float32)
+    for e in range(lc.batch):
+        codes[e], scales[e] = casts.quantize_matrix(x[e], lc.block)
+    return codes.ravel(), scales.ravel().view(np.uint32)
+
+
+def _finish(rk, staged, dst_locals):
+    for u, lc in enumerate(rk.locals):
+        if lc.block:
+            codes, scales = _quantize_local(lc, staged[u])
+            dst_locals[u] = codes
+            dst_locals[lc.scale] = scales
+    return dst_locals
+
+
+def unpack(plan: Plan, d: int, recv_buf: np.ndarray) -> list[np.ndarray]:
+    """Rollout rank d's tensors from its receive buffer: each segment's payload
+    is read row-major and written through the receiver's placement, cast to the
+    local dtype; quantised tensors are staged in fp32 and quantised blockwise."""
+    rk = plan.rollout.ranks[d]
+    dst = [np.zeros(lc.numel, dtype=CODE_DTYPE[lc.dtype]) for lc in rk.locals]
+    staged = {u: np.zeros(lc.numel, dtype=np.uint32) for u, lc in enumerate(rk.locals) if lc.block}
+    for g in plan.segments:
+        if g.d != d:
+            continue
+        q = rk.placements[g.dst_pl]
+        lc = rk.locals[q.u]
+        sp = plan.trainer.ranks[g.s].placements[g.src_pl]
+        src_dtype = plan.trainer.ranks[g.s].locals[sp.u].dtype
+        r = g.rect
+        payload = recv_buf[g.recv_off:g.recv_off + g.nbytes].view(CODE_DTYPE[src_dtype])
+        payload = payload.reshape(r.r1 - r.r0, r.c1 - r.c0)
+        i, j = _grid(r.r0, r.r1, r.c0, r.c1)
+        idx = local_index(q, i, j)
+        if lc.block:
+            staged[q.u][idx] = _to_f32(payload, src_dtype)
+        else:
+            dst[q.u][idx] = _convert(payload, src_dtype, lc.dtype)
+    return _finish(rk, staged, dst)
+
+
+def expected_rollout(rollout: Layout, d: int, values, src_dtype: str) -> list[np.ndarray]:
+    """What rollout rank d must hold, straight from its layout and the
+    checkpoint (no plan involved): dst = cast(checkpoint slice)."""
+    rk = rollout.ranks[d]
+    dst = [np.zeros(lc.numel, dtype=CODE_DTYPE[lc.dtype]) for lc in rk.locals]
+    staged = {u: np.zeros(lc.numel, dtype=np.uint32) for u, lc in enumerate(rk.locals) if lc.block}
+    for q in rk.placements:
+        lc = rk.locals[q.u]
+        i, j = _grid(q.r0, q.r1, q.c0, q.c1)
+        idx = local_index(q, i, j)
+        src = values(q.t)[q.r0:q.r1, q.c0:q.c1]
+        if lc.block:
+            staged[q.u][idx] = _to_f32(src, src_dtype)
+        else:
+            dst[q.u][idx] = _convert(src, src_dtype, lc.dtype)
+    return _finish(rk, staged, dst)
+
+
+def bytes_of(layout: Layout, rank: int) -> int:
+    return sum(lc.numel * DTYPE_BYTES[lc.dtype] for lc in layout.ranks[rank].locals)

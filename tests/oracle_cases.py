@@ -1,0 +1,66 @@
+"""Small hand-built and random layouts shared by the plan tests (oracle types)."""
+
+from __future__ import annotations
+
+import numpy as np
+
+from oracle.catalog import CkptTensor, ModelShapes
+from oracle.layout import Layout, Local, Parallelism, Placement, RankLayout, describe_layout
+
+
+def hand_replicated_pair():
+    """The layout pair of tests/golden/hand_plan_replicated.txt."""
+    cat = [CkptTensor("T0", 4, 6), CkptTensor("T1", 1, 10)]
+    full = RankLayout([Local("a", "f32", 1, 4, 6), Local("b", "f32", 1, 1, 10)],
+                      [Placement(0, 0, 4, 0, 6, 0, 0, 6), Placement(1, 0, 1, 0, 10, 1, 0, 10)])
+    only_t1 = RankLayout([Local("b", "f32", 1, 1, 10)], [Placement(1, 0, 1, 0, 10, 0, 0, 10)])
+    trainer = Layout(cat, [full, RankLayout(list(full.locals), list(full.placements)), only_t1])
+    r0 = RankLayout([Local("x", "bf16", 1, 2, 6), Local("y", "bf16", 1, 1, 10)],
+                    [Placement(0, 0, 2, 0, 6, 0, 0, 6), Placement(1, 0, 1, 0, 10, 1, 0, 10)])
+    r1 = RankLayout([Local("x", "bf16", 1, 6, 2), Local("y", "bf16", 1, 1, 5)],
+                    [Placement(0, 2, 4, 0, 6, 0, 0, 2, 1), Placement(1, 0, 1, 5, 10, 1, 0, 5)])
+    rollout = Layout(cat, [r0, r1])
+    return trainer, rollout
+
+
+def random_model(rng) -> ModelShapes:
+    fam = ["dense", "mixtral", "moe_only"][int(rng.integers(0, 3))]
+    nkv = int(rng.choice([1, 2, 4]))
+    qpg = int(rng.choice([1, 2]))
+    return ModelShapes(fam, num_layers=int(rng.integers(1, 3)), hidden=int(rng.choice([8, 12, 16, 20])),
+                       num_heads=nkv * qpg, num_kv_heads=nkv, head_dim=int(rng.choice([2, 4])),
+                       ffn=int(rng.choice([8, 12, 24])), vocab=int(rng.choice([8, 16, 24])),
+                       num_experts=int(rng.choice([2, 4, 8])), num_shared_experts=1)
+
+
+def random_par(rng, m: ModelShapes, side: str) -> Parallelism:
+    """A random parallelism valid for model m (trainer or rollout side)."""
+    dtype = ["f32", "bf16"][int(rng.integers(0, 2))]
+    while True:
+        style = ["fsdp_flat", "megatron"][int(rng.integers(0, 2))] if side == "trainer" else "serving"
+        tp = int(rng.choice([1, 2, 4]))
+        ep = int(rng.choice([1, 2, 4])) if m.family != "dense" else 1
+        dp = int(rng.choice([1, 1, 2]))
+        try:
+            if style == "fsdp_flat":
+                p = Parallelism(style, dtype, fsdp=int(rng.integers(1, 6)), ep=ep, dp=dp)
+            elif style == "megatron":
+                p = Parallelism(style, dtype, tp=tp if m.family == "dense" else 1, ep=ep, dp=dp,
+                                transposed_row_parallel=bool(rng.integers(0, 2)))
+            else:
+                q = "f8e4m3" if rng.integers(0, 3) == 0 else ""
+                p = Parallelism(style, "bf16" if q else dtype, tp=tp, ep=ep, dp=dp, quant=q,
+                                quant_block=int(rng.choice([4, 8])))
+            describe_layout(m, p)
+            return p
+        except ValueError:
+            continue
+
+
+def id_values(catalog):
+    """Checkpoint tensors whose elements hold unique identifiers (1-based)."""
+    out, off = [], 1
+    for t in catalog:
+        out.append(np.arange(off, off + t.numel, dtype=np.int64).reshape(t.rows, t.cols))
+        off += t.numel
+    return out
