@@ -1,0 +1,250 @@
+"""Benchmark of the resharding hot path on one MI355X.
+
+One step = pack of one trainer rank's shards (wb_pack) followed by the
+assembly of one rollout rank's tensors (wb_unpack), on synthetic seeded
+parameters already resident in HBM, for the Llama-3-8B-shaped workload
+(trainer FSDP=8 flat bf16 shards -> rollout TP=1 bf16 with fused qkv and
+gate_up; pack trainer rank 0, unpack the full rollout replica from the eight
+senders' regions). Other workloads: --workload NAME.
+
+Prints one JSON line: effective GB/s of the step (algorithmic bytes: each
+element read once in the source dtype and written once in the destination
+dtype, plus fp8 scales), the HBM roofline of the dominant kernel from HIP
+events on the launch stream, wb_plan time, and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+DEFAULT_WORKLOAD = "llama3_8b_fsdp8_to_tp1"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_sender_locals(wb, torch, sc, layout, rank, dtype):
+    """Trainer rank's local tensors filled from the synthetic checkpoint through
+    its placements (plain torch slicing; what a trainer's weights look like)."""
+    cat = layout.tensors()
+    locs = wb.allocate_locals(layout, rank, zero=True)
+    flat = [t.view(-1) for t in locs]
+    for (t, r0, r1, c0, c1, u, base, ld, tr) in layout.placements(rank):
+        _, rows, cols = cat[t]
+        block = sc.values_torch(t, rows, cols, dtype, device="cuda", start=r0 * cols, count=(r1 - r0) * cols)
+        block = block.view(r1 - r0, cols)[:, c0:c1]
+        if tr:
+            view = torch.as_strided(flat[u], (r1 - r0, c1 - c0), (1, ld), base)
+        else:
+            view = torch.as_strided(flat[u], (r1 - r0, c1 - c0), (ld, 1), base)
+        view.copy_(block)
+    return locs
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "plan.cpp"):
+        h.update(open(os.path.join(ROOT, "paper_2609_25442_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload, kernel):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_hash") != kernel_source_hash() or kernel not in rec.get("kernels", {}):
+        return None
+    return rec["kernels"][kernel]["hbm_bytes_per_launch"]
+
+
+def cpu_baseline(w, ro_dev_plan_bytes, recv_host_fn, budget_s=15.0):
+    """The oracle as it stands, on a time-bounded sample of the workload:
+    its planner, then its element-by-element unpack over the receiver's
+    segments in plan order until ``budget_s`` seconds have passed."""
+    import dataclasses
+
+    import numpy as np
+
+    from oracle.layout import layout_from_spec
+    from oracle.plan import build_plan
+    from oracle.transfer import unpack as o_unpack
+
+    t0 = time.perf_counter()
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    oplan = build_plan(otr, oro)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    d = w["unpack_rank"]
+    segs = [g for g in oplan.segments if g.d == d]
+    done_bytes, spent, n = 0, 0.0, 0
+    from oracle.layout import DTYPE_BYTES
+    for g in segs:
+        payload = recv_host_fn(g.recv_off, g.nbytes)
+        buf = np.zeros(g.recv_off + g.nbytes, dtype=np.uint8)
+        buf[g.recv_off:] = payload
+        sub = dataclasses.replace(oplan, segments=[g])
+        t1 = time.perf_counter()
+        o_unpack(sub, d, buf)
+        spent += time.perf_counter() - t1
+        q = oro.ranks[d].placements[g.dst_pl]
+        done_bytes += g.nbytes + g.rect.numel * DTYPE_BYTES[oro.ranks[d].locals[q.u].dtype]
+        n += 1
+        if spent >= budget_s:
+            break
+    return {"value": round(done_bytes / spent / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle unpack of the first {n} of {len(segs)} segments of rollout rank {d} "
+                      f"({done_bytes / 1e9:.2f} GB read+written) in {spent:.1f} s; oracle plan {plan_ms:.0f} ms",
+            "plan_ms": round(plan_ms, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the resharding hot path here runs on a single MI355X "
+              "(pack of one trainer rank, unpack of one rollout rank); --gpus above 1 is not supported.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_25442_amd as wb
+    import synthetic_checkpoint as sc
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    src_dtype = w["trainer"]["dtype"]
+    s0, d = w["pack_rank"], w["unpack_rank"]
+    torch.cuda.set_device(0)
+
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    plan_ms = {}
+    for label, role, rank in (("unpack", wb.RECEIVER, d), ("pack", wb.SENDER, s0)):
+        ts = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            p = wb.Plan(tr, ro, role, rank)
+            ts.append((time.perf_counter() - t0) * 1e3)
+        plan_ms[label] = round(statistics.median(ts), 2)
+    rplan = wb.Plan(tr, ro, wb.RECEIVER, d)
+    splan = wb.Plan(tr, ro, wb.SENDER, s0)
+    rws = torch.empty(rplan.workspace_bytes, dtype=torch.uint8, device="cuda")
+    sws = torch.empty(splan.workspace_bytes, dtype=torch.uint8, device="cuda")
+    rplan.upload(rws)
+    splan.upload(sws)
+    log(f"[bench] {args.workload}: plan ms {plan_ms}; recv {rplan.buffer_bytes / 1e9:.2f} GB")
+
+    # inputs: every sender's region for the receiver, through real packs
+    recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, device="cuda")
+    send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, device="cuda")
+    src0 = None
+    for s in range(tr.nranks):
+        so, roff, nb = rplan.region(s, d)
+        if nb == 0 and s != s0:
+            continue
+        locs = build_sender_locals(wb, torch, sc, tr, s, src_dtype)
+        p = splan if s == s0 else wb.Plan(tr, ro, wb.SENDER, s)
+        if s != s0:
+            ws = torch.empty(p.workspace_bytes, dtype=torch.uint8, device="cuda")
+            p.upload(ws)
+        buf = send0 if s == s0 else torch.empty(p.buffer_bytes, dtype=torch.uint8, device="cuda")
+        p.pack(locs, buf)
+        if nb:
+            recv[roff:roff + nb] = buf[so:so + nb]
+        if s == s0:
+            src0 = locs
+        else:
+            del locs, buf, p, ws
+        torch.cuda.synchronize()
+    dst = wb.allocate_locals(ro, d)
+    torch.cuda.synchronize()
+    log("[bench] inputs resident")
+
+    pr, pw = splan.traffic()
+    ur, uw = rplan.traffic()
+    pack_bytes, unpack_bytes = pr + pw, ur + uw
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        splan.pack(src0, send0, stream)
+        if ev:
+            ev[1].record(stream)
+        rplan.unpack(recv, dst, stream)
+        if ev:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    pack_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in events)
+    unpack_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in events)
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = (pack_bytes + unpack_bytes) / (ms_per_step * 1e-3) / 1e9
+
+    n_tasks, n_blocks, _ = rplan.work_counts()
+    dom = "wb::wb_qblock_kernel" if n_blocks and not n_tasks else "wb::wb_tasks_kernel"
+    achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
+    traffic = stored_traffic(args.workload, "unpack")
+    out = {
+        "metric": "pack+unpack effective GB/s per GPU (% of HBM peak); wb_plan ms",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": src_dtype if src_dtype == w["rollout"]["dtype"] and not w["rollout"].get("quant")
+        else f"{src_dtype}->{w['rollout'].get('quant') or w['rollout']['dtype']}",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "trainer": w["trainer"], "rollout": w["rollout"],
+                   "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "plan_ms": plan_ms,
+        "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
+        "unpack": {"ms": round(unpack_ms, 4), "GB/s": round(achieved, 1), "bytes": unpack_bytes},
+        "roofline": {"bound": "hbm", "kernel": dom + " (unpack)", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        def recv_host(off, nb):
+            return recv[off:off + nb].cpu().numpy()
+        out["cpu_baseline"] = cpu_baseline(w, rplan.buffer_bytes, recv_host)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

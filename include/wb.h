@@ -1,0 +1,253 @@
+/*
+ * wb.h -- C ABI of libwb, the MI355X (gfx950) resharding library for
+ * trainer-to-rollout weight transfer (WeightBridge, arXiv 2609.25442).
+ *
+ * The library covers the data-parallel hot path of the paper's transfer:
+ *   1. describe a side's layout as slice-copy placements (Sec. 3.1: a worker's
+ *      source map is the sequence of slice copies, each optionally transposed,
+ *      that its weight loader performs from the full checkpoint);
+ *   2. plan (Sec. 3.2, "Generating an efficient routing plan"): intersect trainer
+ *      and rollout source maps in the checkpoint index space, give every needed
+ *      element exactly one sender, split replicated tensors into distinct
+ *      slices so the trainers send one copy, and balance bytes over replicas;
+ *   3. pack (Sec. 3.2, packing kernel): coalesce one trainer rank's shards, in
+ *      checkpoint row-major order, into one contiguous region per receiver;
+ *   4. unpack (Sec. 3.2, assembly kernel): scatter the received regions into
+ *      one rollout rank's tensors, casting fp32 -> bf16 (round to nearest
+ *      even) or quantising to fp8 E4M3FN with 128x128 blockwise fp32 scales
+ *      (s = amax / 448, q = RNE(x / s)); the paper assumes matched precision
+ *      and names conversion as future work (Sec. 5).
+ *
+ * Conventions for every call:
+ *   - Return value: WB_OK (0) or a negative wb_status. On error a message for
+ *     the calling thread is available from wb_last_error().
+ *   - Host structs passed in are copied; the caller keeps ownership.
+ *   - Objects returned through an out-pointer are owned by the library and are
+ *     released with the matching *_destroy call.
+ *   - "stream" arguments are hipStream_t values passed as void* (NULL is the
+ *     null stream). Device pointers must be device memory or pinned host memory
+ *     addressable from the current HIP device, and 16-byte aligned.
+ *   - The library never allocates device memory. It allocates host memory and,
+ *     for the pointer tables of wb_pack/wb_unpack, a small pinned host buffer.
+ */
+#ifndef WB_H
+#define WB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum wb_status {
+  WB_OK = 0,
+  WB_EINVAL = -1,        /* bad argument: null pointer, bad degree, out-of-range rank or index */
+  WB_EUNSUPPORTED = -2,  /* valid request outside what the library implements */
+  WB_ENOMEM = -3,        /* host allocation failed */
+  WB_EHIP = -4,          /* a HIP runtime call failed (message has the HIP error) */
+  WB_ESIZE = -5          /* caller buffer too small (see the "needed" out-argument) */
+} wb_status;
+
+typedef enum wb_dtype { WB_F32 = 0, WB_BF16 = 1, WB_F8E4M3 = 2, WB_DTYPE_NONE = -1 } wb_dtype;
+
+/* Model families whose checkpoint catalog wb_describe_layout knows. The catalog
+ * is the ordered list of checkpoint tensors, each at most 2-D ([rows, cols];
+ * vectors are [1, n]):
+ *   DENSE    : embed [V,H]; per layer attn_norm [1,H], q [nq*hd,H], k, v [nkv*hd,H],
+ *              o [H,nq*hd], mlp_norm [1,H], gate, up [F,H], down [H,F];
+ *              final_norm [1,H]; lm_head [V,H]
+ *   MIXTRAL  : embed; per layer the six attention tensors, router [E,H], then for
+ *              each expert e gate_e, up_e [F,H], down_e [H,F]; final_norm; lm_head
+ *   MOE_ONLY : per layer router [E,H], shared gate, up [F*S,H], shared down
+ *              [H,F*S], then the E routed experts as above (no attention). */
+typedef enum wb_family { WB_FAMILY_DENSE = 0, WB_FAMILY_MIXTRAL = 1, WB_FAMILY_MOE_ONLY = 2 } wb_family;
+
+typedef struct wb_model_shapes {
+  int32_t family;             /* wb_family */
+  int32_t num_layers;
+  int32_t hidden;             /* H */
+  int32_t num_heads;          /* nq */
+  int32_t num_kv_heads;       /* nkv */
+  int32_t head_dim;           /* hd */
+  int32_t ffn;                /* F (per expert for MoE families) */
+  int32_t vocab;              /* V */
+  int32_t num_experts;        /* E */
+  int32_t num_shared_experts; /* S */
+} wb_model_shapes;
+
+/* Layout styles:
+ *   FSDP_FLAT : FSDP1-style flat units (embed; each layer, or each layer's
+ *               non-expert part and each expert-parallel group's experts;
+ *               final_norm + lm_head), each unit's concatenation padded to a
+ *               multiple of fsdp; rank f holds the f-th equal piece as a 1-D
+ *               tensor. Non-expert units are replicated over ep and dp.
+ *               rank = (dp_i * ep + ep_i) * fsdp + f.
+ *   MEGATRON  : trainer tensor/expert parallel. Vocab-row embed/lm_head; fused
+ *               qkv grouped per kv head [q heads of the group; k; v]; fused
+ *               gate_up [gate rows; up rows]; row-parallel o/down column slabs,
+ *               stored transposed when transposed_row_parallel is set; MoE
+ *               experts stacked per ep rank (w1, w3 [E/ep,F,H], w2), router and
+ *               shared expert replicated (MoE needs tp == 1).
+ *               rank = (dp_i * ep + ep_i) * tp + tp_i.
+ *   SERVING   : rollout tensor/expert parallel. qkv [q slab; k slab; v slab];
+ *               gate_up [gate slab; up slab]; o/down column slabs; experts
+ *               stacked w13 [E/ep, 2F/tp, H] (expert j = [gate_j; up_j]) and
+ *               w2 [E/ep, H, F/tp]; attention, norms, router replicated over ep.
+ *               With quant_dtype = WB_F8E4M3 the linear weights (qkv, o,
+ *               gate_up, down, w13, w2, shared w13/w2) are fp8 E4M3FN, each
+ *               followed by an fp32 scale tensor [batch, ceil(rows/B), ceil(cols/B)].
+ *               rank = (dp_i * ep + ep_i) * tp + tp_i. */
+typedef enum wb_style { WB_STYLE_FSDP_FLAT = 0, WB_STYLE_MEGATRON = 1, WB_STYLE_SERVING = 2 } wb_style;
+
+typedef struct wb_parallelism {
+  int32_t style;                   /* wb_style */
+  int32_t dtype;                   /* local parameter dtype: WB_F32 or WB_BF16 */
+  int32_t tp, ep, fsdp, dp;        /* degrees, each >= 1 */
+  int32_t transposed_row_parallel; /* MEGATRON only: 0 or 1 */
+  int32_t quant_dtype;             /* SERVING only: WB_DTYPE_NONE or WB_F8E4M3 */
+  int32_t quant_block;             /* block edge for quant_dtype (1..128) */
+} wb_parallelism;
+
+typedef struct wb_layout_t wb_layout_t;
+typedef struct wb_plan_t wb_plan_t;
+
+/* One slice-copy (Sec. 3.1): rows r0..r1-1, cols c0..c1-1 of checkpoint tensor t
+ * are stored in local tensor u of the rank at
+ *   local[u][base + (i - r0) * ld + (j - c0)]   (transposed == 0)
+ *   local[u][base + (j - c0) * ld + (i - r0)]   (transposed == 1)
+ * Offsets are in elements of the local tensor's dtype. */
+typedef struct wb_placement {
+  int32_t t, u;
+  int64_t r0, r1, c0, c1;
+  int64_t base, ld;
+  int32_t transposed;
+  int32_t reserved;
+} wb_placement;
+
+typedef struct wb_tensor_desc {
+  const char* name;
+  int64_t rows, cols;
+} wb_tensor_desc;
+
+typedef struct wb_local_info {
+  const char* name;      /* valid while the layout lives */
+  int32_t dtype;         /* wb_dtype */
+  int32_t quant_block;   /* > 0 for fp8 tensors with a scale companion */
+  int64_t batch, rows, cols;
+  int32_t scale_index;   /* index of the companion scale tensor, or -1 */
+  int32_t scales_index;  /* for a scale tensor: index of the tensor it scales, else -1 */
+} wb_local_info;
+
+/* ---- layouts --------------------------------------------------------- */
+
+/* All ranks of one side for a known model family and parallelism style.
+ * Errors: WB_EINVAL (null, degree < 1, degrees that do not divide vocab, heads,
+ * kv heads, ffn or experts, bad dtype), WB_EUNSUPPORTED (style/family
+ * combinations listed above as unsupported). */
+int wb_describe_layout(const wb_model_shapes* shapes, const wb_parallelism* par, wb_layout_t** out);
+
+/* Generic layouts (a source map declared directly, e.g. recovered by probing a
+ * weight loader). wb_layout_add_local with dtype WB_F8E4M3 and quant_block > 0
+ * also appends the fp32 scale companion right after it. */
+int wb_layout_create(const wb_tensor_desc* catalog, int32_t num_tensors, int32_t num_ranks, wb_layout_t** out);
+int wb_layout_add_local(wb_layout_t* layout, int32_t rank, const char* name, int32_t dtype, int64_t batch,
+                        int64_t rows, int64_t cols, int32_t quant_block, int32_t* out_index);
+/* Errors: WB_EINVAL when the rectangle or the addressed local elements fall
+ * outside the tensor, or when u names a scale tensor. */
+int wb_layout_add_placement(wb_layout_t* layout, int32_t rank, const wb_placement* p);
+
+int wb_layout_num_ranks(const wb_layout_t* layout, int32_t* out);
+int wb_layout_num_tensors(const wb_layout_t* layout, int32_t* out);
+int wb_layout_tensor(const wb_layout_t* layout, int32_t t, wb_tensor_desc* out);
+int wb_layout_num_locals(const wb_layout_t* layout, int32_t rank, int32_t* out);
+int wb_layout_local(const wb_layout_t* layout, int32_t rank, int32_t index, wb_local_info* out);
+int wb_layout_num_placements(const wb_layout_t* layout, int32_t rank, int32_t* out);
+int wb_layout_placement(const wb_layout_t* layout, int32_t rank, int32_t index, wb_placement* out);
+/* Canonical text form. Writes at most cap bytes (NUL-terminated) and the full
+ * size including the NUL to *needed; WB_ESIZE if cap is too small. */
+int wb_layout_dump(const wb_layout_t* layout, char* buf, size_t cap, size_t* needed);
+void wb_layout_destroy(wb_layout_t* layout);
+
+/* ---- plans ----------------------------------------------------------- */
+
+typedef enum wb_role { WB_SENDER = 0, WB_RECEIVER = 1 } wb_role;
+
+/* Build the global routing plan of the two layouts (deterministic: every rank
+ * computes the same assignment) and keep the view of one rank: a trainer rank
+ * for WB_SENDER, a rollout rank for WB_RECEIVER. Canonical rules:
+ *   groups  : identical trainer rectangles of a tensor form one group; distinct
+ *             groups must be disjoint;
+ *   order   : rollout rank ascending, its placements in layout order, groups by
+ *             (r0, c0, r1, c1); each overlap is a region;
+ *   split   : a region held by k > 1 ranks is cut into k near-equal parts
+ *             (rows if it has >= k rows, else columns) handed out, largest
+ *             first, to the owner furthest below its even share of that owner
+ *             set (ties: lower part index, lower rank);
+ *   wire    : per (sender, receiver) the payloads in canonical order, each a
+ *             row-major copy of its rectangle in the sender dtype starting at a
+ *             multiple of 256 bytes; buffers hold regions by ascending peer,
+ *             each starting at a multiple of 4096 bytes.
+ * Errors: WB_EINVAL (null, rank out of range, catalogs differ, a rollout
+ * element held by no trainer, rollout tensors not exactly covered),
+ * WB_EUNSUPPORTED (overlapping non-identical trainer rectangles, replicas with
+ * different dtypes, an unsupported cast, an fp8 placement that is transposed
+ * or not a sub-rectangle of one matrix, quant_block > 128). */
+int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out);
+
+int wb_plan_num_segments(const wb_plan_t* plan, int64_t* out);        /* global */
+int wb_plan_buffer_bytes(const wb_plan_t* plan, int64_t* out);        /* this rank's send or receive buffer */
+int wb_plan_num_peers(const wb_plan_t* plan, int32_t* out);           /* regions in this rank's buffer */
+/* i-th region of this rank's buffer (ascending peer): peer rank, byte offset, bytes. */
+int wb_plan_peer(const wb_plan_t* plan, int32_t i, int32_t* peer, int64_t* offset, int64_t* bytes);
+/* Region of any (sender, receiver) pair: offset in the sender's buffer, offset in
+ * the receiver's buffer, bytes (0 when the pair exchanges nothing). */
+int wb_plan_region(const wb_plan_t* plan, int32_t sender, int32_t receiver, int64_t* send_offset,
+                   int64_t* recv_offset, int64_t* bytes);
+/* Global buffer size of any sender (role WB_SENDER) or receiver (WB_RECEIVER). */
+int wb_plan_rank_buffer_bytes(const wb_plan_t* plan, int32_t role, int32_t rank, int64_t* out);
+/* Number of local tensors of this rank: the length of src_ptrs / dst_ptrs. */
+int wb_plan_num_local_tensors(const wb_plan_t* plan, int32_t* out);
+/* Bytes of device workspace wb_plan_upload needs. */
+int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
+/* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */
+int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* write_bytes);
+/* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
+int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
+/* Canonical text form of the global plan (one line per segment). */
+int wb_plan_dump(const wb_plan_t* plan, char* buf, size_t cap, size_t* needed);
+
+/* Copy this rank's work tables into caller-owned device memory (at least
+ * wb_plan_workspace_bytes, 256-byte aligned), enqueued on stream. The caller
+ * keeps the workspace alive and unmodified while the plan is used.
+ * Errors: WB_EINVAL (null, too small, misaligned), WB_EHIP. */
+int wb_plan_upload(wb_plan_t* plan, void* workspace, size_t bytes, void* stream);
+
+/* Enqueue the packing kernel of a sender plan: src_ptrs[i] is local tensor i of
+ * the rank (wb_plan_num_local_tensors entries), send_buf holds at least
+ * wb_plan_buffer_bytes bytes. Writes every payload byte of the rank's regions;
+ * bytes between payloads are left as they were. One kernel launch.
+ * Errors (synchronous): WB_EINVAL (wrong role, not uploaded, null or misaligned
+ * pointer), WB_EHIP (launch failure). Device faults surface at stream sync. */
+int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* stream);
+
+/* Enqueue the assembly of a receiver plan: recv_buf holds the regions of all
+ * senders at the offsets the plan gives (wb_plan_peer / wb_plan_region); every
+ * element of every local tensor (dst_ptrs, wb_plan_num_local_tensors entries,
+ * scale tensors included) is written exactly once. One launch for copy/cast
+ * work and one for fp8 blocks when the rank has fp8 tensors.
+ * Errors as for wb_pack. Calls on one plan must not overlap in time from several
+ * host threads (the pointer table is per plan). */
+int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void* stream);
+
+void wb_plan_destroy(wb_plan_t* plan);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* wb_last_error(void);
+const char* wb_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WB_H */

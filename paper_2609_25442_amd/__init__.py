@@ -1,0 +1,334 @@
+"""Python binding of libwb, the gfx950 resharding library (WeightBridge,
+arXiv 2609.25442, Sec. 3.1-3.2): layouts as slice-copy source maps, the
+routing plan, and the packing and assembly kernels.
+
+Argument marshalling only: every step runs in libwb.so (host planner in C++,
+kernels in HIP). Importing this package fails if the library is not built
+(``python -m paper_2609_25442_amd.build``); there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_char_p, c_int32, c_int64, c_size_t, c_void_p
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwb.so")
+
+WB_OK, WB_EINVAL, WB_EUNSUPPORTED, WB_ENOMEM, WB_EHIP, WB_ESIZE = 0, -1, -2, -3, -4, -5
+DTYPES = {"f32": 0, "bf16": 1, "f8e4m3": 2}
+DTYPE_NAMES = {v: k for k, v in DTYPES.items()}
+DTYPE_BYTES = {"f32": 4, "bf16": 2, "f8e4m3": 1}
+FAMILIES = {"dense": 0, "mixtral": 1, "moe_only": 2}
+STYLES = {"fsdp_flat": 0, "megatron": 1, "serving": 2}
+SENDER, RECEIVER = 0, 1
+
+
+class WbError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libwb error {code}: {msg}")
+        self.code = code
+
+
+class ModelShapes(ctypes.Structure):
+    _fields_ = [(n, c_int32) for n in ("family", "num_layers", "hidden", "num_heads", "num_kv_heads", "head_dim",
+                                       "ffn", "vocab", "num_experts", "num_shared_experts")]
+
+
+class Parallelism(ctypes.Structure):
+    _fields_ = [(n, c_int32) for n in ("style", "dtype", "tp", "ep", "fsdp", "dp", "transposed_row_parallel",
+                                       "quant_dtype", "quant_block")]
+
+
+class Placement(ctypes.Structure):
+    _fields_ = [("t", c_int32), ("u", c_int32), ("r0", c_int64), ("r1", c_int64), ("c0", c_int64), ("c1", c_int64),
+                ("base", c_int64), ("ld", c_int64), ("transposed", c_int32), ("reserved", c_int32)]
+
+
+class TensorDesc(ctypes.Structure):
+    _fields_ = [("name", c_char_p), ("rows", c_int64), ("cols", c_int64)]
+
+
+class LocalInfo(ctypes.Structure):
+    _fields_ = [("name", c_char_p), ("dtype", c_int32), ("quant_block", c_int32), ("batch", c_int64),
+                ("rows", c_int64), ("cols", c_int64), ("scale_index", c_int32), ("scales_index", c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_25442_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, L = c_void_p, c_void_p
+    sig = {
+        "wb_describe_layout": [POINTER(ModelShapes), POINTER(Parallelism), POINTER(L)],
+        "wb_layout_create": [POINTER(TensorDesc), c_int32, c_int32, POINTER(L)],
+        "wb_layout_add_local": [L, c_int32, c_char_p, c_int32, c_int64, c_int64, c_int64, c_int32, POINTER(c_int32)],
+        "wb_layout_add_placement": [L, c_int32, POINTER(Placement)],
+        "wb_layout_num_ranks": [L, POINTER(c_int32)],
+        "wb_layout_num_tensors": [L, POINTER(c_int32)],
+        "wb_layout_tensor": [L, c_int32, POINTER(TensorDesc)],
+        "wb_layout_num_locals": [L, c_int32, POINTER(c_int32)],
+        "wb_layout_local": [L, c_int32, c_int32, POINTER(LocalInfo)],
+        "wb_layout_num_placements": [L, c_int32, POINTER(c_int32)],
+        "wb_layout_placement": [L, c_int32, c_int32, POINTER(Placement)],
+        "wb_layout_dump": [L, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
+        "wb_plan": [L, L, c_int32, c_int32, POINTER(P)],
+        "wb_plan_num_segments": [P, POINTER(c_int64)],
+        "wb_plan_buffer_bytes": [P, POINTER(c_int64)],
+        "wb_plan_num_peers": [P, POINTER(c_int32)],
+        "wb_plan_peer": [P, c_int32, POINTER(c_int32), POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_region": [P, c_int32, c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_rank_buffer_bytes": [P, c_int32, c_int32, POINTER(c_int64)],
+        "wb_plan_num_local_tensors": [P, POINTER(c_int32)],
+        "wb_plan_workspace_bytes": [P, POINTER(c_int64)],
+        "wb_plan_traffic_bytes": [P, POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_work_counts": [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_dump": [P, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
+        "wb_plan_upload": [P, c_void_p, c_size_t, c_void_p],
+        "wb_pack": [P, POINTER(c_void_p), c_void_p, c_void_p],
+        "wb_unpack": [P, c_void_p, POINTER(c_void_p), c_void_p],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = c_int32
+    lib.wb_layout_destroy.argtypes = [L]
+    lib.wb_layout_destroy.restype = None
+    lib.wb_plan_destroy.argtypes = [P]
+    lib.wb_plan_destroy.restype = None
+    lib.wb_last_error.restype = c_char_p
+    lib.wb_version.restype = c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def _check(rc: int):
+    if rc != WB_OK:
+        raise WbError(rc, lib.wb_last_error().decode())
+
+
+def _text(fn, handle) -> str:
+    need = c_size_t(0)
+    fn(handle, None, 0, byref(need))
+    buf = ctypes.create_string_buffer(need.value)
+    _check(fn(handle, buf, need.value, byref(need)))
+    return buf.value.decode()
+
+
+def _stream_handle(stream) -> int | None:
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ptr(x) -> int:
+    return x if isinstance(x, int) else x.data_ptr()
+
+
+class Layout:
+    """All ranks of one side: a checkpoint catalog and per-rank local tensors
+    and placements."""
+
+    def __init__(self, handle: int):
+        self._h = c_void_p(handle)
+
+    @classmethod
+    def describe(cls, model: dict, par: dict) -> "Layout":
+        m = ModelShapes(FAMILIES[model["family"]], model["num_layers"], model["hidden"], model.get("num_heads", 0),
+                        model.get("num_kv_heads", 0), model.get("head_dim", 0), model.get("ffn", 0),
+                        model.get("vocab", 0), model.get("num_experts", 0), model.get("num_shared_experts", 0))
+        q = par.get("quant", "")
+        p = Parallelism(STYLES[par["style"]], DTYPES[par["dtype"]], par.get("tp", 1), par.get("ep", 1),
+                        par.get("fsdp", 1), par.get("dp", 1), int(bool(par.get("transposed_row_parallel", False))),
+                        DTYPES[q] if q else -1, par.get("quant_block", 128) if q else 0)
+        h = c_void_p()
+        _check(lib.wb_describe_layout(byref(m), byref(p), byref(h)))
+        return cls(h.value)
+
+    @classmethod
+    def create(cls, catalog, nranks: int) -> "Layout":
+        """Empty generic layout over ``catalog`` = [(name, rows, cols), ...]."""
+        arr = (TensorDesc * max(1, len(catalog)))()
+        keep = []
+        for i, (n, r, c) in enumerate(catalog):
+            b = n.encode()
+            keep.append(b)
+            arr[i] = TensorDesc(b, r, c)
+        h = c_void_p()
+        _check(lib.wb_layout_create(arr, len(catalog), nranks, byref(h)))
+        return cls(h.value)
+
+    def add_local(self, rank, name, dtype, batch, rows, cols, quant_block=0) -> int:
+        out = c_int32()
+        _check(lib.wb_layout_add_local(self._h, rank, name.encode(), DTYPES[dtype], batch, rows, cols, quant_block,
+                                       byref(out)))
+        return out.value
+
+    def add_placement(self, rank, t, r0, r1, c0, c1, u, base, ld, transposed=0):
+        p = Placement(t, u, r0, r1, c0, c1, base, ld, transposed, 0)
+        _check(lib.wb_layout_add_placement(self._h, rank, byref(p)))
+
+    @property
+    def nranks(self) -> int:
+        n = c_int32()
+        _check(lib.wb_layout_num_ranks(self._h, byref(n)))
+        return n.value
+
+    def tensors(self):
+        n = c_int32()
+        _check(lib.wb_layout_num_tensors(self._h, byref(n)))
+        out = []
+        for t in range(n.value):
+            d = TensorDesc()
+            _check(lib.wb_layout_tensor(self._h, t, byref(d)))
+            out.append((d.name.decode(), d.rows, d.cols))
+        return out
+
+    def locals(self, rank: int):
+        n = c_int32()
+        _check(lib.wb_layout_num_locals(self._h, rank, byref(n)))
+        out = []
+        for u in range(n.value):
+            i = LocalInfo()
+            _check(lib.wb_layout_local(self._h, rank, u, byref(i)))
+            out.append(dict(name=i.name.decode(), dtype=DTYPE_NAMES[i.dtype], block=i.quant_block, batch=i.batch,
+                            rows=i.rows, cols=i.cols, scale=i.scale_index, scales=i.scales_index,
+                            numel=i.batch * i.rows * i.cols))
+        return out
+
+    def placements(self, rank: int):
+        n = c_int32()
+        _check(lib.wb_layout_num_placements(self._h, rank, byref(n)))
+        out = []
+        for k in range(n.value):
+            p = Placement()
+            _check(lib.wb_layout_placement(self._h, rank, k, byref(p)))
+            out.append((p.t, p.r0, p.r1, p.c0, p.c1, p.u, p.base, p.ld, p.transposed))
+        return out
+
+    def dump(self) -> str:
+        return _text(lib.wb_layout_dump, self._h)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib.wb_layout_destroy(self._h)
+            self._h = c_void_p()
+
+
+class Plan:
+    """The global routing plan seen from one rank (a sender or a receiver)."""
+
+    def __init__(self, trainer: Layout, rollout: Layout, role: int, rank: int):
+        h = c_void_p()
+        _check(lib.wb_plan(trainer._h, rollout._h, role, rank, byref(h)))
+        self._h = h
+        self.role, self.rank = role, rank
+        self._workspace = None
+
+    def _i64(self, fn):
+        v = c_int64()
+        _check(fn(self._h, byref(v)))
+        return v.value
+
+    @property
+    def num_segments(self) -> int:
+        return self._i64(lib.wb_plan_num_segments)
+
+    @property
+    def buffer_bytes(self) -> int:
+        return self._i64(lib.wb_plan_buffer_bytes)
+
+    @property
+    def workspace_bytes(self) -> int:
+        return self._i64(lib.wb_plan_workspace_bytes)
+
+    @property
+    def num_local_tensors(self) -> int:
+        v = c_int32()
+        _check(lib.wb_plan_num_local_tensors(self._h, byref(v)))
+        return v.value
+
+    def rank_buffer_bytes(self, role: int, rank: int) -> int:
+        v = c_int64()
+        _check(lib.wb_plan_rank_buffer_bytes(self._h, role, rank, byref(v)))
+        return v.value
+
+    def peers(self):
+        """[(peer rank, offset, bytes)] of the regions in this rank's buffer."""
+        n = c_int32()
+        _check(lib.wb_plan_num_peers(self._h, byref(n)))
+        out = []
+        for i in range(n.value):
+            p, o, b = c_int32(), c_int64(), c_int64()
+            _check(lib.wb_plan_peer(self._h, i, byref(p), byref(o), byref(b)))
+            out.append((p.value, o.value, b.value))
+        return out
+
+    def region(self, sender: int, receiver: int):
+        """(offset in the sender's buffer, offset in the receiver's buffer, bytes)."""
+        s, r, b = c_int64(), c_int64(), c_int64()
+        _check(lib.wb_plan_region(self._h, sender, receiver, byref(s), byref(r), byref(b)))
+        return s.value, r.value, b.value
+
+    def traffic(self):
+        r, w = c_int64(), c_int64()
+        _check(lib.wb_plan_traffic_bytes(self._h, byref(r), byref(w)))
+        return r.value, w.value
+
+    def work_counts(self):
+        a, b, c = c_int64(), c_int64(), c_int64()
+        _check(lib.wb_plan_work_counts(self._h, byref(a), byref(b), byref(c)))
+        return a.value, b.value, c.value
+
+    def dump(self) -> str:
+        return _text(lib.wb_plan_dump, self._h)
+
+    def upload(self, workspace, stream=None):
+        """Copy the work tables into ``workspace`` (a device tensor or pointer of
+        at least ``workspace_bytes`` bytes); the plan keeps a reference to it."""
+        nbytes = workspace.numel() * workspace.element_size() if hasattr(workspace, "numel") else self.workspace_bytes
+        _check(lib.wb_plan_upload(self._h, _ptr(workspace), nbytes, _stream_handle(stream)))
+        self._workspace = workspace
+
+    def pack(self, src, send_buf, stream=None):
+        ptrs = (c_void_p * max(1, len(src)))(*[_ptr(x) for x in src])
+        _check(lib.wb_pack(self._h, ptrs, _ptr(send_buf), _stream_handle(stream)))
+
+    def unpack(self, recv_buf, dst, stream=None):
+        ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
+        _check(lib.wb_unpack(self._h, _ptr(recv_buf), ptrs, _stream_handle(stream)))
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib.wb_plan_destroy(self._h)
+            self._h = c_void_p()
+
+
+def version() -> str:
+    return lib.wb_version().decode()
+
+
+def torch_dtype(name: str):
+    import torch
+
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f8e4m3": torch.float8_e4m3fn}[name]
+
+
+def allocate_locals(layout: Layout, rank: int, device="cuda", zero=False):
+    """Torch tensors for every local tensor of ``rank`` (shape [batch, rows, cols]
+    squeezed as the layout gives it)."""
+    import torch
+
+    out = []
+    for lc in layout.locals(rank):
+        shape = (lc["batch"], lc["rows"], lc["cols"]) if lc["batch"] > 1 else (lc["rows"], lc["cols"])
+        mk = torch.zeros if zero else torch.empty
+        out.append(mk(shape, dtype=torch_dtype(lc["dtype"]), device=device))
+    return out

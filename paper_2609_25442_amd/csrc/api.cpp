@@ -1,0 +1,489 @@
+// C ABI of libwb (declared in include/wb.h): argument checks, error strings,
+// work-table upload and the per-call pointer tables of wb_pack / wb_unpack.
+#include <hip/hip_runtime_api.h>
+
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "wb_internal.hpp"
+
+namespace {
+
+thread_local std::string g_error;
+
+int set_error(int code, const std::string& msg) {
+  g_error = msg;
+  return code;
+}
+
+template <class F>
+int guarded(F&& f) {
+  try {
+    g_error.clear();
+    return f();
+  } catch (const wb::Error& e) {
+    return set_error(e.code, e.what());
+  } catch (const std::bad_alloc&) {
+    return set_error(WB_ENOMEM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return set_error(WB_EINVAL, e.what());
+  }
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return set_error(WB_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int copy_text(const std::string& s, char* buf, size_t cap, size_t* needed) {
+  if (needed) *needed = s.size() + 1;
+  if (!buf || cap < s.size() + 1) return set_error(WB_ESIZE, "buffer too small for the text");
+  std::memcpy(buf, s.c_str(), s.size() + 1);
+  return WB_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Refuse a pointer whose device allocation is smaller than what the kernels
+// will touch. Memory the runtime cannot size (e.g. pinned host memory) is
+// accepted as given.
+int check_extent(const void* p, int64_t bytes, const char* what) {
+  if (!p) return set_error(WB_EINVAL, std::string(what) + " is null");
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return set_error(WB_EINVAL, std::string(what) + " is not 16-byte aligned");
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return WB_OK;
+  }
+  const uintptr_t end = reinterpret_cast<uintptr_t>(base) + size;
+  if (reinterpret_cast<uintptr_t>(p) + uint64_t(bytes) > end)
+    return set_error(WB_EINVAL, std::string(what) + " is smaller than the plan needs (" + std::to_string(bytes) + " bytes)");
+  return WB_OK;
+}
+
+// Stage a new pointer table into the workspace when the pointers changed.
+int update_pointers(wb_plan_t* P, const std::vector<uint64_t>& ptrs, void* stream) {
+  if (ptrs == P->last_ptrs) return WB_OK;
+  hipEvent_t ev = static_cast<hipEvent_t>(P->ptr_event);
+  hipError_t e = hipEventSynchronize(ev);  // the previous staging copy has left the pinned buffer
+  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  std::memcpy(P->ptr_stage, ptrs.data(), ptrs.size() * sizeof(uint64_t));
+  e = hipMemcpyAsync(P->ws + P->off_ptrs, P->ptr_stage, ptrs.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
+                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
+  e = hipEventRecord(ev, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  P->last_ptrs = ptrs;
+  return WB_OK;
+}
+
+int64_t local_bytes(const wb::Local& l) { return l.numel() * wb::dtype_bytes(l.dtype); }
+
+const wb::Rank& rank_of(const wb_plan_t* P) {
+  return P->role == WB_SENDER ? P->trainer.ranks[P->rank] : P->rollout.ranks[P->rank];
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* wb_last_error(void) { return g_error.c_str(); }
+const char* wb_version(void) { return "wb 0.1.0 (gfx950)"; }
+
+int wb_describe_layout(const wb_model_shapes* shapes, const wb_parallelism* par, wb_layout_t** out) {
+  return guarded([&]() -> int {
+    if (!shapes || !par || !out) return set_error(WB_EINVAL, "null argument");
+    *out = nullptr;
+    auto* L = new wb_layout_t;
+    try {
+      wb::describe(*shapes, *par, *L);
+    } catch (...) {
+      delete L;
+      throw;
+    }
+    *out = L;
+    return WB_OK;
+  });
+}
+
+int wb_layout_create(const wb_tensor_desc* catalog, int32_t num_tensors, int32_t num_ranks, wb_layout_t** out) {
+  return guarded([&]() -> int {
+    if (!out || (num_tensors > 0 && !catalog) || num_tensors < 0 || num_ranks < 1)
+      return set_error(WB_EINVAL, "bad catalog or rank count");
+    *out = nullptr;
+    auto* L = new wb_layout_t;
+    for (int i = 0; i < num_tensors; ++i) {
+      if (!catalog[i].name || catalog[i].rows < 1 || catalog[i].cols < 1) {
+        delete L;
+        return set_error(WB_EINVAL, "catalog tensors need a name and positive shape");
+      }
+      L->catalog.push_back({catalog[i].name, catalog[i].rows, catalog[i].cols});
+    }
+    L->ranks.resize(num_ranks);
+    *out = L;
+    return WB_OK;
+  });
+}
+
+int wb_layout_add_local(wb_layout_t* L, int32_t rank, const char* name, int32_t dtype, int64_t batch, int64_t rows,
+                        int64_t cols, int32_t quant_block, int32_t* out_index) {
+  return guarded([&]() -> int {
+    if (!L || !name || rank < 0 || rank >= static_cast<int>(L->ranks.size()))
+      return set_error(WB_EINVAL, "bad layout, rank or name");
+    if (batch < 1 || rows < 1 || cols < 1) return set_error(WB_EINVAL, "local tensor shape must be positive");
+    if (dtype != WB_F32 && dtype != WB_BF16 && dtype != WB_F8E4M3) return set_error(WB_EINVAL, "bad dtype");
+    if ((dtype == WB_F8E4M3) != (quant_block > 0))
+      return set_error(WB_EUNSUPPORTED, "fp8 local tensors need a quant_block (and only they take one)");
+    if (quant_block > 128) return set_error(WB_EUNSUPPORTED, "quant_block above 128");
+    wb::Rank& R = L->ranks[rank];
+    const int u = static_cast<int>(R.locals.size());
+    wb::Local l;
+    l.name = name;
+    l.dtype = dtype;
+    l.batch = batch;
+    l.rows = rows;
+    l.cols = cols;
+    if (quant_block > 0) {
+      l.block = quant_block;
+      l.scale = u + 1;
+      R.locals.push_back(l);
+      wb::Local s;
+      s.name = std::string(name) + "_scale";
+      s.dtype = WB_F32;
+      s.batch = batch;
+      s.rows = (rows + quant_block - 1) / quant_block;
+      s.cols = (cols + quant_block - 1) / quant_block;
+      s.scales = u;
+      R.locals.push_back(s);
+    } else {
+      R.locals.push_back(l);
+    }
+    if (out_index) *out_index = u;
+    return WB_OK;
+  });
+}
+
+int wb_layout_add_placement(wb_layout_t* L, int32_t rank, const wb_placement* p) {
+  return guarded([&]() -> int {
+    if (!L || !p) return set_error(WB_EINVAL, "null argument");
+    wb::Placement q;
+    q.t = p->t;
+    q.u = p->u;
+    q.r0 = p->r0;
+    q.r1 = p->r1;
+    q.c0 = p->c0;
+    q.c1 = p->c1;
+    q.base = p->base;
+    q.ld = p->ld;
+    q.tr = p->transposed;
+    wb::check_placement(*L, rank, q);
+    L->ranks[rank].pls.push_back(q);
+    return WB_OK;
+  });
+}
+
+int wb_layout_num_ranks(const wb_layout_t* L, int32_t* out) {
+  if (!L || !out) return set_error(WB_EINVAL, "null argument");
+  *out = static_cast<int32_t>(L->ranks.size());
+  return WB_OK;
+}
+
+int wb_layout_num_tensors(const wb_layout_t* L, int32_t* out) {
+  if (!L || !out) return set_error(WB_EINVAL, "null argument");
+  *out = static_cast<int32_t>(L->catalog.size());
+  return WB_OK;
+}
+
+int wb_layout_tensor(const wb_layout_t* L, int32_t t, wb_tensor_desc* out) {
+  if (!L || !out || t < 0 || t >= static_cast<int>(L->catalog.size())) return set_error(WB_EINVAL, "bad tensor index");
+  out->name = L->catalog[t].name.c_str();
+  out->rows = L->catalog[t].rows;
+  out->cols = L->catalog[t].cols;
+  return WB_OK;
+}
+
+int wb_layout_num_locals(const wb_layout_t* L, int32_t rank, int32_t* out) {
+  if (!L || !out || rank < 0 || rank >= static_cast<int>(L->ranks.size())) return set_error(WB_EINVAL, "bad rank");
+  *out = static_cast<int32_t>(L->ranks[rank].locals.size());
+  return WB_OK;
+}
+
+int wb_layout_local(const wb_layout_t* L, int32_t rank, int32_t index, wb_local_info* out) {
+  if (!L || !out || rank < 0 || rank >= static_cast<int>(L->ranks.size())) return set_error(WB_EINVAL, "bad rank");
+  const wb::Rank& R = L->ranks[rank];
+  if (index < 0 || index >= static_cast<int>(R.locals.size())) return set_error(WB_EINVAL, "bad local index");
+  const wb::Local& l = R.locals[index];
+  out->name = l.name.c_str();
+  out->dtype = l.dtype;
+  out->quant_block = l.block;
+  out->batch = l.batch;
+  out->rows = l.rows;
+  out->cols = l.cols;
+  out->scale_index = l.scale;
+  out->scales_index = l.scales;
+  return WB_OK;
+}
+
+int wb_layout_num_placements(const wb_layout_t* L, int32_t rank, int32_t* out) {
+  if (!L || !out || rank < 0 || rank >= static_cast<int>(L->ranks.size())) return set_error(WB_EINVAL, "bad rank");
+  *out = static_cast<int32_t>(L->ranks[rank].pls.size());
+  return WB_OK;
+}
+
+int wb_layout_placement(const wb_layout_t* L, int32_t rank, int32_t index, wb_placement* out) {
+  if (!L || !out || rank < 0 || rank >= static_cast<int>(L->ranks.size())) return set_error(WB_EINVAL, "bad rank");
+  const wb::Rank& R = L->ranks[rank];
+  if (index < 0 || index >= static_cast<int>(R.pls.size())) return set_error(WB_EINVAL, "bad placement index");
+  const wb::Placement& p = R.pls[index];
+  *out = wb_placement{p.t, p.u, p.r0, p.r1, p.c0, p.c1, p.base, p.ld, p.tr, 0};
+  return WB_OK;
+}
+
+int wb_layout_dump(const wb_layout_t* L, char* buf, size_t cap, size_t* needed) {
+  return guarded([&]() -> int {
+    if (!L) return set_error(WB_EINVAL, "null layout");
+    return copy_text(wb::dump_layout(*L), buf, cap, needed);
+  });
+}
+
+void wb_layout_destroy(wb_layout_t* L) { delete L; }
+
+int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out) {
+  return guarded([&]() -> int {
+    if (!trainer || !rollout || !out) return set_error(WB_EINVAL, "null argument");
+    *out = nullptr;
+    auto* P = new wb_plan_t;
+    try {
+      wb::build_plan(*trainer, *rollout, role, rank, *P);
+      P->trainer = *trainer;
+      P->rollout = *rollout;
+      const wb::Rank& R = rank_of(P);
+      if (R.locals.size() + 1 > 65535) wb::fail(WB_EUNSUPPORTED, "too many local tensors on one rank");
+      if (P->tasks.size() > 0x7FFFFFFF || P->qblocks.size() > 0x7FFFFFFF)
+        wb::fail(WB_EUNSUPPORTED, "too many work items for one launch");
+    } catch (...) {
+      delete P;
+      throw;
+    }
+    *out = P;
+    return WB_OK;
+  });
+}
+
+int wb_plan_num_segments(const wb_plan_t* P, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  *out = static_cast<int64_t>(P->segs.size());
+  return WB_OK;
+}
+
+int wb_plan_buffer_bytes(const wb_plan_t* P, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  *out = P->role == WB_SENDER ? P->send_bytes[P->rank] : P->recv_bytes[P->rank];
+  return WB_OK;
+}
+
+int wb_plan_rank_buffer_bytes(const wb_plan_t* P, int32_t role, int32_t rank, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  if (role == WB_SENDER && rank >= 0 && rank < P->n_send) { *out = P->send_bytes[rank]; return WB_OK; }
+  if (role == WB_RECEIVER && rank >= 0 && rank < P->n_recv) { *out = P->recv_bytes[rank]; return WB_OK; }
+  return set_error(WB_EINVAL, "bad role or rank");
+}
+
+int wb_plan_num_peers(const wb_plan_t* P, int32_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  int n = 0;
+  const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
+  for (int o = 0; o < others; ++o) {
+    const size_t k = P->role == WB_SENDER ? size_t(P->rank) * P->n_recv + o : size_t(o) * P->n_recv + P->rank;
+    n += P->send_region[k] >= 0;
+  }
+  *out = n;
+  return WB_OK;
+}
+
+int wb_plan_peer(const wb_plan_t* P, int32_t i, int32_t* peer, int64_t* offset, int64_t* bytes) {
+  if (!P || !peer || !offset || !bytes) return set_error(WB_EINVAL, "null argument");
+  const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
+  int n = 0;
+  for (int o = 0; o < others; ++o) {
+    const size_t k = P->role == WB_SENDER ? size_t(P->rank) * P->n_recv + o : size_t(o) * P->n_recv + P->rank;
+    if (P->send_region[k] < 0) continue;
+    if (n++ == i) {
+      *peer = o;
+      *offset = P->role == WB_SENDER ? P->send_region[k] : P->recv_region[k];
+      *bytes = P->region_bytes[k];
+      return WB_OK;
+    }
+  }
+  return set_error(WB_EINVAL, "peer index out of range");
+}
+
+int wb_plan_region(const wb_plan_t* P, int32_t s, int32_t d, int64_t* send_offset, int64_t* recv_offset,
+                   int64_t* bytes) {
+  if (!P || !send_offset || !recv_offset || !bytes) return set_error(WB_EINVAL, "null argument");
+  if (s < 0 || s >= P->n_send || d < 0 || d >= P->n_recv) return set_error(WB_EINVAL, "rank out of range");
+  const size_t k = size_t(s) * P->n_recv + d;
+  *send_offset = P->send_region[k] < 0 ? 0 : P->send_region[k];
+  *recv_offset = P->recv_region[k] < 0 ? 0 : P->recv_region[k];
+  *bytes = P->region_bytes[k];
+  return WB_OK;
+}
+
+int wb_plan_num_local_tensors(const wb_plan_t* P, int32_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  *out = P->n_locals;
+  return WB_OK;
+}
+
+static void workspace_layout(const wb_plan_t* P, size_t* ptrs, size_t* tasks, size_t* qb, size_t* qp, size_t* total) {
+  size_t off = 0;
+  *ptrs = off;
+  off = align256(off + sizeof(uint64_t) * (P->n_locals + 1));
+  *tasks = off;
+  off = align256(off + sizeof(wb::Task) * P->tasks.size());
+  *qb = off;
+  off = align256(off + sizeof(wb::QBlock) * P->qblocks.size());
+  *qp = off;
+  off = align256(off + sizeof(wb::QPiece) * P->qpieces.size());
+  *total = off;
+}
+
+int wb_plan_workspace_bytes(const wb_plan_t* P, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  size_t a, b, c, d, total;
+  workspace_layout(P, &a, &b, &c, &d, &total);
+  *out = static_cast<int64_t>(total);
+  return WB_OK;
+}
+
+int wb_plan_traffic_bytes(const wb_plan_t* P, int64_t* read_bytes, int64_t* write_bytes) {
+  if (!P || !read_bytes || !write_bytes) return set_error(WB_EINVAL, "null argument");
+  *read_bytes = P->read_bytes;
+  *write_bytes = P->write_bytes;
+  return WB_OK;
+}
+
+int wb_plan_work_counts(const wb_plan_t* P, int64_t* tasks, int64_t* blocks, int64_t* pieces) {
+  if (!P || !tasks || !blocks || !pieces) return set_error(WB_EINVAL, "null argument");
+  *tasks = static_cast<int64_t>(P->tasks.size());
+  *blocks = static_cast<int64_t>(P->qblocks.size());
+  *pieces = static_cast<int64_t>(P->qpieces.size());
+  return WB_OK;
+}
+
+int wb_plan_dump(const wb_plan_t* P, char* buf, size_t cap, size_t* needed) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    return copy_text(wb::dump_plan(*P), buf, cap, needed);
+  });
+}
+
+int wb_plan_upload(wb_plan_t* P, void* workspace, size_t bytes, void* stream) {
+  return guarded([&]() -> int {
+    if (!P || !workspace) return set_error(WB_EINVAL, "null argument");
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return set_error(WB_EINVAL, "workspace must be 256-byte aligned");
+    size_t total;
+    workspace_layout(P, &P->off_ptrs, &P->off_tasks, &P->off_qblocks, &P->off_qpieces, &total);
+    if (bytes < total) return set_error(WB_EINVAL, "workspace smaller than wb_plan_workspace_bytes");
+    int rc = check_extent(workspace, static_cast<int64_t>(total), "workspace");
+    if (rc != WB_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipError_t e;
+    if (!P->tasks.empty() &&
+        (e = hipMemcpyAsync(ws + P->off_tasks, P->tasks.data(), sizeof(wb::Task) * P->tasks.size(),
+                            hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (tasks)");
+    if (!P->qblocks.empty() &&
+        (e = hipMemcpyAsync(ws + P->off_qblocks, P->qblocks.data(), sizeof(wb::QBlock) * P->qblocks.size(),
+                            hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (fp8 blocks)");
+    if (!P->qpieces.empty() &&
+        (e = hipMemcpyAsync(ws + P->off_qpieces, P->qpieces.data(), sizeof(wb::QPiece) * P->qpieces.size(),
+                            hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (fp8 pieces)");
+    if (!P->ptr_stage) {
+      if ((e = hipHostMalloc(&P->ptr_stage, sizeof(uint64_t) * (P->n_locals + 1), hipHostMallocDefault)) != hipSuccess) {
+        P->ptr_stage = nullptr;
+        return hip_fail(e, "hipHostMalloc (pointer staging)");
+      }
+      hipEvent_t ev;
+      if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "hipEventCreateWithFlags");
+      P->ptr_event = ev;
+    }
+    // the host tables must stay valid until the copies above have run
+    if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    P->ws = ws;
+    P->ws_bytes = bytes;
+    P->last_ptrs.clear();
+    return WB_OK;
+  });
+}
+
+int wb_pack(wb_plan_t* P, const void* const* src_ptrs, void* send_buf, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    if (P->role != WB_SENDER) return set_error(WB_EINVAL, "wb_pack needs a sender plan");
+    if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
+    if (!src_ptrs && P->n_locals > 0) return set_error(WB_EINVAL, "src_ptrs is null");
+    const wb::Rank& R = rank_of(P);
+    std::vector<uint64_t> ptrs(P->n_locals + 1);
+    ptrs[0] = reinterpret_cast<uint64_t>(send_buf);
+    for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(src_ptrs[i]);
+    if (ptrs != P->last_ptrs) {
+      int rc = check_extent(send_buf, P->send_bytes[P->rank], "send_buf");
+      for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
+        rc = check_extent(src_ptrs[i], local_bytes(R.locals[i]), ("src_ptrs[" + std::to_string(i) + "]").c_str());
+      if (rc != WB_OK) return rc;
+      if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
+    }
+    const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
+    const int e = wb::launch_tasks(reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks),
+                                   static_cast<uint32_t>(P->tasks.size()), table, stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("pack launch: ") + wb::hip_error_string(e));
+    return WB_OK;
+  });
+}
+
+int wb_unpack(wb_plan_t* P, const void* recv_buf, void* const* dst_ptrs, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    if (P->role != WB_RECEIVER) return set_error(WB_EINVAL, "wb_unpack needs a receiver plan");
+    if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
+    if (!dst_ptrs && P->n_locals > 0) return set_error(WB_EINVAL, "dst_ptrs is null");
+    const wb::Rank& R = rank_of(P);
+    std::vector<uint64_t> ptrs(P->n_locals + 1);
+    ptrs[0] = reinterpret_cast<uint64_t>(recv_buf);
+    for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(dst_ptrs[i]);
+    if (ptrs != P->last_ptrs) {
+      int rc = check_extent(recv_buf, P->recv_bytes[P->rank], "recv_buf");
+      for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
+        rc = check_extent(dst_ptrs[i], local_bytes(R.locals[i]), ("dst_ptrs[" + std::to_string(i) + "]").c_str());
+      if (rc != WB_OK) return rc;
+      if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
+    }
+    const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
+    int e = wb::launch_tasks(reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks),
+                             static_cast<uint32_t>(P->tasks.size()), table, stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("unpack launch: ") + wb::hip_error_string(e));
+    e = wb::launch_qblocks(reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks),
+                           static_cast<uint32_t>(P->qblocks.size()),
+                           reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table, stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
+    return WB_OK;
+  });
+}
+
+void wb_plan_destroy(wb_plan_t* P) {
+  if (!P) return;
+  if (P->ptr_event) {
+    (void)hipEventSynchronize(static_cast<hipEvent_t>(P->ptr_event));
+    (void)hipEventDestroy(static_cast<hipEvent_t>(P->ptr_event));
+  }
+  if (P->ptr_stage) (void)hipHostFree(P->ptr_stage);
+  delete P;
+}
+
+}  // extern "C"

@@ -1,0 +1,355 @@
+// gfx950 kernels of the packing and assembly steps (WeightBridge Sec. 3.2:
+// a packing kernel coalesces a round's tensors into per-receiver buffers in
+// checkpoint format; an assembly kernel scatters them into the inference
+// tensors). Both are batched across tensors: one launch walks a flat table of
+// work items, one 256-thread workgroup per item.
+//
+//  * wb_tasks_kernel  -- copy/cast work items: 16-byte vectorised row copies,
+//    fp32 -> bf16 (v_cvt_pk_bf16_f32, round to nearest even), bf16 -> fp32,
+//    an element-wise fallback for unaligned or odd cases, and 64 x 64 tiles
+//    transposed through LDS where a trainer stores a shard transposed.
+//  * wb_qblock_kernel -- one fp8 E4M3FN block (<= 128 x 128) per workgroup,
+//    gathered from its wire pieces into registers: amax by wavefront
+//    shuffles plus LDS across the four waves, s = amax / 448 (IEEE division),
+//    q = RN(x / s) computed with one reciprocal per block and a remainder
+//    correction (exact in the range that reaches E4M3), then
+//    v_cvt_pk_fp8_f32. The scale is written by thread 0.
+// The work is bandwidth bound: no matrix cores are involved.
+#include <hip/hip_runtime.h>
+
+#include "wb_internal.hpp"
+
+namespace wb {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  const bf16x2 h = __builtin_convertvector(f32x2{a, b}, bf16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+__device__ __forceinline__ u32x4 cvt8_f32_bf16(const f32x4& a, const f32x4& b) {
+  return u32x4{pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w)};
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Walks the flattened (row, vector) index space of a rows x vpr block with
+// stride kThreads, keeping row and column incrementally (one division per task).
+struct Walker {
+  uint32_t r, c, dr, dc, vpr;
+  __device__ Walker(uint32_t start, uint32_t vpr_) : vpr(vpr_) {
+    r = start / vpr;
+    c = start % vpr;
+    dr = kThreads / vpr;
+    dc = kThreads % vpr;
+  }
+  __device__ __forceinline__ void step() {
+    c += dc;
+    r += dr;
+    if (c >= vpr) {
+      c -= vpr;
+      ++r;
+    }
+  }
+};
+
+// 16-byte row copy; cols, strides and offsets in bytes.
+__device__ void run_copy16(const Task& t, const char* src, char* dst) {
+  const uint32_t vpr = t.cols >> 4;
+  if (t.rows == 1) {
+    const u32x4* s = reinterpret_cast<const u32x4*>(src);
+    u32x4* d = reinterpret_cast<u32x4*>(dst);
+    uint32_t i = threadIdx.x;
+    for (; i + (kUnroll - 1) * kThreads < vpr; i += kUnroll * kThreads) {
+      u32x4 v[kUnroll];
+#pragma unroll
+      for (int k = 0; k < kUnroll; ++k) v[k] = __builtin_nontemporal_load(s + i + k * kThreads);
+#pragma unroll
+      for (int k = 0; k < kUnroll; ++k) __builtin_nontemporal_store(v[k], d + i + k * kThreads);
+    }
+    for (; i < vpr; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+    return;
+  }
+  const uint64_t total = uint64_t(t.rows) * vpr;
+  Walker w(threadIdx.x, vpr);
+  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
+    u32x4 v[kUnroll];
+    u32x4* dp[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      dp[k] = nullptr;
+      if (q + uint64_t(k) * kThreads < total) {
+        const u32x4* sp = reinterpret_cast<const u32x4*>(src + uint64_t(w.r) * t.src_ld) + w.c;
+        dp[k] = reinterpret_cast<u32x4*>(dst + uint64_t(w.r) * t.dst_ld) + w.c;
+        v[k] = __builtin_nontemporal_load(sp);
+      }
+      w.step();
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dp[k]) __builtin_nontemporal_store(v[k], dp[k]);
+  }
+}
+
+// fp32 -> bf16, 8 elements per vector; strides in elements.
+__device__ void run_f32_bf16(const Task& t, const char* src, char* dst) {
+  const uint32_t vpr = t.cols >> 3;
+  const uint64_t total = uint64_t(t.rows) * vpr;
+  Walker w(threadIdx.x, vpr);
+  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
+    f32x4 a[kUnroll], b[kUnroll];
+    u32x4* dp[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      dp[k] = nullptr;
+      if (q + uint64_t(k) * kThreads < total) {
+        const f32x4* sp = reinterpret_cast<const f32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 4);
+        dp[k] = reinterpret_cast<u32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 2);
+        a[k] = __builtin_nontemporal_load(sp);
+        b[k] = __builtin_nontemporal_load(sp + 1);
+      }
+      w.step();
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dp[k]) __builtin_nontemporal_store(cvt8_f32_bf16(a[k], b[k]), dp[k]);
+  }
+}
+
+// bf16 -> fp32, 8 elements per vector; strides in elements.
+__device__ void run_bf16_f32(const Task& t, const char* src, char* dst) {
+  const uint32_t vpr = t.cols >> 3;
+  const uint64_t total = uint64_t(t.rows) * vpr;
+  Walker w(threadIdx.x, vpr);
+  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
+    u32x4 v[kUnroll];
+    f32x4* dp[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      dp[k] = nullptr;
+      if (q + uint64_t(k) * kThreads < total) {
+        const u32x4* sp = reinterpret_cast<const u32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 2);
+        dp[k] = reinterpret_cast<f32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 4);
+        v[k] = __builtin_nontemporal_load(sp);
+      }
+      w.step();
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dp[k]) {
+        const u32x4 x = v[k];
+        __builtin_nontemporal_store(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, dp[k]);
+        __builtin_nontemporal_store(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, dp[k] + 1);
+      }
+  }
+}
+
+// Raw bits of one element, widened to 32 bits.
+__device__ __forceinline__ uint32_t load_bits(const char* p, int dt) {
+  if (dt == WB_F32) return *reinterpret_cast<const uint32_t*>(p);
+  if (dt == WB_BF16) return *reinterpret_cast<const uint16_t*>(p);
+  return *reinterpret_cast<const uint8_t*>(p);
+}
+
+__device__ __forceinline__ void store_converted(char* p, uint32_t bits, int sdt, int ddt) {
+  if (ddt == WB_F32) {
+    *reinterpret_cast<uint32_t*>(p) = sdt == WB_BF16 ? bits << 16 : bits;
+  } else if (ddt == WB_BF16) {
+    const uint32_t w = sdt == WB_F32 ? pack_bf16x2(__uint_as_float(bits), 0.0f) : bits;
+    *reinterpret_cast<uint16_t*>(p) = static_cast<uint16_t>(w);
+  } else {
+    *reinterpret_cast<uint8_t*>(p) = static_cast<uint8_t>(bits);
+  }
+}
+
+__device__ __forceinline__ int dt_bytes(int dt) { return dt == WB_F32 ? 4 : (dt == WB_BF16 ? 2 : 1); }
+
+// Element by element; strides in elements.
+__device__ void run_scalar(const Task& t, const char* src, char* dst) {
+  const int ss = dt_bytes(t.sdt), ds = dt_bytes(t.ddt);
+  const uint64_t total = uint64_t(t.rows) * t.cols;
+  Walker w(threadIdx.x, t.cols);
+  for (uint64_t q = threadIdx.x; q < total; q += kThreads) {
+    const uint32_t bits = load_bits(src + (uint64_t(w.r) * t.src_ld + w.c) * ss, t.sdt);
+    store_converted(dst + (uint64_t(w.r) * t.dst_ld + w.c) * ds, bits, t.sdt, t.ddt);
+    w.step();
+  }
+}
+
+// dst[c][r] = cvt(src[r][c]) for one tile of up to 64 x 64, through LDS.
+__device__ void run_transpose(const Task& t, const char* src, char* dst) {
+  __shared__ uint32_t tile[64][65];
+  const int ss = dt_bytes(t.sdt), ds = dt_bytes(t.ddt);
+  const uint32_t R = t.rows, C = t.cols;
+  for (uint32_t i = threadIdx.x; i < 64 * 64; i += kThreads) {
+    const uint32_t r = i >> 6, c = i & 63;
+    if (r < R && c < C) tile[r][c] = load_bits(src + (uint64_t(r) * t.src_ld + c) * ss, t.sdt);
+  }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < 64 * 64; i += kThreads) {
+    const uint32_t c = i >> 6, r = i & 63;
+    if (r < R && c < C) store_converted(dst + (uint64_t(c) * t.dst_ld + r) * ds, tile[r][c], t.sdt, t.ddt);
+  }
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
+                                                            const uint64_t* __restrict__ ptrs) {
+  const Task t = tasks[blockIdx.x];
+  const char* src = reinterpret_cast<const char*>(ptrs[t.src_idx]) + t.src_off;
+  char* dst = reinterpret_cast<char*>(ptrs[t.dst_idx]) + t.dst_off;
+  switch (t.kind) {
+    case TASK_COPY16: run_copy16(t, src, dst); break;
+    case TASK_F32_BF16: run_f32_bf16(t, src, dst); break;
+    case TASK_BF16_F32: run_bf16_f32(t, src, dst); break;
+    case TASK_SCALAR: run_scalar(t, src, dst); break;
+    case TASK_TRANSPOSE: run_transpose(t, src, dst); break;
+    default: break;
+  }
+}
+
+// ---- fp8 E4M3FN blocks ---------------------------------------------------
+
+namespace {
+
+__device__ __forceinline__ float load_f32(const char* p, int dt) {
+  return dt == WB_F32 ? *reinterpret_cast<const float*>(p) : __uint_as_float(uint32_t(*reinterpret_cast<const uint16_t*>(p)) << 16);
+}
+
+// Element (r, c) of the block from its pieces (the block is exactly covered).
+__device__ __forceinline__ float gather_one(const QPiece* __restrict__ pcs, int n, const char* recv, int r, int c) {
+  for (int i = 0; i < n; ++i) {
+    const QPiece p = pcs[i];
+    if (r >= p.r0 && r <= p.r1m1 && c >= p.c0 && c <= p.c1m1) {
+      const int es = p.sdt == WB_F32 ? 4 : 2;
+      return load_f32(recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (c - p.c0)) * es, p.sdt);
+    }
+  }
+  return 0.0f;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
+                                                             const QPiece* __restrict__ pieces,
+                                                             const uint64_t* __restrict__ ptrs) {
+  __shared__ float wave_max[kThreads / 64];
+  const QBlock b = blocks[blockIdx.x];
+  const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
+  const char* recv = reinterpret_cast<const char*>(ptrs[0]);
+  const QPiece* pcs = pieces + b.piece0;
+  const int n = b.npieces;
+  const int cg = (threadIdx.x & 15) * 8;  // first of this thread's 8 columns
+  const int rb = threadIdx.x >> 4;        // rows rb, rb + 16, ..., rb + 112
+  float v[8][8];
+  float amax = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int r = rb + 16 * k;
+#pragma unroll
+    for (int m = 0; m < 8; ++m) v[k][m] = 0.0f;
+    if (r >= rows || cg >= cols) continue;
+    // fast path: the 8 columns lie in one bf16 piece and the load is 16-byte aligned
+    int hit = -1;
+    for (int i = 0; i < n; ++i) {
+      const QPiece& p = pcs[i];
+      if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) { hit = i; break; }
+    }
+    bool done = false;
+    if (hit >= 0 && pcs[hit].sdt == WB_BF16) {
+      const QPiece& p = pcs[hit];
+      const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
+      if ((reinterpret_cast<uintptr_t>(a) & 15) == 0) {
+        const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a));
+        v[k][0] = bf16_lo(x.x); v[k][1] = bf16_hi(x.x); v[k][2] = bf16_lo(x.y); v[k][3] = bf16_hi(x.y);
+        v[k][4] = bf16_lo(x.z); v[k][5] = bf16_hi(x.z); v[k][6] = bf16_lo(x.w); v[k][7] = bf16_hi(x.w);
+        done = true;
+      }
+    }
+    if (!done) {
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+        if (cg + m < cols) v[k][m] = gather_one(pcs, n, recv, r, cg + m);
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) amax = fmaxf(amax, fabsf(v[k][m]));
+  }
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(wave_max[0], wave_max[1]), fmaxf(wave_max[2], wave_max[3]));
+
+  const float s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
+  // RN(x / s): with s = m * 2^E (m in [1, 2)) take x' = x * 2^-E and s' = m,
+  // r' = RN(1 / s'), q0 = RN(x' r'), e = x' - q0 s' (exact, by FMA),
+  // q = RN(q0 + e r'). For |q| >= 2^-10, the smallest magnitude that does not
+  // round to zero in E4M3, all of this stays in the normal range. A block
+  // whose scale is subnormal uses IEEE division per element.
+  const uint32_t sbits = __float_as_uint(s);
+  const int sexp = int((sbits >> 23) & 0xFF);
+  const bool fast = sexp != 0;
+  const float pw = __uint_as_float(uint32_t(254 - sexp) << 23);  // 2^-(sexp - 127)
+  const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);
+  const float rp = 1.0f / sp;
+  uint8_t* q8 = reinterpret_cast<uint8_t*>(ptrs[b.dst_idx]) + b.dst_off;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int r = rb + 16 * k;
+    if (r >= rows || cg >= cols) continue;
+    float q[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      float qq;
+      if (fast) {
+        const float xp = v[k][m] * pw;
+        const float q0 = xp * rp;
+        const float e = fmaf(-q0, sp, xp);
+        qq = fmaf(e, rp, q0);
+      } else {
+        qq = v[k][m] / s;
+      }
+      q[m] = __builtin_amdgcn_fmed3f(qq, -448.0f, 448.0f);
+    }
+    uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
+    uint32_t hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
+    uint8_t* dst = q8 + uint64_t(r) * b.dst_ld + cg;
+    if ((b.flags & QB_VEC_STORE) && cg + 8 <= cols) {
+      __builtin_nontemporal_store(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
+    } else {
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+        if (cg + m < cols) dst[m] = static_cast<uint8_t>((m < 4 ? lo : hi) >> (8 * (m & 3)));
+    }
+  }
+  if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
+}
+
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, void* stream) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(wb_tasks_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), tasks, ptrs);
+  return hipGetLastError();
+}
+
+int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, void* stream) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(wb_qblock_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), blocks, pieces,
+                     ptrs);
+  return hipGetLastError();
+}
+
+const char* hip_error_string(int err) { return hipGetErrorString(static_cast<hipError_t>(err)); }
+
+}  // namespace wb

@@ -1,0 +1,559 @@
+// Routing plan (WeightBridge Sec. 3.2, "Generating an efficient routing plan")
+// and the per-rank kernel work derived from it.
+//
+// Correspondence is the overlap of trainer and rollout source maps in the
+// checkpoint index space (Sec. 3.1). Identical trainer rectangles held by
+// several ranks are replicas: each region they serve is cut into distinct
+// slices, one per replica, so the trainers together send a single copy, and
+// slices go to the replica furthest below its even share (Sec. 3.2: no
+// redundant transfer, no single-source bottleneck). This file follows the
+// canonical rules stated in wb.h so that every rank derives the same plan.
+#include <algorithm>
+#include <cstdlib>
+#include <map>
+#include <numeric>
+#include <sstream>
+
+#include "wb_internal.hpp"
+
+namespace wb {
+namespace {
+
+constexpr int64_t kPayloadAlign = 256;
+constexpr int64_t kRegionAlign = 4096;
+
+int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+bool intersect(const Rect& a, const Rect& b, Rect& out) {
+  out.r0 = std::max(a.r0, b.r0);
+  out.r1 = std::min(a.r1, b.r1);
+  out.c0 = std::max(a.c0, b.c0);
+  out.c1 = std::min(a.c1, b.c1);
+  return out.r0 < out.r1 && out.c0 < out.c1;
+}
+
+Rect rect_of(const Placement& p) { return {p.r0, p.r1, p.c0, p.c1}; }
+
+struct Group {
+  Rect x;
+  std::vector<int> owners;  // ascending ranks
+  std::vector<int> pls;     // placement index of each owner
+  int set = -1;             // interned owner set
+  int esize = 0;
+};
+
+void validate_layout(const wb_layout_t& L, bool exact_cover, const char* side) {
+  for (size_t r = 0; r < L.ranks.size(); ++r) {
+    const Rank& R = L.ranks[r];
+    std::vector<int64_t> covered(R.locals.size(), 0);
+    for (const Placement& p : R.pls) {
+      check_placement(L, static_cast<int>(r), p);
+      covered[p.u] += p.numel();
+    }
+    if (!exact_cover) continue;
+    for (size_t u = 0; u < R.locals.size(); ++u) {
+      if (R.locals[u].scales >= 0) continue;
+      if (covered[u] != R.locals[u].numel())
+        fail(WB_EINVAL, std::string(side) + " rank " + std::to_string(r) + " tensor " + R.locals[u].name +
+                            " is not exactly covered by its placements");
+    }
+  }
+}
+
+// ---- task builders (copy/cast kernel work) ------------------------------
+
+struct TaskSink {
+  std::vector<Task>& out;
+  int64_t task_bytes;
+
+  void push(uint8_t kind, int sidx, uint64_t soff, uint32_t sld, int sdt, int didx, uint64_t doff, uint32_t dld,
+            int ddt, int64_t rows, int64_t cols) {
+    Task t{};
+    t.src_off = soff;
+    t.dst_off = doff;
+    t.rows = static_cast<uint32_t>(rows);
+    t.cols = static_cast<uint32_t>(cols);
+    t.src_ld = sld;
+    t.dst_ld = dld;
+    t.src_idx = static_cast<uint16_t>(sidx);
+    t.dst_idx = static_cast<uint16_t>(didx);
+    t.kind = kind;
+    t.sdt = static_cast<uint8_t>(sdt);
+    t.ddt = static_cast<uint8_t>(ddt);
+    out.push_back(t);
+  }
+
+  // Elements per vector of a vector kind and the kind itself, or false.
+  static bool vector_kind(int sdt, int ddt, uint8_t& kind, int64_t& v) {
+    if (sdt == ddt) { kind = TASK_COPY16; v = 16 / dtype_bytes(sdt); return true; }
+    if (sdt == WB_F32 && ddt == WB_BF16) { kind = TASK_F32_BF16; v = 8; return true; }
+    if (sdt == WB_BF16 && ddt == WB_F32) { kind = TASK_BF16_F32; v = 8; return true; }
+    return false;
+  }
+
+  // One vector-kind task; COPY16 tasks are expressed in bytes.
+  void push_vec(uint8_t kind, int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld,
+                int ddt, int64_t rows, int64_t cols) {
+    if (kind == TASK_COPY16) {
+      const int es = dtype_bytes(sdt);
+      push(kind, sidx, soff, static_cast<uint32_t>(sld * es), sdt, didx, doff, static_cast<uint32_t>(dld * es), ddt,
+           rows, cols * es);
+    } else {
+      push(kind, sidx, soff, static_cast<uint32_t>(sld), sdt, didx, doff, static_cast<uint32_t>(dld), ddt, rows, cols);
+    }
+  }
+
+  // rows x cols elements; src/dst row strides in elements; offsets in bytes.
+  void copy_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
+                 int64_t rows, int64_t cols) {
+    const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
+    const int64_t per_task = std::max<int64_t>(16, task_bytes / std::max(ss, ds));
+    uint8_t kind;
+    int64_t v;
+    const bool vk = vector_kind(sdt, ddt, kind, v);
+    if (rows == 1 || (cols == sld && cols == dld)) {
+      // contiguous on both sides: one linear run
+      const int64_t n = rows * cols;
+      int64_t head = -1;
+      if (vk)
+        for (int64_t e = 0; e < v && e < n; ++e)
+          if ((soff + e * ss) % 16 == 0 && (doff + e * ds) % 16 == 0) { head = e; break; }
+      if (head < 0) {
+        for (int64_t a = 0; a < n; a += per_task)
+          push(TASK_SCALAR, sidx, soff + a * ss, 0, sdt, didx, doff + a * ds, 0, ddt, 1, std::min(per_task, n - a));
+        return;
+      }
+      if (head > 0) push(TASK_SCALAR, sidx, soff, 0, sdt, didx, doff, 0, ddt, 1, head);
+      const int64_t body = (n - head) / v * v;
+      const int64_t chunk = std::max<int64_t>(v, per_task / v * v);
+      for (int64_t a = 0; a < body; a += chunk) {
+        const int64_t len = std::min(chunk, body - a);
+        push_vec(kind, sidx, soff + (head + a) * ss, len, sdt, didx, doff + (head + a) * ds, len, ddt, 1, len);
+      }
+      const int64_t tail = n - head - body;
+      if (tail > 0)
+        push(TASK_SCALAR, sidx, soff + (head + body) * ss, 0, sdt, didx, doff + (head + body) * ds, 0, ddt, 1, tail);
+      return;
+    }
+    const bool vec = vk && soff % 16 == 0 && doff % 16 == 0 && cols % v == 0 && (sld * ss) % 16 == 0 &&
+                     (dld * ds) % 16 == 0;
+    const int64_t unit = vec ? v : 1;
+    const int64_t col_chunk = cols <= per_task ? cols : std::max(unit, per_task / unit * unit);
+    const int64_t rows_per = std::max<int64_t>(1, per_task / col_chunk);
+    for (int64_t r = 0; r < rows; r += rows_per) {
+      const int64_t nr = std::min(rows_per, rows - r);
+      for (int64_t c = 0; c < cols; c += col_chunk) {
+        const int64_t nc = std::min(col_chunk, cols - c);
+        const uint64_t so = soff + (r * sld + c) * ss, dof = doff + (r * dld + c) * ds;
+        if (vec)
+          push_vec(kind, sidx, so, sld, sdt, didx, dof, dld, ddt, nr, nc);
+        else
+          push(TASK_SCALAR, sidx, so, static_cast<uint32_t>(sld), sdt, didx, dof, static_cast<uint32_t>(dld), ddt, nr,
+               nc);
+      }
+    }
+  }
+
+  // dst[c][r] = src[r][c] for an R x C source block, in 64 x 64 tiles.
+  void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
+                      int64_t R, int64_t C) {
+    const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
+    for (int64_t r = 0; r < R; r += 64)
+      for (int64_t c = 0; c < C; c += 64)
+        push(TASK_TRANSPOSE, sidx, soff + (r * sld + c) * ss, static_cast<uint32_t>(sld), sdt, didx,
+             doff + (c * dld + r) * ds, static_cast<uint32_t>(dld), ddt, std::min<int64_t>(64, R - r),
+             std::min<int64_t>(64, C - c));
+  }
+};
+
+bool cast_supported(int sdt, int ddt) {
+  if (sdt != WB_F32 && sdt != WB_BF16) return false;
+  return ddt == WB_F32 || ddt == WB_BF16 || ddt == WB_F8E4M3;
+}
+
+int64_t env_task_bytes() {
+  const char* s = std::getenv("WB_TASK_BYTES");
+  const int64_t v = s ? std::atoll(s) : 0;
+  return v >= 1024 ? v : (int64_t(1) << 18);
+}
+
+void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_plan_t& P) {
+  TaskSink sink{P.tasks, env_task_bytes()};
+  if (P.role == WB_SENDER) {
+    const Rank& R = trainer.ranks[P.rank];
+    P.n_locals = static_cast<int>(R.locals.size());
+    for (const Segment& g : P.segs) {
+      if (g.s != P.rank) continue;
+      const Placement& sp = R.pls[g.src_pl];
+      const int dt = R.locals[sp.u].dtype, es = dtype_bytes(dt);
+      const int64_t C = g.x.cols(), Rr = g.x.rows();
+      P.read_bytes += g.bytes;
+      P.write_bytes += g.bytes;
+      if (!sp.tr) {
+        const int64_t start = sp.base + (g.x.r0 - sp.r0) * sp.ld + (g.x.c0 - sp.c0);
+        sink.copy_rect(1 + sp.u, uint64_t(start) * es, sp.ld, dt, 0, g.send_off, C, dt, Rr, C);
+      } else {
+        // local holds the transpose: rows are checkpoint columns
+        const int64_t start = sp.base + (g.x.c0 - sp.c0) * sp.ld + (g.x.r0 - sp.r0);
+        sink.transpose_rect(1 + sp.u, uint64_t(start) * es, sp.ld, dt, 0, g.send_off, C, dt, C, Rr);
+      }
+    }
+    return;
+  }
+  const Rank& R = rollout.ranks[P.rank];
+  P.n_locals = static_cast<int>(R.locals.size());
+  // fp8 block bookkeeping: first block id of every quantised local
+  std::vector<int64_t> block_base(R.locals.size(), -1);
+  int64_t nblocks = 0;
+  for (size_t u = 0; u < R.locals.size(); ++u) {
+    const Local& l = R.locals[u];
+    if (l.block <= 0) continue;
+    block_base[u] = nblocks;
+    nblocks += l.batch * ((l.rows + l.block - 1) / l.block) * ((l.cols + l.block - 1) / l.block);
+    P.write_bytes += R.locals[l.scale].numel() * 4;
+  }
+  struct Span {
+    const Segment* g;
+    int64_t e, row0, col0;
+  };
+  std::vector<Span> qspans;
+  for (const Segment& g : P.segs) {
+    if (g.d != P.rank) continue;
+    const Placement& q = R.pls[g.dst_pl];
+    const Local& dl = R.locals[q.u];
+    const Rank& S = trainer.ranks[g.s];
+    const int sdt = S.locals[S.pls[g.src_pl].u].dtype;
+    if (!cast_supported(sdt, dl.dtype))
+      fail(WB_EUNSUPPORTED, std::string("unsupported cast ") + dtype_name(sdt) + " -> " + dtype_name(dl.dtype));
+    const int64_t C = g.x.cols(), Rr = g.x.rows();
+    P.read_bytes += g.bytes;
+    if (dl.block > 0) {
+      P.write_bytes += g.x.numel();
+      if (q.tr) fail(WB_EUNSUPPORTED, "fp8 destinations cannot be transposed");
+      const int64_t f0 = q.base + (g.x.r0 - q.r0) * q.ld + (g.x.c0 - q.c0);
+      const int64_t mat = dl.rows * dl.cols;
+      const int64_t e = f0 / mat, row0 = (f0 % mat) / dl.cols, col0 = f0 % dl.cols;
+      if (col0 + C > dl.cols || row0 + Rr > dl.rows || (Rr > 1 && q.ld != dl.cols))
+        fail(WB_EUNSUPPORTED, "an fp8 placement must be a sub-rectangle of one matrix of its tensor");
+      qspans.push_back({&g, e, row0, col0});
+      continue;
+    }
+    const int ddt = dl.dtype, ds = dtype_bytes(ddt);
+    P.write_bytes += g.x.numel() * ds;
+    if (!q.tr) {
+      const int64_t start = q.base + (g.x.r0 - q.r0) * q.ld + (g.x.c0 - q.c0);
+      sink.copy_rect(0, g.recv_off, C, sdt, 1 + q.u, uint64_t(start) * ds, q.ld, ddt, Rr, C);
+    } else {
+      const int64_t start = q.base + (g.x.c0 - q.c0) * q.ld + (g.x.r0 - q.r0);
+      sink.transpose_rect(0, g.recv_off, C, sdt, 1 + q.u, uint64_t(start) * ds, q.ld, ddt, Rr, C);
+    }
+  }
+  if (nblocks == 0) return;
+  // pieces: count per block, prefix, fill (canonical segment order within a block)
+  std::vector<uint32_t> count(nblocks + 1, 0);
+  auto for_blocks = [&](const Span& sp, auto&& fn) {
+    const Placement& q = R.pls[sp.g->dst_pl];
+    const Local& dl = R.locals[q.u];
+    const int64_t B = dl.block, nbr = (dl.rows + B - 1) / B, nbc = (dl.cols + B - 1) / B;
+    const int64_t Rr = sp.g->x.rows(), C = sp.g->x.cols();
+    for (int64_t bi = sp.row0 / B; bi <= (sp.row0 + Rr - 1) / B; ++bi)
+      for (int64_t bj = sp.col0 / B; bj <= (sp.col0 + C - 1) / B; ++bj)
+        fn(block_base[q.u] + (sp.e * nbr + bi) * nbc + bj, bi, bj, B);
+  };
+  for (const Span& sp : qspans) for_blocks(sp, [&](int64_t id, int64_t, int64_t, int64_t) { ++count[id + 1]; });
+  for (int64_t i = 0; i < nblocks; ++i) count[i + 1] += count[i];
+  P.qpieces.resize(count[nblocks]);
+  std::vector<uint32_t> fill(count.begin(), count.end() - 1);
+  std::vector<int64_t> area(nblocks, 0);
+  for (const Span& sp : qspans) {
+    const Segment& g = *sp.g;
+    const Rank& S = trainer.ranks[g.s];
+    const int sdt = S.locals[S.pls[g.src_pl].u].dtype, ss = dtype_bytes(sdt);
+    const int64_t Rr = g.x.rows(), C = g.x.cols();
+    for_blocks(sp, [&](int64_t id, int64_t bi, int64_t bj, int64_t B) {
+      const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
+      const int64_t b0 = std::max(sp.col0, bj * B), b1 = std::min(sp.col0 + C, (bj + 1) * B);
+      QPiece pc{};
+      pc.src_off = g.recv_off + uint64_t(((a0 - sp.row0) * C + (b0 - sp.col0)) * ss);
+      pc.src_ld = static_cast<uint32_t>(C);
+      pc.r0 = static_cast<uint8_t>(a0 - bi * B);
+      pc.r1m1 = static_cast<uint8_t>(a1 - bi * B - 1);
+      pc.c0 = static_cast<uint8_t>(b0 - bj * B);
+      pc.c1m1 = static_cast<uint8_t>(b1 - bj * B - 1);
+      pc.sdt = static_cast<uint8_t>(sdt);
+      P.qpieces[fill[id]++] = pc;
+      area[id] += (a1 - a0) * (b1 - b0);
+    });
+  }
+  P.qblocks.resize(nblocks);
+  for (size_t u = 0; u < R.locals.size(); ++u) {
+    const Local& l = R.locals[u];
+    if (l.block <= 0) continue;
+    const int64_t B = l.block, nbr = (l.rows + B - 1) / B, nbc = (l.cols + B - 1) / B;
+    for (int64_t e = 0; e < l.batch; ++e)
+      for (int64_t bi = 0; bi < nbr; ++bi)
+        for (int64_t bj = 0; bj < nbc; ++bj) {
+          const int64_t id = block_base[u] + (e * nbr + bi) * nbc + bj;
+          const int64_t rows = std::min(B, l.rows - bi * B), cols = std::min(B, l.cols - bj * B);
+          if (area[id] != rows * cols) fail(WB_EINVAL, "fp8 block of " + l.name + " is not exactly covered");
+          if (count[id + 1] - count[id] > 65535) fail(WB_EUNSUPPORTED, "too many pieces in one fp8 block");
+          QBlock b{};
+          b.dst_off = uint64_t((e * l.rows + bi * B) * l.cols + bj * B);
+          b.piece0 = count[id];
+          b.npieces = static_cast<uint16_t>(count[id + 1] - count[id]);
+          b.dst_ld = static_cast<uint32_t>(l.cols);
+          b.scale_off = static_cast<uint32_t>((e * nbr + bi) * nbc + bj);
+          b.dst_idx = static_cast<uint16_t>(1 + u);
+          b.scale_idx = static_cast<uint16_t>(1 + l.scale);
+          b.rows_m1 = static_cast<uint8_t>(rows - 1);
+          b.cols_m1 = static_cast<uint8_t>(cols - 1);
+          b.flags = (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) ? QB_VEC_STORE : 0;
+          P.qblocks[id] = b;
+        }
+  }
+}
+
+// Every byte a work item touches lies inside its buffer, and vector work items
+// meet the alignment their loads and stores assume (base pointers are 16-byte
+// aligned, which wb_pack / wb_unpack check). Run on every plan.
+void check_work(const wb_plan_t& P, const Rank& R) {
+  std::vector<int64_t> size(R.locals.size() + 1);
+  size[0] = P.role == WB_SENDER ? P.send_bytes[P.rank] : P.recv_bytes[P.rank];
+  for (size_t u = 0; u < R.locals.size(); ++u) size[u + 1] = R.locals[u].numel() * dtype_bytes(R.locals[u].dtype);
+  auto inside = [&](int idx, uint64_t off, uint64_t len, const char* what) {
+    if (idx < 0 || idx >= static_cast<int>(size.size()) || len == 0 || off + len > uint64_t(size[idx]))
+      fail(WB_EINVAL, std::string("internal: ") + what + " work item out of bounds");
+  };
+  for (const Task& t : P.tasks) {
+    if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
+    const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
+    switch (t.kind) {
+      case TASK_COPY16:
+        if (t.src_off % 16 || t.dst_off % 16 || t.cols % 16 || (t.rows > 1 && (t.src_ld % 16 || t.dst_ld % 16)))
+          fail(WB_EINVAL, "internal: misaligned copy work item");
+        inside(t.src_idx, t.src_off, uint64_t(t.rows - 1) * t.src_ld + t.cols, "copy source");
+        inside(t.dst_idx, t.dst_off, uint64_t(t.rows - 1) * t.dst_ld + t.cols, "copy destination");
+        break;
+      case TASK_F32_BF16:
+      case TASK_BF16_F32:
+        if (t.src_off % 16 || t.dst_off % 16 || t.cols % 8 ||
+            (t.rows > 1 && ((t.src_ld * ss) % 16 || (t.dst_ld * ds) % 16)))
+          fail(WB_EINVAL, "internal: misaligned cast work item");
+        [[fallthrough]];
+      case TASK_SCALAR:
+        inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "source");
+        inside(t.dst_idx, t.dst_off, (uint64_t(t.rows - 1) * t.dst_ld + t.cols) * ds, "destination");
+        break;
+      case TASK_TRANSPOSE:
+        if (t.rows > 64 || t.cols > 64) fail(WB_EINVAL, "internal: transpose tile above 64 x 64");
+        inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
+        inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
+        break;
+      default:
+        fail(WB_EINVAL, "internal: unknown work item");
+    }
+  }
+  for (const QBlock& b : P.qblocks) {
+    const uint64_t rows = b.rows_m1 + 1u, cols = b.cols_m1 + 1u;
+    inside(b.dst_idx, b.dst_off, (rows - 1) * b.dst_ld + cols, "fp8 block");
+    inside(b.scale_idx, uint64_t(b.scale_off) * 4, 4, "fp8 scale");
+    if (R.locals[b.dst_idx - 1].dtype != WB_F8E4M3 || R.locals[b.scale_idx - 1].dtype != WB_F32)
+      fail(WB_EINVAL, "internal: fp8 block targets the wrong tensors");
+    if ((b.flags & QB_VEC_STORE) && (b.dst_off % 8 || b.dst_ld % 8)) fail(WB_EINVAL, "internal: misaligned fp8 store");
+    if (uint64_t(b.piece0) + b.npieces > P.qpieces.size() || b.npieces == 0)
+      fail(WB_EINVAL, "internal: fp8 block pieces out of range");
+    for (uint32_t i = b.piece0; i < b.piece0 + b.npieces; ++i) {
+      const QPiece& q = P.qpieces[i];
+      if (q.r1m1 < q.r0 || q.c1m1 < q.c0 || q.r1m1 >= rows || q.c1m1 >= cols)
+        fail(WB_EINVAL, "internal: fp8 piece outside its block");
+      const uint64_t es = dtype_bytes(q.sdt);
+      inside(0, q.src_off, (uint64_t(q.r1m1 - q.r0) * q.src_ld + (q.c1m1 - q.c0) + 1) * es, "fp8 piece");
+    }
+  }
+}
+
+}  // namespace
+
+void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, wb_plan_t& P) {
+  if (role != WB_SENDER && role != WB_RECEIVER) fail(WB_EINVAL, "role must be WB_SENDER or WB_RECEIVER");
+  const int ns = static_cast<int>(trainer.ranks.size()), nd = static_cast<int>(rollout.ranks.size());
+  if (ns < 1 || nd < 1) fail(WB_EINVAL, "layouts need at least one rank");
+  if (rank < 0 || rank >= (role == WB_SENDER ? ns : nd)) fail(WB_EINVAL, "rank out of range");
+  if (trainer.catalog.size() != rollout.catalog.size()) fail(WB_EINVAL, "trainer and rollout catalogs differ");
+  for (size_t t = 0; t < trainer.catalog.size(); ++t) {
+    const Tensor &a = trainer.catalog[t], &b = rollout.catalog[t];
+    if (a.name != b.name || a.rows != b.rows || a.cols != b.cols) fail(WB_EINVAL, "trainer and rollout catalogs differ");
+  }
+  validate_layout(trainer, false, "trainer");
+  validate_layout(rollout, true, "rollout");
+  for (const Rank& R : rollout.ranks)
+    for (const Local& l : R.locals)
+      if (l.block > 128) fail(WB_EUNSUPPORTED, "quant_block above 128");
+
+  // 1. trainer groups, ordered by (t, r0, c0, r1, c1), owners ascending
+  struct Entry {
+    int t;
+    Rect x;
+    int s, pl;
+  };
+  std::vector<Entry> entries;
+  for (int s = 0; s < ns; ++s)
+    for (size_t i = 0; i < trainer.ranks[s].pls.size(); ++i) {
+      const Placement& p = trainer.ranks[s].pls[i];
+      entries.push_back({p.t, rect_of(p), s, static_cast<int>(i)});
+    }
+  std::sort(entries.begin(), entries.end(), [](const Entry& a, const Entry& b) {
+    if (a.t != b.t) return a.t < b.t;
+    if (a.x.r0 != b.x.r0) return a.x.r0 < b.x.r0;
+    if (a.x.c0 != b.x.c0) return a.x.c0 < b.x.c0;
+    if (a.x.r1 != b.x.r1) return a.x.r1 < b.x.r1;
+    if (a.x.c1 != b.x.c1) return a.x.c1 < b.x.c1;
+    return a.s < b.s;
+  });
+  std::vector<std::vector<Group>> groups(trainer.catalog.size());
+  std::map<std::vector<int>, int> set_ids;
+  for (size_t i = 0; i < entries.size();) {
+    size_t j = i;
+    Group g;
+    g.x = entries[i].x;
+    while (j < entries.size() && entries[j].t == entries[i].t && entries[j].x.r0 == g.x.r0 &&
+           entries[j].x.r1 == g.x.r1 && entries[j].x.c0 == g.x.c0 && entries[j].x.c1 == g.x.c1) {
+      if (!g.owners.empty() && g.owners.back() == entries[j].s)
+        fail(WB_EINVAL, "a trainer rank holds the same rectangle twice");
+      g.owners.push_back(entries[j].s);
+      g.pls.push_back(entries[j].pl);
+      ++j;
+    }
+    int es = 0;
+    for (size_t k = 0; k < g.owners.size(); ++k) {
+      const Rank& S = trainer.ranks[g.owners[k]];
+      const int e = dtype_bytes(S.locals[S.pls[g.pls[k]].u].dtype);
+      if (es && e != es) fail(WB_EUNSUPPORTED, "replicas of one rectangle hold different dtypes");
+      es = e;
+    }
+    g.esize = es;
+    auto it = set_ids.emplace(g.owners, static_cast<int>(set_ids.size())).first;
+    g.set = it->second;
+    groups[entries[i].t].push_back(std::move(g));
+    i = j;
+  }
+  for (auto& gl : groups)
+    for (size_t a = 0; a < gl.size(); ++a)
+      for (size_t b = a + 1; b < gl.size(); ++b) {
+        Rect tmp;
+        if (intersect(gl[a].x, gl[b].x, tmp))
+          fail(WB_EUNSUPPORTED, "overlapping, non-identical trainer rectangles");
+      }
+
+  // 2./3. regions and segments in canonical order, deficit assignment per owner set
+  std::vector<std::vector<int64_t>> deficit(set_ids.size());
+  for (const auto& kv : set_ids) deficit[kv.second].assign(kv.first.size(), 0);
+  P.segs.clear();
+  std::vector<Rect> parts;
+  std::vector<int> order, who;
+  for (int d = 0; d < nd; ++d) {
+    const Rank& R = rollout.ranks[d];
+    for (size_t qi = 0; qi < R.pls.size(); ++qi) {
+      const Placement& q = R.pls[qi];
+      int64_t covered = 0;
+      for (const Group& g : groups[q.t]) {
+        Rect x;
+        if (!intersect(rect_of(q), g.x, x)) continue;
+        covered += x.numel();
+        const int k = static_cast<int>(g.owners.size());
+        if (k == 1) {
+          P.segs.push_back({g.owners[0], d, q.t, x, g.pls[0], static_cast<int>(qi), x.numel() * g.esize});
+          continue;
+        }
+        const bool by_rows = x.rows() >= k;
+        const int64_t n = by_rows ? x.rows() : x.cols();
+        parts.clear();
+        for (int j = 0; j < k; ++j) {
+          const int64_t a = j * n / k, b = (j + 1) * n / k;
+          if (a == b) continue;
+          parts.push_back(by_rows ? Rect{x.r0 + a, x.r0 + b, x.c0, x.c1} : Rect{x.r0, x.r1, x.c0 + a, x.c0 + b});
+        }
+        std::vector<int64_t>& E = deficit[g.set];
+        for (int64_t& e : E) e -= x.numel() * g.esize;
+        order.resize(parts.size());
+        std::iota(order.begin(), order.end(), 0);
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int a, int b) { return parts[a].numel() > parts[b].numel(); });
+        who.assign(parts.size(), -1);
+        for (int j : order) {
+          int best = 0;
+          for (int o = 1; o < k; ++o)
+            if (E[o] < E[best]) best = o;  // owners ascending, so ties keep the lower rank
+          E[best] += int64_t(k) * parts[j].numel() * g.esize;
+          who[j] = best;
+        }
+        for (size_t j = 0; j < parts.size(); ++j)
+          P.segs.push_back({g.owners[who[j]], d, q.t, parts[j], g.pls[who[j]], static_cast<int>(qi),
+                            parts[j].numel() * g.esize});
+      }
+      if (covered != q.numel())
+        fail(WB_EINVAL, "rollout rank " + std::to_string(d) + " needs elements no trainer holds");
+    }
+  }
+
+  // 4. wire offsets
+  P.n_send = ns;
+  P.n_recv = nd;
+  std::vector<int64_t> end(size_t(ns) * nd, -1);
+  for (Segment& g : P.segs) {
+    int64_t& e = end[size_t(g.s) * nd + g.d];
+    const int64_t off = e < 0 ? 0 : align_up(e, kPayloadAlign);
+    g.send_off = g.recv_off = off;
+    e = off + g.bytes;
+  }
+  P.region_bytes.assign(size_t(ns) * nd, 0);
+  P.send_region.assign(size_t(ns) * nd, -1);
+  P.recv_region.assign(size_t(ns) * nd, -1);
+  P.send_bytes.assign(ns, 0);
+  P.recv_bytes.assign(nd, 0);
+  for (int s = 0; s < ns; ++s) {
+    int64_t pos = 0;
+    for (int d = 0; d < nd; ++d) {
+      const int64_t b = end[size_t(s) * nd + d];
+      if (b < 0) continue;
+      pos = align_up(pos, kRegionAlign);
+      P.send_region[size_t(s) * nd + d] = pos;
+      P.region_bytes[size_t(s) * nd + d] = b;
+      pos += b;
+    }
+    P.send_bytes[s] = pos;
+  }
+  for (int d = 0; d < nd; ++d) {
+    int64_t pos = 0;
+    for (int s = 0; s < ns; ++s) {
+      const int64_t b = end[size_t(s) * nd + d];
+      if (b < 0) continue;
+      pos = align_up(pos, kRegionAlign);
+      P.recv_region[size_t(s) * nd + d] = pos;
+      pos += b;
+    }
+    P.recv_bytes[d] = pos;
+  }
+  for (Segment& g : P.segs) {
+    g.send_off += P.send_region[size_t(g.s) * nd + g.d];
+    g.recv_off += P.recv_region[size_t(g.s) * nd + g.d];
+  }
+
+  P.role = role;
+  P.rank = rank;
+  build_rank_view(trainer, rollout, P);
+  check_work(P, role == WB_SENDER ? trainer.ranks[rank] : rollout.ranks[rank]);
+}
+
+std::string dump_plan(const wb_plan_t& P) {
+  std::ostringstream o;
+  o << "plan trainer_ranks=" << P.n_send << " rollout_ranks=" << P.n_recv << " segments=" << P.segs.size() << "\n";
+  for (int s = 0; s < P.n_send; ++s) o << "send " << s << " " << P.send_bytes[s] << "\n";
+  for (int d = 0; d < P.n_recv; ++d) o << "recv " << d << " " << P.recv_bytes[d] << "\n";
+  for (const Segment& g : P.segs)
+    o << "seg " << g.s << " " << g.d << " " << g.t << " " << g.x.r0 << " " << g.x.r1 << " " << g.x.c0 << " " << g.x.c1
+      << " " << g.src_pl << " " << g.dst_pl << " " << g.send_off << " " << g.recv_off << " " << g.bytes << "\n";
+  return o.str();
+}
+
+}  // namespace wb

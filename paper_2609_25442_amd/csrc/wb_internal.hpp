@@ -1,0 +1,178 @@
+// Internal types of libwb: layouts, the global plan, one rank's kernel work.
+#pragma once
+
+#include <cstdint>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "../../include/wb.h"
+
+namespace wb {
+
+// Error carried from deep inside the planner to the C ABI boundary.
+struct Error : std::runtime_error {
+  int code;
+  Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+[[noreturn]] inline void fail(int code, const std::string& msg) { throw Error(code, msg); }
+
+inline int dtype_bytes(int dt) {
+  switch (dt) {
+    case WB_F32: return 4;
+    case WB_BF16: return 2;
+    case WB_F8E4M3: return 1;
+    default: return 0;
+  }
+}
+inline const char* dtype_name(int dt) {
+  switch (dt) {
+    case WB_F32: return "f32";
+    case WB_BF16: return "bf16";
+    case WB_F8E4M3: return "f8e4m3";
+    default: return "?";
+  }
+}
+
+struct Tensor {
+  std::string name;
+  int64_t rows = 0, cols = 0;
+  int64_t numel() const { return rows * cols; }
+};
+
+struct Local {
+  std::string name;
+  int dtype = WB_F32;
+  int64_t batch = 1, rows = 1, cols = 1;
+  int block = 0;    // quantisation block edge; 0 when not quantised
+  int scale = -1;   // companion scale tensor of a quantised tensor
+  int scales = -1;  // for a scale tensor: the tensor it serves
+  int64_t numel() const { return batch * rows * cols; }
+};
+
+struct Placement {
+  int t = 0, u = 0;
+  int64_t r0 = 0, r1 = 0, c0 = 0, c1 = 0, base = 0, ld = 0;
+  int tr = 0;
+  int64_t rows() const { return r1 - r0; }
+  int64_t cols() const { return c1 - c0; }
+  int64_t numel() const { return rows() * cols(); }
+};
+
+struct Rank {
+  std::vector<Local> locals;
+  std::vector<Placement> pls;
+};
+
+}  // namespace wb
+
+struct wb_layout_t {
+  std::vector<wb::Tensor> catalog;
+  std::vector<wb::Rank> ranks;
+};
+
+namespace wb {
+
+struct Rect {
+  int64_t r0, r1, c0, c1;
+  int64_t rows() const { return r1 - r0; }
+  int64_t cols() const { return c1 - c0; }
+  int64_t numel() const { return rows() * cols(); }
+};
+
+// One piece of the routing plan: a rectangle of checkpoint tensor t that
+// sender s ships to receiver d.
+struct Segment {
+  int s, d, t;
+  Rect x;
+  int src_pl, dst_pl;
+  int64_t bytes;
+  int64_t send_off = 0, recv_off = 0;
+};
+
+// Work item of the copy/cast kernel: a rows x cols block of elements.
+// Offsets are bytes from pointer-table entries; strides are in elements.
+enum TaskKind : uint8_t {
+  TASK_COPY16 = 0,     // byte copy, 16-byte vectors (cols, lds and offsets in bytes)
+  TASK_F32_BF16 = 1,   // fp32 -> bf16, 8 elements per vector
+  TASK_BF16_F32 = 2,   // bf16 -> fp32, 8 elements per vector
+  TASK_SCALAR = 3,     // any supported pair, element by element
+  TASK_TRANSPOSE = 4,  // dst[c][r] = cvt(src[r][c]), one LDS tile of up to 64 x 64
+};
+
+struct Task {
+  uint64_t src_off, dst_off;
+  uint32_t rows, cols;
+  uint32_t src_ld, dst_ld;
+  uint16_t src_idx, dst_idx;
+  uint8_t kind, sdt, ddt, pad0;
+  uint32_t pad1;
+  uint32_t pad2;
+};
+static_assert(sizeof(Task) == 48, "Task layout");
+
+// One fp8 destination block and the wire pieces that fill it.
+struct QBlock {
+  uint64_t dst_off;     // bytes from the fp8 tensor to the block origin
+  uint32_t piece0;      // first piece
+  uint32_t dst_ld;      // row stride of the fp8 matrix (elements = bytes)
+  uint32_t scale_off;   // element index of the block's scale
+  uint16_t npieces, dst_idx, scale_idx;
+  uint8_t rows_m1, cols_m1;  // block extent minus one (blocks are at most 128 x 128)
+  uint8_t flags, pad0;
+  uint16_t pad1;
+  uint32_t pad2;
+};
+static_assert(sizeof(QBlock) == 40, "QBlock layout");
+
+struct QPiece {
+  uint64_t src_off;     // bytes from recv_buf to the piece's first element
+  uint32_t src_ld;      // wire row length in elements
+  uint8_t r0, r1m1, c0, c1m1;  // block-local rectangle [r0, r1m1] x [c0, c1m1]
+  uint8_t sdt, pad0;
+  uint16_t pad1;
+  uint32_t pad2;
+};
+static_assert(sizeof(QPiece) == 24, "QPiece layout");
+
+enum QBlockFlags : uint8_t { QB_VEC_STORE = 1 };
+
+}  // namespace wb
+
+struct wb_plan_t {
+  // global plan
+  int n_send = 0, n_recv = 0;
+  std::vector<wb::Segment> segs;
+  std::vector<int64_t> send_bytes, recv_bytes;
+  std::vector<int64_t> send_region, recv_region, region_bytes;  // [s * n_recv + d]
+  // view of one rank
+  int role = WB_SENDER, rank = 0;
+  int n_locals = 0;
+  int64_t read_bytes = 0, write_bytes = 0;
+  std::vector<wb::Task> tasks;
+  std::vector<wb::QBlock> qblocks;
+  std::vector<wb::QPiece> qpieces;
+  // copies of the two layouts used for dumps and queries
+  wb_layout_t trainer, rollout;
+  // device state after wb_plan_upload
+  uint8_t* ws = nullptr;
+  size_t ws_bytes = 0;
+  size_t off_ptrs = 0, off_tasks = 0, off_qblocks = 0, off_qpieces = 0;
+  void* ptr_stage = nullptr;     // pinned host staging of the pointer table
+  void* ptr_event = nullptr;     // hipEvent_t of the last staging copy
+  std::vector<uint64_t> last_ptrs;
+};
+
+namespace wb {
+// layout.cpp
+void describe(const wb_model_shapes& m, const wb_parallelism& p, wb_layout_t& out);
+void check_placement(const wb_layout_t& L, int rank, const Placement& p);
+std::string dump_layout(const wb_layout_t& L);
+// plan.cpp
+void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, wb_plan_t& out);
+std::string dump_plan(const wb_plan_t& P);
+// kernels.hip
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, void* stream);
+int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, void* stream);
+const char* hip_error_string(int err);
+}  // namespace wb

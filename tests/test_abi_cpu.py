@@ -1,0 +1,150 @@
+"""The C ABI without a GPU: the library loads, exports every declared call, and
+its host planner (layouts, plan, wire offsets) equals the oracle's, line for
+line, on every workload at scaled and full size, on random tiny layouts and on
+the hand-derived golden plan. Error paths return error codes."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_25442_amd as wb
+from oracle.layout import describe_layout, layout_from_spec
+from oracle.plan import build_plan, dump, dump_layout
+from synthetic_checkpoint.workloads import ORDER, WORKLOADS, scaled
+
+from oracle_cases import hand_replicated_pair, random_model, random_par
+from wb_cases import to_wb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_call():
+    names = set()
+    for h in os.listdir(os.path.join(ROOT, "include")):
+        if h.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", h)).read()
+            names |= set(re.findall(r"^\s*(?:int|void|const char\*)\s+(wb_\w+)\s*\(", text, re.M))
+    assert len(names) >= 30
+    for n in sorted(names):
+        assert hasattr(wb.lib, n), n
+
+
+def test_version():
+    assert "gfx950" in wb.version()
+
+
+@pytest.mark.parametrize("full", [False, True], ids=["scaled", "full"])
+@pytest.mark.parametrize("name", ORDER)
+def test_layouts_and_plans_equal_oracle(name, full):
+    w = WORKLOADS[name] if full else scaled(name)
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    assert tr.dump() == dump_layout(otr)
+    assert ro.dump() == dump_layout(oro)
+    want = dump(build_plan(otr, oro))
+    for role, rank in ((wb.SENDER, w["pack_rank"]), (wb.RECEIVER, w["unpack_rank"])):
+        assert wb.Plan(tr, ro, role, rank).dump() == want
+
+
+def test_generic_builder_hand_plan():
+    tr, ro = hand_replicated_pair()
+    golden = "".join(l for l in open(os.path.join(ROOT, "tests", "golden", "hand_plan_replicated.txt"))
+                     if not l.startswith("#"))
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 1)
+    assert p.dump() == golden
+    assert p.buffer_bytes == 8200
+    assert p.peers() == [(0, 0, 260), (1, 4096, 264), (2, 8192, 8)]
+    assert p.region(2, 1) == (4096, 8192, 8)
+    s = wb.Plan(to_wb(tr), to_wb(ro), wb.SENDER, 0)
+    assert s.buffer_bytes == 4356 and s.peers() == [(0, 0, 272), (1, 4096, 260)]
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_tiny_plans_equal_oracle(seed):
+    rng = np.random.default_rng(seed)
+    m = random_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout"))
+    want = dump(build_plan(otr, oro))
+    tr, ro = to_wb(otr), to_wb(oro)
+    assert tr.dump() == dump_layout(otr) and ro.dump() == dump_layout(oro)
+    for d in range(oro.nranks):
+        assert wb.Plan(tr, ro, wb.RECEIVER, d).dump() == want
+    assert wb.Plan(tr, ro, wb.SENDER, otr.nranks - 1).dump() == want
+
+
+def test_traffic_counts():
+    w = WORKLOADS["llama3_8b_fsdp8_to_tp1"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    assert p.traffic() == (2 * 8030261248, 2 * 8030261248)
+    s = wb.Plan(tr, ro, wb.SENDER, 0)
+    r, wr = s.traffic()
+    assert r == wr and abs(r - 2 * 8030261248 / 8) < 8 * 4096
+    w = WORKLOADS["dsv3_ep64_to_ep8_fp8"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    n = 16 * (33 * 3 * 2048 * 7168 + 256 * 7168)
+    scales = 16 * (32 * 32 * 56 + 32 * 56 * 16 + 32 * 56 + 56 * 16)
+    assert p.traffic() == (2 * n, n - 16 * 256 * 7168 + 2 * 16 * 256 * 7168 + 4 * scales)
+    assert p.work_counts()[1] == scales
+
+
+def _expect(code, fn, *a):
+    with pytest.raises(wb.WbError) as e:
+        fn(*a)
+    assert e.value.code == code, str(e.value)
+
+
+def test_error_paths():
+    m = dict(WORKLOADS["llama3_8b_fsdp8_to_tp1"]["model"])
+    _expect(wb.WB_EINVAL, wb.Layout.describe, m, dict(style="serving", dtype="bf16", tp=3))
+    _expect(wb.WB_EINVAL, wb.Layout.describe, m, dict(style="fsdp_flat", dtype="bf16", fsdp=0))
+    _expect(wb.WB_EINVAL, wb.Layout.describe, m, dict(style="serving", dtype="f8e4m3"))
+    _expect(wb.WB_EUNSUPPORTED, wb.Layout.describe, dict(WORKLOADS["mixtral_ep8fsdp2_to_ep2"]["model"]),
+            dict(style="megatron", dtype="bf16", tp=2, ep=2))
+    _expect(wb.WB_EUNSUPPORTED, wb.Layout.describe, m,
+            dict(style="serving", dtype="bf16", quant="f8e4m3", quant_block=256))
+    tr = wb.Layout.describe(m, dict(style="fsdp_flat", dtype="bf16", fsdp=8))
+    ro = wb.Layout.describe(m, dict(style="serving", dtype="bf16"))
+    _expect(wb.WB_EINVAL, wb.Plan, tr, ro, wb.SENDER, 8)
+    _expect(wb.WB_EINVAL, wb.Plan, tr, ro, wb.RECEIVER, 1)
+    _expect(wb.WB_EINVAL, wb.Plan, tr, ro, 7, 0)
+    other = wb.Layout.describe(dict(m, num_layers=2), dict(style="serving", dtype="bf16"))
+    _expect(wb.WB_EINVAL, wb.Plan, tr, other, wb.RECEIVER, 0)
+    # a placement outside its tensor / local
+    L = wb.Layout.create([("T", 4, 4)], 1)
+    L.add_local(0, "a", "f32", 1, 4, 4)
+    _expect(wb.WB_EINVAL, L.add_placement, 0, 0, 0, 5, 0, 4, 0, 0, 4)
+    _expect(wb.WB_EINVAL, L.add_placement, 0, 0, 0, 4, 0, 4, 0, 1, 4)
+    _expect(wb.WB_EINVAL, L.add_placement, 0, 0, 0, 4, 0, 4, 1, 0, 4)
+    _expect(wb.WB_EUNSUPPORTED, L.add_local, 0, "q", "f8e4m3", 1, 4, 4, 0)
+    # overlapping, non-identical trainer rectangles
+    T = wb.Layout.create([("T", 4, 4)], 2)
+    for r, (a, b) in enumerate([(0, 2), (1, 4)]):
+        T.add_local(r, "a", "f32", 1, b - a, 4)
+        T.add_placement(r, 0, a, b, 0, 4, 0, 0, 4)
+    R = wb.Layout.create([("T", 4, 4)], 1)
+    R.add_local(0, "x", "f32", 1, 4, 4)
+    R.add_placement(0, 0, 0, 4, 0, 4, 0, 0, 4)
+    _expect(wb.WB_EUNSUPPORTED, wb.Plan, T, R, wb.RECEIVER, 0)
+    # rollout element held by no trainer
+    T2 = wb.Layout.create([("T", 4, 4)], 1)
+    T2.add_local(0, "a", "f32", 1, 2, 4)
+    T2.add_placement(0, 0, 0, 2, 0, 4, 0, 0, 4)
+    _expect(wb.WB_EINVAL, wb.Plan, T2, R, wb.RECEIVER, 0)
+    # rollout tensor not exactly covered
+    R2 = wb.Layout.create([("T", 4, 4)], 1)
+    R2.add_local(0, "x", "f32", 1, 5, 4)
+    R2.add_placement(0, 0, 0, 4, 0, 4, 0, 0, 4)
+    _expect(wb.WB_EINVAL, wb.Plan, T2, R2, wb.RECEIVER, 0)
+    # pack/unpack before upload, or with the wrong role
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    _expect(wb.WB_EINVAL, p.unpack, 0, [0] * p.num_local_tensors, 0)
+    _expect(wb.WB_EINVAL, p.pack, [0] * p.num_local_tensors, 0, 0)

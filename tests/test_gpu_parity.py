@@ -1,0 +1,86 @@
+"""GPU parity through the C ABI: pack -> network stand-in -> unpack, bit for bit
+against the oracle, on every scaled workload (several tiles, ragged tails,
+partial and multi-piece fp8 blocks), random tiny layouts with odd shapes and
+unaligned flat-shard boundaries, a transposed destination, and a sender with
+nothing to send."""
+
+import numpy as np
+import pytest
+import torch
+
+import synthetic_checkpoint as sc
+import paper_2609_25442_amd as wb
+from oracle.catalog import CkptTensor
+from oracle.layout import Layout, Local, Placement, RankLayout, describe_layout, layout_from_spec
+from synthetic_checkpoint.workloads import ORDER, scaled
+
+from gpu_util import roundtrip, say
+from oracle_cases import hand_replicated_pair, random_model, random_par
+
+pytestmark = pytest.mark.gpu
+
+
+def _values(catalog, dtype):
+    cache = {}
+
+    def get(t):
+        if t not in cache:
+            c = catalog[t]
+            cache[t] = sc.values_numpy(t, np.arange(c.numel), dtype).reshape(c.rows, c.cols)
+        return cache[t]
+    return get
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_scaled_workload_parity(name):
+    w = scaled(name)
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    roundtrip(otr, oro, _values(otr.catalog, w["trainer"]["dtype"]), tr, ro, label=name)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_tiny_layout_parity(seed):
+    rng = np.random.default_rng(1000 + seed)
+    m = random_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout"))
+    dtype = otr.ranks[0].locals[0].dtype
+    roundtrip(otr, oro, _values(otr.catalog, dtype), label=f"random{seed}")
+
+
+def test_hand_layout_with_transposed_destination():
+    tr, ro = hand_replicated_pair()
+    roundtrip(tr, ro, _values(tr.catalog, "f32"), label="hand")
+
+
+def test_sender_with_nothing_to_send():
+    cat = [CkptTensor("T0", 3, 5), CkptTensor("T1", 2, 7)]
+    tr = Layout(cat, [RankLayout([Local("a", "bf16", 1, 3, 5)], [Placement(0, 0, 3, 0, 5, 0, 0, 5)]),
+                      RankLayout([Local("b", "bf16", 1, 2, 7)], [Placement(1, 0, 2, 0, 7, 0, 0, 7)])])
+    ro = Layout(cat, [RankLayout([Local("x", "bf16", 1, 5, 3)], [Placement(0, 0, 3, 0, 5, 0, 0, 3, 1)])])
+    roundtrip(tr, ro, _values(cat, "bf16"), label="idle-sender")
+
+
+def test_odd_widths_and_unaligned_runs():
+    # FSDP flat shards of odd-width tensors: runs start at every offset mod 8
+    from oracle.catalog import ModelShapes
+    from oracle.layout import Parallelism
+    m = ModelShapes("dense", num_layers=2, hidden=13, num_heads=2, num_kv_heads=1, head_dim=3, ffn=11, vocab=7)
+    for fsdp, dt in ((3, "f32"), (5, "bf16"), (7, "f32")):
+        otr = describe_layout(m, Parallelism("fsdp_flat", dt, fsdp=fsdp))
+        for rp in (Parallelism("serving", "bf16"), Parallelism("serving", "f32"),
+                   Parallelism("serving", "bf16", quant="f8e4m3", quant_block=4)):
+            oro = describe_layout(m, rp)
+            roundtrip(otr, oro, _values(otr.catalog, dt), label=f"odd-fsdp{fsdp}-{dt}-{rp.dtype}{rp.quant}")
+
+
+def test_generator_matches_on_gpu():
+    for t, (r, c) in [(0, (129, 4097)), (5000, (7, 33))]:
+        for dt in ("f32", "bf16"):
+            x = sc.values_torch(t, r, c, dt, device="cuda").reshape(-1)
+            bits = x.view(torch.int32 if dt == "f32" else torch.int16).cpu().numpy()
+            bits = bits.view(np.uint32 if dt == "f32" else np.uint16)
+            assert np.array_equal(bits, sc.values_numpy(t, np.arange(r * c), dt))
