@@ -211,6 +211,20 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     value = (pack_bytes + unpack_bytes) / (ms_per_step * 1e-3) / 1e9
 
+    # practical ceiling: a plain device copy of the receive buffer (also the
+    # known-size copy that calibrates the HBM byte counters)
+    scratch = torch.empty_like(recv)
+    scratch.copy_(recv)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(3):
+        scratch.copy_(recv)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = c0.elapsed_time(c1) / 3
+    del scratch
+
     n_tasks, n_blocks, _ = rplan.work_counts()
     dom = "wb::wb_qblock_kernel" if n_blocks and not n_tasks else "wb::wb_tasks_kernel"
     achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
@@ -235,6 +249,8 @@ def main():
         "plan_ms": plan_ms,
         "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
         "unpack": {"ms": round(unpack_ms, 4), "GB/s": round(achieved, 1), "bytes": unpack_bytes},
+        "device_copy": {"GB/s": round(2 * recv.numel() / (copy_ms * 1e-3) / 1e9, 1), "bytes": 2 * recv.numel(),
+                        "what": "torch copy_ of the receive buffer (hipMemcpy device-to-device)"},
         "roofline": {"bound": "hbm", "kernel": dom + " (unpack)", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},

@@ -14,7 +14,8 @@ import os
 from ctypes import POINTER, byref, c_char_p, c_int32, c_int64, c_size_t, c_void_p
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libwb.so")
+# WB_LIB selects another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("WB_LIB") or os.path.join(_HERE, "libwb.so")
 
 WB_OK, WB_EINVAL, WB_EUNSUPPORTED, WB_ENOMEM, WB_EHIP, WB_ESIZE = 0, -1, -2, -3, -4, -5
 DTYPES = {"f32": 0, "bf16": 1, "f8e4m3": 2}

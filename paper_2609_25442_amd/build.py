@@ -33,8 +33,10 @@ def _run(cmd):
     return r
 
 
-def build(verbose: bool = False) -> str:
-    bdir = os.path.join(ROOT, "_build")
+def build(verbose: bool = False, out: str = OUT, defines=()) -> str:
+    """Compile and link libwb.so at ``out``; ``defines`` are extra -D flags for
+    the kernels (tuning knobs such as WB_UNROLL)."""
+    bdir = os.path.join(ROOT, "_build", os.path.basename(out) + ".d")
     os.makedirs(bdir, exist_ok=True)
     objs = []
     for s in HOST_SOURCES:
@@ -43,14 +45,14 @@ def build(verbose: bool = False) -> str:
         objs.append(o)
     for s in DEVICE_SOURCES:
         o = os.path.join(bdir, s + ".o")
-        _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, s), "-o", o])
+        _run([HIPCC, *DEVICE_FLAGS, *["-D" + d for d in defines], "-c", os.path.join(CSRC, s), "-o", o])
         objs.append(o)
-    tmp = OUT + ".tmp"
+    tmp = out + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
     if verbose:
-        print("built", OUT)
-    return OUT
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -12,7 +12,8 @@
 //    gathered from its wire pieces into registers: amax by wavefront
 //    shuffles plus LDS across the four waves, s = amax / 448 (IEEE division),
 //    q = RN(x / s) computed with one reciprocal per block and a remainder
-//    correction (exact in the range that reaches E4M3), then
+//    correction for bf16 sources (exact in the range that reaches E4M3;
+//    checked for every bf16 input pair), IEEE division otherwise, then
 //    v_cvt_pk_fp8_f32. The scale is written by thread 0.
 // The work is bandwidth bound: no matrix cores are involved.
 #include <hip/hip_runtime.h>
@@ -22,8 +23,37 @@
 namespace wb {
 namespace {
 
+// Tuning knobs (build-time): 16-byte vectors in flight per lane, and whether
+// loads / stores carry the non-temporal hint (every byte is touched once).
+#ifndef WB_UNROLL
+#define WB_UNROLL 4
+#endif
+#ifndef WB_NT_LOAD
+#define WB_NT_LOAD 1
+#endif
+#ifndef WB_NT_STORE
+#define WB_NT_STORE 1
+#endif
+
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = WB_UNROLL;
+
+template <class T>
+__device__ __forceinline__ T ld(const T* p) {
+#if WB_NT_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+template <class T>
+__device__ __forceinline__ void st(T v, T* p) {
+#if WB_NT_STORE
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -73,11 +103,11 @@ __device__ void run_copy16(const Task& t, const char* src, char* dst) {
     for (; i + (kUnroll - 1) * kThreads < vpr; i += kUnroll * kThreads) {
       u32x4 v[kUnroll];
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) v[k] = __builtin_nontemporal_load(s + i + k * kThreads);
+      for (int k = 0; k < kUnroll; ++k) v[k] = ld(s + i + k * kThreads);
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) __builtin_nontemporal_store(v[k], d + i + k * kThreads);
+      for (int k = 0; k < kUnroll; ++k) st(v[k], d + i + k * kThreads);
     }
-    for (; i < vpr; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+    for (; i < vpr; i += kThreads) st(ld(s + i), d + i);
     return;
   }
   const uint64_t total = uint64_t(t.rows) * vpr;
@@ -91,13 +121,13 @@ __device__ void run_copy16(const Task& t, const char* src, char* dst) {
       if (q + uint64_t(k) * kThreads < total) {
         const u32x4* sp = reinterpret_cast<const u32x4*>(src + uint64_t(w.r) * t.src_ld) + w.c;
         dp[k] = reinterpret_cast<u32x4*>(dst + uint64_t(w.r) * t.dst_ld) + w.c;
-        v[k] = __builtin_nontemporal_load(sp);
+        v[k] = ld(sp);
       }
       w.step();
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) __builtin_nontemporal_store(v[k], dp[k]);
+      if (dp[k]) st(v[k], dp[k]);
   }
 }
 
@@ -115,14 +145,14 @@ __device__ void run_f32_bf16(const Task& t, const char* src, char* dst) {
       if (q + uint64_t(k) * kThreads < total) {
         const f32x4* sp = reinterpret_cast<const f32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 4);
         dp[k] = reinterpret_cast<u32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 2);
-        a[k] = __builtin_nontemporal_load(sp);
-        b[k] = __builtin_nontemporal_load(sp + 1);
+        a[k] = ld(sp);
+        b[k] = ld(sp + 1);
       }
       w.step();
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) __builtin_nontemporal_store(cvt8_f32_bf16(a[k], b[k]), dp[k]);
+      if (dp[k]) st(cvt8_f32_bf16(a[k], b[k]), dp[k]);
   }
 }
 
@@ -140,7 +170,7 @@ __device__ void run_bf16_f32(const Task& t, const char* src, char* dst) {
       if (q + uint64_t(k) * kThreads < total) {
         const u32x4* sp = reinterpret_cast<const u32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 2);
         dp[k] = reinterpret_cast<f32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 4);
-        v[k] = __builtin_nontemporal_load(sp);
+        v[k] = ld(sp);
       }
       w.step();
     }
@@ -148,8 +178,8 @@ __device__ void run_bf16_f32(const Task& t, const char* src, char* dst) {
     for (int k = 0; k < kUnroll; ++k)
       if (dp[k]) {
         const u32x4 x = v[k];
-        __builtin_nontemporal_store(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, dp[k]);
-        __builtin_nontemporal_store(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, dp[k] + 1);
+        st(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, dp[k]);
+        st(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, dp[k] + 1);
       }
   }
 }
@@ -271,7 +301,7 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
       const QPiece& p = pcs[hit];
       const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
       if ((reinterpret_cast<uintptr_t>(a) & 15) == 0) {
-        const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a));
+        const u32x4 x = ld(reinterpret_cast<const u32x4*>(a));
         v[k][0] = bf16_lo(x.x); v[k][1] = bf16_hi(x.x); v[k][2] = bf16_lo(x.y); v[k][3] = bf16_hi(x.y);
         v[k][4] = bf16_lo(x.z); v[k][5] = bf16_hi(x.z); v[k][6] = bf16_lo(x.w); v[k][7] = bf16_hi(x.w);
         done = true;
@@ -298,7 +328,9 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   // whose scale is subnormal uses IEEE division per element.
   const uint32_t sbits = __float_as_uint(s);
   const int sexp = int((sbits >> 23) & 0xFF);
-  const bool fast = sexp != 0;
+  // the fast path is verified exhaustively for every bf16 (x, amax) pair; fp32
+  // sources take IEEE division
+  const bool fast = sexp != 0 && (b.flags & QB_BF16_SOURCE);
   const float pw = __uint_as_float(uint32_t(254 - sexp) << 23);  // 2^-(sexp - 127)
   const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);
   const float rp = 1.0f / sp;
@@ -315,7 +347,9 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
         const float xp = v[k][m] * pw;
         const float q0 = xp * rp;
         const float e = fmaf(-q0, sp, xp);
-        qq = fmaf(e, rp, q0);
+        // x' can underflow to a zero whose sign the correction loses; x / s
+        // always carries the sign of x
+        qq = __builtin_copysignf(fmaf(e, rp, q0), v[k][m]);
       } else {
         qq = v[k][m] / s;
       }
@@ -327,7 +361,7 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
     hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
     uint8_t* dst = q8 + uint64_t(r) * b.dst_ld + cg;
     if ((b.flags & QB_VEC_STORE) && cg + 8 <= cols) {
-      __builtin_nontemporal_store(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
+      st(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
     } else {
 #pragma unroll
       for (int m = 0; m < 8; ++m)

@@ -308,6 +308,9 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           b.rows_m1 = static_cast<uint8_t>(rows - 1);
           b.cols_m1 = static_cast<uint8_t>(cols - 1);
           b.flags = (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) ? QB_VEC_STORE : 0;
+          bool bf16 = true;
+          for (uint32_t i = count[id]; i < count[id + 1]; ++i) bf16 = bf16 && P.qpieces[i].sdt == WB_BF16;
+          if (bf16) b.flags |= QB_BF16_SOURCE;
           P.qblocks[id] = b;
         }
   }

@@ -135,7 +135,7 @@ struct QPiece {
 };
 static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
-enum QBlockFlags : uint8_t { QB_VEC_STORE = 1 };
+enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2 };
 
 }  // namespace wb
 
