@@ -63,7 +63,7 @@ def kernel_source_hash():
 def stored_traffic(workload, kernel):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
     taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic-{workload}.txt")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -72,14 +72,17 @@ def stored_traffic(workload, kernel):
     return rec["kernels"][kernel]["hbm_bytes_per_launch"]
 
 
-def cpu_baseline(w, ro_dev_plan_bytes, recv_host_fn, budget_s=15.0):
-    """The oracle as it stands, on a time-bounded sample of the workload:
-    its planner, then its element-by-element unpack over the receiver's
-    segments in plan order until ``budget_s`` seconds have passed."""
+def cpu_baseline(w, recv_host_fn, budget_s=15.0):
+    """The oracle as it stands, on a time-bounded sample of the workload: its
+    planner, then its element-by-element unpack of the receiver's tensors, one
+    destination tensor at a time in layout order (every segment that feeds
+    the tensor, then its blockwise quantisation when it is fp8), until
+    ``budget_s`` seconds have passed."""
     import dataclasses
 
     import numpy as np
 
+    from oracle.layout import DTYPE_BYTES, Layout
     from oracle.layout import layout_from_spec
     from oracle.plan import build_plan
     from oracle.transfer import unpack as o_unpack
@@ -90,26 +93,121 @@ def cpu_baseline(w, ro_dev_plan_bytes, recv_host_fn, budget_s=15.0):
     oplan = build_plan(otr, oro)
     plan_ms = (time.perf_counter() - t0) * 1e3
     d = w["unpack_rank"]
-    segs = [g for g in oplan.segments if g.d == d]
-    done_bytes, spent, n = 0, 0.0, 0
-    from oracle.layout import DTYPE_BYTES
-    for g in segs:
-        payload = recv_host_fn(g.recv_off, g.nbytes)
-        buf = np.zeros(g.recv_off + g.nbytes, dtype=np.uint8)
-        buf[g.recv_off:] = payload
-        sub = dataclasses.replace(oplan, segments=[g])
+    rk = oro.ranks[d]
+    by_local = {}
+    for g in oplan.segments:
+        if g.d == d:
+            by_local.setdefault(rk.placements[g.dst_pl].u, []).append(g)
+    done_bytes, spent, n_t, n_seg = 0, 0.0, 0, 0
+    for u, lc in enumerate(rk.locals):
+        segs = by_local.get(u)
+        if not segs:
+            continue
+        # a receiver layout holding just this tensor (and its scale companion)
+        keep = [u] + ([lc.scale] if lc.block else [])
+        sub_locals = [rk.locals[k] if k in keep else dataclasses.replace(rk.locals[k], batch=0) for k in range(len(rk.locals))]
+        sub_rank = dataclasses.replace(rk, locals=sub_locals)
+        sub_ro = Layout(oro.catalog, [sub_rank if r == d else oro.ranks[r] for r in range(oro.nranks)])
+        lo = min(g.recv_off for g in segs)
+        hi = max(g.recv_off + g.nbytes for g in segs)
+        buf = np.zeros(hi, dtype=np.uint8)
+        buf[lo:hi] = recv_host_fn(lo, hi - lo)
+        sub = dataclasses.replace(oplan, rollout=sub_ro, segments=segs)
         t1 = time.perf_counter()
         o_unpack(sub, d, buf)
         spent += time.perf_counter() - t1
-        q = oro.ranks[d].placements[g.dst_pl]
-        done_bytes += g.nbytes + g.rect.numel * DTYPE_BYTES[oro.ranks[d].locals[q.u].dtype]
-        n += 1
+        done_bytes += sum(g.nbytes for g in segs) + lc.numel * DTYPE_BYTES[lc.dtype]
+        if lc.block:
+            done_bytes += rk.locals[lc.scale].numel * 4
+        n_t += 1
+        n_seg += len(segs)
         if spent >= budget_s:
             break
     return {"value": round(done_bytes / spent / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"oracle unpack of the first {n} of {len(segs)} segments of rollout rank {d} "
-                      f"({done_bytes / 1e9:.2f} GB read+written) in {spent:.1f} s; oracle plan {plan_ms:.0f} ms",
+            "sample": f"oracle unpack of the first {n_t} rollout tensors of rank {d} ({n_seg} segments, "
+                      f"{done_bytes / 1e9:.2f} GB read+written) in {spent:.1f} s, single-threaded numpy; "
+                      f"oracle plan {plan_ms:.0f} ms",
             "plan_ms": round(plan_ms, 1)}
+
+
+def _read_csv(path):
+    import csv
+
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _launch_grids(w):
+    """Grid sizes (threads) of the pack and unpack launches of a workload,
+    from the library's host planner (no GPU needed)."""
+    import paper_2609_25442_amd as wb
+
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    rp = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"])
+    sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
+    rt, rb, _ = rp.work_counts()
+    st, _, _ = sp.work_counts()
+    return {"pack": (st * 256, "wb_tasks_kernel", sp.traffic()), "unpack": (rt * 256, "wb_tasks_kernel", rp.traffic()),
+            "unpack_fp8": (rb * 256, "wb_qblock_kernel", None)}, rp.buffer_bytes
+
+
+def summarize_counters(workload, fetch_csv, write_csv):
+    """HBM bytes per launch of the pack and unpack kernels from two rocprofv3
+    --pmc runs of this benchmark (FETCH_SIZE, then WRITE_SIZE, KiB per
+    dispatch), each scaled by what the counter reads for the benchmark's plain
+    device copy of known size."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    grids, recv_bytes = _launch_grids(WORKLOADS[workload])
+    copy_bytes = min(recv_bytes, 16 << 30)
+    out = {"workload": workload, "source_hash": kernel_source_hash(), "kernels": {}, "calibration": {}}
+    per = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = [r for r in _read_csv(path) if r["Counter_Name"] == counter]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        copies = sorted(copies)[-3:]                       # the timed reference copies
+        factor = statistics.mean(copies) * 1024 / copy_bytes
+        out["calibration"][counter] = {"copy_bytes": copy_bytes, "copy_kib": statistics.mean(copies),
+                                       "factor": round(factor, 5)}
+        for label, (grid, kname, _) in grids.items():
+            vals = [float(r["Counter_Value"]) for r in rows
+                    if kname in r["Kernel_Name"] and int(r["Grid_Size"]) == grid and grid > 0]
+            if vals:
+                per.setdefault(label, {})[counter] = (statistics.mean(vals), len(vals), factor)
+    for label, c in per.items():
+        if "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+            continue
+        fk, n, ff = c["FETCH_SIZE"]
+        wk, _, wf = c["WRITE_SIZE"]
+        rd, wr = fk * 1024 / ff, wk * 1024 / wf
+        alg = grids[label][2]
+        out["kernels"][label] = {"dispatches": n, "fetch_kib": fk, "write_kib": wk, "hbm_read_bytes": round(rd),
+                                 "hbm_write_bytes": round(wr), "hbm_bytes_per_launch": round(rd + wr),
+                                 "algorithmic_bytes": (alg[0] + alg[1]) if alg else None}
+    return out
+
+
+def summarize_trace(workload, trace_csv):
+    """Per-launch durations of the pack, unpack and reference-copy kernels from
+    a rocprofv3 --kernel-trace run of this benchmark."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    grids, recv_bytes = _launch_grids(WORKLOADS[workload])
+    rows = _read_csv(trace_csv)
+    res = {}
+    for label, (grid, kname, alg) in grids.items():
+        ds = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows
+              if kname in r["Kernel_Name"] and int(r["Grid_Size_X"]) == grid and grid > 0]
+        if ds:
+            res[label] = {"launches": len(ds), "avg_us": round(statistics.mean(ds) / 1e3, 2),
+                          "min_us": round(min(ds) / 1e3, 2), "max_us": round(max(ds) / 1e3, 2),
+                          "GB/s_at_avg": round((alg[0] + alg[1]) / statistics.mean(ds), 1) if alg else None}
+    copies = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+    if copies:
+        top = sorted(copies)[-3:]
+        res["device_copy"] = {"launches": len(top), "avg_us": round(statistics.mean(top) / 1e3, 2)}
+    return res
 
 
 def main():
@@ -119,7 +217,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print HBM traffic per launch from two rocprofv3 --pmc runs of this benchmark")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
     args = ap.parse_args()
+    if args.summarize_counters:
+        print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
+        return
+    if args.summarize_trace:
+        print(json.dumps(summarize_trace(args.workload, args.summarize_trace), indent=1))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the resharding hot path here runs on a single MI355X "
               "(pack of one trainer rank, unpack of one rollout rank); --gpus above 1 is not supported.",
@@ -213,20 +321,26 @@ def main():
 
     # practical ceiling: a plain device copy of the receive buffer (also the
     # known-size copy that calibrates the HBM byte counters)
-    scratch = torch.empty_like(recv)
-    scratch.copy_(recv)
+    csrc = recv[:min(recv.numel(), 16 << 30)]
+    scratch = torch.empty_like(csrc)
+    scratch.copy_(csrc)
     torch.cuda.synchronize()
     c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     c0.record(stream)
     for _ in range(3):
-        scratch.copy_(recv)
+        scratch.copy_(csrc)
     c1.record(stream)
     torch.cuda.synchronize()
     copy_ms = c0.elapsed_time(c1) / 3
     del scratch
 
     n_tasks, n_blocks, _ = rplan.work_counts()
-    dom = "wb::wb_qblock_kernel" if n_blocks and not n_tasks else "wb::wb_tasks_kernel"
+    if n_blocks and n_tasks:
+        dom = "wb::wb_qblock_kernel + wb::wb_tasks_kernel (one wb_unpack, timed together)"
+    elif n_blocks:
+        dom = "wb::wb_qblock_kernel (unpack)"
+    else:
+        dom = "wb::wb_tasks_kernel (unpack)"
     achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
     traffic = stored_traffic(args.workload, "unpack")
     out = {
@@ -249,16 +363,16 @@ def main():
         "plan_ms": plan_ms,
         "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
         "unpack": {"ms": round(unpack_ms, 4), "GB/s": round(achieved, 1), "bytes": unpack_bytes},
-        "device_copy": {"GB/s": round(2 * recv.numel() / (copy_ms * 1e-3) / 1e9, 1), "bytes": 2 * recv.numel(),
-                        "what": "torch copy_ of the receive buffer (hipMemcpy device-to-device)"},
-        "roofline": {"bound": "hbm", "kernel": dom + " (unpack)", "achieved": round(achieved, 1),
+        "device_copy": {"GB/s": round(2 * csrc.numel() / (copy_ms * 1e-3) / 1e9, 1), "bytes": 2 * csrc.numel(),
+                        "what": "torch copy_ of (up to 16 GiB of) the receive buffer: hipMemcpy device to device"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
     }
     if not args.no_cpu_baseline:
         def recv_host(off, nb):
             return recv[off:off + nb].cpu().numpy()
-        out["cpu_baseline"] = cpu_baseline(w, rplan.buffer_bytes, recv_host)
+        out["cpu_baseline"] = cpu_baseline(w, recv_host)
     print(json.dumps(out), flush=True)
 
 

@@ -232,6 +232,31 @@ __device__ void run_transpose(const Task& t, const char* src, char* dst) {
   }
 }
 
+// dst[c][r] = src[r][c] for 2-byte elements, 64 rows x (64..256) columns: each
+// wave takes one 64 x 64 tile, each lane an 8 x 8 sub-tile that it loads as
+// eight 16-byte rows, transposes in registers and stores as eight 16-byte rows.
+// Lanes 8i..8i+7 cover one 128-byte span of a row on both sides.
+__device__ void run_transpose16(const Task& t, const char* src, char* dst) {
+  const uint32_t w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (w * 64 >= t.cols) return;
+  const uint32_t c0 = w * 64 + 8 * (l & 7), r0 = 8 * (l >> 3);
+  u32x4 a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    a[i] = ld(reinterpret_cast<const u32x4*>(src + (uint64_t(r0 + i) * t.src_ld + c0) * 2));
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    // column j of the sub-tile: element j of each loaded row
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t x = a[2 * k][j >> 1], y = a[2 * k + 1][j >> 1];
+      o[k] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+    }
+    st(u32x4{o[0], o[1], o[2], o[3]}, reinterpret_cast<u32x4*>(dst + (uint64_t(c0 + j) * t.dst_ld + r0) * 2));
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
@@ -245,6 +270,7 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
     case TASK_BF16_F32: run_bf16_f32(t, src, dst); break;
     case TASK_SCALAR: run_scalar(t, src, dst); break;
     case TASK_TRANSPOSE: run_transpose(t, src, dst); break;
+    case TASK_TRANSPOSE16: run_transpose16(t, src, dst); break;
     default: break;
   }
 }
@@ -258,9 +284,9 @@ __device__ __forceinline__ float load_f32(const char* p, int dt) {
 }
 
 // Element (r, c) of the block from its pieces (the block is exactly covered).
-__device__ __forceinline__ float gather_one(const QPiece* __restrict__ pcs, int n, const char* recv, int r, int c) {
+__device__ __forceinline__ float gather_one(const QPiece* pcs, int n, const char* recv, int r, int c) {
   for (int i = 0; i < n; ++i) {
-    const QPiece p = pcs[i];
+    const QPiece& p = pcs[i];
     if (r >= p.r0 && r <= p.r1m1 && c >= p.c0 && c <= p.c1m1) {
       const int es = p.sdt == WB_F32 ? 4 : 2;
       return load_f32(recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (c - p.c0)) * es, p.sdt);
@@ -269,52 +295,84 @@ __device__ __forceinline__ float gather_one(const QPiece* __restrict__ pcs, int 
   return 0.0f;
 }
 
+__device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
+  v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
+  v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+}
+
+constexpr int kLdsPieces = 32;
+
 }  // namespace
 
 __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
                                                              const QPiece* __restrict__ pieces,
                                                              const uint64_t* __restrict__ ptrs) {
   __shared__ float wave_max[kThreads / 64];
+  __shared__ QPiece lds_pcs[kLdsPieces];
   const QBlock b = blocks[blockIdx.x];
   const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
   const char* recv = reinterpret_cast<const char*>(ptrs[0]);
-  const QPiece* pcs = pieces + b.piece0;
-  const int n = b.npieces;
   const int cg = (threadIdx.x & 15) * 8;  // first of this thread's 8 columns
   const int rb = threadIdx.x >> 4;        // rows rb, rb + 16, ..., rb + 112
   float v[8][8];
-  float amax = 0.0f;
+  if (b.flags & QB_SINGLE) {
+    // one aligned bf16 piece covers the block: eight independent 16-byte loads
+    const char* base = recv + b.src_off + uint64_t(cg) * 2;
+    u32x4 raw[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int r = rb + 16 * k;
-#pragma unroll
-    for (int m = 0; m < 8; ++m) v[k][m] = 0.0f;
-    if (r >= rows || cg >= cols) continue;
-    // fast path: the 8 columns lie in one bf16 piece and the load is 16-byte aligned
-    int hit = -1;
-    for (int i = 0; i < n; ++i) {
-      const QPiece& p = pcs[i];
-      if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) { hit = i; break; }
+    for (int k = 0; k < 8; ++k) {
+      const int r = rb + 16 * k;
+      raw[k] = u32x4{0u, 0u, 0u, 0u};
+      if (r < rows && cg < cols) raw[k] = ld(reinterpret_cast<const u32x4*>(base + uint64_t(r) * b.src_ld * 2));
     }
-    bool done = false;
-    if (hit >= 0 && pcs[hit].sdt == WB_BF16) {
-      const QPiece& p = pcs[hit];
-      const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
-      if ((reinterpret_cast<uintptr_t>(a) & 15) == 0) {
-        const u32x4 x = ld(reinterpret_cast<const u32x4*>(a));
-        v[k][0] = bf16_lo(x.x); v[k][1] = bf16_hi(x.x); v[k][2] = bf16_lo(x.y); v[k][3] = bf16_hi(x.y);
-        v[k][4] = bf16_lo(x.z); v[k][5] = bf16_hi(x.z); v[k][6] = bf16_lo(x.w); v[k][7] = bf16_hi(x.w);
-        done = true;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) unpack8(raw[k], v[k]);
+  } else {
+    // several pieces (or an unaligned / fp32 one): stage the piece list in LDS,
+    // resolve each row chunk's source first, then issue the loads
+    const int n = b.npieces;
+    const QPiece* pcs = pieces + b.piece0;
+    if (n <= kLdsPieces) {
+      for (int i = threadIdx.x; i < n; i += kThreads) lds_pcs[i] = pcs[i];
+      __syncthreads();
+      pcs = lds_pcs;
+    }
+    const char* src[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int r = rb + 16 * k;
+      src[k] = nullptr;
+      if (r >= rows || cg >= cols) continue;
+      for (int i = 0; i < n; ++i) {
+        const QPiece& p = pcs[i];
+        if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) {
+          const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
+          if (p.sdt == WB_BF16 && (reinterpret_cast<uintptr_t>(a) & 15) == 0) src[k] = a;
+          break;
+        }
       }
     }
-    if (!done) {
+    u32x4 raw[8];
 #pragma unroll
-      for (int m = 0; m < 8; ++m)
-        if (cg + m < cols) v[k][m] = gather_one(pcs, n, recv, r, cg + m);
+    for (int k = 0; k < 8; ++k) {
+      raw[k] = u32x4{0u, 0u, 0u, 0u};
+      if (src[k]) raw[k] = ld(reinterpret_cast<const u32x4*>(src[k]));
     }
 #pragma unroll
-    for (int m = 0; m < 8; ++m) amax = fmaxf(amax, fabsf(v[k][m]));
+    for (int k = 0; k < 8; ++k) {
+      unpack8(raw[k], v[k]);
+      const int r = rb + 16 * k;
+      if (!src[k] && r < rows && cg < cols) {
+#pragma unroll
+        for (int m = 0; m < 8; ++m) v[k][m] = cg + m < cols ? gather_one(pcs, n, recv, r, cg + m) : 0.0f;
+      }
+    }
   }
+  float amax = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+#pragma unroll
+    for (int m = 0; m < 8; ++m) amax = fmaxf(amax, fabsf(v[k][m]));
   for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
   if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = amax;
   __syncthreads();

@@ -154,15 +154,30 @@ struct TaskSink {
     }
   }
 
-  // dst[c][r] = src[r][c] for an R x C source block, in 64 x 64 tiles.
+  // dst[c][r] = src[r][c] for an R x C source block: aligned 2-byte data in
+  // register-transposed 64 x 256 pieces, everything else in 64 x 64 LDS tiles.
   void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
                       int64_t R, int64_t C) {
     const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
-    for (int64_t r = 0; r < R; r += 64)
-      for (int64_t c = 0; c < C; c += 64)
+    const bool fast = ss == 2 && ds == 2 && sdt == ddt && soff % 16 == 0 && doff % 16 == 0 && (sld * 2) % 16 == 0 &&
+                      (dld * 2) % 16 == 0;
+    for (int64_t r = 0; r < R; r += 64) {
+      int64_t c = 0;
+      if (fast && r + 64 <= R)
+        for (; c + 64 <= C; c += 256) {
+          const int64_t w = std::min<int64_t>(256, (C - c) / 64 * 64);
+          push(TASK_TRANSPOSE16, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
+               doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, 64, w);
+          if (w < 256) {
+            c += w;
+            break;
+          }
+        }
+      for (; c < C; c += 64)
         push(TASK_TRANSPOSE, sidx, soff + (r * sld + c) * ss, static_cast<uint32_t>(sld), sdt, didx,
              doff + (c * dld + r) * ds, static_cast<uint32_t>(dld), ddt, std::min<int64_t>(64, R - r),
              std::min<int64_t>(64, C - c));
+    }
   }
 };
 
@@ -311,6 +326,15 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           bool bf16 = true;
           for (uint32_t i = count[id]; i < count[id + 1]; ++i) bf16 = bf16 && P.qpieces[i].sdt == WB_BF16;
           if (bf16) b.flags |= QB_BF16_SOURCE;
+          if (b.npieces == 1) {
+            const QPiece& q = P.qpieces[b.piece0];
+            if (bf16 && q.r0 == 0 && q.c0 == 0 && q.r1m1 == rows - 1 && q.c1m1 == cols - 1 && cols % 8 == 0 &&
+                q.src_off % 16 == 0 && (uint64_t(q.src_ld) * 2) % 16 == 0) {
+              b.flags |= QB_SINGLE;
+              b.src_off = q.src_off;
+              b.src_ld = q.src_ld;
+            }
+          }
           P.qblocks[id] = b;
         }
   }
@@ -352,6 +376,13 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
         inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
         break;
+      case TASK_TRANSPOSE16:
+        if (t.rows != 64 || t.cols % 64 || t.cols > 256 || ss != 2 || ds != 2 || t.src_off % 16 || t.dst_off % 16 ||
+            (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
+          fail(WB_EINVAL, "internal: bad register-transpose work item");
+        inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
+        inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
+        break;
       default:
         fail(WB_EINVAL, "internal: unknown work item");
     }
@@ -363,6 +394,11 @@ void check_work(const wb_plan_t& P, const Rank& R) {
     if (R.locals[b.dst_idx - 1].dtype != WB_F8E4M3 || R.locals[b.scale_idx - 1].dtype != WB_F32)
       fail(WB_EINVAL, "internal: fp8 block targets the wrong tensors");
     if ((b.flags & QB_VEC_STORE) && (b.dst_off % 8 || b.dst_ld % 8)) fail(WB_EINVAL, "internal: misaligned fp8 store");
+    if (b.flags & QB_SINGLE) {
+      if (b.src_off % 16 || (uint64_t(b.src_ld) * 2) % 16 || cols % 8 || !(b.flags & QB_BF16_SOURCE))
+        fail(WB_EINVAL, "internal: misaligned single-piece fp8 block");
+      inside(0, b.src_off, ((rows - 1) * b.src_ld + cols) * 2, "fp8 single-piece source");
+    }
     if (uint64_t(b.piece0) + b.npieces > P.qpieces.size() || b.npieces == 0)
       fail(WB_EINVAL, "internal: fp8 block pieces out of range");
     for (uint32_t i = b.piece0; i < b.piece0 + b.npieces; ++i) {

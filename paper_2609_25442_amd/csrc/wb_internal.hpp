@@ -98,6 +98,7 @@ enum TaskKind : uint8_t {
   TASK_BF16_F32 = 2,   // bf16 -> fp32, 8 elements per vector
   TASK_SCALAR = 3,     // any supported pair, element by element
   TASK_TRANSPOSE = 4,  // dst[c][r] = cvt(src[r][c]), one LDS tile of up to 64 x 64
+  TASK_TRANSPOSE16 = 5,  // 2-byte dst[c][r] = src[r][c], 64 rows x (64..256) cols, in registers
 };
 
 struct Task {
@@ -111,9 +112,13 @@ struct Task {
 };
 static_assert(sizeof(Task) == 48, "Task layout");
 
-// One fp8 destination block and the wire pieces that fill it.
+// One fp8 destination block and the wire pieces that fill it. Blocks filled by
+// a single 16-byte aligned bf16 piece (QB_SINGLE) carry its source address
+// here, so the kernel needs no piece lookups for them.
 struct QBlock {
   uint64_t dst_off;     // bytes from the fp8 tensor to the block origin
+  uint64_t src_off;     // QB_SINGLE: bytes from recv_buf to the block's first element
+  uint32_t src_ld;      // QB_SINGLE: wire row length in elements
   uint32_t piece0;      // first piece
   uint32_t dst_ld;      // row stride of the fp8 matrix (elements = bytes)
   uint32_t scale_off;   // element index of the block's scale
@@ -121,9 +126,8 @@ struct QBlock {
   uint8_t rows_m1, cols_m1;  // block extent minus one (blocks are at most 128 x 128)
   uint8_t flags, pad0;
   uint16_t pad1;
-  uint32_t pad2;
 };
-static_assert(sizeof(QBlock) == 40, "QBlock layout");
+static_assert(sizeof(QBlock) == 48, "QBlock layout");
 
 struct QPiece {
   uint64_t src_off;     // bytes from recv_buf to the piece's first element
@@ -135,7 +139,7 @@ struct QPiece {
 };
 static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
-enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2 };
+enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
 
 }  // namespace wb
 

@@ -84,3 +84,18 @@ def test_generator_matches_on_gpu():
             bits = x.view(torch.int32 if dt == "f32" else torch.int16).cpu().numpy()
             bits = bits.view(np.uint32 if dt == "f32" else np.uint16)
             assert np.array_equal(bits, sc.values_numpy(t, np.arange(r * c), dt))
+
+
+@pytest.mark.parametrize("rows,cols,split", [(520, 200, 1), (640, 264, 2), (130, 77, 1), (1024, 512, 3)])
+def test_transposed_trainer_shards(rows, cols, split):
+    """Trainer ranks hold column slabs of T stored transposed (row-parallel
+    shards); the rollout wants T row-major in one tensor. Large aligned slabs
+    take the register-transpose path, ragged edges and odd widths the tiles."""
+    cat = [CkptTensor("T", rows, cols)]
+    cuts = [cols * k // split for k in range(split + 1)]
+    ranks = []
+    for a, b in zip(cuts, cuts[1:]):
+        ranks.append(RankLayout([Local("t", "bf16", 1, b - a, rows)], [Placement(0, 0, rows, a, b, 0, 0, rows, 1)]))
+    tr = Layout(cat, ranks)
+    ro = Layout(cat, [RankLayout([Local("x", "bf16", 1, rows, cols)], [Placement(0, 0, rows, 0, cols, 0, 0, cols)])])
+    roundtrip(tr, ro, _values(cat, "bf16"), label=f"transposed-{rows}x{cols}/{split}")
