@@ -148,8 +148,9 @@ def _launch_grids(w):
     sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
     rt, rb, _ = rp.work_counts()
     st, _, _ = sp.work_counts()
-    return {"pack": (st * 256, "wb_tasks_kernel", sp.traffic()), "unpack": (rt * 256, "wb_tasks_kernel", rp.traffic()),
-            "unpack_fp8": (rb * 256, "wb_qblock_kernel", None)}, rp.buffer_bytes
+    return {"pack": (st * 256, "wb_tasks_kernel", sp.traffic()),
+            "unpack": (rt * 256, "wb_tasks_kernel", rp.kernel_traffic(0)),
+            "unpack_fp8": (rb * 256, "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
 
 
 def summarize_counters(workload, fetch_csv, write_csv):
@@ -217,14 +218,26 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--staged", action="store_true",
+                    help="send and receive buffers in pinned host memory (PCIe-bound; not the headline value)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print HBM traffic per launch from two rocprofv3 --pmc runs of this benchmark")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="print this GPU's read, write and copy stream ceilings (paper_2609_25442_amd/wb_ceilings)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
     args = ap.parse_args()
     if args.summarize_counters:
         print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
         return
+    if args.ceilings:
+        import subprocess
+
+        exe = os.path.join(ROOT, "paper_2609_25442_amd", "wb_ceilings")
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+        sys.stderr.write(r.stderr)
+        print(r.stdout.strip())
+        sys.exit(r.returncode)
     if args.summarize_trace:
         print(json.dumps(summarize_trace(args.workload, args.summarize_trace), indent=1))
         return
@@ -264,8 +277,12 @@ def main():
     log(f"[bench] {args.workload}: plan ms {plan_ms}; recv {rplan.buffer_bytes / 1e9:.2f} GB")
 
     # inputs: every sender's region for the receiver, through real packs
-    recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, device="cuda")
-    send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, device="cuda")
+    if args.staged:
+        recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, pin_memory=True)
+        send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, pin_memory=True)
+    else:
+        recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, device="cuda")
+        send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, device="cuda")
     src0 = None
     for s in range(tr.nranks):
         so, roff, nb = rplan.region(s, d)
@@ -321,7 +338,7 @@ def main():
 
     # practical ceiling: a plain device copy of the receive buffer (also the
     # known-size copy that calibrates the HBM byte counters)
-    csrc = recv[:min(recv.numel(), 16 << 30)]
+    csrc = recv[:min(recv.numel(), 16 << 30)].cuda() if args.staged else recv[:min(recv.numel(), 16 << 30)]
     scratch = torch.empty_like(csrc)
     scratch.copy_(csrc)
     torch.cuda.synchronize()
@@ -358,7 +375,8 @@ def main():
         else f"{src_dtype}->{w['rollout'].get('quant') or w['rollout']['dtype']}",
         "data": "synthetic",
         "config": {"workload": args.workload, "trainer": w["trainer"], "rollout": w["rollout"],
-                   "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes},
+                   "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes,
+                   "buffers": "pinned host (PCIe)" if args.staged else "device"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "plan_ms": plan_ms,
         "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},

@@ -212,6 +212,9 @@ int wb_plan_num_local_tensors(const wb_plan_t* plan, int32_t* out);
 int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
 /* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */
 int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* write_bytes);
+/* The same split by launch: launch 0 is the copy/cast kernel, launch 1 the fp8
+ * block kernel (receivers with fp8 tensors only; 0 otherwise). */
+int wb_plan_kernel_traffic(const wb_plan_t* plan, int32_t launch, int64_t* read_bytes, int64_t* write_bytes);
 /* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
 int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
 /* Canonical text form of the global plan (one line per segment). */

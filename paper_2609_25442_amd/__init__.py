@@ -4,7 +4,7 @@ routing plan, and the packing and assembly kernels.
 
 Argument marshalling only: every step runs in libwb.so (host planner in C++,
 kernels in HIP). Importing this package fails if the library is not built
-(``python -m paper_2609_25442_amd.build``); there is no fallback path.
+(``python paper_2609_25442_amd/build.py``); there is no fallback path.
 """
 
 from __future__ import annotations
@@ -58,7 +58,7 @@ class LocalInfo(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_25442_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_25442_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     P, L = c_void_p, c_void_p
     sig = {
@@ -85,6 +85,7 @@ def _load():
         "wb_plan_workspace_bytes": [P, POINTER(c_int64)],
         "wb_plan_traffic_bytes": [P, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_work_counts": [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_kernel_traffic": [P, c_int32, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_dump": [P, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
         "wb_plan_upload": [P, c_void_p, c_size_t, c_void_p],
         "wb_pack": [P, POINTER(c_void_p), c_void_p, c_void_p],
@@ -281,6 +282,12 @@ class Plan:
     def traffic(self):
         r, w = c_int64(), c_int64()
         _check(lib.wb_plan_traffic_bytes(self._h, byref(r), byref(w)))
+        return r.value, w.value
+
+    def kernel_traffic(self, launch: int):
+        """(read, write) algorithmic bytes of launch 0 (copy/cast) or 1 (fp8 blocks)."""
+        r, w = c_int64(), c_int64()
+        _check(lib.wb_plan_kernel_traffic(self._h, launch, byref(r), byref(w)))
         return r.value, w.value
 
     def work_counts(self):

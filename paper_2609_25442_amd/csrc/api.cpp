@@ -364,6 +364,13 @@ int wb_plan_traffic_bytes(const wb_plan_t* P, int64_t* read_bytes, int64_t* writ
   return WB_OK;
 }
 
+int wb_plan_kernel_traffic(const wb_plan_t* P, int32_t launch, int64_t* read_bytes, int64_t* write_bytes) {
+  if (!P || !read_bytes || !write_bytes || launch < 0 || launch > 1) return set_error(WB_EINVAL, "bad argument");
+  *read_bytes = launch == 0 ? P->read_bytes - P->q_read_bytes : P->q_read_bytes;
+  *write_bytes = launch == 0 ? P->write_bytes - P->q_write_bytes : P->q_write_bytes;
+  return WB_OK;
+}
+
 int wb_plan_work_counts(const wb_plan_t* P, int64_t* tasks, int64_t* blocks, int64_t* pieces) {
   if (!P || !tasks || !blocks || !pieces) return set_error(WB_EINVAL, "null argument");
   *tasks = static_cast<int64_t>(P->tasks.size());

@@ -226,6 +226,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     block_base[u] = nblocks;
     nblocks += l.batch * ((l.rows + l.block - 1) / l.block) * ((l.cols + l.block - 1) / l.block);
     P.write_bytes += R.locals[l.scale].numel() * 4;
+    P.q_write_bytes += R.locals[l.scale].numel() * 4;
   }
   struct Span {
     const Segment* g;
@@ -244,6 +245,8 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     P.read_bytes += g.bytes;
     if (dl.block > 0) {
       P.write_bytes += g.x.numel();
+      P.q_write_bytes += g.x.numel();
+      P.q_read_bytes += g.bytes;
       if (q.tr) fail(WB_EUNSUPPORTED, "fp8 destinations cannot be transposed");
       const int64_t f0 = q.base + (g.x.r0 - q.r0) * q.ld + (g.x.c0 - q.c0);
       const int64_t mat = dl.rows * dl.cols;

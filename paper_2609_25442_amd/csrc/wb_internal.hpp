@@ -153,6 +153,7 @@ struct wb_plan_t {
   int role = WB_SENDER, rank = 0;
   int n_locals = 0;
   int64_t read_bytes = 0, write_bytes = 0;
+  int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
   std::vector<wb::Task> tasks;
   std::vector<wb::QBlock> qblocks;
   std::vector<wb::QPiece> qpieces;

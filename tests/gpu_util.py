@@ -38,11 +38,20 @@ def workspace_for(plan: "wb.Plan") -> torch.Tensor:
     return torch.empty(max(256, plan.workspace_bytes), dtype=torch.uint8, device="cuda")
 
 
-def roundtrip(otr, oro, values, tr=None, ro=None, label=""):
+def _buffer(nbytes, fill, staged):
+    """A send or receive buffer in device memory, or in pinned host memory
+    that the kernels reach over PCIe (the host-staged modes)."""
+    if staged:
+        return torch.full((max(1, nbytes),), fill, dtype=torch.uint8, pin_memory=True)
+    return torch.full((max(1, nbytes),), fill, dtype=torch.uint8, device="cuda")
+
+
+def roundtrip(otr, oro, values, tr=None, ro=None, label="", staged=False):
     """Pack every trainer rank and unpack every rollout rank on the GPU through
     the C ABI; compare every payload byte with the oracle's pack, check that
     padding between payloads is untouched, and compare every rollout tensor
-    with the oracle's plan-free expectation."""
+    with the oracle's plan-free expectation. With ``staged`` the send and
+    receive buffers live in pinned host memory."""
     from wb_cases import to_wb
 
     tr = tr or to_wb(otr)
@@ -59,7 +68,7 @@ def roundtrip(otr, oro, values, tr=None, ro=None, label=""):
         ws = workspace_for(p)
         p.upload(ws)
         src = [codes_to_gpu(c, lc.dtype) for c, lc in zip(o_locals, otr.ranks[s].locals)]
-        buf = torch.full((max(1, p.buffer_bytes),), FILL, dtype=torch.uint8, device="cuda")
+        buf = _buffer(p.buffer_bytes, FILL, staged)
         p.pack(src, buf)
         torch.cuda.synchronize()
         got = buf.cpu().numpy()[:p.buffer_bytes]
@@ -76,7 +85,7 @@ def roundtrip(otr, oro, values, tr=None, ro=None, label=""):
         p = wb.Plan(tr, ro, wb.RECEIVER, d)
         ws = workspace_for(p)
         p.upload(ws)
-        recv = torch.zeros(max(1, p.buffer_bytes), dtype=torch.uint8, device="cuda")
+        recv = _buffer(p.buffer_bytes, 0, staged)
         for s in range(otr.nranks):
             so, ro_off, nb = p.region(s, d)
             if nb:
