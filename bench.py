@@ -218,6 +218,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--round-budget", type=int, default=0,
+                    help="bytes per rank per round (0: one round); each step packs and unpacks every round")
     ap.add_argument("--staged", action="store_true",
                     help="send and receive buffers in pinned host memory (PCIe-bound; not the headline value)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -268,35 +270,42 @@ def main():
             p = wb.Plan(tr, ro, role, rank)
             ts.append((time.perf_counter() - t0) * 1e3)
         plan_ms[label] = round(statistics.median(ts), 2)
-    rplan = wb.Plan(tr, ro, wb.RECEIVER, d)
-    splan = wb.Plan(tr, ro, wb.SENDER, s0)
+    rb = args.round_budget
+    rplan = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=rb)
+    splan = wb.Plan(tr, ro, wb.SENDER, s0, round_budget=rb)
+    nr = rplan.num_rounds
     rws = torch.empty(rplan.workspace_bytes, dtype=torch.uint8, device="cuda")
     sws = torch.empty(splan.workspace_bytes, dtype=torch.uint8, device="cuda")
     rplan.upload(rws)
     splan.upload(sws)
     log(f"[bench] {args.workload}: plan ms {plan_ms}; recv {rplan.buffer_bytes / 1e9:.2f} GB")
 
-    # inputs: every sender's region for the receiver, through real packs
-    if args.staged:
-        recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, pin_memory=True)
-        send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, pin_memory=True)
-    else:
-        recv = torch.empty(rplan.buffer_bytes, dtype=torch.uint8, device="cuda")
-        send0 = torch.empty(splan.buffer_bytes, dtype=torch.uint8, device="cuda")
+    # inputs: every sender's region for the receiver, through real packs. With
+    # rounds, each round has its receive buffer (what the network delivers) and
+    # the sender alternates between two send buffers.
+    def alloc(n):
+        if args.staged:
+            return torch.empty(max(1, n), dtype=torch.uint8, pin_memory=True)
+        return torch.empty(max(1, n), dtype=torch.uint8, device="cuda")
+
+    recvs = [alloc(rplan.round_buffer_bytes(k)) for k in range(nr)]
+    sends = [alloc(splan.buffer_bytes) for _ in range(min(2, nr))]
+    recv, send0 = recvs[0], sends[0]
     src0 = None
     for s in range(tr.nranks):
-        so, roff, nb = rplan.region(s, d)
-        if nb == 0 and s != s0:
+        if s != s0 and not any(rplan.round_region(k, s, d)[2] for k in range(nr)):
             continue
         locs = build_sender_locals(wb, torch, sc, tr, s, src_dtype)
-        p = splan if s == s0 else wb.Plan(tr, ro, wb.SENDER, s)
+        p = splan if s == s0 else wb.Plan(tr, ro, wb.SENDER, s, round_budget=rb)
         if s != s0:
             ws = torch.empty(p.workspace_bytes, dtype=torch.uint8, device="cuda")
             p.upload(ws)
-        buf = send0 if s == s0 else torch.empty(p.buffer_bytes, dtype=torch.uint8, device="cuda")
-        p.pack(locs, buf)
-        if nb:
-            recv[roff:roff + nb] = buf[so:so + nb]
+        buf = send0 if s == s0 else alloc(p.buffer_bytes)
+        for k in range(nr):
+            so, roff, nb = rplan.round_region(k, s, d)
+            if nb:
+                (p.pack_round(k, locs, buf) if nr > 1 else p.pack(locs, buf))
+                recvs[k][roff:roff + nb] = buf[so:so + nb]
         if s == s0:
             src0 = locs
         else:
@@ -312,14 +321,19 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
-        if ev:
-            ev[0].record(stream)
-        splan.pack(src0, send0, stream)
-        if ev:
-            ev[1].record(stream)
-        rplan.unpack(recv, dst, stream)
-        if ev:
-            ev[2].record(stream)
+        if nr == 1:
+            if ev:
+                ev[0].record(stream)
+            splan.pack(src0, send0, stream)
+            if ev:
+                ev[1].record(stream)
+            rplan.unpack(recv, dst, stream)
+            if ev:
+                ev[2].record(stream)
+            return
+        for k in range(nr):
+            splan.pack_round(k, src0, sends[k % 2], stream)
+            rplan.unpack_round(k, recvs[k], dst, stream)
 
     for _ in range(args.warmup):
         step()
@@ -331,9 +345,23 @@ def main():
         step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    pack_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in events)
-    unpack_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in events)
     ms_per_step = elapsed * 1e3 / args.steps
+    if nr == 1:
+        pack_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in events)
+        unpack_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in events)
+    else:
+        # per-kernel times of a round-based step: one more pass timing the
+        # packs and the unpacks of all rounds separately
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        for k in range(nr):
+            splan.pack_round(k, src0, sends[k % 2], stream)
+        e[1].record(stream)
+        for k in range(nr):
+            rplan.unpack_round(k, recvs[k], dst, stream)
+        e[2].record(stream)
+        torch.cuda.synchronize()
+        pack_ms, unpack_ms = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])
     value = (pack_bytes + unpack_bytes) / (ms_per_step * 1e-3) / 1e9
 
     # practical ceiling: a plain device copy of the receive buffer (also the
@@ -376,7 +404,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "trainer": w["trainer"], "rollout": w["rollout"],
                    "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes,
-                   "buffers": "pinned host (PCIe)" if args.staged else "device"},
+                   "buffers": "pinned host (PCIe)" if args.staged else "device",
+                   "rounds": nr, "round_budget": rb},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "plan_ms": plan_ms,
         "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
@@ -387,7 +416,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and nr == 1:
         def recv_host(off, nb):
             return recv[off:off + nb].cpu().numpy()
         out["cpu_baseline"] = cpu_baseline(w, recv_host)

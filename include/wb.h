@@ -195,16 +195,38 @@ typedef enum wb_role { WB_SENDER = 0, WB_RECEIVER = 1 } wb_role;
  * or not a sub-rectangle of one matrix, quant_block > 128). */
 int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out);
 
+/* The same plan cut into rounds (Sec. 3.2: the model is transferred in roughly
+ * equal chunks, one per round, so that buffers stay bounded; App. D: the round
+ * count follows from the registered-buffer budget). round_budget > 0 bounds the
+ * bytes any sender or receiver handles in one round: checkpoint tensors are
+ * grouped into units (tensors whose images share an fp8 destination block are
+ * one unit, so no block spans rounds), units are visited in catalog order and
+ * a unit that would push some rank past the budget opens the next round (a
+ * unit larger than the budget is a round of its own). Segments, owners and
+ * balance equal those of wb_plan; each round has its own wire offsets under
+ * the same rules. round_budget == 0 gives one round (wb_plan).
+ * Errors: as wb_plan; WB_EINVAL for a negative budget. */
+int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
+                   int64_t round_budget, wb_plan_t** out);
+int wb_plan_num_rounds(const wb_plan_t* plan, int32_t* out);
+/* This rank's send (sender) or receive (receiver) buffer size in one round. */
+int wb_plan_round_buffer_bytes(const wb_plan_t* plan, int32_t round, int64_t* out);
+/* Region of a (sender, receiver) pair in one round, as wb_plan_region. */
+int wb_plan_round_region(const wb_plan_t* plan, int32_t round, int32_t sender, int32_t receiver,
+                         int64_t* send_offset, int64_t* recv_offset, int64_t* bytes);
+
 int wb_plan_num_segments(const wb_plan_t* plan, int64_t* out);        /* global */
-int wb_plan_buffer_bytes(const wb_plan_t* plan, int64_t* out);        /* this rank's send or receive buffer */
-int wb_plan_num_peers(const wb_plan_t* plan, int32_t* out);           /* regions in this rank's buffer */
-/* i-th region of this rank's buffer (ascending peer): peer rank, byte offset, bytes. */
+/* This rank's send or receive buffer size: the largest over the plan's rounds. */
+int wb_plan_buffer_bytes(const wb_plan_t* plan, int64_t* out);
+int wb_plan_num_peers(const wb_plan_t* plan, int32_t* out);           /* regions in this rank's round-0 buffer */
+/* i-th region of this rank's round-0 buffer (ascending peer): peer rank, byte offset, bytes. */
 int wb_plan_peer(const wb_plan_t* plan, int32_t i, int32_t* peer, int64_t* offset, int64_t* bytes);
-/* Region of any (sender, receiver) pair: offset in the sender's buffer, offset in
- * the receiver's buffer, bytes (0 when the pair exchanges nothing). */
+/* Round-0 region of any (sender, receiver) pair: offset in the sender's buffer,
+ * offset in the receiver's buffer, bytes (0 when the pair exchanges nothing). */
 int wb_plan_region(const wb_plan_t* plan, int32_t sender, int32_t receiver, int64_t* send_offset,
                    int64_t* recv_offset, int64_t* bytes);
-/* Global buffer size of any sender (role WB_SENDER) or receiver (WB_RECEIVER). */
+/* Buffer size of any sender (role WB_SENDER) or receiver (WB_RECEIVER), the
+ * largest over the rounds. */
 int wb_plan_rank_buffer_bytes(const wb_plan_t* plan, int32_t role, int32_t rank, int64_t* out);
 /* Number of local tensors of this rank: the length of src_ptrs / dst_ptrs. */
 int wb_plan_num_local_tensors(const wb_plan_t* plan, int32_t* out);
@@ -242,6 +264,15 @@ int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* 
  * Errors as for wb_pack. Calls on one plan must not overlap in time from several
  * host threads (the pointer table is per plan). */
 int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void* stream);
+
+/* One round of a multi-round plan: the same contracts as wb_pack / wb_unpack for
+ * the round's work items and buffer (wb_plan_round_buffer_bytes). The send or
+ * receive buffer is a launch argument, so consecutive rounds may alternate
+ * between buffers (double buffering) without restaging the pointer table;
+ * the local tensors must stay the same, or calls must be stream-ordered.
+ * wb_pack / wb_unpack refuse (WB_EINVAL) plans with more than one round. */
+int wb_pack_round(wb_plan_t* plan, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream);
+int wb_unpack_round(wb_plan_t* plan, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream);
 
 void wb_plan_destroy(wb_plan_t* plan);
 

@@ -25,6 +25,16 @@ them:
    the owner with the smallest E_q (ties: lower rank). Since the E_q of a set
    sum to zero after every region and a part always goes to a negative E_q,
    no owner ever exceeds its even share of the set by more than one part.
+5. Rounds (Sec. 3.2: the model is cut into roughly equal chunks, one per
+   round; App. D: the round count follows from the registered-buffer budget).
+   With a budget B > 0 the checkpoint tensors are grouped into *units*: two
+   tensors share a unit when their images in one fp8 destination matrix touch
+   a common quantisation block (so no block spans two rounds). Units are
+   visited in order of their first tensor; a unit joins the current round
+   unless that would take some sender's or receiver's bytes in the round above
+   B, in which case it opens the next round (a unit larger than B is a round of
+   its own). Segments keep their canonical order; each round has its own wire
+   offsets, computed by rule 4 over that round's segments.
 4. Wire format (Sec. 3.2, the packing kernel coalesces the tensors for one
    receiver into one contiguous buffer): the payloads of sender s for receiver
    d follow the canonical order, each a row-major copy of its rectangle in the
@@ -70,6 +80,7 @@ class Segment:
     dst_pl: int     # placement index in the receiver's layout
     nbytes: int     # payload bytes (sender dtype)
     region: int = -1  # index of the region the segment was cut from
+    round: int = 0
     send_off: int = 0
     recv_off: int = 0
 
@@ -81,6 +92,12 @@ class Region:
 
 
 @dataclass
+class Round:
+    send_bytes: list[int]
+    recv_bytes: list[int]
+
+
+@dataclass
 class Plan:
     trainer: Layout
     rollout: Layout
@@ -88,6 +105,7 @@ class Plan:
     regions: list[Region]
     send_bytes: list[int]
     recv_bytes: list[int]
+    rounds: list[Round] = None
 
 
 def _align(x: int, a: int) -> int:
@@ -98,7 +116,7 @@ class PlanError(ValueError):
     pass
 
 
-def build_plan(trainer: Layout, rollout: Layout) -> Plan:
+def build_plan(trainer: Layout, rollout: Layout, round_budget: int = 0) -> Plan:
     cat = trainer.catalog
     if [(t.name, t.rows, t.cols) for t in cat] != [(t.name, t.rows, t.cols) for t in rollout.catalog]:
         raise PlanError("trainer and rollout catalogs differ")
@@ -167,16 +185,23 @@ def build_plan(trainer: Layout, rollout: Layout) -> Plan:
             if covered != q.numel:
                 raise PlanError(f"rollout rank {d} placement {qi} is not fully held by the trainers")
 
-    # 4. wire offsets
+    # 5. rounds, then 4. wire offsets per round
     ns, nd = trainer.nranks, rollout.nranks
+    nrounds = _assign_rounds(trainer, rollout, segments, round_budget) if round_budget > 0 else 1
+    rounds = [_wire(segments, r, ns, nd) for r in range(nrounds)]
+    return Plan(trainer, rollout, segments, regions, rounds[0].send_bytes, rounds[0].recv_bytes, rounds)
+
+
+def _wire(segments, r, ns, nd) -> Round:
+    """Rule 4 over the segments of round r (their offsets are set in place)."""
     payload_end: dict[tuple, int] = {}
-    for sg in segments:
+    mine = [sg for sg in segments if sg.round == r]
+    for sg in mine:
         off = _align(payload_end.get((sg.s, sg.d), 0), PAYLOAD_ALIGN)
         sg.send_off = off
         sg.recv_off = off
         payload_end[(sg.s, sg.d)] = off + sg.nbytes
-    send_region = {}
-    send_bytes = []
+    send_region, send_bytes = {}, []
     for s in range(ns):
         pos = 0
         for d in range(nd):
@@ -185,8 +210,7 @@ def build_plan(trainer: Layout, rollout: Layout) -> Plan:
                 send_region[(s, d)] = pos
                 pos += payload_end[(s, d)]
         send_bytes.append(pos)
-    recv_region = {}
-    recv_bytes = []
+    recv_region, recv_bytes = {}, []
     for d in range(nd):
         pos = 0
         for s in range(ns):
@@ -195,20 +219,91 @@ def build_plan(trainer: Layout, rollout: Layout) -> Plan:
                 recv_region[(s, d)] = pos
                 pos += payload_end[(s, d)]
         recv_bytes.append(pos)
-    for sg in segments:
+    for sg in mine:
         sg.send_off += send_region[(sg.s, sg.d)]
         sg.recv_off += recv_region[(sg.s, sg.d)]
-    return Plan(trainer, rollout, segments, regions, send_bytes, recv_bytes)
+    return Round(send_bytes, recv_bytes)
+
+
+def _block_units(rollout: Layout, ntensors: int) -> list[int]:
+    """Unit id of every checkpoint tensor: tensors whose images in one
+    quantised destination matrix share a block are joined (union-find)."""
+    parent = list(range(ntensors))
+
+    def find(a):
+        while parent[a] != a:
+            parent[a] = parent[parent[a]]
+            a = parent[a]
+        return a
+
+    for rk in rollout.ranks:
+        per_matrix: dict[tuple, list] = {}
+        for p in rk.placements:
+            lc = rk.locals[p.u]
+            if not lc.block:
+                continue
+            mat = lc.rows * lc.cols
+            e, row0, col0 = p.base // mat, (p.base % mat) // lc.cols, p.base % lc.cols
+            if p.tr or col0 + p.cols > lc.cols or row0 + p.rows > lc.rows or (p.rows > 1 and p.ld != lc.cols):
+                raise PlanError("an fp8 placement must be a non-transposed sub-rectangle of one matrix")
+            B = lc.block
+            per_matrix.setdefault((p.u, e), []).append(
+                (row0 // B, (row0 + p.rows - 1) // B, col0 // B, (col0 + p.cols - 1) // B, p.t))
+        for items in per_matrix.values():
+            for a in range(len(items)):
+                for b in range(a + 1, len(items)):
+                    x, y = items[a], items[b]
+                    if x[0] <= y[1] and y[0] <= x[1] and x[2] <= y[3] and y[2] <= x[3]:
+                        parent[find(x[4])] = find(y[4])
+    return [find(t) for t in range(ntensors)]
+
+
+def _assign_rounds(trainer: Layout, rollout: Layout, segments, budget: int) -> int:
+    unit = _block_units(rollout, len(trainer.catalog))
+    members: dict[int, list] = {}
+    for sg in segments:
+        members.setdefault(unit[sg.t], []).append(sg)
+    order = sorted(members, key=lambda u: min(sg.t for sg in members[u]))
+    rnd, cur_s, cur_d = 0, {}, {}
+    for u in order:
+        add_s, add_d = {}, {}
+        for sg in members[u]:
+            add_s[sg.s] = add_s.get(sg.s, 0) + sg.nbytes
+            add_d[sg.d] = add_d.get(sg.d, 0) + sg.nbytes
+        over = any(cur_s.get(k, 0) + v > budget for k, v in add_s.items()) or \
+            any(cur_d.get(k, 0) + v > budget for k, v in add_d.items())
+        if over and (cur_s or cur_d):
+            rnd, cur_s, cur_d = rnd + 1, {}, {}
+        for k, v in add_s.items():
+            cur_s[k] = cur_s.get(k, 0) + v
+        for k, v in add_d.items():
+            cur_d[k] = cur_d.get(k, 0) + v
+        for sg in members[u]:
+            sg.round = rnd
+    return rnd + 1
 
 
 def dump(plan: Plan) -> str:
-    """Canonical text form of a plan, one line per segment."""
-    out = [f"plan trainer_ranks={plan.trainer.nranks} rollout_ranks={plan.rollout.nranks} segments={len(plan.segments)}"]
-    out += [f"send {s} {b}" for s, b in enumerate(plan.send_bytes)]
-    out += [f"recv {d} {b}" for d, b in enumerate(plan.recv_bytes)]
-    for g in plan.segments:
+    """Canonical text form of a plan, one line per segment (grouped by round
+    when there are several)."""
+    def segline(g):
         r = g.rect
-        out.append(f"seg {g.s} {g.d} {g.t} {r.r0} {r.r1} {r.c0} {r.c1} {g.src_pl} {g.dst_pl} {g.send_off} {g.recv_off} {g.nbytes}")
+        return f"seg {g.s} {g.d} {g.t} {r.r0} {r.r1} {r.c0} {r.c1} {g.src_pl} {g.dst_pl} {g.send_off} {g.recv_off} {g.nbytes}"
+
+    head = f"plan trainer_ranks={plan.trainer.nranks} rollout_ranks={plan.rollout.nranks} segments={len(plan.segments)}"
+    rounds = plan.rounds or [Round(plan.send_bytes, plan.recv_bytes)]
+    if len(rounds) == 1:
+        out = [head]
+        out += [f"send {s} {b}" for s, b in enumerate(rounds[0].send_bytes)]
+        out += [f"recv {d} {b}" for d, b in enumerate(rounds[0].recv_bytes)]
+        out += [segline(g) for g in plan.segments]
+        return "\n".join(out) + "\n"
+    out = [head + f" rounds={len(rounds)}"]
+    for k, rd in enumerate(rounds):
+        out.append(f"round {k}")
+        out += [f"send {s} {b}" for s, b in enumerate(rd.send_bytes)]
+        out += [f"recv {d} {b}" for d, b in enumerate(rd.recv_bytes)]
+        out += [segline(g) for g in plan.segments if g.round == k]
     return "\n".join(out) + "\n"
 
 

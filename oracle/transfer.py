@@ -47,13 +47,15 @@ def materialize(layout: Layout, rank: int, values, dtype=None) -> list[np.ndarra
     return out
 
 
-def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray]) -> np.ndarray:
-    """Send buffer of trainer rank s: every segment's rectangle, read through
-    the sender's placement, written row-major at its send offset."""
-    buf = np.zeros(plan.send_bytes[s], dtype=np.uint8)
+def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray], rnd: int = 0) -> np.ndarray:
+    """Send buffer of trainer rank s in round ``rnd``: every segment's
+    rectangle, read through the sender's placement, written row-major at its
+    send offset."""
+    rounds = plan.rounds or [None]
+    buf = np.zeros((rounds[rnd].send_bytes if rounds[rnd] else plan.send_bytes)[s], dtype=np.uint8)
     rk = plan.trainer.ranks[s]
     for g in plan.segments:
-        if g.s != s:
+        if g.s != s or g.round != rnd:
             continue
         p = rk.placements[g.src_pl]
         lc = rk.locals[p.u]
@@ -65,11 +67,13 @@ def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray]) -> np.ndarray:
     return buf
 
 
-def network(plan: Plan, d: int, send_bufs: dict[int, np.ndarray]) -> np.ndarray:
-    """Receive buffer of rollout rank d: each sender's region for d, copied."""
-    buf = np.zeros(plan.recv_bytes[d], dtype=np.uint8)
+def network(plan: Plan, d: int, send_bufs: dict[int, np.ndarray], rnd: int = 0) -> np.ndarray:
+    """Receive buffer of rollout rank d in round ``rnd``: each sender's region
+    for d, copied."""
+    rounds = plan.rounds or [None]
+    buf = np.zeros((rounds[rnd].recv_bytes if rounds[rnd] else plan.recv_bytes)[d], dtype=np.uint8)
     for g in plan.segments:
-        if g.d == d:
+        if g.d == d and g.round == rnd:
             buf[g.recv_off:g.recv_off + g.nbytes] = send_bufs[g.s][g.send_off:g.send_off + g.nbytes]
     return buf
 
@@ -108,16 +112,19 @@ def _finish(rk, staged, dst_locals):
     return dst_locals
 
 
-def unpack(plan: Plan, d: int, recv_buf: np.ndarray) -> list[np.ndarray]:
-    """Rollout rank d's tensors from its receive buffer: each segment's payload
-    is read row-major and written through the receiver's placement, cast to the
-    local dtype; quantised tensors are staged in fp32 and quantised blockwise."""
+def unpack(plan: Plan, d: int, recv_buf, rounds=None) -> list[np.ndarray]:
+    """Rollout rank d's tensors from its receive buffer(s): each segment's
+    payload is read row-major and written through the receiver's placement,
+    cast to the local dtype; quantised tensors are staged in fp32 and quantised
+    blockwise. With rounds, ``recv_buf`` is the list of the rounds' buffers."""
     rk = plan.rollout.ranks[d]
     dst = [np.zeros(lc.numel, dtype=CODE_DTYPE[lc.dtype]) for lc in rk.locals]
     staged = {u: np.zeros(lc.numel, dtype=np.uint32) for u, lc in enumerate(rk.locals) if lc.block}
+    bufs = recv_buf if isinstance(recv_buf, list) else [recv_buf]
     for g in plan.segments:
         if g.d != d:
             continue
+        recv_buf = bufs[g.round]
         q = rk.placements[g.dst_pl]
         lc = rk.locals[q.u]
         sp = plan.trainer.ranks[g.s].placements[g.src_pl]

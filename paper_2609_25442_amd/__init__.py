@@ -9,8 +9,10 @@ kernels in HIP). Importing this package fails if the library is not built
 
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 from ctypes import POINTER, byref, c_char_p, c_int32, c_int64, c_size_t, c_void_p
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -57,6 +59,11 @@ class LocalInfo(ctypes.Structure):
 
 
 def _load():
+    # libwb.so and torch's HIP extension both need libamdhip64.so.7; whichever is
+    # loaded first serves the whole process. Load torch's first so that the
+    # tensors' runtime and the library's kernels share one HIP runtime.
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_25442_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
@@ -75,6 +82,12 @@ def _load():
         "wb_layout_placement": [L, c_int32, c_int32, POINTER(Placement)],
         "wb_layout_dump": [L, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
         "wb_plan": [L, L, c_int32, c_int32, POINTER(P)],
+        "wb_plan_rounds": [L, L, c_int32, c_int32, c_int64, POINTER(P)],
+        "wb_plan_num_rounds": [P, POINTER(c_int32)],
+        "wb_plan_round_buffer_bytes": [P, c_int32, POINTER(c_int64)],
+        "wb_plan_round_region": [P, c_int32, c_int32, c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
+        "wb_pack_round": [P, c_int32, POINTER(c_void_p), c_void_p, c_void_p],
+        "wb_unpack_round": [P, c_int32, c_void_p, POINTER(c_void_p), c_void_p],
         "wb_plan_num_segments": [P, POINTER(c_int64)],
         "wb_plan_buffer_bytes": [P, POINTER(c_int64)],
         "wb_plan_num_peers": [P, POINTER(c_int32)],
@@ -120,6 +133,27 @@ def _text(fn, handle) -> str:
     return buf.value.decode()
 
 
+_live = weakref.WeakSet()
+
+
+@atexit.register
+def _release_all():
+    # free what is still alive while the interpreter is intact
+    for obj in list(_live):
+        _release(obj)
+
+
+def _release(obj):
+    """Free a library object once; quiet when the interpreter is shutting down."""
+    h, fn = getattr(obj, "_h", None), getattr(obj, "_destroy", None)
+    if h is not None and h.value and callable(fn):
+        try:
+            fn(h)
+        except Exception:
+            pass
+        obj._h = c_void_p()
+
+
 def _stream_handle(stream) -> int | None:
     if stream is None:
         import torch
@@ -140,6 +174,8 @@ class Layout:
 
     def __init__(self, handle: int):
         self._h = c_void_p(handle)
+        self._destroy = lib.wb_layout_destroy
+        _live.add(self)
 
     @classmethod
     def describe(cls, model: dict, par: dict) -> "Layout":
@@ -219,18 +255,19 @@ class Layout:
         return _text(lib.wb_layout_dump, self._h)
 
     def __del__(self):
-        if getattr(self, "_h", None) and self._h.value:
-            lib.wb_layout_destroy(self._h)
-            self._h = c_void_p()
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _release(self)
 
 
 class Plan:
     """The global routing plan seen from one rank (a sender or a receiver)."""
 
-    def __init__(self, trainer: Layout, rollout: Layout, role: int, rank: int):
+    def __init__(self, trainer: Layout, rollout: Layout, role: int, rank: int, round_budget: int = 0):
         h = c_void_p()
-        _check(lib.wb_plan(trainer._h, rollout._h, role, rank, byref(h)))
+        _check(lib.wb_plan_rounds(trainer._h, rollout._h, role, rank, round_budget, byref(h)))
         self._h = h
+        self._destroy = lib.wb_plan_destroy
+        _live.add(self)
         self.role, self.rank = role, rank
         self._workspace = None
 
@@ -256,6 +293,30 @@ class Plan:
         v = c_int32()
         _check(lib.wb_plan_num_local_tensors(self._h, byref(v)))
         return v.value
+
+    @property
+    def num_rounds(self) -> int:
+        v = c_int32()
+        _check(lib.wb_plan_num_rounds(self._h, byref(v)))
+        return v.value
+
+    def round_buffer_bytes(self, rnd: int) -> int:
+        v = c_int64()
+        _check(lib.wb_plan_round_buffer_bytes(self._h, rnd, byref(v)))
+        return v.value
+
+    def round_region(self, rnd: int, sender: int, receiver: int):
+        s, r, b = c_int64(), c_int64(), c_int64()
+        _check(lib.wb_plan_round_region(self._h, rnd, sender, receiver, byref(s), byref(r), byref(b)))
+        return s.value, r.value, b.value
+
+    def pack_round(self, rnd, src, send_buf, stream=None):
+        ptrs = (c_void_p * max(1, len(src)))(*[_ptr(x) for x in src])
+        _check(lib.wb_pack_round(self._h, rnd, ptrs, _ptr(send_buf), _stream_handle(stream)))
+
+    def unpack_round(self, rnd, recv_buf, dst, stream=None):
+        ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
+        _check(lib.wb_unpack_round(self._h, rnd, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
     def rank_buffer_bytes(self, role: int, rank: int) -> int:
         v = c_int64()
@@ -314,9 +375,8 @@ class Plan:
         _check(lib.wb_unpack(self._h, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
     def __del__(self):
-        if getattr(self, "_h", None) and self._h.value:
-            lib.wb_plan_destroy(self._h)
-            self._h = c_void_p()
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _release(self)
 
 
 def version() -> str:

@@ -2,6 +2,7 @@
 // work-table upload and the per-call pointer tables of wb_pack / wb_unpack.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstring>
 #include <new>
 #include <string>
@@ -249,13 +250,15 @@ int wb_layout_dump(const wb_layout_t* L, char* buf, size_t cap, size_t* needed) 
 
 void wb_layout_destroy(wb_layout_t* L) { delete L; }
 
-int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out) {
+int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
+                   int64_t round_budget, wb_plan_t** out) {
   return guarded([&]() -> int {
     if (!trainer || !rollout || !out) return set_error(WB_EINVAL, "null argument");
+    if (round_budget < 0) return set_error(WB_EINVAL, "round budget must be >= 0");
     *out = nullptr;
     auto* P = new wb_plan_t;
     try {
-      wb::build_plan(*trainer, *rollout, role, rank, *P);
+      wb::build_plan(*trainer, *rollout, role, rank, round_budget, *P);
       P->trainer = *trainer;
       P->rollout = *rollout;
       const wb::Rank& R = rank_of(P);
@@ -271,32 +274,59 @@ int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role
   });
 }
 
+int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out) {
+  return wb_plan_rounds(trainer, rollout, role, rank, 0, out);
+}
+
 int wb_plan_num_segments(const wb_plan_t* P, int64_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
   *out = static_cast<int64_t>(P->segs.size());
   return WB_OK;
 }
 
+int wb_plan_num_rounds(const wb_plan_t* P, int32_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  *out = static_cast<int32_t>(P->rounds.size());
+  return WB_OK;
+}
+
+static int64_t rank_bytes(const wb_plan_t* P, size_t k, int role, int rank) {
+  return role == WB_SENDER ? P->rounds[k].send_bytes[rank] : P->rounds[k].recv_bytes[rank];
+}
+
+int wb_plan_round_buffer_bytes(const wb_plan_t* P, int32_t round, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+  *out = rank_bytes(P, round, P->role, P->rank);
+  return WB_OK;
+}
+
 int wb_plan_buffer_bytes(const wb_plan_t* P, int64_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
-  *out = P->role == WB_SENDER ? P->send_bytes[P->rank] : P->recv_bytes[P->rank];
+  int64_t m = 0;
+  for (size_t k = 0; k < P->rounds.size(); ++k) m = std::max(m, rank_bytes(P, k, P->role, P->rank));
+  *out = m;
   return WB_OK;
 }
 
 int wb_plan_rank_buffer_bytes(const wb_plan_t* P, int32_t role, int32_t rank, int64_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
-  if (role == WB_SENDER && rank >= 0 && rank < P->n_send) { *out = P->send_bytes[rank]; return WB_OK; }
-  if (role == WB_RECEIVER && rank >= 0 && rank < P->n_recv) { *out = P->recv_bytes[rank]; return WB_OK; }
-  return set_error(WB_EINVAL, "bad role or rank");
+  if (!((role == WB_SENDER && rank >= 0 && rank < P->n_send) || (role == WB_RECEIVER && rank >= 0 && rank < P->n_recv)))
+    return set_error(WB_EINVAL, "bad role or rank");
+  int64_t m = 0;
+  for (size_t k = 0; k < P->rounds.size(); ++k) m = std::max(m, rank_bytes(P, k, role, rank));
+  *out = m;
+  return WB_OK;
 }
 
 int wb_plan_num_peers(const wb_plan_t* P, int32_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  const wb::RoundWire& W = P->rounds[0];
   int n = 0;
   const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
   for (int o = 0; o < others; ++o) {
     const size_t k = P->role == WB_SENDER ? size_t(P->rank) * P->n_recv + o : size_t(o) * P->n_recv + P->rank;
-    n += P->send_region[k] >= 0;
+    n += W.send_region[k] >= 0;
   }
   *out = n;
   return WB_OK;
@@ -304,30 +334,38 @@ int wb_plan_num_peers(const wb_plan_t* P, int32_t* out) {
 
 int wb_plan_peer(const wb_plan_t* P, int32_t i, int32_t* peer, int64_t* offset, int64_t* bytes) {
   if (!P || !peer || !offset || !bytes) return set_error(WB_EINVAL, "null argument");
+  const wb::RoundWire& W = P->rounds[0];
   const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
   int n = 0;
   for (int o = 0; o < others; ++o) {
     const size_t k = P->role == WB_SENDER ? size_t(P->rank) * P->n_recv + o : size_t(o) * P->n_recv + P->rank;
-    if (P->send_region[k] < 0) continue;
+    if (W.send_region[k] < 0) continue;
     if (n++ == i) {
       *peer = o;
-      *offset = P->role == WB_SENDER ? P->send_region[k] : P->recv_region[k];
-      *bytes = P->region_bytes[k];
+      *offset = P->role == WB_SENDER ? W.send_region[k] : W.recv_region[k];
+      *bytes = W.region_bytes[k];
       return WB_OK;
     }
   }
   return set_error(WB_EINVAL, "peer index out of range");
 }
 
+int wb_plan_round_region(const wb_plan_t* P, int32_t round, int32_t s, int32_t d, int64_t* send_offset,
+                         int64_t* recv_offset, int64_t* bytes) {
+  if (!P || !send_offset || !recv_offset || !bytes) return set_error(WB_EINVAL, "null argument");
+  if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+  if (s < 0 || s >= P->n_send || d < 0 || d >= P->n_recv) return set_error(WB_EINVAL, "rank out of range");
+  const wb::RoundWire& W = P->rounds[round];
+  const size_t k = size_t(s) * P->n_recv + d;
+  *send_offset = W.send_region[k] < 0 ? 0 : W.send_region[k];
+  *recv_offset = W.recv_region[k] < 0 ? 0 : W.recv_region[k];
+  *bytes = W.region_bytes[k];
+  return WB_OK;
+}
+
 int wb_plan_region(const wb_plan_t* P, int32_t s, int32_t d, int64_t* send_offset, int64_t* recv_offset,
                    int64_t* bytes) {
-  if (!P || !send_offset || !recv_offset || !bytes) return set_error(WB_EINVAL, "null argument");
-  if (s < 0 || s >= P->n_send || d < 0 || d >= P->n_recv) return set_error(WB_EINVAL, "rank out of range");
-  const size_t k = size_t(s) * P->n_recv + d;
-  *send_offset = P->send_region[k] < 0 ? 0 : P->send_region[k];
-  *recv_offset = P->recv_region[k] < 0 ? 0 : P->recv_region[k];
-  *bytes = P->region_bytes[k];
-  return WB_OK;
+  return wb_plan_round_region(P, 0, s, d, send_offset, recv_offset, bytes);
 }
 
 int wb_plan_num_local_tensors(const wb_plan_t* P, int32_t* out) {
@@ -429,57 +467,64 @@ int wb_plan_upload(wb_plan_t* P, void* workspace, size_t bytes, void* stream) {
   });
 }
 
+// One round of a pack (sender) or unpack (receiver): check the pointers, stage
+// the local-tensor table when it changed, launch the round's work items.
+static int run_round(wb_plan_t* P, int round, const void* const* locals, const void* buf, void* stream, int role) {
+  if (P->role != role)
+    return set_error(WB_EINVAL, role == WB_SENDER ? "packing needs a sender plan" : "unpacking needs a receiver plan");
+  if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
+  if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+  if (!locals && P->n_locals > 0) return set_error(WB_EINVAL, "local tensor pointer array is null");
+  const wb::Rank& R = rank_of(P);
+  int rc = check_extent(buf, rank_bytes(P, round, P->role, P->rank), role == WB_SENDER ? "send_buf" : "recv_buf");
+  if (rc != WB_OK) return rc;
+  std::vector<uint64_t> ptrs(P->n_locals + 1, 0);
+  for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(locals[i]);
+  if (ptrs != P->last_ptrs) {
+    for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
+      rc = check_extent(locals[i], local_bytes(R.locals[i]), ("local tensor " + std::to_string(i)).c_str());
+    if (rc != WB_OK) return rc;
+    if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
+  }
+  const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
+  const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
+  int e = wb::launch_tasks(tasks + P->round_tasks[round], P->round_tasks[round + 1] - P->round_tasks[round], table,
+                           buf, stream);
+  if (e != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(e));
+  const auto* blocks = reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks);
+  e = wb::launch_qblocks(blocks + P->round_qblocks[round], P->round_qblocks[round + 1] - P->round_qblocks[round],
+                         reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table, buf, stream);
+  if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
+  return WB_OK;
+}
+
+int wb_pack_round(wb_plan_t* P, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    return run_round(P, round, src_ptrs, send_buf, stream, WB_SENDER);
+  });
+}
+
+int wb_unpack_round(wb_plan_t* P, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    return run_round(P, round, const_cast<const void* const*>(dst_ptrs), recv_buf, stream, WB_RECEIVER);
+  });
+}
+
 int wb_pack(wb_plan_t* P, const void* const* src_ptrs, void* send_buf, void* stream) {
   return guarded([&]() -> int {
     if (!P) return set_error(WB_EINVAL, "null plan");
-    if (P->role != WB_SENDER) return set_error(WB_EINVAL, "wb_pack needs a sender plan");
-    if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
-    if (!src_ptrs && P->n_locals > 0) return set_error(WB_EINVAL, "src_ptrs is null");
-    const wb::Rank& R = rank_of(P);
-    std::vector<uint64_t> ptrs(P->n_locals + 1);
-    ptrs[0] = reinterpret_cast<uint64_t>(send_buf);
-    for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(src_ptrs[i]);
-    if (ptrs != P->last_ptrs) {
-      int rc = check_extent(send_buf, P->send_bytes[P->rank], "send_buf");
-      for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
-        rc = check_extent(src_ptrs[i], local_bytes(R.locals[i]), ("src_ptrs[" + std::to_string(i) + "]").c_str());
-      if (rc != WB_OK) return rc;
-      if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
-    }
-    const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
-    const int e = wb::launch_tasks(reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks),
-                                   static_cast<uint32_t>(P->tasks.size()), table, stream);
-    if (e != 0) return set_error(WB_EHIP, std::string("pack launch: ") + wb::hip_error_string(e));
-    return WB_OK;
+    if (P->rounds.size() != 1) return set_error(WB_EINVAL, "the plan has several rounds: use wb_pack_round");
+    return run_round(P, 0, src_ptrs, send_buf, stream, WB_SENDER);
   });
 }
 
 int wb_unpack(wb_plan_t* P, const void* recv_buf, void* const* dst_ptrs, void* stream) {
   return guarded([&]() -> int {
     if (!P) return set_error(WB_EINVAL, "null plan");
-    if (P->role != WB_RECEIVER) return set_error(WB_EINVAL, "wb_unpack needs a receiver plan");
-    if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
-    if (!dst_ptrs && P->n_locals > 0) return set_error(WB_EINVAL, "dst_ptrs is null");
-    const wb::Rank& R = rank_of(P);
-    std::vector<uint64_t> ptrs(P->n_locals + 1);
-    ptrs[0] = reinterpret_cast<uint64_t>(recv_buf);
-    for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(dst_ptrs[i]);
-    if (ptrs != P->last_ptrs) {
-      int rc = check_extent(recv_buf, P->recv_bytes[P->rank], "recv_buf");
-      for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
-        rc = check_extent(dst_ptrs[i], local_bytes(R.locals[i]), ("dst_ptrs[" + std::to_string(i) + "]").c_str());
-      if (rc != WB_OK) return rc;
-      if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
-    }
-    const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
-    int e = wb::launch_tasks(reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks),
-                             static_cast<uint32_t>(P->tasks.size()), table, stream);
-    if (e != 0) return set_error(WB_EHIP, std::string("unpack launch: ") + wb::hip_error_string(e));
-    e = wb::launch_qblocks(reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks),
-                           static_cast<uint32_t>(P->qblocks.size()),
-                           reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table, stream);
-    if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
-    return WB_OK;
+    if (P->rounds.size() != 1) return set_error(WB_EINVAL, "the plan has several rounds: use wb_unpack_round");
+    return run_round(P, 0, const_cast<const void* const*>(dst_ptrs), recv_buf, stream, WB_RECEIVER);
   });
 }
 

@@ -260,10 +260,10 @@ __device__ void run_transpose16(const Task& t, const char* src, char* dst) {
 }  // namespace
 
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
-                                                            const uint64_t* __restrict__ ptrs) {
+                                                            const uint64_t* __restrict__ ptrs, const char* buf) {
   const Task t = tasks[blockIdx.x];
-  const char* src = reinterpret_cast<const char*>(ptrs[t.src_idx]) + t.src_off;
-  char* dst = reinterpret_cast<char*>(ptrs[t.dst_idx]) + t.dst_off;
+  const char* src = (t.src_idx ? reinterpret_cast<const char*>(ptrs[t.src_idx]) : buf) + t.src_off;
+  char* dst = (t.dst_idx ? reinterpret_cast<char*>(ptrs[t.dst_idx]) : const_cast<char*>(buf)) + t.dst_off;
   switch (t.kind) {
     case TASK_COPY16: run_copy16(t, src, dst); break;
     case TASK_F32_BF16: run_f32_bf16(t, src, dst); break;
@@ -306,12 +306,11 @@ constexpr int kLdsPieces = 32;
 
 __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
                                                              const QPiece* __restrict__ pieces,
-                                                             const uint64_t* __restrict__ ptrs) {
+                                                             const uint64_t* __restrict__ ptrs, const char* recv) {
   __shared__ float wave_max[kThreads / 64];
   __shared__ QPiece lds_pcs[kLdsPieces];
   const QBlock b = blocks[blockIdx.x];
   const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
-  const char* recv = reinterpret_cast<const char*>(ptrs[0]);
   const int cg = (threadIdx.x & 15) * 8;  // first of this thread's 8 columns
   const int rb = threadIdx.x >> 4;        // rows rb, rb + 16, ..., rb + 112
   float v[8][8];
@@ -429,16 +428,18 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, void* stream) {
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_tasks_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), tasks, ptrs);
+  hipLaunchKernelGGL(wb_tasks_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), tasks, ptrs,
+                     static_cast<const char*>(buf));
   return hipGetLastError();
 }
 
-int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, void* stream) {
+int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
+                   void* stream) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(wb_qblock_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), blocks, pieces,
-                     ptrs);
+                     ptrs, static_cast<const char*>(buf));
   return hipGetLastError();
 }
 

@@ -194,10 +194,17 @@ int64_t env_task_bytes() {
 
 void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_plan_t& P) {
   TaskSink sink{P.tasks, env_task_bytes()};
+  const int nrounds = static_cast<int>(P.rounds.size());
+  std::vector<std::vector<const Segment*>> by_round(nrounds);
+  for (const Segment& g : P.segs) by_round[g.round].push_back(&g);
+  P.round_tasks.assign(nrounds + 1, 0);
+  P.round_qblocks.assign(nrounds + 1, 0);
   if (P.role == WB_SENDER) {
     const Rank& R = trainer.ranks[P.rank];
     P.n_locals = static_cast<int>(R.locals.size());
-    for (const Segment& g : P.segs) {
+    for (int k = 0; k < nrounds; ++k) {
+    for (const Segment* gp : by_round[k]) {
+      const Segment& g = *gp;
       if (g.s != P.rank) continue;
       const Placement& sp = R.pls[g.src_pl];
       const int dt = R.locals[sp.u].dtype, es = dtype_bytes(dt);
@@ -212,6 +219,8 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
         const int64_t start = sp.base + (g.x.c0 - sp.c0) * sp.ld + (g.x.r0 - sp.r0);
         sink.transpose_rect(1 + sp.u, uint64_t(start) * es, sp.ld, dt, 0, g.send_off, C, dt, C, Rr);
       }
+    }
+    P.round_tasks[k + 1] = static_cast<uint32_t>(P.tasks.size());
     }
     return;
   }
@@ -233,7 +242,9 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     int64_t e, row0, col0;
   };
   std::vector<Span> qspans;
-  for (const Segment& g : P.segs) {
+  for (int k = 0; k < nrounds; ++k) {
+  for (const Segment* gp : by_round[k]) {
+    const Segment& g = *gp;
     if (g.d != P.rank) continue;
     const Placement& q = R.pls[g.dst_pl];
     const Local& dl = R.locals[q.u];
@@ -266,6 +277,8 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
       sink.transpose_rect(0, g.recv_off, C, sdt, 1 + q.u, uint64_t(start) * ds, q.ld, ddt, Rr, C);
     }
   }
+  P.round_tasks[k + 1] = static_cast<uint32_t>(P.tasks.size());
+  }
   if (nblocks == 0) return;
   // pieces: count per block, prefix, fill (canonical segment order within a block)
   std::vector<uint32_t> count(nblocks + 1, 0);
@@ -283,6 +296,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   P.qpieces.resize(count[nblocks]);
   std::vector<uint32_t> fill(count.begin(), count.end() - 1);
   std::vector<int64_t> area(nblocks, 0);
+  std::vector<int> block_round(nblocks, -1);
   for (const Span& sp : qspans) {
     const Segment& g = *sp.g;
     const Rank& S = trainer.ranks[g.s];
@@ -301,6 +315,8 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
       pc.sdt = static_cast<uint8_t>(sdt);
       P.qpieces[fill[id]++] = pc;
       area[id] += (a1 - a0) * (b1 - b0);
+      if (block_round[id] >= 0 && block_round[id] != g.round) fail(WB_EINVAL, "internal: fp8 block spans rounds");
+      block_round[id] = g.round;
     });
   }
   P.qblocks.resize(nblocks);
@@ -341,6 +357,17 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           P.qblocks[id] = b;
         }
   }
+  // group the blocks by round (stable: canonical block order within a round)
+  std::vector<uint32_t> order(nblocks);
+  std::iota(order.begin(), order.end(), 0u);
+  std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return block_round[a] < block_round[b]; });
+  std::vector<QBlock> sorted(nblocks);
+  for (int64_t i = 0; i < nblocks; ++i) {
+    sorted[i] = P.qblocks[order[i]];
+    P.round_qblocks[block_round[order[i]] + 1] = static_cast<uint32_t>(i + 1);
+  }
+  for (int k = 0; k < nrounds; ++k) P.round_qblocks[k + 1] = std::max(P.round_qblocks[k + 1], P.round_qblocks[k]);
+  P.qblocks.swap(sorted);
 }
 
 // Every byte a work item touches lies inside its buffer, and vector work items
@@ -348,13 +375,18 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
 // aligned, which wb_pack / wb_unpack check). Run on every plan.
 void check_work(const wb_plan_t& P, const Rank& R) {
   std::vector<int64_t> size(R.locals.size() + 1);
-  size[0] = P.role == WB_SENDER ? P.send_bytes[P.rank] : P.recv_bytes[P.rank];
   for (size_t u = 0; u < R.locals.size(); ++u) size[u + 1] = R.locals[u].numel() * dtype_bytes(R.locals[u].dtype);
   auto inside = [&](int idx, uint64_t off, uint64_t len, const char* what) {
     if (idx < 0 || idx >= static_cast<int>(size.size()) || len == 0 || off + len > uint64_t(size[idx]))
       fail(WB_EINVAL, std::string("internal: ") + what + " work item out of bounds");
   };
-  for (const Task& t : P.tasks) {
+  if (P.round_tasks.size() != P.rounds.size() + 1 || P.round_tasks.back() != P.tasks.size() ||
+      P.round_qblocks.size() != P.rounds.size() + 1 || P.round_qblocks.back() != P.qblocks.size())
+    fail(WB_EINVAL, "internal: round ranges");
+  for (size_t k = 0; k < P.rounds.size(); ++k) {
+  size[0] = P.role == WB_SENDER ? P.rounds[k].send_bytes[P.rank] : P.rounds[k].recv_bytes[P.rank];
+  for (uint32_t ti = P.round_tasks[k]; ti < P.round_tasks[k + 1]; ++ti) {
+    const Task& t = P.tasks[ti];
     if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
     const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
     switch (t.kind) {
@@ -390,7 +422,8 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         fail(WB_EINVAL, "internal: unknown work item");
     }
   }
-  for (const QBlock& b : P.qblocks) {
+  for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
+    const QBlock& b = P.qblocks[bi];
     const uint64_t rows = b.rows_m1 + 1u, cols = b.cols_m1 + 1u;
     inside(b.dst_idx, b.dst_off, (rows - 1) * b.dst_ld + cols, "fp8 block");
     inside(b.scale_idx, uint64_t(b.scale_off) * 4, 4, "fp8 scale");
@@ -412,11 +445,147 @@ void check_work(const wb_plan_t& P, const Rank& R) {
       inside(0, q.src_off, (uint64_t(q.r1m1 - q.r0) * q.src_ld + (q.c1m1 - q.c0) + 1) * es, "fp8 piece");
     }
   }
+  }
+}
+
+// ---- rounds (Sec. 3.2 round-based transfer; App. D buffer budget) --------
+
+// Unit of every checkpoint tensor: tensors whose images in one quantised
+// destination matrix touch a common block share a unit, so no fp8 block is
+// fed from two rounds.
+std::vector<int> block_units(const wb_layout_t& rollout, int ntensors) {
+  std::vector<int> parent(ntensors);
+  std::iota(parent.begin(), parent.end(), 0);
+  auto find = [&](int a) {
+    while (parent[a] != a) a = parent[a] = parent[parent[a]];
+    return a;
+  };
+  struct Img {
+    int64_t bi0, bi1, bj0, bj1;
+    int t;
+  };
+  for (const Rank& R : rollout.ranks) {
+    std::map<std::pair<int, int64_t>, std::vector<Img>> per_matrix;
+    for (const Placement& p : R.pls) {
+      const Local& l = R.locals[p.u];
+      if (l.block <= 0) continue;
+      const int64_t mat = l.rows * l.cols;
+      const int64_t e = p.base / mat, row0 = (p.base % mat) / l.cols, col0 = p.base % l.cols;
+      if (p.tr || col0 + p.cols() > l.cols || row0 + p.rows() > l.rows || (p.rows() > 1 && p.ld != l.cols))
+        fail(WB_EUNSUPPORTED, "an fp8 placement must be a non-transposed sub-rectangle of one matrix");
+      const int64_t B = l.block;
+      per_matrix[{p.u, e}].push_back({row0 / B, (row0 + p.rows() - 1) / B, col0 / B, (col0 + p.cols() - 1) / B, p.t});
+    }
+    for (auto& kv : per_matrix) {
+      const std::vector<Img>& v = kv.second;
+      for (size_t a = 0; a < v.size(); ++a)
+        for (size_t b = a + 1; b < v.size(); ++b)
+          if (v[a].bi0 <= v[b].bi1 && v[b].bi0 <= v[a].bi1 && v[a].bj0 <= v[b].bj1 && v[b].bj0 <= v[a].bj1)
+            parent[find(v[a].t)] = find(v[b].t);
+    }
+  }
+  std::vector<int> unit(ntensors);
+  for (int t = 0; t < ntensors; ++t) unit[t] = find(t);
+  return unit;
+}
+
+// Greedy rounds over units in order of their first tensor; returns the count.
+int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::vector<Segment>& segs,
+                  int64_t budget) {
+  const int nt = static_cast<int>(trainer.catalog.size());
+  const std::vector<int> unit = block_units(rollout, nt);
+  std::vector<std::vector<size_t>> members(nt);  // indexed by unit root
+  std::vector<int> first(nt, nt);
+  for (size_t i = 0; i < segs.size(); ++i) {
+    const int u = unit[segs[i].t];
+    members[u].push_back(i);
+    first[u] = std::min(first[u], segs[i].t);
+  }
+  std::vector<int> order;
+  for (int u = 0; u < nt; ++u)
+    if (!members[u].empty()) order.push_back(u);
+  std::sort(order.begin(), order.end(), [&](int a, int b) { return first[a] < first[b]; });
+  const size_t ns = trainer.ranks.size(), nd = rollout.ranks.size();
+  std::vector<int64_t> cur_s(ns, 0), cur_d(nd, 0), add_s(ns, 0), add_d(nd, 0);
+  bool empty = true;
+  int rnd = 0;
+  for (int u : order) {
+    std::vector<int> ts, td;
+    for (size_t i : members[u]) {
+      const Segment& g = segs[i];
+      if (add_s[g.s] == 0) ts.push_back(g.s);
+      if (add_d[g.d] == 0) td.push_back(g.d);
+      add_s[g.s] += g.bytes;
+      add_d[g.d] += g.bytes;
+    }
+    bool over = false;
+    for (int s : ts) over = over || cur_s[s] + add_s[s] > budget;
+    for (int d : td) over = over || cur_d[d] + add_d[d] > budget;
+    if (over && !empty) {
+      ++rnd;
+      std::fill(cur_s.begin(), cur_s.end(), 0);
+      std::fill(cur_d.begin(), cur_d.end(), 0);
+    }
+    for (int s : ts) cur_s[s] += add_s[s], add_s[s] = 0;
+    for (int d : td) cur_d[d] += add_d[d], add_d[d] = 0;
+    empty = false;
+    for (size_t i : members[u]) segs[i].round = rnd;
+  }
+  return rnd + 1;
+}
+
+// Wire offsets of round k (segments in canonical order, payloads at multiples
+// of 256 bytes within their region, regions at multiples of 4096 bytes).
+void wire_round(wb_plan_t& P, int k) {
+  const int ns = P.n_send, nd = P.n_recv;
+  RoundWire& W = P.rounds[k];
+  std::vector<int64_t> end(size_t(ns) * nd, -1);
+  for (Segment& g : P.segs) {
+    if (g.round != k) continue;
+    int64_t& e = end[size_t(g.s) * nd + g.d];
+    const int64_t off = e < 0 ? 0 : align_up(e, kPayloadAlign);
+    g.send_off = g.recv_off = off;
+    e = off + g.bytes;
+  }
+  W.region_bytes.assign(size_t(ns) * nd, 0);
+  W.send_region.assign(size_t(ns) * nd, -1);
+  W.recv_region.assign(size_t(ns) * nd, -1);
+  W.send_bytes.assign(ns, 0);
+  W.recv_bytes.assign(nd, 0);
+  for (int s = 0; s < ns; ++s) {
+    int64_t pos = 0;
+    for (int d = 0; d < nd; ++d) {
+      const int64_t b = end[size_t(s) * nd + d];
+      if (b < 0) continue;
+      pos = align_up(pos, kRegionAlign);
+      W.send_region[size_t(s) * nd + d] = pos;
+      W.region_bytes[size_t(s) * nd + d] = b;
+      pos += b;
+    }
+    W.send_bytes[s] = pos;
+  }
+  for (int d = 0; d < nd; ++d) {
+    int64_t pos = 0;
+    for (int s = 0; s < ns; ++s) {
+      const int64_t b = end[size_t(s) * nd + d];
+      if (b < 0) continue;
+      pos = align_up(pos, kRegionAlign);
+      W.recv_region[size_t(s) * nd + d] = pos;
+      pos += b;
+    }
+    W.recv_bytes[d] = pos;
+  }
+  for (Segment& g : P.segs) {
+    if (g.round != k) continue;
+    g.send_off += W.send_region[size_t(g.s) * nd + g.d];
+    g.recv_off += W.recv_region[size_t(g.s) * nd + g.d];
+  }
 }
 
 }  // namespace
 
-void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, wb_plan_t& P) {
+void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, int64_t round_budget,
+                wb_plan_t& P) {
   if (role != WB_SENDER && role != WB_RECEIVER) fail(WB_EINVAL, "role must be WB_SENDER or WB_RECEIVER");
   const int ns = static_cast<int>(trainer.ranks.size()), nd = static_cast<int>(rollout.ranks.size());
   if (ns < 1 || nd < 1) fail(WB_EINVAL, "layouts need at least one rank");
@@ -538,48 +707,12 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
     }
   }
 
-  // 4. wire offsets
+  // 5. rounds, then 4. wire offsets per round
   P.n_send = ns;
   P.n_recv = nd;
-  std::vector<int64_t> end(size_t(ns) * nd, -1);
-  for (Segment& g : P.segs) {
-    int64_t& e = end[size_t(g.s) * nd + g.d];
-    const int64_t off = e < 0 ? 0 : align_up(e, kPayloadAlign);
-    g.send_off = g.recv_off = off;
-    e = off + g.bytes;
-  }
-  P.region_bytes.assign(size_t(ns) * nd, 0);
-  P.send_region.assign(size_t(ns) * nd, -1);
-  P.recv_region.assign(size_t(ns) * nd, -1);
-  P.send_bytes.assign(ns, 0);
-  P.recv_bytes.assign(nd, 0);
-  for (int s = 0; s < ns; ++s) {
-    int64_t pos = 0;
-    for (int d = 0; d < nd; ++d) {
-      const int64_t b = end[size_t(s) * nd + d];
-      if (b < 0) continue;
-      pos = align_up(pos, kRegionAlign);
-      P.send_region[size_t(s) * nd + d] = pos;
-      P.region_bytes[size_t(s) * nd + d] = b;
-      pos += b;
-    }
-    P.send_bytes[s] = pos;
-  }
-  for (int d = 0; d < nd; ++d) {
-    int64_t pos = 0;
-    for (int s = 0; s < ns; ++s) {
-      const int64_t b = end[size_t(s) * nd + d];
-      if (b < 0) continue;
-      pos = align_up(pos, kRegionAlign);
-      P.recv_region[size_t(s) * nd + d] = pos;
-      pos += b;
-    }
-    P.recv_bytes[d] = pos;
-  }
-  for (Segment& g : P.segs) {
-    g.send_off += P.send_region[size_t(g.s) * nd + g.d];
-    g.recv_off += P.recv_region[size_t(g.s) * nd + g.d];
-  }
+  const int nrounds = round_budget > 0 ? assign_rounds(trainer, rollout, P.segs, round_budget) : 1;
+  P.rounds.assign(nrounds, RoundWire{});
+  for (int k = 0; k < nrounds; ++k) wire_round(P, k);
 
   P.role = role;
   P.rank = rank;
@@ -589,12 +722,28 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
 
 std::string dump_plan(const wb_plan_t& P) {
   std::ostringstream o;
-  o << "plan trainer_ranks=" << P.n_send << " rollout_ranks=" << P.n_recv << " segments=" << P.segs.size() << "\n";
-  for (int s = 0; s < P.n_send; ++s) o << "send " << s << " " << P.send_bytes[s] << "\n";
-  for (int d = 0; d < P.n_recv; ++d) o << "recv " << d << " " << P.recv_bytes[d] << "\n";
-  for (const Segment& g : P.segs)
+  auto seg = [&](const Segment& g) {
     o << "seg " << g.s << " " << g.d << " " << g.t << " " << g.x.r0 << " " << g.x.r1 << " " << g.x.c0 << " " << g.x.c1
       << " " << g.src_pl << " " << g.dst_pl << " " << g.send_off << " " << g.recv_off << " " << g.bytes << "\n";
+  };
+  auto sizes = [&](const RoundWire& W) {
+    for (int s = 0; s < P.n_send; ++s) o << "send " << s << " " << W.send_bytes[s] << "\n";
+    for (int d = 0; d < P.n_recv; ++d) o << "recv " << d << " " << W.recv_bytes[d] << "\n";
+  };
+  o << "plan trainer_ranks=" << P.n_send << " rollout_ranks=" << P.n_recv << " segments=" << P.segs.size();
+  if (P.rounds.size() == 1) {
+    o << "\n";
+    sizes(P.rounds[0]);
+    for (const Segment& g : P.segs) seg(g);
+    return o.str();
+  }
+  o << " rounds=" << P.rounds.size() << "\n";
+  for (size_t k = 0; k < P.rounds.size(); ++k) {
+    o << "round " << k << "\n";
+    sizes(P.rounds[k]);
+    for (const Segment& g : P.segs)
+      if (g.round == static_cast<int>(k)) seg(g);
+  }
   return o.str();
 }
 

@@ -87,7 +87,15 @@ struct Segment {
   Rect x;
   int src_pl, dst_pl;
   int64_t bytes;
-  int64_t send_off = 0, recv_off = 0;
+  int64_t send_off = 0, recv_off = 0;  // within the segment's round
+  int round = 0;
+};
+
+// Wire layout of one round: per-rank buffer sizes and per-(sender, receiver)
+// region offsets and sizes, indexed [s * n_recv + d] (-1 when the pair is idle).
+struct RoundWire {
+  std::vector<int64_t> send_bytes, recv_bytes;
+  std::vector<int64_t> send_region, recv_region, region_bytes;
 };
 
 // Work item of the copy/cast kernel: a rows x cols block of elements.
@@ -147,16 +155,16 @@ struct wb_plan_t {
   // global plan
   int n_send = 0, n_recv = 0;
   std::vector<wb::Segment> segs;
-  std::vector<int64_t> send_bytes, recv_bytes;
-  std::vector<int64_t> send_region, recv_region, region_bytes;  // [s * n_recv + d]
+  std::vector<wb::RoundWire> rounds;
   // view of one rank
   int role = WB_SENDER, rank = 0;
   int n_locals = 0;
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
-  std::vector<wb::Task> tasks;
-  std::vector<wb::QBlock> qblocks;
+  std::vector<wb::Task> tasks;          // grouped by round
+  std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
+  std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
   // copies of the two layouts used for dumps and queries
   wb_layout_t trainer, rollout;
   // device state after wb_plan_upload
@@ -174,10 +182,13 @@ void describe(const wb_model_shapes& m, const wb_parallelism& p, wb_layout_t& ou
 void check_placement(const wb_layout_t& L, int rank, const Placement& p);
 std::string dump_layout(const wb_layout_t& L);
 // plan.cpp
-void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, wb_plan_t& out);
+void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, int64_t round_budget,
+                wb_plan_t& out);
 std::string dump_plan(const wb_plan_t& P);
 // kernels.hip
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, void* stream);
-int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, void* stream);
+// ptrs[1 + u] is local tensor u; work items with index 0 use buf.
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, void* stream);
+int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
+                   void* stream);
 const char* hip_error_string(int err);
 }  // namespace wb

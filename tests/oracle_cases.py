@@ -64,3 +64,20 @@ def id_values(catalog):
         out.append(np.arange(off, off + t.numel, dtype=np.int64).reshape(t.rows, t.cols))
         off += t.numel
     return out
+
+
+def hand_rounds_pair():
+    """The layout pair of tests/golden/hand_plan_rounds.txt."""
+    cat = [CkptTensor("T0", 4, 6), CkptTensor("T1", 2, 8), CkptTensor("T2", 1, 16), CkptTensor("A", 1, 4),
+           CkptTensor("B", 2, 4)]
+    tl = [Local("t0", "f32", 1, 4, 6), Local("t1", "f32", 1, 2, 8), Local("t2", "f32", 1, 1, 16),
+          Local("a", "f32", 1, 1, 4), Local("b", "f32", 1, 2, 4)]
+    tp = [Placement(0, 0, 4, 0, 6, 0, 0, 6), Placement(1, 0, 2, 0, 8, 1, 0, 8), Placement(2, 0, 1, 0, 16, 2, 0, 16),
+          Placement(3, 0, 1, 0, 4, 3, 0, 4), Placement(4, 0, 2, 0, 4, 4, 0, 4)]
+    trainer = Layout(cat, [RankLayout(tl, tp)])
+    rl = [Local("x0", "bf16", 1, 4, 6), Local("x1", "bf16", 1, 2, 8), Local("x2", "bf16", 1, 1, 16),
+          Local("q", "f8e4m3", 1, 3, 4, 2, scale=4), Local("q_scale", "f32", 1, 2, 2, scales=3)]
+    rp = [Placement(0, 0, 4, 0, 6, 0, 0, 6), Placement(1, 0, 2, 0, 8, 1, 0, 8), Placement(2, 0, 1, 0, 16, 2, 0, 16),
+          Placement(3, 0, 1, 0, 4, 3, 0, 4), Placement(4, 0, 2, 0, 4, 3, 4, 4)]
+    rollout = Layout(cat, [RankLayout(rl, rp)])
+    return trainer, rollout

@@ -148,3 +148,53 @@ def test_error_paths():
     p = wb.Plan(tr, ro, wb.RECEIVER, 0)
     _expect(wb.WB_EINVAL, p.unpack, 0, [0] * p.num_local_tensors, 0)
     _expect(wb.WB_EINVAL, p.pack, [0] * p.num_local_tensors, 0, 0)
+
+
+def test_hand_rounds_golden():
+    from oracle_cases import hand_rounds_pair
+    tr, ro = hand_rounds_pair()
+    golden = "".join(l for l in open(os.path.join(ROOT, "tests", "golden", "hand_plan_rounds.txt"))
+                     if not l.startswith("#"))
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0, round_budget=160)
+    assert p.dump() == golden
+    assert p.num_rounds == 2 and p.round_buffer_bytes(0) == 320 and p.round_buffer_bytes(1) == 544
+    assert p.buffer_bytes == 544
+    assert p.round_region(1, 0, 0) == (0, 0, 544)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_round_plans_equal_oracle(seed):
+    rng = np.random.default_rng(700 + seed)
+    m = random_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout"))
+    budget = int(rng.integers(64, 8192))
+    want = dump(build_plan(otr, oro, round_budget=budget))
+    tr, ro = to_wb(otr), to_wb(oro)
+    assert wb.Plan(tr, ro, wb.RECEIVER, int(rng.integers(0, oro.nranks)), round_budget=budget).dump() == want
+    assert wb.Plan(tr, ro, wb.SENDER, int(rng.integers(0, otr.nranks)), round_budget=budget).dump() == want
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_workload_round_plans_equal_oracle(name):
+    for w, budgets in ((scaled(name), (3000, 50000)), (WORKLOADS[name], (1 << 30, 4 << 30))):
+        tr = wb.Layout.describe(w["model"], w["trainer"])
+        ro = wb.Layout.describe(w["model"], w["rollout"])
+        otr = layout_from_spec(w["model"], w["trainer"])
+        oro = layout_from_spec(w["model"], w["rollout"])
+        for b in budgets:
+            want = dump(build_plan(otr, oro, round_budget=b))
+            p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=b)
+            assert p.dump() == want, (name, b)
+            assert wb.Plan(tr, ro, wb.SENDER, w["pack_rank"], round_budget=b).dump() == want
+
+
+def test_round_calls_need_round_plans():
+    w = scaled("llama3_8b_fsdp8_to_tp1")
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0, round_budget=50000)
+    assert p.num_rounds > 1
+    _expect(wb.WB_EINVAL, p.unpack, 0, [0] * p.num_local_tensors, 0)       # not uploaded, and several rounds
+    _expect(wb.WB_EINVAL, p.unpack_round, p.num_rounds, 0, [0] * p.num_local_tensors, 0)
+    _expect(wb.WB_EINVAL, wb.Plan, tr, ro, wb.RECEIVER, 0, -1)
