@@ -235,7 +235,9 @@ int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
 /* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */
 int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* write_bytes);
 /* The same split by launch: launch 0 is the copy/cast kernel, launch 1 the fp8
- * block kernel (receivers with fp8 tensors only; 0 otherwise). */
+ * block kernel (receivers with fp8 tensors only; 0 otherwise); launches 2 and 3
+ * are the forward packings of exchange stages 1 and 2 over all rounds
+ * (receivers of three-stage plans; 0 otherwise). */
 int wb_plan_kernel_traffic(const wb_plan_t* plan, int32_t launch, int64_t* read_bytes, int64_t* write_bytes);
 /* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
 int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
@@ -273,6 +275,57 @@ int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void
  * wb_pack / wb_unpack refuse (WB_EINVAL) plans with more than one round. */
 int wb_pack_round(wb_plan_t* plan, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream);
 int wb_unpack_round(wb_plan_t* plan, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream);
+
+/* ---- three-stage plans: rollout-side de-duplication and exchange ------ */
+
+/* The plan of wb_plan_rounds plus rollout-side de-duplication and the two
+ * exchange stages (Sec. 3.2: each rollout node should take in one copy of what
+ * it needs over the inter-node network and share it inside the node; Figure 5).
+ * node_size > 0 groups rollout ranks into nodes of node_size consecutive ranks
+ * (node_size == 0 gives exactly wb_plan_rounds). Rules on top of wb_plan's:
+ *   rollout groups : identical rollout rectangles of a tensor held by m > 1
+ *                    ranks are cut into m parts by wb_plan's split rule and
+ *                    handed out over the holders by its deficit rule counted in
+ *                    elements (groups taken when their lowest holder's
+ *                    placement is visited); in the receive stage (0) every
+ *                    holder asks the trainers for its parts only;
+ *   external (1)   : every stage-0 segment of such a group is forwarded, byte
+ *                    for byte, to one holder in each other node: position
+ *                    (i mod n_v) of that node's holder list, where i is the
+ *                    position of the forwarding rank in its own node's list;
+ *   internal (2)   : every stage-0 and stage-1 segment of such a group is
+ *                    forwarded to each other holder in the receiver's node.
+ * Forwarded payloads keep the trainer dtype. A rollout rank's receive buffer
+ * holds the stage-0 regions, then the stage-1 regions, then the stage-2
+ * regions, each non-empty section starting at a multiple of 4096 bytes; every
+ * forwarding rank has one forward buffer per exchange stage, laid out like a
+ * send buffer. wb_plan_round_buffer_bytes of a receiver covers all sections;
+ * wb_unpack_round reads all of them, so it runs after both exchange stages of
+ * the round have landed.
+ * Errors: as wb_plan_rounds; WB_EINVAL for a negative node size or a rollout
+ * rank holding one rectangle twice. */
+int wb_plan_exchange(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
+                     int64_t round_budget, int32_t node_size, wb_plan_t** out);
+int wb_plan_node_size(const wb_plan_t* plan, int32_t* out);
+/* Region of a (sender, receiver) pair in one stage of one round: stage 0 as
+ * wb_plan_round_region; stages 1 and 2 pair rollout ranks, send_offset in the
+ * sender's forward buffer of that stage, recv_offset in the receiver's whole
+ * receive buffer. bytes is 0 when the pair exchanges nothing. */
+int wb_plan_stage_region(const wb_plan_t* plan, int32_t round, int32_t stage, int32_t sender, int32_t receiver,
+                         int64_t* send_offset, int64_t* recv_offset, int64_t* bytes);
+/* This receiver's forward buffer size for exchange stage 1 or 2 in one round
+ * (round -1: the largest over the rounds); 0 for senders. */
+int wb_plan_forward_bytes(const wb_plan_t* plan, int32_t round, int32_t stage, int64_t* out);
+/* Enqueue the forward packing of a receiver plan for exchange stage 1 or 2 of
+ * one round: every payload this rank forwards in that stage is copied from
+ * where it landed in recv_buf (wb_plan_round_buffer_bytes) to its offset in
+ * fwd_buf (wb_plan_forward_bytes). One launch of the copy kernel; nothing is
+ * enqueued (and the buffers are not checked) when the rank forwards nothing.
+ * Stage 1 reads the stage-0 section, stage 2 the stage-0 and stage-1 sections,
+ * so each must have landed. Errors as for wb_pack; wb_plan_kernel_traffic
+ * launches 2 and 3 give its algorithmic bytes. */
+int wb_forward_round(wb_plan_t* plan, int32_t round, int32_t stage, const void* recv_buf, void* fwd_buf,
+                     void* stream);
 
 void wb_plan_destroy(wb_plan_t* plan);
 

@@ -55,7 +55,7 @@ def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray], rnd: int = 0) -> 
     buf = np.zeros((rounds[rnd].send_bytes if rounds[rnd] else plan.send_bytes)[s], dtype=np.uint8)
     rk = plan.trainer.ranks[s]
     for g in plan.segments:
-        if g.s != s or g.round != rnd:
+        if g.s != s or g.round != rnd or g.stage != 0:
             continue
         p = rk.placements[g.src_pl]
         lc = rk.locals[p.u]
@@ -67,15 +67,46 @@ def pack(plan: Plan, s: int, trainer_locals: list[np.ndarray], rnd: int = 0) -> 
     return buf
 
 
-def network(plan: Plan, d: int, send_bufs: dict[int, np.ndarray], rnd: int = 0) -> np.ndarray:
-    """Receive buffer of rollout rank d in round ``rnd``: each sender's region
-    for d, copied."""
+def network(plan: Plan, d: int, send_bufs: dict[int, np.ndarray], rnd: int = 0, stage: int = 0,
+            into: np.ndarray | None = None) -> np.ndarray:
+    """Receive buffer of rollout rank d in round ``rnd`` after ``stage``: each
+    sender's region for d in that stage copied into its section (into
+    ``into`` when given, else into a new zeroed buffer). Stage 0 senders are
+    trainer ranks; exchange-stage senders are rollout ranks and ``send_bufs``
+    holds their forward buffers of that stage."""
     rounds = plan.rounds or [None]
-    buf = np.zeros((rounds[rnd].recv_bytes if rounds[rnd] else plan.recv_bytes)[d], dtype=np.uint8)
+    buf = into if into is not None else np.zeros(
+        (rounds[rnd].recv_bytes if rounds[rnd] else plan.recv_bytes)[d], dtype=np.uint8)
     for g in plan.segments:
-        if g.d == d and g.round == rnd:
+        if g.d == d and g.round == rnd and g.stage == stage:
             buf[g.recv_off:g.recv_off + g.nbytes] = send_bufs[g.s][g.send_off:g.send_off + g.nbytes]
     return buf
+
+
+def forward(plan: Plan, r: int, recv_buf: np.ndarray, stage: int, rnd: int = 0) -> np.ndarray:
+    """Forward buffer of rollout rank r for exchange ``stage`` (1 external, 2
+    internal) in round ``rnd``: each forwarded segment's bytes, copied from
+    where r received them, at the segment's send offset."""
+    buf = np.zeros(plan.rounds[rnd].fwd_bytes[stage - 1][r], dtype=np.uint8)
+    for g in plan.segments:
+        if g.s == r and g.round == rnd and g.stage == stage:
+            buf[g.send_off:g.send_off + g.nbytes] = recv_buf[g.src_off:g.src_off + g.nbytes]
+    return buf
+
+
+def run_stages(plan: Plan, trainer_locals: dict[int, list[np.ndarray]], rnd: int = 0) -> dict[int, np.ndarray]:
+    """Every rollout rank's receive buffer for round ``rnd`` after the receive
+    stage and, for plans with exchange stages, the external and internal
+    exchanges, each stage starting when the previous one has landed."""
+    nd = plan.rollout.nranks
+    sends = {s: pack(plan, s, trainer_locals[s], rnd) for s in trainer_locals}
+    recv = {d: network(plan, d, sends, rnd) for d in range(nd)}
+    if plan.node_size:
+        for stage in (1, 2):
+            fwd = {r: forward(plan, r, recv[r], stage, rnd) for r in range(nd)}
+            for d in range(nd):
+                network(plan, d, fwd, rnd, stage, into=recv[d])
+    return recv
 
 
 def _convert(codes: np.ndarray, src: str, dst: str) -> np.ndarray:
@@ -127,8 +158,7 @@ def unpack(plan: Plan, d: int, recv_buf, rounds=None) -> list[np.ndarray]:
         recv_buf = bufs[g.round]
         q = rk.placements[g.dst_pl]
         lc = rk.locals[q.u]
-        sp = plan.trainer.ranks[g.s].placements[g.src_pl]
-        src_dtype = plan.trainer.ranks[g.s].locals[sp.u].dtype
+        src_dtype = g.wire                                       # the trainer dtype the bytes travel in
         r = g.rect
         payload = recv_buf[g.recv_off:g.recv_off + g.nbytes].view(CODE_DTYPE[src_dtype])
         payload = payload.reshape(r.r1 - r.r0, r.c1 - r.c0)

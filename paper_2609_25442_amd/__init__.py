@@ -103,6 +103,12 @@ def _load():
         "wb_plan_upload": [P, c_void_p, c_size_t, c_void_p],
         "wb_pack": [P, POINTER(c_void_p), c_void_p, c_void_p],
         "wb_unpack": [P, c_void_p, POINTER(c_void_p), c_void_p],
+        "wb_plan_exchange": [L, L, c_int32, c_int32, c_int64, c_int32, POINTER(P)],
+        "wb_plan_node_size": [P, POINTER(c_int32)],
+        "wb_plan_stage_region": [P, c_int32, c_int32, c_int32, c_int32, POINTER(c_int64), POINTER(c_int64),
+                                 POINTER(c_int64)],
+        "wb_plan_forward_bytes": [P, c_int32, c_int32, POINTER(c_int64)],
+        "wb_forward_round": [P, c_int32, c_int32, c_void_p, c_void_p, c_void_p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -262,9 +268,10 @@ class Layout:
 class Plan:
     """The global routing plan seen from one rank (a sender or a receiver)."""
 
-    def __init__(self, trainer: Layout, rollout: Layout, role: int, rank: int, round_budget: int = 0):
+    def __init__(self, trainer: Layout, rollout: Layout, role: int, rank: int, round_budget: int = 0,
+                 node_size: int = 0):
         h = c_void_p()
-        _check(lib.wb_plan_rounds(trainer._h, rollout._h, role, rank, round_budget, byref(h)))
+        _check(lib.wb_plan_exchange(trainer._h, rollout._h, role, rank, round_budget, node_size, byref(h)))
         self._h = h
         self._destroy = lib.wb_plan_destroy
         _live.add(self)
@@ -318,6 +325,28 @@ class Plan:
         ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
         _check(lib.wb_unpack_round(self._h, rnd, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
+    @property
+    def node_size(self) -> int:
+        v = c_int32()
+        _check(lib.wb_plan_node_size(self._h, byref(v)))
+        return v.value
+
+    def stage_region(self, rnd: int, stage: int, sender: int, receiver: int):
+        """(offset in the sender's send or forward buffer, offset in the
+        receiver's receive buffer, bytes) of one stage of one round."""
+        s, r, b = c_int64(), c_int64(), c_int64()
+        _check(lib.wb_plan_stage_region(self._h, rnd, stage, sender, receiver, byref(s), byref(r), byref(b)))
+        return s.value, r.value, b.value
+
+    def forward_bytes(self, stage: int, rnd: int = -1) -> int:
+        v = c_int64()
+        _check(lib.wb_plan_forward_bytes(self._h, rnd, stage, byref(v)))
+        return v.value
+
+    def forward_round(self, rnd, stage, recv_buf, fwd_buf, stream=None):
+        _check(lib.wb_forward_round(self._h, rnd, stage, _ptr(recv_buf), _ptr(fwd_buf) if fwd_buf is not None else 0,
+                                    _stream_handle(stream)))
+
     def rank_buffer_bytes(self, role: int, rank: int) -> int:
         v = c_int64()
         _check(lib.wb_plan_rank_buffer_bytes(self._h, role, rank, byref(v)))
@@ -346,7 +375,8 @@ class Plan:
         return r.value, w.value
 
     def kernel_traffic(self, launch: int):
-        """(read, write) algorithmic bytes of launch 0 (copy/cast) or 1 (fp8 blocks)."""
+        """(read, write) algorithmic bytes of launch 0 (copy/cast), 1 (fp8 blocks),
+        2 or 3 (forward packing of exchange stage 1 or 2)."""
         r, w = c_int64(), c_int64()
         _check(lib.wb_plan_kernel_traffic(self._h, launch, byref(r), byref(w)))
         return r.value, w.value

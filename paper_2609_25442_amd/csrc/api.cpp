@@ -250,15 +250,16 @@ int wb_layout_dump(const wb_layout_t* L, char* buf, size_t cap, size_t* needed) 
 
 void wb_layout_destroy(wb_layout_t* L) { delete L; }
 
-int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
-                   int64_t round_budget, wb_plan_t** out) {
+int wb_plan_exchange(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
+                     int64_t round_budget, int32_t node_size, wb_plan_t** out) {
   return guarded([&]() -> int {
     if (!trainer || !rollout || !out) return set_error(WB_EINVAL, "null argument");
     if (round_budget < 0) return set_error(WB_EINVAL, "round budget must be >= 0");
+    if (node_size < 0) return set_error(WB_EINVAL, "node size must be >= 0");
     *out = nullptr;
     auto* P = new wb_plan_t;
     try {
-      wb::build_plan(*trainer, *rollout, role, rank, round_budget, *P);
+      wb::build_plan(*trainer, *rollout, role, rank, round_budget, node_size, *P);
       P->trainer = *trainer;
       P->rollout = *rollout;
       const wb::Rank& R = rank_of(P);
@@ -274,8 +275,19 @@ int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32
   });
 }
 
+int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
+                   int64_t round_budget, wb_plan_t** out) {
+  return wb_plan_exchange(trainer, rollout, role, rank, round_budget, 0, out);
+}
+
 int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank, wb_plan_t** out) {
-  return wb_plan_rounds(trainer, rollout, role, rank, 0, out);
+  return wb_plan_exchange(trainer, rollout, role, rank, 0, 0, out);
+}
+
+int wb_plan_node_size(const wb_plan_t* P, int32_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  *out = P->node_size;
+  return WB_OK;
 }
 
 int wb_plan_num_segments(const wb_plan_t* P, int64_t* out) {
@@ -291,7 +303,7 @@ int wb_plan_num_rounds(const wb_plan_t* P, int32_t* out) {
 }
 
 static int64_t rank_bytes(const wb_plan_t* P, size_t k, int role, int rank) {
-  return role == WB_SENDER ? P->rounds[k].send_bytes[rank] : P->rounds[k].recv_bytes[rank];
+  return role == WB_SENDER ? P->rounds[k].st[0].send_bytes[rank] : P->rounds[k].recv_total[rank];
 }
 
 int wb_plan_round_buffer_bytes(const wb_plan_t* P, int32_t round, int64_t* out) {
@@ -321,7 +333,7 @@ int wb_plan_rank_buffer_bytes(const wb_plan_t* P, int32_t role, int32_t rank, in
 
 int wb_plan_num_peers(const wb_plan_t* P, int32_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
-  const wb::RoundWire& W = P->rounds[0];
+  const wb::StageWire& W = P->rounds[0].st[0];
   int n = 0;
   const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
   for (int o = 0; o < others; ++o) {
@@ -334,7 +346,7 @@ int wb_plan_num_peers(const wb_plan_t* P, int32_t* out) {
 
 int wb_plan_peer(const wb_plan_t* P, int32_t i, int32_t* peer, int64_t* offset, int64_t* bytes) {
   if (!P || !peer || !offset || !bytes) return set_error(WB_EINVAL, "null argument");
-  const wb::RoundWire& W = P->rounds[0];
+  const wb::StageWire& W = P->rounds[0].st[0];
   const int others = P->role == WB_SENDER ? P->n_recv : P->n_send;
   int n = 0;
   for (int o = 0; o < others; ++o) {
@@ -355,11 +367,38 @@ int wb_plan_round_region(const wb_plan_t* P, int32_t round, int32_t s, int32_t d
   if (!P || !send_offset || !recv_offset || !bytes) return set_error(WB_EINVAL, "null argument");
   if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
   if (s < 0 || s >= P->n_send || d < 0 || d >= P->n_recv) return set_error(WB_EINVAL, "rank out of range");
-  const wb::RoundWire& W = P->rounds[round];
+  const wb::StageWire& W = P->rounds[round].st[0];
   const size_t k = size_t(s) * P->n_recv + d;
   *send_offset = W.send_region[k] < 0 ? 0 : W.send_region[k];
   *recv_offset = W.recv_region[k] < 0 ? 0 : W.recv_region[k];
   *bytes = W.region_bytes[k];
+  return WB_OK;
+}
+
+int wb_plan_stage_region(const wb_plan_t* P, int32_t round, int32_t stage, int32_t s, int32_t d,
+                         int64_t* send_offset, int64_t* recv_offset, int64_t* bytes) {
+  if (!P || !send_offset || !recv_offset || !bytes) return set_error(WB_EINVAL, "null argument");
+  if (stage == 0) return wb_plan_round_region(P, round, s, d, send_offset, recv_offset, bytes);
+  if (stage != 1 && stage != 2) return set_error(WB_EINVAL, "stage must be 0, 1 or 2");
+  if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+  if (s < 0 || s >= P->n_recv || d < 0 || d >= P->n_recv) return set_error(WB_EINVAL, "rank out of range");
+  const wb::StageWire& W = P->rounds[round].st[stage];
+  const size_t k = size_t(s) * P->n_recv + d;
+  *send_offset = W.send_region[k] < 0 ? 0 : W.send_region[k];
+  *recv_offset = W.recv_region[k] < 0 ? 0 : W.recv_region[k];
+  *bytes = W.region_bytes[k];
+  return WB_OK;
+}
+
+int wb_plan_forward_bytes(const wb_plan_t* P, int32_t round, int32_t stage, int64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  if (stage != 1 && stage != 2) return set_error(WB_EINVAL, "stage must be 1 or 2");
+  if (round < -1 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+  int64_t m = 0;
+  if (P->role == WB_RECEIVER)
+    for (size_t k = 0; k < P->rounds.size(); ++k)
+      if (round < 0 || static_cast<int>(k) == round) m = std::max(m, P->rounds[k].st[stage].send_bytes[P->rank]);
+  *out = m;
   return WB_OK;
 }
 
@@ -403,7 +442,11 @@ int wb_plan_traffic_bytes(const wb_plan_t* P, int64_t* read_bytes, int64_t* writ
 }
 
 int wb_plan_kernel_traffic(const wb_plan_t* P, int32_t launch, int64_t* read_bytes, int64_t* write_bytes) {
-  if (!P || !read_bytes || !write_bytes || launch < 0 || launch > 1) return set_error(WB_EINVAL, "bad argument");
+  if (!P || !read_bytes || !write_bytes || launch < 0 || launch > 3) return set_error(WB_EINVAL, "bad argument");
+  if (launch >= 2) {
+    *read_bytes = *write_bytes = P->fwd_bytes[launch - 2];
+    return WB_OK;
+  }
   *read_bytes = launch == 0 ? P->read_bytes - P->q_read_bytes : P->q_read_bytes;
   *write_bytes = launch == 0 ? P->write_bytes - P->q_write_bytes : P->q_write_bytes;
   return WB_OK;
@@ -489,7 +532,7 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
   const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
   const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
   int e = wb::launch_tasks(tasks + P->round_tasks[round], P->round_tasks[round + 1] - P->round_tasks[round], table,
-                           buf, stream);
+                           buf, nullptr, stream);
   if (e != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(e));
   const auto* blocks = reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks);
   e = wb::launch_qblocks(blocks + P->round_qblocks[round], P->round_qblocks[round + 1] - P->round_qblocks[round],
@@ -509,6 +552,26 @@ int wb_unpack_round(wb_plan_t* P, int32_t round, const void* recv_buf, void* con
   return guarded([&]() -> int {
     if (!P) return set_error(WB_EINVAL, "null plan");
     return run_round(P, round, const_cast<const void* const*>(dst_ptrs), recv_buf, stream, WB_RECEIVER);
+  });
+}
+
+int wb_forward_round(wb_plan_t* P, int32_t round, int32_t stage, const void* recv_buf, void* fwd_buf, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    if (P->role != WB_RECEIVER) return set_error(WB_EINVAL, "forwarding needs a receiver plan");
+    if (!P->ws) return set_error(WB_EINVAL, "plan not uploaded (wb_plan_upload)");
+    if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+    if (stage != 1 && stage != 2) return set_error(WB_EINVAL, "stage must be 1 (external) or 2 (internal)");
+    const uint32_t a = P->round_fwd[stage - 1][round], b = P->round_fwd[stage - 1][round + 1];
+    if (a == b) return WB_OK;
+    int rc = check_extent(recv_buf, P->rounds[round].recv_total[P->rank], "recv_buf");
+    if (rc == WB_OK) rc = check_extent(fwd_buf, P->rounds[round].st[stage].send_bytes[P->rank], "fwd_buf");
+    if (rc != WB_OK) return rc;
+    const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
+    const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
+    const int e = wb::launch_tasks(tasks + a, b - a, table, recv_buf, fwd_buf, stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("forward launch: ") + wb::hip_error_string(e));
+    return WB_OK;
   });
 }
 

@@ -259,11 +259,16 @@ __device__ void run_transpose16(const Task& t, const char* src, char* dst) {
 
 }  // namespace
 
+__device__ __forceinline__ const char* base_of(uint16_t idx, const uint64_t* ptrs, const char* buf, const char* aux) {
+  return idx == 0 ? buf : idx == kAuxBuffer ? aux : reinterpret_cast<const char*>(ptrs[idx]);
+}
+
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
-                                                            const uint64_t* __restrict__ ptrs, const char* buf) {
+                                                            const uint64_t* __restrict__ ptrs, const char* buf,
+                                                            const char* aux) {
   const Task t = tasks[blockIdx.x];
-  const char* src = (t.src_idx ? reinterpret_cast<const char*>(ptrs[t.src_idx]) : buf) + t.src_off;
-  char* dst = (t.dst_idx ? reinterpret_cast<char*>(ptrs[t.dst_idx]) : const_cast<char*>(buf)) + t.dst_off;
+  const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
+  char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
   switch (t.kind) {
     case TASK_COPY16: run_copy16(t, src, dst); break;
     case TASK_F32_BF16: run_f32_bf16(t, src, dst); break;
@@ -428,10 +433,10 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, void* stream) {
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, const void* aux, void* stream) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(wb_tasks_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), tasks, ptrs,
-                     static_cast<const char*>(buf));
+                     static_cast<const char*>(buf), static_cast<const char*>(aux));
   return hipGetLastError();
 }
 

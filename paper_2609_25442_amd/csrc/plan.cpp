@@ -9,6 +9,7 @@
 // redundant transfer, no single-source bottleneck). This file follows the
 // canonical rules stated in wb.h so that every rank derives the same plan.
 #include <algorithm>
+#include <array>
 #include <cstdlib>
 #include <map>
 #include <numeric>
@@ -33,6 +34,40 @@ bool intersect(const Rect& a, const Rect& b, Rect& out) {
 }
 
 Rect rect_of(const Placement& p) { return {p.r0, p.r1, p.c0, p.c1}; }
+
+// k parts of x: by rows when it has at least k rows, else by columns; part j
+// spans [j n / k, (j + 1) n / k) of that axis; empty parts are left out.
+void split_parts(const Rect& x, int k, std::vector<Rect>& parts) {
+  const bool by_rows = x.rows() >= k;
+  const int64_t n = by_rows ? x.rows() : x.cols();
+  parts.clear();
+  for (int j = 0; j < k; ++j) {
+    const int64_t a = j * n / k, b = (j + 1) * n / k;
+    if (a == b) continue;
+    parts.push_back(by_rows ? Rect{x.r0 + a, x.r0 + b, x.c0, x.c1} : Rect{x.r0, x.r1, x.c0 + a, x.c0 + b});
+  }
+}
+
+// Deficit hand-out over k owners (ascending ranks): every owner's counter
+// drops by the region's weight, then the parts, largest first (stable), each
+// go to the owner with the lowest counter (the lower rank on ties), whose
+// counter rises by k times the part's weight. who[j] is an owner position.
+void deal(const std::vector<Rect>& parts, std::vector<int64_t>& E, int64_t total, int64_t per_elem,
+          std::vector<int>& who) {
+  const int k = static_cast<int>(E.size());
+  for (int64_t& e : E) e -= total;
+  std::vector<int> order(parts.size());
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return parts[a].numel() > parts[b].numel(); });
+  who.assign(parts.size(), -1);
+  for (int j : order) {
+    int best = 0;
+    for (int o = 1; o < k; ++o)
+      if (E[o] < E[best]) best = o;
+    E[best] += int64_t(k) * parts[j].numel() * per_elem;
+    who[j] = best;
+  }
+}
 
 struct Group {
   Rect x;
@@ -192,6 +227,14 @@ int64_t env_task_bytes() {
   return v >= 1024 ? v : (int64_t(1) << 18);
 }
 
+// The dtype a segment's bytes travel in: that of the trainer placement they
+// were packed from (forwarded segments keep it).
+int wire_dtype(const wb_layout_t& trainer, const std::vector<Segment>& segs, const Segment& g) {
+  const Segment& o = g.stage == 0 ? g : segs[g.origin];
+  const Rank& S = trainer.ranks[o.s];
+  return S.locals[S.pls[o.src_pl].u].dtype;
+}
+
 void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_plan_t& P) {
   TaskSink sink{P.tasks, env_task_bytes()};
   const int nrounds = static_cast<int>(P.rounds.size());
@@ -205,7 +248,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     for (int k = 0; k < nrounds; ++k) {
     for (const Segment* gp : by_round[k]) {
       const Segment& g = *gp;
-      if (g.s != P.rank) continue;
+      if (g.stage != 0 || g.s != P.rank) continue;
       const Placement& sp = R.pls[g.src_pl];
       const int dt = R.locals[sp.u].dtype, es = dtype_bytes(dt);
       const int64_t C = g.x.cols(), Rr = g.x.rows();
@@ -222,6 +265,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     }
     P.round_tasks[k + 1] = static_cast<uint32_t>(P.tasks.size());
     }
+    for (auto& r : P.round_fwd) r.assign(nrounds + 1, static_cast<uint32_t>(P.tasks.size()));
     return;
   }
   const Rank& R = rollout.ranks[P.rank];
@@ -248,8 +292,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     if (g.d != P.rank) continue;
     const Placement& q = R.pls[g.dst_pl];
     const Local& dl = R.locals[q.u];
-    const Rank& S = trainer.ranks[g.s];
-    const int sdt = S.locals[S.pls[g.src_pl].u].dtype;
+    const int sdt = wire_dtype(trainer, P.segs, g);
     if (!cast_supported(sdt, dl.dtype))
       fail(WB_EUNSUPPORTED, std::string("unsupported cast ") + dtype_name(sdt) + " -> " + dtype_name(dl.dtype));
     const int64_t C = g.x.cols(), Rr = g.x.rows();
@@ -279,6 +322,22 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   }
   P.round_tasks[k + 1] = static_cast<uint32_t>(P.tasks.size());
   }
+  // forward work of the exchange stages: each segment this rank forwards is a
+  // byte copy from where it landed in the receive buffer (buf) to its place in
+  // the stage's forward buffer (aux)
+  for (int st = 0; st < 2; ++st) {
+    P.round_fwd[st].assign(nrounds + 1, static_cast<uint32_t>(P.tasks.size()));
+    for (int k = 0; k < nrounds; ++k) {
+      for (const Segment* gp : by_round[k]) {
+        const Segment& g = *gp;
+        if (g.stage != st + 1 || g.s != P.rank) continue;
+        const int dt = wire_dtype(trainer, P.segs, g);
+        sink.copy_rect(0, g.src_off, g.x.numel(), dt, kAuxBuffer, g.send_off, g.x.numel(), dt, 1, g.x.numel());
+        P.fwd_bytes[st] += g.bytes;
+      }
+      P.round_fwd[st][k + 1] = static_cast<uint32_t>(P.tasks.size());
+    }
+  }
   if (nblocks == 0) return;
   // pieces: count per block, prefix, fill (canonical segment order within a block)
   std::vector<uint32_t> count(nblocks + 1, 0);
@@ -299,8 +358,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   std::vector<int> block_round(nblocks, -1);
   for (const Span& sp : qspans) {
     const Segment& g = *sp.g;
-    const Rank& S = trainer.ranks[g.s];
-    const int sdt = S.locals[S.pls[g.src_pl].u].dtype, ss = dtype_bytes(sdt);
+    const int sdt = wire_dtype(trainer, P.segs, g), ss = dtype_bytes(sdt);
     const int64_t Rr = g.x.rows(), C = g.x.cols();
     for_blocks(sp, [&](int64_t id, int64_t bi, int64_t bj, int64_t B) {
       const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
@@ -376,17 +434,27 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
 void check_work(const wb_plan_t& P, const Rank& R) {
   std::vector<int64_t> size(R.locals.size() + 1);
   for (size_t u = 0; u < R.locals.size(); ++u) size[u + 1] = R.locals[u].numel() * dtype_bytes(R.locals[u].dtype);
+  int64_t aux_size = 0;
   auto inside = [&](int idx, uint64_t off, uint64_t len, const char* what) {
-    if (idx < 0 || idx >= static_cast<int>(size.size()) || len == 0 || off + len > uint64_t(size[idx]))
+    const bool known = idx == kAuxBuffer || (idx >= 0 && idx < static_cast<int>(size.size()));
+    if (!known || len == 0 || off + len > uint64_t(idx == kAuxBuffer ? aux_size : size[idx]))
       fail(WB_EINVAL, std::string("internal: ") + what + " work item out of bounds");
   };
-  if (P.round_tasks.size() != P.rounds.size() + 1 || P.round_tasks.back() != P.tasks.size() ||
-      P.round_qblocks.size() != P.rounds.size() + 1 || P.round_qblocks.back() != P.qblocks.size())
-    fail(WB_EINVAL, "internal: round ranges");
-  for (size_t k = 0; k < P.rounds.size(); ++k) {
-  size[0] = P.role == WB_SENDER ? P.rounds[k].send_bytes[P.rank] : P.rounds[k].recv_bytes[P.rank];
-  for (uint32_t ti = P.round_tasks[k]; ti < P.round_tasks[k + 1]; ++ti) {
-    const Task& t = P.tasks[ti];
+  const size_t nr = P.rounds.size();
+  bool ranges = P.round_tasks.size() == nr + 1 && P.round_qblocks.size() == nr + 1 &&
+                P.round_qblocks.back() == P.qblocks.size() && P.round_qblocks[0] == 0 && P.round_tasks[0] == 0;
+  uint32_t prev = ranges ? P.round_tasks.back() : 0;
+  for (const auto& r : P.round_fwd) {
+    ranges = ranges && r.size() == nr + 1 && r[0] == prev;
+    if (ranges) prev = r.back();
+  }
+  ranges = ranges && prev == P.tasks.size();
+  for (size_t k = 0; ranges && k < nr; ++k) {
+    ranges = P.round_tasks[k] <= P.round_tasks[k + 1] && P.round_qblocks[k] <= P.round_qblocks[k + 1];
+    for (const auto& r : P.round_fwd) ranges = ranges && r[k] <= r[k + 1];
+  }
+  if (!ranges) fail(WB_EINVAL, "internal: round ranges");
+  auto check_task = [&](const Task& t) {
     if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
     const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
     switch (t.kind) {
@@ -420,6 +488,24 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         break;
       default:
         fail(WB_EINVAL, "internal: unknown work item");
+    }
+  };
+  for (size_t k = 0; k < nr; ++k) {
+  const RoundWire& W = P.rounds[k];
+  size[0] = P.role == WB_SENDER ? W.st[0].send_bytes[P.rank] : W.recv_total[P.rank];
+  aux_size = 0;
+  for (uint32_t ti = P.round_tasks[k]; ti < P.round_tasks[k + 1]; ++ti) {
+    if (P.tasks[ti].src_idx == kAuxBuffer || P.tasks[ti].dst_idx == kAuxBuffer)
+      fail(WB_EINVAL, "internal: pack or unpack work item on the forward buffer");
+    check_task(P.tasks[ti]);
+  }
+  for (int st = 0; st < 2; ++st) {
+    aux_size = P.role == WB_SENDER ? 0 : W.st[st + 1].send_bytes[P.rank];
+    for (uint32_t ti = P.round_fwd[st][k]; ti < P.round_fwd[st][k + 1]; ++ti) {
+      const Task& t = P.tasks[ti];
+      if (t.kind != TASK_COPY16 && t.kind != TASK_SCALAR) fail(WB_EINVAL, "internal: forward work item kind");
+      if (t.src_idx != 0 || t.dst_idx != kAuxBuffer) fail(WB_EINVAL, "internal: forward work item buffers");
+      check_task(t);
     }
   }
   for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
@@ -513,9 +599,11 @@ int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::v
     std::vector<int> ts, td;
     for (size_t i : members[u]) {
       const Segment& g = segs[i];
-      if (add_s[g.s] == 0) ts.push_back(g.s);
+      if (g.stage == 0) {
+        if (add_s[g.s] == 0) ts.push_back(g.s);
+        add_s[g.s] += g.bytes;
+      }
       if (add_d[g.d] == 0) td.push_back(g.d);
-      add_s[g.s] += g.bytes;
       add_d[g.d] += g.bytes;
     }
     bool over = false;
@@ -534,14 +622,14 @@ int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::v
   return rnd + 1;
 }
 
-// Wire offsets of round k (segments in canonical order, payloads at multiples
-// of 256 bytes within their region, regions at multiples of 4096 bytes).
-void wire_round(wb_plan_t& P, int k) {
-  const int ns = P.n_send, nd = P.n_recv;
-  RoundWire& W = P.rounds[k];
+// Wire offsets of one stage of round k (segments in canonical order, payloads
+// at multiples of 256 bytes within their region, regions at multiples of 4096
+// bytes; senders' buffers by ascending receiver, receivers' by ascending
+// sender). Offsets are relative to the stage's receive section.
+void wire_stage(std::vector<Segment>& segs, int k, int stage, int ns, int nd, StageWire& W) {
   std::vector<int64_t> end(size_t(ns) * nd, -1);
-  for (Segment& g : P.segs) {
-    if (g.round != k) continue;
+  for (Segment& g : segs) {
+    if (g.round != k || g.stage != stage) continue;
     int64_t& e = end[size_t(g.s) * nd + g.d];
     const int64_t off = e < 0 ? 0 : align_up(e, kPayloadAlign);
     g.send_off = g.recv_off = off;
@@ -575,17 +663,44 @@ void wire_round(wb_plan_t& P, int k) {
     }
     W.recv_bytes[d] = pos;
   }
-  for (Segment& g : P.segs) {
-    if (g.round != k) continue;
+  for (Segment& g : segs) {
+    if (g.round != k || g.stage != stage) continue;
     g.send_off += W.send_region[size_t(g.s) * nd + g.d];
     g.recv_off += W.recv_region[size_t(g.s) * nd + g.d];
+  }
+}
+
+// All stages of round k: the exchange sections follow the receive section in
+// every rollout rank's buffer (a non-empty section starts on a 4096-byte
+// boundary); forwarded segments read where their source segment landed.
+void wire_round(wb_plan_t& P, int k) {
+  const int ns = P.n_send, nd = P.n_recv;
+  RoundWire& W = P.rounds[k];
+  wire_stage(P.segs, k, 0, ns, nd, W.st[0]);
+  W.recv_total = W.st[0].recv_bytes;
+  for (int stage = 1; stage <= 2; ++stage) {
+    StageWire& S = W.st[stage];
+    wire_stage(P.segs, k, stage, nd, nd, S);
+    std::vector<int64_t> base(nd);
+    for (int d = 0; d < nd; ++d) {
+      if (S.recv_bytes[d]) W.recv_total[d] = align_up(W.recv_total[d], kRegionAlign);
+      base[d] = W.recv_total[d];
+      W.recv_total[d] += S.recv_bytes[d];
+    }
+    for (size_t i = 0; i < S.recv_region.size(); ++i)
+      if (S.recv_region[i] >= 0) S.recv_region[i] += base[i % nd];
+    for (Segment& g : P.segs) {
+      if (g.round != k || g.stage != stage) continue;
+      g.recv_off += base[g.d];
+      g.src_off = P.segs[g.src_seg].recv_off;
+    }
   }
 }
 
 }  // namespace
 
 void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, int64_t round_budget,
-                wb_plan_t& P) {
+                int node_size, wb_plan_t& P) {
   if (role != WB_SENDER && role != WB_RECEIVER) fail(WB_EINVAL, "role must be WB_SENDER or WB_RECEIVER");
   const int ns = static_cast<int>(trainer.ranks.size()), nd = static_cast<int>(rollout.ranks.size());
   if (ns < 1 || nd < 1) fail(WB_EINVAL, "layouts need at least one rank");
@@ -656,60 +771,140 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
           fail(WB_EUNSUPPORTED, "overlapping, non-identical trainer rectangles");
       }
 
-  // 2./3. regions and segments in canonical order, deficit assignment per owner set
+  // 6. rollout groups (identical rollout rectangles, holders ascending) and
+  // the hand-out of a replicated group's parts over its holders
+  if (node_size < 0) fail(WB_EINVAL, "node size must be >= 0");
+  const int G = node_size;
+  struct RGroup {
+    std::vector<int> holders, pls, who;
+    std::vector<Rect> parts;
+  };
+  std::vector<RGroup> rgroups;
+  std::vector<std::vector<int>> rg_of(nd);
+  if (G > 0) {
+    std::map<std::array<int64_t, 5>, int> by_key;
+    for (int d = 0; d < nd; ++d) {
+      const Rank& R = rollout.ranks[d];
+      rg_of[d].assign(R.pls.size(), -1);
+      for (size_t qi = 0; qi < R.pls.size(); ++qi) {
+        const Placement& q = R.pls[qi];
+        auto it = by_key.emplace(std::array<int64_t, 5>{q.t, q.r0, q.r1, q.c0, q.c1}, static_cast<int>(rgroups.size()));
+        if (it.second) rgroups.emplace_back();
+        RGroup& h = rgroups[it.first->second];
+        if (!h.holders.empty() && h.holders.back() == d) fail(WB_EINVAL, "a rollout rank holds the same rectangle twice");
+        h.holders.push_back(d);
+        h.pls.push_back(static_cast<int>(qi));
+        rg_of[d][qi] = it.first->second;
+      }
+    }
+    std::map<std::vector<int>, std::vector<int64_t>> rdeficit;
+    for (int d = 0; d < nd; ++d)
+      for (size_t qi = 0; qi < rollout.ranks[d].pls.size(); ++qi) {
+        RGroup& h = rgroups[rg_of[d][qi]];
+        if (h.holders.size() == 1 || h.holders[0] != d) continue;
+        const Rect x = rect_of(rollout.ranks[d].pls[qi]);
+        split_parts(x, static_cast<int>(h.holders.size()), h.parts);
+        std::vector<int64_t>& E = rdeficit.emplace(h.holders, std::vector<int64_t>(h.holders.size(), 0)).first->second;
+        deal(h.parts, E, x.numel(), 1, h.who);
+      }
+  }
+
+  // 2./3. regions and stage-0 segments in canonical order, deficit assignment
+  // per owner set; with exchange stages a replicated rollout group asks the
+  // trainers only for each holder's parts
   std::vector<std::vector<int64_t>> deficit(set_ids.size());
   for (const auto& kv : set_ids) deficit[kv.second].assign(kv.first.size(), 0);
   P.segs.clear();
-  std::vector<Rect> parts;
-  std::vector<int> order, who;
+  std::vector<Rect> parts, needs;
+  std::vector<int> who;
   for (int d = 0; d < nd; ++d) {
     const Rank& R = rollout.ranks[d];
     for (size_t qi = 0; qi < R.pls.size(); ++qi) {
       const Placement& q = R.pls[qi];
-      int64_t covered = 0;
-      for (const Group& g : groups[q.t]) {
-        Rect x;
-        if (!intersect(rect_of(q), g.x, x)) continue;
-        covered += x.numel();
-        const int k = static_cast<int>(g.owners.size());
-        if (k == 1) {
-          P.segs.push_back({g.owners[0], d, q.t, x, g.pls[0], static_cast<int>(qi), x.numel() * g.esize});
-          continue;
-        }
-        const bool by_rows = x.rows() >= k;
-        const int64_t n = by_rows ? x.rows() : x.cols();
-        parts.clear();
-        for (int j = 0; j < k; ++j) {
-          const int64_t a = j * n / k, b = (j + 1) * n / k;
-          if (a == b) continue;
-          parts.push_back(by_rows ? Rect{x.r0 + a, x.r0 + b, x.c0, x.c1} : Rect{x.r0, x.r1, x.c0 + a, x.c0 + b});
-        }
-        std::vector<int64_t>& E = deficit[g.set];
-        for (int64_t& e : E) e -= x.numel() * g.esize;
-        order.resize(parts.size());
-        std::iota(order.begin(), order.end(), 0);
-        std::stable_sort(order.begin(), order.end(),
-                         [&](int a, int b) { return parts[a].numel() > parts[b].numel(); });
-        who.assign(parts.size(), -1);
-        for (int j : order) {
-          int best = 0;
-          for (int o = 1; o < k; ++o)
-            if (E[o] < E[best]) best = o;  // owners ascending, so ties keep the lower rank
-          E[best] += int64_t(k) * parts[j].numel() * g.esize;
-          who[j] = best;
-        }
-        for (size_t j = 0; j < parts.size(); ++j)
-          P.segs.push_back({g.owners[who[j]], d, q.t, parts[j], g.pls[who[j]], static_cast<int>(qi),
-                            parts[j].numel() * g.esize});
+      needs.clear();
+      if (G > 0 && rgroups[rg_of[d][qi]].holders.size() > 1) {
+        const RGroup& h = rgroups[rg_of[d][qi]];
+        for (size_t j = 0; j < h.parts.size(); ++j)
+          if (h.holders[h.who[j]] == d) needs.push_back(h.parts[j]);
+      } else {
+        needs.push_back(rect_of(q));
       }
-      if (covered != q.numel())
-        fail(WB_EINVAL, "rollout rank " + std::to_string(d) + " needs elements no trainer holds");
+      for (const Rect& need : needs) {
+        int64_t covered = 0;
+        for (const Group& g : groups[q.t]) {
+          Rect x;
+          if (!intersect(need, g.x, x)) continue;
+          covered += x.numel();
+          const int k = static_cast<int>(g.owners.size());
+          if (k == 1) {
+            P.segs.push_back({g.owners[0], d, q.t, x, g.pls[0], static_cast<int>(qi), x.numel() * g.esize});
+            P.segs.back().origin = static_cast<int>(P.segs.size() - 1);
+            continue;
+          }
+          split_parts(x, k, parts);
+          deal(parts, deficit[g.set], x.numel() * g.esize, g.esize, who);
+          for (size_t j = 0; j < parts.size(); ++j) {
+            P.segs.push_back({g.owners[who[j]], d, q.t, parts[j], g.pls[who[j]], static_cast<int>(qi),
+                              parts[j].numel() * g.esize});
+            P.segs.back().origin = static_cast<int>(P.segs.size() - 1);
+          }
+        }
+        if (covered != need.numel())
+          fail(WB_EINVAL, "rollout rank " + std::to_string(d) + " needs elements no trainer holds");
+      }
+    }
+  }
+
+  // 6. exchange stages: stage 1 sends every stage-0 segment of a replicated
+  // group to one holder in each other node (same position in that node's
+  // holder list, modulo its length); stage 2 sends every stage-0 and stage-1
+  // segment to the other holders in the receiver's node
+  if (G > 0) {
+    const size_t n0 = P.segs.size();
+    for (size_t gi = 0; gi < n0; ++gi) {
+      const Segment g = P.segs[gi];
+      const RGroup& h = rgroups[rg_of[g.d][g.dst_pl]];
+      if (h.holders.size() == 1) continue;
+      int pos = 0;
+      for (int x : h.holders) {
+        if (x == g.d) break;
+        if (x / G == g.d / G) ++pos;
+      }
+      for (size_t a = 0; a < h.holders.size();) {
+        const int v = h.holders[a] / G;
+        size_t b = a;
+        while (b < h.holders.size() && h.holders[b] / G == v) ++b;
+        if (v != g.d / G) {
+          const size_t k = a + size_t(pos) % (b - a);
+          Segment f{g.d, h.holders[k], g.t, g.x, -1, h.pls[k], g.bytes};
+          f.stage = 1;
+          f.src_seg = static_cast<int>(gi);
+          f.origin = g.origin;
+          P.segs.push_back(f);
+        }
+        a = b;
+      }
+    }
+    const size_t n1 = P.segs.size();
+    for (size_t gi = 0; gi < n1; ++gi) {
+      const Segment g = P.segs[gi];
+      const RGroup& h = rgroups[rg_of[g.d][g.dst_pl]];
+      for (size_t k = 0; k < h.holders.size(); ++k) {
+        const int z = h.holders[k];
+        if (z == g.d || z / G != g.d / G) continue;
+        Segment f{g.d, z, g.t, g.x, -1, h.pls[k], g.bytes};
+        f.stage = 2;
+        f.src_seg = static_cast<int>(gi);
+        f.origin = g.origin;
+        P.segs.push_back(f);
+      }
     }
   }
 
   // 5. rounds, then 4. wire offsets per round
   P.n_send = ns;
   P.n_recv = nd;
+  P.node_size = G;
   const int nrounds = round_budget > 0 ? assign_rounds(trainer, rollout, P.segs, round_budget) : 1;
   P.rounds.assign(nrounds, RoundWire{});
   for (int k = 0; k < nrounds; ++k) wire_round(P, k);
@@ -723,14 +918,24 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
 std::string dump_plan(const wb_plan_t& P) {
   std::ostringstream o;
   auto seg = [&](const Segment& g) {
-    o << "seg " << g.s << " " << g.d << " " << g.t << " " << g.x.r0 << " " << g.x.r1 << " " << g.x.c0 << " " << g.x.c1
-      << " " << g.src_pl << " " << g.dst_pl << " " << g.send_off << " " << g.recv_off << " " << g.bytes << "\n";
+    static const char* kTag[3] = {"seg ", "xseg ", "iseg "};
+    o << kTag[g.stage] << g.s << " " << g.d << " " << g.t << " " << g.x.r0 << " " << g.x.r1 << " " << g.x.c0 << " "
+      << g.x.c1 << " ";
+    if (g.stage == 0)
+      o << g.src_pl;
+    else
+      o << g.src_off;
+    o << " " << g.dst_pl << " " << g.send_off << " " << g.recv_off << " " << g.bytes << "\n";
   };
   auto sizes = [&](const RoundWire& W) {
-    for (int s = 0; s < P.n_send; ++s) o << "send " << s << " " << W.send_bytes[s] << "\n";
-    for (int d = 0; d < P.n_recv; ++d) o << "recv " << d << " " << W.recv_bytes[d] << "\n";
+    for (int s = 0; s < P.n_send; ++s) o << "send " << s << " " << W.st[0].send_bytes[s] << "\n";
+    for (int d = 0; d < P.n_recv; ++d) o << "recv " << d << " " << W.recv_total[d] << "\n";
+    if (P.node_size)
+      for (int st = 1; st <= 2; ++st)
+        for (int d = 0; d < P.n_recv; ++d) o << "fwd" << st << " " << d << " " << W.st[st].send_bytes[d] << "\n";
   };
   o << "plan trainer_ranks=" << P.n_send << " rollout_ranks=" << P.n_recv << " segments=" << P.segs.size();
+  if (P.node_size) o << " node_size=" << P.node_size;
   if (P.rounds.size() == 1) {
     o << "\n";
     sizes(P.rounds[0]);

@@ -81,21 +81,36 @@ struct Rect {
 };
 
 // One piece of the routing plan: a rectangle of checkpoint tensor t that
-// sender s ships to receiver d.
+// sender s ships to receiver d. In the receive stage (0) s is a trainer rank;
+// in the external (1) and internal (2) exchange stages s is a rollout rank that
+// forwards bytes it received earlier in the same round.
 struct Segment {
   int s, d, t;
   Rect x;
-  int src_pl, dst_pl;
+  int src_pl, dst_pl;   // src_pl: the trainer placement (stage 0 only)
   int64_t bytes;
-  int64_t send_off = 0, recv_off = 0;  // within the segment's round
+  int64_t send_off = 0, recv_off = 0;  // within the segment's round; recv_off spans all sections
   int round = 0;
+  int stage = 0;
+  int src_seg = -1;     // exchange stages: the segment whose received bytes are forwarded
+  int origin = -1;      // the stage-0 segment the bytes left the trainers in
+  int64_t src_off = 0;  // exchange stages: where those bytes sit in the forwarding rank's receive buffer
 };
 
-// Wire layout of one round: per-rank buffer sizes and per-(sender, receiver)
-// region offsets and sizes, indexed [s * n_recv + d] (-1 when the pair is idle).
-struct RoundWire {
+// Wire layout of one stage of one round: per-rank buffer sizes and
+// per-(sender, receiver) region offsets and sizes, indexed [s * receivers + d]
+// (-1 when the pair is idle). recv_region is an offset in the whole receive
+// buffer (the stage's section included).
+struct StageWire {
   std::vector<int64_t> send_bytes, recv_bytes;
   std::vector<int64_t> send_region, recv_region, region_bytes;
+};
+
+// Stage 0 pairs trainer and rollout ranks; stages 1 and 2 pair rollout ranks.
+// A rollout rank's receive buffer holds the three stages' sections in order.
+struct RoundWire {
+  StageWire st[3];
+  std::vector<int64_t> recv_total;
 };
 
 // Work item of the copy/cast kernel: a rows x cols block of elements.
@@ -154,6 +169,7 @@ enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4
 struct wb_plan_t {
   // global plan
   int n_send = 0, n_recv = 0;
+  int node_size = 0;                    // rollout ranks per node; 0: no exchange stages
   std::vector<wb::Segment> segs;
   std::vector<wb::RoundWire> rounds;
   // view of one rank
@@ -161,10 +177,12 @@ struct wb_plan_t {
   int n_locals = 0;
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
-  std::vector<wb::Task> tasks;          // grouped by round
+  std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
+  std::vector<uint32_t> round_fwd[2];   // forward work of exchange stage 1 + i, round k: [k] .. [k + 1]
+  int64_t fwd_bytes[2] = {0, 0};        // bytes this rank forwards in each exchange stage (all rounds)
   // copies of the two layouts used for dumps and queries
   wb_layout_t trainer, rollout;
   // device state after wb_plan_upload
@@ -183,11 +201,13 @@ void check_placement(const wb_layout_t& L, int rank, const Placement& p);
 std::string dump_layout(const wb_layout_t& L);
 // plan.cpp
 void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role, int rank, int64_t round_budget,
-                wb_plan_t& out);
+                int node_size, wb_plan_t& out);
 std::string dump_plan(const wb_plan_t& P);
 // kernels.hip
-// ptrs[1 + u] is local tensor u; work items with index 0 use buf.
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, void* stream);
+// ptrs[1 + u] is local tensor u; work items with index 0 use buf, with index
+// kAuxBuffer aux (the second buffer of a forward launch).
+constexpr uint16_t kAuxBuffer = 0xFFFF;
+int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, const void* aux, void* stream);
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream);
 const char* hip_error_string(int err);

@@ -81,3 +81,16 @@ def hand_rounds_pair():
           Placement(3, 0, 1, 0, 4, 3, 0, 4), Placement(4, 0, 2, 0, 4, 3, 4, 4)]
     rollout = Layout(cat, [RankLayout(rl, rp)])
     return trainer, rollout
+
+
+def hand_exchange_pair():
+    """The layout pair of tests/golden/hand_plan_exchange.txt (node size 2)."""
+    cat = [CkptTensor("T0", 4, 4), CkptTensor("T1", 1, 8)]
+    tr = []
+    for r0 in (0, 2):
+        tr.append(RankLayout([Local("a", "f32", 1, 2, 4), Local("b", "f32", 1, 1, 8)],
+                             [Placement(0, r0, r0 + 2, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 8, 1, 0, 8)]))
+    both = RankLayout([Local("x", "bf16", 1, 4, 4), Local("y", "bf16", 1, 1, 8)],
+                      [Placement(0, 0, 4, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 8, 1, 0, 8)])
+    only_x = RankLayout([Local("x", "bf16", 1, 4, 4)], [Placement(0, 0, 4, 0, 4, 0, 0, 4)])
+    return Layout(cat, tr), Layout(cat, [both, only_x, RankLayout(list(both.locals), list(both.placements))])

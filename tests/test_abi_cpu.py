@@ -198,3 +198,76 @@ def test_round_calls_need_round_plans():
     _expect(wb.WB_EINVAL, p.unpack, 0, [0] * p.num_local_tensors, 0)       # not uploaded, and several rounds
     _expect(wb.WB_EINVAL, p.unpack_round, p.num_rounds, 0, [0] * p.num_local_tensors, 0)
     _expect(wb.WB_EINVAL, wb.Plan, tr, ro, wb.RECEIVER, 0, -1)
+
+
+def test_hand_exchange_golden():
+    from oracle_cases import hand_exchange_pair
+    tr, ro = hand_exchange_pair()
+    golden = "".join(l for l in open(os.path.join(ROOT, "tests", "golden", "hand_plan_exchange.txt"))
+                     if not l.startswith("#"))
+    for d in range(3):
+        p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, d, node_size=2)
+        assert p.dump() == golden
+        assert p.node_size == 2
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0, node_size=2)
+    assert p.buffer_bytes == 12304
+    assert p.forward_bytes(1) == 520 and p.forward_bytes(2) == 272
+    assert p.stage_region(0, 1, 2, 0) == (0, 8192, 520)
+    assert p.stage_region(0, 2, 1, 0) == (0, 12288, 16)
+    assert p.stage_region(0, 0, 1, 0) == (0, 4096, 264)
+    assert p.kernel_traffic(2) == (8 + 8 + 32, 48) and p.kernel_traffic(3) == (32 + 16, 48)
+    s = wb.Plan(to_wb(tr), to_wb(ro), wb.SENDER, 1, node_size=2)
+    assert s.forward_bytes(1) == 0 and s.buffer_bytes == 4104
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_random_exchange_plans_equal_oracle(seed):
+    rng = np.random.default_rng(1900 + seed)
+    m = random_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout"))
+    G = int(rng.integers(1, oro.nranks + 1))
+    budget = int(rng.choice([0, 0, 300, 3000]))
+    want = dump(build_plan(otr, oro, round_budget=budget, node_size=G))
+    tr, ro = to_wb(otr), to_wb(oro)
+    for d in range(oro.nranks):
+        assert wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=budget, node_size=G).dump() == want
+    assert wb.Plan(tr, ro, wb.SENDER, int(rng.integers(0, otr.nranks)), round_budget=budget,
+                   node_size=G).dump() == want
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_workload_exchange_plans_equal_oracle(name):
+    for w, full in ((scaled(name), False), (WORKLOADS[name], True)):
+        tr = wb.Layout.describe(w["model"], w["trainer"])
+        ro = wb.Layout.describe(w["model"], w["rollout"])
+        otr = layout_from_spec(w["model"], w["trainer"])
+        oro = layout_from_spec(w["model"], w["rollout"])
+        for G in sorted({1, max(1, oro.nranks // 2)}):
+            budget = (4 << 30) if full else 0
+            want = dump(build_plan(otr, oro, round_budget=budget, node_size=G))
+            p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=budget, node_size=G)
+            assert p.dump() == want, (name, G)
+            assert wb.Plan(tr, ro, wb.SENDER, w["pack_rank"], round_budget=budget, node_size=G).dump() == want
+
+
+def test_exchange_errors():
+    tr, ro = hand_replicated_pair()
+    _expect(wb.WB_EINVAL, wb.Plan, to_wb(tr), to_wb(ro), wb.RECEIVER, 0, 0, -1)
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0, node_size=1)
+    _expect(wb.WB_EINVAL, p.forward_round, 0, 1, 0, 0, 0)        # not uploaded
+    _expect(wb.WB_EINVAL, p.stage_region, 0, 3, 0, 0)
+    _expect(wb.WB_EINVAL, p.forward_bytes, 0)
+    s = wb.Plan(to_wb(tr), to_wb(ro), wb.SENDER, 0, node_size=1)
+    _expect(wb.WB_EINVAL, s.forward_round, 0, 1, 0, 0, 0)        # senders do not forward
+    # a rollout rank holding one rectangle twice
+    R = wb.Layout.create([("T", 2, 4)], 1)
+    R.add_local(0, "x", "f32", 1, 2, 4)
+    R.add_local(0, "y", "f32", 1, 2, 4)
+    R.add_placement(0, 0, 0, 2, 0, 4, 0, 0, 4)
+    R.add_placement(0, 0, 0, 2, 0, 4, 1, 0, 4)
+    T = wb.Layout.create([("T", 2, 4)], 1)
+    T.add_local(0, "a", "f32", 1, 2, 4)
+    T.add_placement(0, 0, 0, 2, 0, 4, 0, 0, 4)
+    assert wb.Plan(T, R, wb.RECEIVER, 0).num_segments == 2
+    _expect(wb.WB_EINVAL, wb.Plan, T, R, wb.RECEIVER, 0, 0, 1)

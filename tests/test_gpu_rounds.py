@@ -135,3 +135,75 @@ def test_full_size_rounds(name):
     torch.cuda.synchronize()
     say(f"[{name}] full check")
     _check_unpack_full(oro, d, dst, otr.catalog, dt)
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_fsdp8_to_tp1", "mixtral_ep8fsdp2_to_ep2", "dsv3_ep64_to_ep8_fp8"])
+def test_two_stream_pipeline(name):
+    """Depth-2 pipeline (Sec. 3.2 rounds; the two-buffer design of Sec. 4.6): the packs of
+    round k+1 run on one stream while the receiver's stream moves round k's
+    regions out of the senders' send buffers and assembles round k. Each sender
+    alternates between two send buffers and the receiver between two receive
+    buffers; events order only what the buffers require. The rollout tensors
+    must equal the oracle's expectation."""
+    w = scaled(name)
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    dt = w["trainer"]["dtype"]
+    d = w["unpack_rank"]
+    total = sum(g.nbytes for g in build_plan(otr, oro).segments if g.d == d)
+    budget = max(4096, total // 6)
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    rp = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=budget)
+    rws = workspace_for(rp)
+    rp.upload(rws)
+    nr = rp.num_rounds
+    assert nr > 3
+    cache = {}
+
+    def vals(t):
+        if t not in cache:
+            c = otr.catalog[t]
+            cache[t] = sc.values_numpy(t, np.arange(c.numel), dt).reshape(c.rows, c.cols)
+        return cache[t]
+
+    senders = [s for s in range(otr.nranks) if any(rp.round_region(k, s, d)[2] for k in range(nr))]
+    keep = []
+    plans, srcs, sends = {}, {}, {}
+    for s in senders:
+        p = wb.Plan(tr, ro, wb.SENDER, s, round_budget=budget)
+        ws = workspace_for(p)
+        p.upload(ws)
+        keep.append(ws)
+        plans[s] = p
+        srcs[s] = [codes_to_gpu(c, lc.dtype) for c, lc in zip(materialize(otr, s, vals), otr.ranks[s].locals)]
+        sends[s] = [torch.full((max(1, p.buffer_bytes),), FILL, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    recv = [torch.full((max(1, rp.buffer_bytes),), FILL, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    dst = wb.allocate_locals(ro, d)
+    for t in dst:
+        t.view(torch.uint8).fill_(0x7F)
+    torch.cuda.synchronize()
+    P, U = torch.cuda.Stream(), torch.cuda.Stream()
+    packed = [torch.cuda.Event() for _ in range(nr)]
+    moved = [torch.cuda.Event() for _ in range(nr)]
+    say(f"[pipeline {name}] {nr} rounds, {len(senders)} senders")
+    for k in range(nr):
+        if k >= 2:
+            P.wait_event(moved[k - 2])          # send buffers k % 2 drained
+        for s in senders:
+            if rp.round_region(k, s, d)[2]:
+                plans[s].pack_round(k, srcs[s], sends[s][k % 2], P)
+        packed[k].record(P)
+        U.wait_event(packed[k])
+        with torch.cuda.stream(U):              # the network stand-in, then assembly
+            for s in senders:
+                so, roff, nb = rp.round_region(k, s, d)
+                if nb:
+                    recv[k % 2][roff:roff + nb].copy_(sends[s][k % 2][so:so + nb])
+        moved[k].record(U)
+        rp.unpack_round(k, recv[k % 2], dst, U)
+    torch.cuda.synchronize()
+    want = expected_rollout(oro, d, vals, dt)
+    for u, (t, e) in enumerate(zip(dst, want)):
+        lc = oro.ranks[d].locals[u]
+        assert np.array_equal(gpu_to_codes(t, lc.dtype), e), (d, lc.name)
