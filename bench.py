@@ -229,6 +229,74 @@ def summarize_trace(workload, trace_csv):
     return res
 
 
+def run_probe(args):
+    """Source-map probing (App. B, Algorithm 1) of the benchmark's trainer and
+    rollout ranks at full size, through the torch-slicing stand-in loaders;
+    the recovered placements must equal the declared ones. Prints one JSON
+    line: per-rank probe time, the passes, and the diff2 stencil's own rate
+    (HIP events around its launches over every loaded local tensor)."""
+    import torch
+
+    import paper_2609_25442_amd as wb
+    from synthetic_checkpoint import loaders
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    dtype = w["trainer"]["dtype"]
+    torch.cuda.set_device(0)
+    out = {"metric": "source-map probe of one rank (ms); diff2 stencil GB/s", "workload": args.workload,
+           "dtype": dtype, "data": "synthetic", "ranks": {}}
+    for side, rank in (("trainer", w["pack_rank"]), ("rollout", w["unpack_rank"])):
+        par = w[side]
+        fn = loaders.STYLES[par["style"]]
+
+        def load(T, fn=fn, par=par, rank=rank):
+            return [x.contiguous() for x in fn(w["model"], par, T, rank) if x is not None]
+
+        declared = wb.Layout.describe(w["model"], par)
+        cat = declared.tensors()
+        stats = {}
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        got = wb.probe_layout(cat, dtype, [load], stats=stats)
+        ms = (time.perf_counter() - t0) * 1e3
+        keep = [u for u, lc in enumerate(declared.locals(rank)) if lc["scales"] < 0]
+        remap = {u: i for i, u in enumerate(keep)}
+        want = sorted((t, r0, r1, c0, c1, remap[u], b, ld, tr)
+                      for (t, r0, r1, c0, c1, u, b, ld, tr) in declared.placements(rank))
+        same = sorted(got.placements(0)) == want
+        log(f"[probe] {side} rank {rank}: {ms:.0f} ms, recovered == declared: {same}")
+        # the stencil alone, over the loaded tensors of pass 0
+        probe = wb.Probe(cat, dtype)
+        ckpt = {n: torch.empty((r, c), dtype=wb.torch_dtype(dtype), device="cuda") for n, r, c in cat}
+        for t, (n, r, c) in enumerate(cat):
+            wb.make_ids(ckpt[n], dtype, probe.first_id(t), 0)
+        locs = load(ckpt)
+        cap = 1 << 24
+        idx = torch.empty(cap, dtype=torch.int64, device="cuda")
+        val = torch.empty(cap, dtype=torch.int32, device="cuda")
+        counts = torch.zeros(len(locs), dtype=torch.int64, device="cuda")
+        nbytes = sum(x.numel() * x.element_size() for x in locs)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for rep in range(3):
+            ev[0].record()
+            for u, x in enumerate(locs):
+                b, rr, cc = wb._view_shape(x)
+                wb.diff2(x, dtype, b * rr, cc, idx, val, counts[u:u + 1])
+            ev[1].record()
+            torch.cuda.synchronize()
+        stencil_ms = ev[0].elapsed_time(ev[1])
+        out["ranks"][side] = {"rank": rank, "probe_ms": round(ms, 1), "recovered_equals_declared": same,
+                              "placements": len(want), "local_tensors": len(keep),
+                              "passes": stats[0], "scan_ms": round(stats["scan_s"][0] * 1e3, 1),
+                              "diff2": {"launches": len(locs), "bytes": nbytes, "ms": round(stencil_ms, 3),
+                                        "GB/s": round(nbytes / (stencil_ms * 1e-3) / 1e9, 1),
+                                        "frac_of_hbm_peak": round(nbytes / (stencil_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
+        del locs, ckpt, idx, val, got
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,6 +308,8 @@ def main():
                     help="bytes per rank per round (0: one round); each step packs and unpacks every round")
     ap.add_argument("--pipeline", action="store_true",
                     help="with rounds: pack round k+1 on one stream while round k is assembled on another")
+    ap.add_argument("--probe", action="store_true",
+                    help="discover the trainer and rollout ranks' layouts by probing torch loaders (diff2 kernels)")
     ap.add_argument("--staged", action="store_true",
                     help="send and receive buffers in pinned host memory (PCIe-bound; not the headline value)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -268,6 +338,10 @@ def main():
               "(pack of one trainer rank, unpack of one rollout rank); --gpus above 1 is not supported.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.probe:
+        run_probe(args)
+        return
 
     import torch
 

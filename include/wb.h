@@ -111,6 +111,7 @@ typedef struct wb_parallelism {
 
 typedef struct wb_layout_t wb_layout_t;
 typedef struct wb_plan_t wb_plan_t;
+typedef struct wb_probe_t wb_probe_t;
 
 /* One slice-copy (Sec. 3.1): rows r0..r1-1, cols c0..c1-1 of checkpoint tensor t
  * are stored in local tensor u of the rank at
@@ -316,6 +317,22 @@ int wb_plan_stage_region(const wb_plan_t* plan, int32_t round, int32_t stage, in
 /* This receiver's forward buffer size for exchange stage 1 or 2 in one round
  * (round -1: the largest over the rounds); 0 for senders. */
 int wb_plan_forward_bytes(const wb_plan_t* plan, int32_t round, int32_t stage, int64_t* out);
+
+/* One segment of the global plan (0 <= i < wb_plan_num_segments), in the order
+ * of wb_plan_dump: sender and receiver ranks (a trainer and a rollout rank in
+ * stage 0, rollout ranks in stages 1 and 2), checkpoint tensor and rectangle,
+ * stage and round, the trainer placement (stage 0; -1 otherwise) and the
+ * receiver's placement, offsets in the sender's send or forward buffer and in
+ * the receiver's receive buffer, for forwarded segments the offset of the
+ * forwarded bytes in the sender's receive buffer (else 0) and the index of the
+ * stage-0 segment they left the trainers in (a stage-0 segment's own index),
+ * and the payload bytes. Errors: WB_EINVAL (null, index out of range). */
+typedef struct wb_segment_info {
+  int32_t sender, receiver, tensor, stage, round, src_placement, dst_placement, reserved;
+  int64_t r0, r1, c0, c1;
+  int64_t send_offset, recv_offset, src_offset, origin, bytes;
+} wb_segment_info;
+int wb_plan_segment(const wb_plan_t* plan, int64_t i, wb_segment_info* out);
 /* Enqueue the forward packing of a receiver plan for exchange stage 1 or 2 of
  * one round: every payload this rank forwards in that stage is copied from
  * where it landed in recv_buf (wb_plan_round_buffer_bytes) to its offset in
@@ -328,6 +345,69 @@ int wb_forward_round(wb_plan_t* plan, int32_t round, int32_t stage, const void* 
                      void* stream);
 
 void wb_plan_destroy(wb_plan_t* plan);
+
+/* ---- source-map probing (Sec. 3.1; App. B, Algorithm 1) ---------------- */
+
+/* Layouts can also be discovered from a weight loader that copies values
+ * unchanged (a black box), instead of being declared. Every checkpoint element
+ * gets the identifier 2^24 + its flat position in the checkpoint (catalog
+ * order, row-major; 0 marks an element no loader wrote). The checkpoint is
+ * loaded once per 16-bit chunk of the identifiers (wb_probe_chunks passes);
+ * after pass k the caller runs wb_diff2 on every loaded local tensor and hands
+ * the entries to wb_probe_record. The library sums 2^(16 k) times pass k's
+ * entries, which is exactly diff2 of the full identifier field because diff2
+ * is linear (the paper's carry records are not needed for exactness), and
+ * wb_probe_scan turns the result into slice-copy placements without building
+ * the identifier field: between rows and columns that hold entries the field
+ * is a bilinear polynomial given by prefix sums of four moments of the
+ * entries; it must be affine inside every such cell, cells are merged into
+ * maximal affine rectangles, and each rectangle is decoded (flat runs as a
+ * partial head row, whole rows and a partial tail row; slabs; transposed
+ * slabs; anything else row by row or element by element).
+ * ckpt_dtype is WB_F32 or WB_BF16: the chunk travels as the bit pattern of a
+ * bf16 element or as the exact value of an f32 element.
+ * Errors: WB_EINVAL (null, bad catalog), WB_EUNSUPPORTED (other dtypes). */
+int wb_probe_create(const wb_tensor_desc* catalog, int32_t num_tensors, int32_t ckpt_dtype, wb_probe_t** out);
+/* Number of loading passes and identifier bits per pass (16). */
+int wb_probe_chunks(const wb_probe_t* probe, int32_t* num_chunks, int32_t* chunk_bits);
+/* Identifier of element (0, 0) of checkpoint tensor t. */
+int wb_probe_first_id(const wb_probe_t* probe, int32_t t, int64_t* id);
+/* Declare a local tensor of the probed rank, seen as a [batch * rows, cols]
+ * field; dtype is the checkpoint dtype (value-preserving loaders only). */
+int wb_probe_add_local(wb_probe_t* probe, const char* name, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                       int32_t* index);
+/* Host arrays of n entries of pass `chunk` for local tensor `local`: flat
+ * element index and diff2 value (as wb_diff2 writes them). Errors: WB_EINVAL
+ * (index or chunk out of range). */
+int wb_probe_record(wb_probe_t* probe, int32_t local, int32_t chunk, const int64_t* index, const int32_t* value,
+                    int64_t n);
+/* Fill rank `rank` of `layout` (made by wb_layout_create over the same catalog,
+ * with no local tensors yet) with the probe's local tensors and the placements
+ * recovered from the recorded passes. Errors: WB_EINVAL (catalogs differ, rank
+ * already filled), WB_EUNSUPPORTED (a field that is not made of slice copies
+ * of identifiers: the loader changed values or mixed elements). */
+int wb_probe_scan(const wb_probe_t* probe, wb_layout_t* layout, int32_t rank);
+void wb_probe_destroy(wb_probe_t* probe);
+
+/* Write chunk `chunk` (16 bits, chunk_bits = 16) of the identifiers
+ * first_id .. first_id + numel - 1 into a checkpoint tensor of dtype WB_BF16
+ * (bit pattern) or WB_F32 (exact value): Algorithm 1, MakeIdChunk. One launch.
+ * dst needs only element alignment. Errors: WB_EINVAL (null, misaligned, bad
+ * dtype or chunk). */
+int wb_make_ids(void* dst, int32_t dtype, int64_t numel, int64_t first_id, int32_t chunk, int32_t chunk_bits,
+                void* stream);
+/* diff2 (Eqs. diff1, diff2: the outer product of [1, -2, 1] with itself, the
+ * field taken as 0 above and left of the tensor) of the chunk field held by a
+ * loaded local tensor src of dtype WB_BF16 or WB_F32 seen as [rows, cols];
+ * appends the non-zero entries to the device arrays index (flat position) and
+ * value (at most `capacity` of them, order unspecified) and sets the device
+ * counter *count to the number of non-zero entries (which may exceed
+ * capacity: then call again with more room). The counter is reset by the
+ * call. One small and one stencil launch; the stencil reads each element about
+ * once. src, index and value need only element alignment. Errors: WB_EINVAL
+ * (null, misaligned, bad dtype or shape). */
+int wb_diff2(const void* src, int32_t dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
+             int64_t capacity, uint64_t* count, void* stream);
 
 /* Message of the calling thread's last failed call ("" if none). */
 const char* wb_last_error(void);

@@ -53,6 +53,13 @@ class TensorDesc(ctypes.Structure):
     _fields_ = [("name", c_char_p), ("rows", c_int64), ("cols", c_int64)]
 
 
+class SegmentInfo(ctypes.Structure):
+    _fields_ = [(n, c_int32) for n in ("sender", "receiver", "tensor", "stage", "round", "src_placement",
+                                       "dst_placement", "reserved")] + \
+               [(n, c_int64) for n in ("r0", "r1", "c0", "c1", "send_offset", "recv_offset", "src_offset", "origin",
+                                       "bytes")]
+
+
 class LocalInfo(ctypes.Structure):
     _fields_ = [("name", c_char_p), ("dtype", c_int32), ("quant_block", c_int32), ("batch", c_int64),
                 ("rows", c_int64), ("cols", c_int64), ("scale_index", c_int32), ("scales_index", c_int32)]
@@ -109,6 +116,15 @@ def _load():
                                  POINTER(c_int64)],
         "wb_plan_forward_bytes": [P, c_int32, c_int32, POINTER(c_int64)],
         "wb_forward_round": [P, c_int32, c_int32, c_void_p, c_void_p, c_void_p],
+        "wb_plan_segment": [P, c_int64, POINTER(SegmentInfo)],
+        "wb_probe_create": [POINTER(TensorDesc), c_int32, c_int32, POINTER(c_void_p)],
+        "wb_probe_chunks": [c_void_p, POINTER(c_int32), POINTER(c_int32)],
+        "wb_probe_first_id": [c_void_p, c_int32, POINTER(c_int64)],
+        "wb_probe_add_local": [c_void_p, c_char_p, c_int32, c_int64, c_int64, c_int64, POINTER(c_int32)],
+        "wb_probe_record": [c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_int64],
+        "wb_probe_scan": [c_void_p, L, c_int32],
+        "wb_make_ids": [c_void_p, c_int32, c_int64, c_int64, c_int32, c_int32, c_void_p],
+        "wb_diff2": [c_void_p, c_int32, c_int64, c_int64, c_void_p, c_void_p, c_int64, c_void_p, c_void_p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -118,6 +134,8 @@ def _load():
     lib.wb_layout_destroy.restype = None
     lib.wb_plan_destroy.argtypes = [P]
     lib.wb_plan_destroy.restype = None
+    lib.wb_probe_destroy.argtypes = [c_void_p]
+    lib.wb_probe_destroy.restype = None
     lib.wb_last_error.restype = c_char_p
     lib.wb_version.restype = c_char_p
     return lib
@@ -338,6 +356,15 @@ class Plan:
         _check(lib.wb_plan_stage_region(self._h, rnd, stage, sender, receiver, byref(s), byref(r), byref(b)))
         return s.value, r.value, b.value
 
+    def segments(self):
+        """Every segment of the global plan as a dict (the order of dump())."""
+        out = []
+        for i in range(self.num_segments):
+            g = SegmentInfo()
+            _check(lib.wb_plan_segment(self._h, i, byref(g)))
+            out.append({f: getattr(g, f) for f, _ in SegmentInfo._fields_ if f != "reserved"})
+        return out
+
     def forward_bytes(self, stage: int, rnd: int = -1) -> int:
         v = c_int64()
         _check(lib.wb_plan_forward_bytes(self._h, rnd, stage, byref(v)))
@@ -407,6 +434,139 @@ class Plan:
     def __del__(self):
         if getattr(self, "_h", None) is not None and self._h.value:
             _release(self)
+
+
+class Probe:
+    """Source-map probing of one rank (Sec. 3.1; App. B, Algorithm 1): identifier
+    chunks are written into a checkpoint, a weight loader copies them into the
+    rank's tensors, diff2 entries of every pass are recorded and scanned back
+    into placements."""
+
+    def __init__(self, catalog, ckpt_dtype: str):
+        arr = (TensorDesc * len(catalog))()
+        self._names = []
+        for i, (n, r, c) in enumerate(catalog):
+            b = n.encode()
+            self._names.append(b)
+            arr[i] = TensorDesc(b, r, c)
+        h = c_void_p()
+        _check(lib.wb_probe_create(arr, len(catalog), DTYPES[ckpt_dtype], byref(h)))
+        self._h = h
+        self._destroy = lib.wb_probe_destroy
+        _live.add(self)
+        self.catalog = list(catalog)
+        self.dtype = ckpt_dtype
+        n, b = c_int32(), c_int32()
+        _check(lib.wb_probe_chunks(self._h, byref(n), byref(b)))
+        self.num_chunks, self.chunk_bits = n.value, b.value
+
+    def first_id(self, t: int) -> int:
+        v = c_int64()
+        _check(lib.wb_probe_first_id(self._h, t, byref(v)))
+        return v.value
+
+    def add_local(self, name, dtype, batch, rows, cols) -> int:
+        v = c_int32()
+        _check(lib.wb_probe_add_local(self._h, name.encode(), DTYPES[dtype], batch, rows, cols, byref(v)))
+        return v.value
+
+    def record(self, local: int, chunk: int, index, value):
+        """index (int64) and value (int32) host arrays (numpy) of one pass."""
+        import numpy as np
+
+        index = np.ascontiguousarray(index, dtype=np.int64)
+        value = np.ascontiguousarray(value, dtype=np.int32)
+        _check(lib.wb_probe_record(self._h, local, chunk, index.ctypes.data, value.ctypes.data, len(index)))
+
+    def scan(self, layout: "Layout", rank: int):
+        _check(lib.wb_probe_scan(self._h, layout._h, rank))
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _release(self)
+
+
+def make_ids(dst, dtype: str, first_id: int, chunk: int, stream=None):
+    """Write identifier chunk ``chunk`` of first_id, first_id + 1, ... into the
+    tensor ``dst`` (every element, in storage order)."""
+    _check(lib.wb_make_ids(_ptr(dst), DTYPES[dtype], dst.numel(), first_id, chunk, 16, _stream_handle(stream)))
+
+
+def diff2(src, dtype: str, rows: int, cols: int, index, value, count, stream=None):
+    """Non-zero diff2 entries of a [rows, cols] chunk field into the device
+    tensors index (int64), value (int32); count (uint64 device scalar) gets
+    their number (which may exceed the arrays' length)."""
+    _check(lib.wb_diff2(_ptr(src), DTYPES[dtype], rows, cols, _ptr(index), _ptr(value), index.numel(), _ptr(count),
+                        _stream_handle(stream)))
+
+
+def _view_shape(t):
+    if t.dim() == 1:
+        return 1, 1, t.shape[0]
+    if t.dim() == 2:
+        return 1, t.shape[0], t.shape[1]
+    if t.dim() == 3:
+        return t.shape[0], t.shape[1], t.shape[2]
+    raise ValueError("local tensors must be 1-, 2- or 3-D")
+
+
+def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", stats=None) -> "Layout":
+    """Discover a layout from weight loaders: ``loaders[r](ckpt)`` takes the
+    checkpoint as {name: tensor} and returns rank r's local tensors (a list of
+    1-, 2- or 3-D tensors, always the same shapes, values copied unchanged).
+    Returns a Layout with one rank per loader. ``stats`` (a dict) receives
+    timings and entry counts when given."""
+    import time
+
+    import numpy as np
+    import torch
+
+    tdt = torch_dtype(ckpt_dtype)
+    layout = Layout.create(catalog, len(loaders))
+    count = torch.zeros(1, dtype=torch.int64, device=device)
+    ckpt = {n: torch.empty((r, c), dtype=tdt, device=device) for n, r, c in catalog}
+    for r, load in enumerate(loaders):
+        probe = Probe(catalog, ckpt_dtype)
+        shapes = None
+        for k in range(probe.num_chunks):
+            t0 = time.perf_counter()
+            for t, (n, rows, cols) in enumerate(catalog):
+                make_ids(ckpt[n], ckpt_dtype, probe.first_id(t), k)
+            t1 = time.perf_counter()
+            locs = load(ckpt)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            if shapes is None:
+                shapes = [_view_shape(x) for x in locs]
+                for u, (b, rr, cc) in enumerate(shapes):
+                    probe.add_local(names[r][u] if names else f"local{u}", ckpt_dtype, b, rr, cc)
+            entries = 0
+            for u, x in enumerate(locs):
+                if x.dtype != tdt or not x.is_contiguous() or _view_shape(x) != shapes[u]:
+                    raise ValueError(f"loader of rank {r} returned a changed or non-contiguous tensor {u}")
+                b, rr, cc = shapes[u]
+                cap = max(4096, x.numel() // 512)
+                while True:
+                    idx = torch.empty(cap, dtype=torch.int64, device=device)
+                    val = torch.empty(cap, dtype=torch.int32, device=device)
+                    diff2(x, ckpt_dtype, b * rr, cc, idx, val, count)
+                    n_ent = int(count.item())
+                    if n_ent <= cap:
+                        break
+                    cap = n_ent
+                probe.record(u, k, idx[:n_ent].cpu().numpy(), val[:n_ent].cpu().numpy())
+                entries += n_ent
+            del locs
+            t3 = time.perf_counter()
+            if stats is not None:
+                s = stats.setdefault(r, [])
+                s.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries})
+        t4 = time.perf_counter()
+        probe.scan(layout, r)
+        if stats is not None:
+            stats.setdefault("scan_s", []).append(time.perf_counter() - t4)
+        del probe
+    return layout
 
 
 def version() -> str:

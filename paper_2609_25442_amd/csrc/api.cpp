@@ -48,9 +48,10 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // Refuse a pointer whose device allocation is smaller than what the kernels
 // will touch. Memory the runtime cannot size (e.g. pinned host memory) is
 // accepted as given.
-int check_extent(const void* p, int64_t bytes, const char* what) {
+int check_extent(const void* p, int64_t bytes, const char* what, int align = 16) {
   if (!p) return set_error(WB_EINVAL, std::string(what) + " is null");
-  if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return set_error(WB_EINVAL, std::string(what) + " is not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(p) % align != 0)
+    return set_error(WB_EINVAL, std::string(what) + " is not " + std::to_string(align) + "-byte aligned");
   hipDeviceptr_t base = nullptr;
   size_t size = 0;
   if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
@@ -390,6 +391,15 @@ int wb_plan_stage_region(const wb_plan_t* P, int32_t round, int32_t stage, int32
   return WB_OK;
 }
 
+int wb_plan_segment(const wb_plan_t* P, int64_t i, wb_segment_info* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  if (i < 0 || i >= static_cast<int64_t>(P->segs.size())) return set_error(WB_EINVAL, "segment index out of range");
+  const wb::Segment& g = P->segs[i];
+  *out = wb_segment_info{g.s, g.d, g.t, g.stage, g.round, g.src_pl, g.dst_pl, 0, g.x.r0, g.x.r1, g.x.c0, g.x.c1,
+                         g.send_off, g.recv_off, g.src_off, g.origin, g.bytes};
+  return WB_OK;
+}
+
 int wb_plan_forward_bytes(const wb_plan_t* P, int32_t round, int32_t stage, int64_t* out) {
   if (!P || !out) return set_error(WB_EINVAL, "null argument");
   if (stage != 1 && stage != 2) return set_error(WB_EINVAL, "stage must be 1 or 2");
@@ -588,6 +598,105 @@ int wb_unpack(wb_plan_t* P, const void* recv_buf, void* const* dst_ptrs, void* s
     if (!P) return set_error(WB_EINVAL, "null plan");
     if (P->rounds.size() != 1) return set_error(WB_EINVAL, "the plan has several rounds: use wb_unpack_round");
     return run_round(P, 0, const_cast<const void* const*>(dst_ptrs), recv_buf, stream, WB_RECEIVER);
+  });
+}
+
+int wb_probe_create(const wb_tensor_desc* catalog, int32_t num_tensors, int32_t ckpt_dtype, wb_probe_t** out) {
+  return guarded([&]() -> int {
+    if (!out || !catalog || num_tensors < 1) return set_error(WB_EINVAL, "bad catalog");
+    *out = nullptr;
+    auto* P = new wb_probe_t;
+    try {
+      wb::probe_init(*P, catalog, num_tensors, ckpt_dtype);
+    } catch (...) {
+      delete P;
+      throw;
+    }
+    *out = P;
+    return WB_OK;
+  });
+}
+
+int wb_probe_chunks(const wb_probe_t* P, int32_t* num_chunks, int32_t* chunk_bits) {
+  if (!P || !num_chunks || !chunk_bits) return set_error(WB_EINVAL, "null argument");
+  *num_chunks = P->nchunks;
+  *chunk_bits = P->bits;
+  return WB_OK;
+}
+
+int wb_probe_first_id(const wb_probe_t* P, int32_t t, int64_t* id) {
+  if (!P || !id) return set_error(WB_EINVAL, "null argument");
+  if (t < 0 || t >= static_cast<int>(P->first.size())) return set_error(WB_EINVAL, "tensor out of range");
+  *id = P->first[t];
+  return WB_OK;
+}
+
+int wb_probe_add_local(wb_probe_t* P, const char* name, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
+                       int32_t* index) {
+  return guarded([&]() -> int {
+    if (!P || !name || !index) return set_error(WB_EINVAL, "null argument");
+    if (batch < 1 || rows < 1 || cols < 1) return set_error(WB_EINVAL, "local tensor shape must be positive");
+    if (dtype != P->dtype) return set_error(WB_EUNSUPPORTED, "probed local tensors take the checkpoint dtype");
+    wb::ProbeLocal L;
+    L.name = name;
+    L.dtype = dtype;
+    L.batch = batch;
+    L.rows = rows;
+    L.cols = cols;
+    P->locals.push_back(std::move(L));
+    *index = static_cast<int32_t>(P->locals.size() - 1);
+    return WB_OK;
+  });
+}
+
+int wb_probe_record(wb_probe_t* P, int32_t local, int32_t chunk, const int64_t* index, const int32_t* value,
+                    int64_t n) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null probe");
+    wb::probe_record(*P, local, chunk, index, value, n);
+    return WB_OK;
+  });
+}
+
+int wb_probe_scan(const wb_probe_t* P, wb_layout_t* L, int32_t rank) {
+  return guarded([&]() -> int {
+    if (!P || !L) return set_error(WB_EINVAL, "null argument");
+    wb::probe_scan(*P, *L, rank);
+    return WB_OK;
+  });
+}
+
+void wb_probe_destroy(wb_probe_t* P) { delete P; }
+
+int wb_make_ids(void* dst, int32_t dtype, int64_t numel, int64_t first_id, int32_t chunk, int32_t chunk_bits,
+                void* stream) {
+  return guarded([&]() -> int {
+    if (dtype != WB_F32 && dtype != WB_BF16) return set_error(WB_EINVAL, "identifier chunks need f32 or bf16");
+    if (chunk_bits != 16 || chunk < 0 || chunk * chunk_bits >= 64 || numel < 0 || first_id < 0)
+      return set_error(WB_EINVAL, "bad chunk, width, size or first identifier");
+    if (numel == 0) return WB_OK;
+    const int rc = check_extent(dst, numel * wb::dtype_bytes(dtype), "dst", wb::dtype_bytes(dtype));
+    if (rc != WB_OK) return rc;
+    const int e = wb::launch_make_ids(dst, dtype, numel, first_id, chunk * chunk_bits, 0xFFFFu, stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("identifier launch: ") + wb::hip_error_string(e));
+    return WB_OK;
+  });
+}
+
+int wb_diff2(const void* src, int32_t dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
+             int64_t capacity, uint64_t* count, void* stream) {
+  return guarded([&]() -> int {
+    if (dtype != WB_F32 && dtype != WB_BF16) return set_error(WB_EINVAL, "diff2 needs an f32 or bf16 field");
+    if (rows < 1 || cols < 1 || capacity < 0) return set_error(WB_EINVAL, "bad shape or capacity");
+    if (!count || reinterpret_cast<uintptr_t>(count) % 8) return set_error(WB_EINVAL, "count must be 8-byte aligned");
+    int rc = check_extent(src, rows * cols * wb::dtype_bytes(dtype), "src", wb::dtype_bytes(dtype));
+    if (rc == WB_OK && capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
+    if (rc == WB_OK && capacity > 0) rc = check_extent(value, capacity * 4, "value", 4);
+    if (rc != WB_OK) return rc;
+    const int e = wb::launch_diff2(src, dtype, rows, cols, index, value, capacity,
+                                   reinterpret_cast<unsigned long long*>(count), stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("diff2 launch: ") + wb::hip_error_string(e));
+    return WB_OK;
   });
 }
 

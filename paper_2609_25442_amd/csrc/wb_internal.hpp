@@ -4,6 +4,7 @@
 #include <cstdint>
 #include <stdexcept>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/wb.h"
@@ -164,7 +165,23 @@ static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
 enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
 
+// A local tensor of a probed rank and its recombined diff2 entries.
+struct ProbeLocal {
+  std::string name;
+  int dtype = WB_BF16;
+  int64_t batch = 1, rows = 1, cols = 1;
+  std::unordered_map<int64_t, __int128> z;  // flat index -> sum over passes
+};
+
 }  // namespace wb
+
+struct wb_probe_t {
+  std::vector<wb::Tensor> catalog;
+  std::vector<int64_t> first;  // identifier of element (0, 0) of every tensor
+  int64_t end_id = 0;          // one past the last identifier
+  int dtype = WB_BF16, bits = 16, nchunks = 0;
+  std::vector<wb::ProbeLocal> locals;
+};
 
 struct wb_plan_t {
   // global plan
@@ -211,4 +228,12 @@ int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream);
 const char* hip_error_string(int err);
+// probe.cpp
+void probe_init(wb_probe_t& P, const wb_tensor_desc* catalog, int n, int ckpt_dtype);
+void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int32_t* value, int64_t n);
+void probe_scan(const wb_probe_t& P, wb_layout_t& out, int rank);
+// probe.hip
+int launch_make_ids(void* dst, int dtype, int64_t numel, int64_t first_id, int shift, uint32_t mask, void* stream);
+int launch_diff2(const void* src, int dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
+                 int64_t capacity, unsigned long long* count, void* stream);
 }  // namespace wb

@@ -1,9 +1,12 @@
-"""Expected local tensors of each layout style, written with torch slicing.
+"""Stand-in weight loaders of the trainer and rollout engines, written with
+torch slicing.
 
-An independent statement of what each parallelism style stores, built from
-whole-tensor torch operations (chunk, cat, stack, t, flatten) rather than from
-placements, so that it can pin the oracle's placement arithmetic. Used only by
-tests.
+Each style function takes the checkpoint as {name: tensor} and returns one
+rank's local tensors, built from whole-tensor torch operations (chunk, cat,
+stack, t, flatten) rather than from placements. They serve two purposes: an
+independent statement of what each parallelism style stores (pinning the
+declared placements), and the black-box loader whose copies source-map probing
+observes. Copies here never change values.
 """
 
 from __future__ import annotations

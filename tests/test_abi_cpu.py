@@ -271,3 +271,22 @@ def test_exchange_errors():
     T.add_placement(0, 0, 0, 2, 0, 4, 0, 0, 4)
     assert wb.Plan(T, R, wb.RECEIVER, 0).num_segments == 2
     _expect(wb.WB_EINVAL, wb.Plan, T, R, wb.RECEIVER, 0, 0, 1)
+
+
+def test_segment_query_matches_the_oracle():
+    from oracle_cases import hand_exchange_pair
+    tr, ro = hand_exchange_pair()
+    op = build_plan(tr, ro, node_size=2)
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 2, node_size=2)
+    segs = p.segments()
+    assert len(segs) == len(op.segments) == 17
+    for a, g in zip(segs, op.segments):
+        assert (a["sender"], a["receiver"], a["tensor"], a["stage"], a["round"]) == (g.s, g.d, g.t, g.stage, g.round)
+        assert (a["r0"], a["r1"], a["c0"], a["c1"]) == (g.rect.r0, g.rect.r1, g.rect.c0, g.rect.c1)
+        assert (a["send_offset"], a["recv_offset"], a["bytes"], a["origin"]) == (g.send_off, g.recv_off, g.nbytes, g.origin)
+        assert a["src_offset"] == g.src_off and a["dst_placement"] == g.dst_pl
+        assert a["src_placement"] == (g.src_pl if g.stage == 0 else -1)
+    import ctypes
+    info = wb.SegmentInfo()
+    assert wb.lib.wb_plan_segment(p._h, 17, ctypes.byref(info)) == wb.WB_EINVAL
+    assert wb.lib.wb_plan_segment(p._h, -1, ctypes.byref(info)) == wb.WB_EINVAL

@@ -2,7 +2,7 @@
 
 * catalogs against published parameter counts and hand closed forms;
 * every layout style against an independent torch-slicing construction
-  (tests/layout_reference.py), using unique element identifiers, the same
+  (synthetic_checkpoint/loaders.py), using unique element identifiers, the same
   device the paper uses to reveal a loader's source map (Sec. 3.1);
 * full coverage of rollout tensors and in-bounds placements.
 """
@@ -18,7 +18,7 @@ from oracle.layout import Parallelism, describe_layout, flat_run_rects, layout_f
 from oracle.transfer import materialize
 from synthetic_checkpoint.workloads import ORDER, WORKLOADS, scaled
 
-from layout_reference import STYLES, ckpt_shapes
+from synthetic_checkpoint.loaders import STYLES, ckpt_shapes
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
