@@ -306,6 +306,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--round-budget", type=int, default=0,
                     help="bytes per rank per round (0: one round); each step packs and unpacks every round")
+    ap.add_argument("--node-size", type=int, default=0,
+                    help="rollout ranks per node: plan with rollout de-duplication and the two exchange stages; "
+                         "each step also runs the unpack rank's forward packings")
     ap.add_argument("--pipeline", action="store_true",
                     help="with rounds: pack round k+1 on one stream while round k is assembled on another")
     ap.add_argument("--probe", action="store_true",
@@ -364,9 +367,9 @@ def main():
             p = wb.Plan(tr, ro, role, rank)
             ts.append((time.perf_counter() - t0) * 1e3)
         plan_ms[label] = round(statistics.median(ts), 2)
-    rb = args.round_budget
-    rplan = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=rb)
-    splan = wb.Plan(tr, ro, wb.SENDER, s0, round_budget=rb)
+    rb, G = args.round_budget, args.node_size
+    rplan = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=rb, node_size=G)
+    splan = wb.Plan(tr, ro, wb.SENDER, s0, round_budget=rb, node_size=G)
     nr = rplan.num_rounds
     rws = torch.empty(rplan.workspace_bytes, dtype=torch.uint8, device="cuda")
     sws = torch.empty(splan.workspace_bytes, dtype=torch.uint8, device="cuda")
@@ -385,21 +388,37 @@ def main():
     recvs = [alloc(rplan.round_buffer_bytes(k)) for k in range(nr)]
     sends = [alloc(splan.buffer_bytes) for _ in range(min(2, nr))]
     recv, send0 = recvs[0], sends[0]
+    fwds = {st: alloc(rplan.forward_bytes(st)) for st in (1, 2)} if G else {}
+    # with exchange stages, the payloads forwarded to the unpack rank are the
+    # bytes their origin segment left a trainer with: copied out of that
+    # trainer's send buffer into their section of the receive buffer
+    forwarded = {}
+    if G:
+        segs = rplan.segments()
+        for f in segs:
+            if f["stage"] and f["receiver"] == d:
+                o = segs[f["origin"]]
+                forwarded.setdefault(o["sender"], []).append((o, f))
     src0 = None
     for s in range(tr.nranks):
-        if s != s0 and not any(rplan.round_region(k, s, d)[2] for k in range(nr)):
+        if s != s0 and s not in forwarded and not any(rplan.round_region(k, s, d)[2] for k in range(nr)):
             continue
         locs = build_sender_locals(wb, torch, sc, tr, s, src_dtype)
-        p = splan if s == s0 else wb.Plan(tr, ro, wb.SENDER, s, round_budget=rb)
+        p = splan if s == s0 else wb.Plan(tr, ro, wb.SENDER, s, round_budget=rb, node_size=G)
         if s != s0:
             ws = torch.empty(p.workspace_bytes, dtype=torch.uint8, device="cuda")
             p.upload(ws)
         buf = send0 if s == s0 else alloc(p.buffer_bytes)
         for k in range(nr):
             so, roff, nb = rplan.round_region(k, s, d)
-            if nb:
+            mine = [(o, f) for o, f in forwarded.get(s, []) if o["round"] == k]
+            if nb or mine:
                 (p.pack_round(k, locs, buf) if nr > 1 else p.pack(locs, buf))
+            if nb:
                 recvs[k][roff:roff + nb] = buf[so:so + nb]
+            for o, f in mine:
+                recvs[k][f["recv_offset"]:f["recv_offset"] + f["bytes"]] = \
+                    buf[o["send_offset"]:o["send_offset"] + o["bytes"]]
         if s == s0:
             src0 = locs
         else:
@@ -412,7 +431,10 @@ def main():
     pr, pw = splan.traffic()
     ur, uw = rplan.traffic()
     pack_bytes, unpack_bytes = pr + pw, ur + uw
+    fwd_bytes = {st: sum(rplan.kernel_traffic(1 + st)) for st in (1, 2)} if G else {}
     stream = torch.cuda.current_stream()
+    if G and args.pipeline:
+        sys.exit("--pipeline and --node-size are not combined")
 
     if args.pipeline and nr < 2:
         sys.exit("--pipeline needs a round budget that gives more than one round")
@@ -427,9 +449,13 @@ def main():
             splan.pack(src0, send0, stream)
             if ev:
                 ev[1].record(stream)
+            for st in fwds:
+                rplan.forward_round(0, st, recv, fwds[st], stream)
+                if ev:
+                    ev[1 + st].record(stream)
             rplan.unpack(recv, dst, stream)
             if ev:
-                ev[2].record(stream)
+                ev[-1].record(stream)
             return
         if args.pipeline:
             # depth 2: round k+2 reuses the send buffer of round k, so its pack
@@ -450,12 +476,14 @@ def main():
             return
         for k in range(nr):
             splan.pack_round(k, src0, sends[k % 2], stream)
+            for st in fwds:
+                rplan.forward_round(k, st, recvs[k], fwds[st], stream)
             rplan.unpack_round(k, recvs[k], dst, stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 + len(fwds))] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -463,9 +491,12 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
+    fwd_ms = {}
     if nr == 1:
         pack_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in events)
-        unpack_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in events)
+        for st in fwds:
+            fwd_ms[st] = statistics.mean(e[st].elapsed_time(e[1 + st]) for e in events)
+        unpack_ms = statistics.mean(e[-2].elapsed_time(e[-1]) for e in events)
     else:
         # per-kernel times of a round-based step: one more pass timing the
         # packs and the unpacks of all rounds separately
@@ -479,7 +510,7 @@ def main():
         e[2].record(stream)
         torch.cuda.synchronize()
         pack_ms, unpack_ms = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])
-    value = (pack_bytes + unpack_bytes) / (ms_per_step * 1e-3) / 1e9
+    value = (pack_bytes + sum(fwd_bytes.values()) + unpack_bytes) / (ms_per_step * 1e-3) / 1e9
 
     # practical ceiling: a plain device copy of the receive buffer (also the
     # known-size copy that calibrates the HBM byte counters)
@@ -522,7 +553,7 @@ def main():
         "config": {"workload": args.workload, "trainer": w["trainer"], "rollout": w["rollout"],
                    "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes,
                    "buffers": "pinned host (PCIe)" if args.staged else "device",
-                   "rounds": nr, "round_budget": rb, "pipeline": bool(args.pipeline)},
+                   "rounds": nr, "round_budget": rb, "pipeline": bool(args.pipeline), "node_size": G},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "plan_ms": plan_ms,
         "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
@@ -533,7 +564,12 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
     }
-    if not args.no_cpu_baseline and nr == 1:
+    if fwds:
+        out["forward"] = {f"stage{st}": {"bytes": fwd_bytes[st], "ms": round(fwd_ms[st], 4) if st in fwd_ms else None,
+                                         "GB/s": round(fwd_bytes[st] / (fwd_ms[st] * 1e-3) / 1e9, 1)
+                                         if fwd_ms.get(st) else None} for st in fwds}
+        out["config"]["bytes_per_step"] = pack_bytes + sum(fwd_bytes.values()) + unpack_bytes
+    if not args.no_cpu_baseline and nr == 1 and not G:
         def recv_host(off, nb, out):
             torch.from_numpy(out[:nb]).copy_(recv[off:off + nb])
         out["cpu_baseline"] = cpu_baseline(w, recv_host)
