@@ -53,10 +53,18 @@ def build_sender_locals(wb, torch, sc, layout, rank, dtype):
     return locs
 
 
-def kernel_source_hash():
+def work_fingerprint(workload):
+    """What the committed HBM-traffic counters of a workload depend on: the
+    kernels' source and the benchmarked plans' work tables (work-item counts and
+    algorithmic bytes of every launch, under the current task size). The
+    counters are reported only while this is unchanged."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+
     h = hashlib.sha256()
-    for f in ("kernels.hip", "plan.cpp"):
-        h.update(open(os.path.join(ROOT, "paper_2609_25442_amd", "csrc", f), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2609_25442_amd", "csrc", "kernels.hip"), "rb").read())
+    grids, _ = _launch_grids(WORKLOADS[workload])
+    h.update(repr(sorted(grids.items())).encode())
+    h.update(os.environ.get("WB_TASK_BYTES", "").encode())
     return h.hexdigest()[:16]
 
 
@@ -67,7 +75,7 @@ def stored_traffic(workload, kernel):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("source_hash") != kernel_source_hash() or kernel not in rec.get("kernels", {}):
+    if rec.get("work_fingerprint") != work_fingerprint(workload) or kernel not in rec.get("kernels", {}):
         return None
     return rec["kernels"][kernel]["hbm_bytes_per_launch"]
 
@@ -180,7 +188,7 @@ def summarize_counters(workload, fetch_csv, write_csv):
 
     grids, recv_bytes = _launch_grids(WORKLOADS[workload])
     copy_bytes = min(recv_bytes, 16 << 30)
-    out = {"workload": workload, "source_hash": kernel_source_hash(), "kernels": {}, "calibration": {}}
+    out = {"workload": workload, "work_fingerprint": work_fingerprint(workload), "kernels": {}, "calibration": {}}
     per = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         rows = [r for r in _read_csv(path) if r["Counter_Name"] == counter]
@@ -227,6 +235,29 @@ def summarize_trace(workload, trace_csv):
         top = sorted(copies)[-3:]
         res["device_copy"] = {"launches": len(top), "avg_us": round(statistics.mean(top) / 1e3, 2)}
     return res
+
+
+def run_plan_stress():
+    """Host planning time on a DeepSeek-V3-like catalog of 58 MoE layers
+    (44,776 checkpoint tensors), EP64 bf16 trainer -> EP8 fp8 rollout: median of
+    five plans per role, with and without the exchange stages."""
+    import paper_2609_25442_amd as wb
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    w = WORKLOADS["dsv3_ep64_to_ep8_fp8"]
+    m = dict(w["model"], num_layers=58)
+    tr = wb.Layout.describe(m, w["trainer"])
+    ro = wb.Layout.describe(m, w["rollout"])
+    out = {"metric": "wb_plan ms (58-layer DeepSeek-V3-like catalog)", "tensors": len(tr.tensors()), "plan_ms": {}}
+    for label, role, G in (("receiver", wb.RECEIVER, 0), ("sender", wb.SENDER, 0), ("receiver_exchange_G4", wb.RECEIVER, 4)):
+        ts = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            p = wb.Plan(tr, ro, role, 0, node_size=G)
+            ts.append((time.perf_counter() - t0) * 1e3)
+        out["plan_ms"][label] = {"median": round(statistics.median(ts), 1), "segments": p.num_segments,
+                                 "work": p.work_counts()}
+    print(json.dumps(out), flush=True)
 
 
 def run_probe(args):
@@ -311,6 +342,8 @@ def main():
                          "each step also runs the unpack rank's forward packings")
     ap.add_argument("--pipeline", action="store_true",
                     help="with rounds: pack round k+1 on one stream while round k is assembled on another")
+    ap.add_argument("--plan-stress", action="store_true",
+                    help="wb_plan time on a 58-MoE-layer DeepSeek-V3-like catalog (44,776 tensors, EP64 -> EP8 fp8)")
     ap.add_argument("--probe", action="store_true",
                     help="discover the trainer and rollout ranks' layouts by probing torch loaders (diff2 kernels)")
     ap.add_argument("--staged", action="store_true",
@@ -344,6 +377,9 @@ def main():
 
     if args.probe:
         run_probe(args)
+        return
+    if args.plan_stress:
+        run_plan_stress()
         return
 
     import torch

@@ -231,6 +231,9 @@ int wb_plan_region(const wb_plan_t* plan, int32_t sender, int32_t receiver, int6
 int wb_plan_rank_buffer_bytes(const wb_plan_t* plan, int32_t role, int32_t rank, int64_t* out);
 /* Number of local tensors of this rank: the length of src_ptrs / dst_ptrs. */
 int wb_plan_num_local_tensors(const wb_plan_t* plan, int32_t* out);
+/* dtype (wb_dtype) and element count of src_ptrs[i] / dst_ptrs[i] (fp8
+ * tensors' scale companions are entries of their own). Errors: WB_EINVAL. */
+int wb_plan_local_tensor(const wb_plan_t* plan, int32_t i, int32_t* dtype, int64_t* numel);
 /* Bytes of device workspace wb_plan_upload needs. */
 int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
 /* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */

@@ -117,6 +117,7 @@ def _load():
         "wb_plan_forward_bytes": [P, c_int32, c_int32, POINTER(c_int64)],
         "wb_forward_round": [P, c_int32, c_int32, c_void_p, c_void_p, c_void_p],
         "wb_plan_segment": [P, c_int64, POINTER(SegmentInfo)],
+        "wb_plan_local_tensor": [P, c_int32, POINTER(c_int32), POINTER(c_int64)],
         "wb_probe_create": [POINTER(TensorDesc), c_int32, c_int32, POINTER(c_void_p)],
         "wb_probe_chunks": [c_void_p, POINTER(c_int32), POINTER(c_int32)],
         "wb_probe_first_id": [c_void_p, c_int32, POINTER(c_int64)],
@@ -318,6 +319,12 @@ class Plan:
         v = c_int32()
         _check(lib.wb_plan_num_local_tensors(self._h, byref(v)))
         return v.value
+
+    def local_tensor(self, i: int):
+        """(dtype name, element count) of pointer-table entry i."""
+        dt, n = c_int32(), c_int64()
+        _check(lib.wb_plan_local_tensor(self._h, i, byref(dt), byref(n)))
+        return DTYPE_NAMES[dt.value], n.value
 
     @property
     def num_rounds(self) -> int:

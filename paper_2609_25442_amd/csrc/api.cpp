@@ -423,6 +423,15 @@ int wb_plan_num_local_tensors(const wb_plan_t* P, int32_t* out) {
   return WB_OK;
 }
 
+int wb_plan_local_tensor(const wb_plan_t* P, int32_t i, int32_t* dtype, int64_t* numel) {
+  if (!P || !dtype || !numel) return set_error(WB_EINVAL, "null argument");
+  if (i < 0 || i >= P->n_locals) return set_error(WB_EINVAL, "local tensor index out of range");
+  const wb::Local& l = rank_of(P).locals[i];
+  *dtype = l.dtype;
+  *numel = l.numel();
+  return WB_OK;
+}
+
 static void workspace_layout(const wb_plan_t* P, size_t* ptrs, size_t* tasks, size_t* qb, size_t* qp, size_t* total) {
   size_t off = 0;
   *ptrs = off;

@@ -377,7 +377,9 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
       block_round[id] = g.round;
     });
   }
-  P.qblocks.resize(nblocks);
+  // blocks are built in id order (locals, then batch, block row, block column)
+  P.qblocks.clear();
+  P.qblocks.reserve(nblocks);
   for (size_t u = 0; u < R.locals.size(); ++u) {
     const Local& l = R.locals[u];
     if (l.block <= 0) continue;
@@ -412,20 +414,24 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
               b.src_ld = q.src_ld;
             }
           }
-          P.qblocks[id] = b;
+          if (static_cast<int64_t>(P.qblocks.size()) != id) fail(WB_EINVAL, "internal: fp8 block order");
+          P.qblocks.push_back(b);
         }
   }
-  // group the blocks by round (stable: canonical block order within a round)
-  std::vector<uint32_t> order(nblocks);
-  std::iota(order.begin(), order.end(), 0u);
-  std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return block_round[a] < block_round[b]; });
-  std::vector<QBlock> sorted(nblocks);
-  for (int64_t i = 0; i < nblocks; ++i) {
-    sorted[i] = P.qblocks[order[i]];
-    P.round_qblocks[block_round[order[i]] + 1] = static_cast<uint32_t>(i + 1);
+  // group the blocks by round, canonical block order within a round (a
+  // counting placement; one round needs none)
+  std::vector<uint32_t> start(nrounds + 1, 0);
+  for (int64_t i = 0; i < nblocks; ++i) ++start[block_round[i] + 1];
+  for (int k = 0; k < nrounds; ++k) start[k + 1] += start[k];
+  P.round_qblocks.assign(start.begin(), start.end());
+  if (nrounds > 1) {
+    std::vector<uint32_t> at(nblocks);
+    for (int64_t i = 0; i < nblocks; ++i) at[start[block_round[i]]++] = static_cast<uint32_t>(i);
+    std::vector<QBlock> sorted;
+    sorted.reserve(nblocks);
+    for (int64_t i = 0; i < nblocks; ++i) sorted.push_back(P.qblocks[at[i]]);
+    P.qblocks.swap(sorted);
   }
-  for (int k = 0; k < nrounds; ++k) P.round_qblocks[k + 1] = std::max(P.round_qblocks[k + 1], P.round_qblocks[k]);
-  P.qblocks.swap(sorted);
 }
 
 // Every byte a work item touches lies inside its buffer, and vector work items

@@ -290,3 +290,15 @@ def test_segment_query_matches_the_oracle():
     info = wb.SegmentInfo()
     assert wb.lib.wb_plan_segment(p._h, 17, ctypes.byref(info)) == wb.WB_EINVAL
     assert wb.lib.wb_plan_segment(p._h, -1, ctypes.byref(info)) == wb.WB_EINVAL
+
+
+def test_local_tensor_query():
+    w = WORKLOADS["dsv3_ep64_to_ep8_fp8"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    locs = ro.locals(0)
+    assert p.num_local_tensors == len(locs)
+    for i, lc in enumerate(locs):
+        assert p.local_tensor(i) == (lc["dtype"], lc["numel"])
+    _expect(wb.WB_EINVAL, p.local_tensor, len(locs))

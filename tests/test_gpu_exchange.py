@@ -153,3 +153,75 @@ def test_figure5_dp4_three_stage():
     oro = describe_layout(m, Parallelism("serving", "bf16", tp=1, dp=4))
     plan = three_stage(otr, oro, _values(otr), 2, label="figure 5")
     assert {g.stage for g in plan.segments} == {0, 1, 2}
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,G", [("mixtral_ep8fsdp2_to_ep2", 1), ("dsv3_ep64_to_ep8_fp8", 4),
+                                    ("llama3_8b_tp4_to_tp2", 1)])
+def test_full_size_three_stage(name, G):
+    """Full size, in the benchmark's configuration for the exchange stages: the
+    unpack rank's receive buffer holds its stage-0 regions and the payloads
+    forwarded to it (each the bytes its origin segment left a trainer with);
+    its forward packings must copy exactly the bytes they forward, and its
+    tensors, assembled from all three sections, are checked in full against
+    torch and sampled against the oracle."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+    from test_gpu_full import SENTINEL, _check_unpack_full, _check_unpack_sampled, _sender_locals
+
+    w = WORKLOADS[name]
+    dt = w["trainer"]["dtype"]
+    d = w["unpack_rank"]
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    rp = wb.Plan(tr, ro, wb.RECEIVER, d, node_size=G)
+    rws = workspace_for(rp)
+    rp.upload(rws)
+    segs = rp.segments()
+    forwarded = {}
+    for f in segs:
+        if f["stage"] and f["receiver"] == d:
+            o = segs[f["origin"]]
+            forwarded.setdefault(o["sender"], []).append((o, f))
+    assert forwarded, "the unpack rank must receive forwarded payloads"
+    recv = torch.full((rp.buffer_bytes,), FILL, dtype=torch.uint8, device="cuda")
+    say(f"[{name} G={G}] receive buffer {rp.buffer_bytes / 1e9:.2f} GB, "
+        f"{sum(len(v) for v in forwarded.values())} forwarded payloads")
+    for s in range(otr.nranks):
+        so, roff, nb = rp.region(s, d)
+        if not nb and s not in forwarded:
+            continue
+        locs = _sender_locals(otr, s, dt)
+        p = wb.Plan(tr, ro, wb.SENDER, s, node_size=G)
+        ws = workspace_for(p)
+        p.upload(ws)
+        send = torch.empty(max(1, p.buffer_bytes), dtype=torch.uint8, device="cuda")
+        p.pack(locs, send)
+        if nb:
+            recv[roff:roff + nb] = send[so:so + nb]
+        for o, f in forwarded.get(s, []):
+            recv[f["recv_offset"]:f["recv_offset"] + f["bytes"]] = send[o["send_offset"]:o["send_offset"] + o["bytes"]]
+        torch.cuda.synchronize()
+        del locs, send, p, ws
+    for st in (1, 2):
+        fwd = torch.full((max(1, rp.forward_bytes(st)),), FILL, dtype=torch.uint8, device="cuda")
+        rp.forward_round(0, st, recv, fwd)
+        torch.cuda.synchronize()
+        mine = [f for f in segs if f["stage"] == st and f["sender"] == d]
+        say(f"[{name} G={G}] stage {st}: {len(mine)} forwarded payloads checked")
+        for f in mine:
+            a = fwd[f["send_offset"]:f["send_offset"] + f["bytes"]]
+            b = recv[f["src_offset"]:f["src_offset"] + f["bytes"]]
+            assert torch.equal(a, b), (st, f)
+        del fwd
+    dst = wb.allocate_locals(ro, d)
+    for t, lc in zip(dst, oro.ranks[d].locals):
+        t.view(torch.uint8).fill_(SENTINEL[lc.dtype])
+    rp.unpack(recv, dst)
+    torch.cuda.synchronize()
+    say(f"[{name} G={G}] full check against torch")
+    _check_unpack_full(oro, d, dst, otr.catalog, dt)
+    _check_unpack_sampled(oro, d, dst, otr.catalog, dt, np.random.default_rng(12))
+    del recv, dst
+    torch.cuda.empty_cache()
