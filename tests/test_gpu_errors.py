@@ -1,0 +1,107 @@
+"""Call-time argument checks on the GPU: every call below is refused on the
+host with WB_EINVAL before anything is launched (null, misaligned or
+too-small buffers, a workspace below the plan's size, calls before upload)."""
+
+import pytest
+import torch
+
+import paper_2609_25442_amd as wb
+from synthetic_checkpoint.workloads import WORKLOADS
+
+from gpu_util import workspace_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _expect_einval(fn, *a):
+    with pytest.raises(wb.WbError) as e:
+        fn(*a)
+    assert e.value.code == wb.WB_EINVAL, str(e.value)
+    return str(e.value)
+
+
+@pytest.fixture(autouse=True)
+def fresh_cache():
+    # allocation-range checks see the caching allocator's segments: start each
+    # test with none cached, so a small tensor sits in a small segment
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    yield
+
+
+@pytest.fixture(scope="module")
+def plans():
+    w = WORKLOADS["llama3_8b_fsdp8_to_tp1"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    rp = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    sp = wb.Plan(tr, ro, wb.SENDER, 0)
+    return tr, ro, rp, sp
+
+
+def test_upload_checks(plans):
+    tr, ro, rp, sp = plans
+    small = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    assert rp.workspace_bytes > small.numel()
+    _expect_einval(rp.upload, small)
+    ws = workspace_for(rp)
+    _expect_einval(lambda: wb._check(wb.lib.wb_plan_upload(rp._h, ws.data_ptr() + 16, ws.numel() - 16, None)))
+
+
+def test_unpack_buffer_checks(plans):
+    tr, ro, rp, sp = plans
+    ws = workspace_for(rp)
+    rp.upload(ws)
+    dst = wb.allocate_locals(ro, 0)
+    small = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    assert "smaller" in _expect_einval(rp.unpack, small, dst)
+    recv = torch.empty(rp.buffer_bytes + 64, dtype=torch.uint8, device="cuda")
+    assert "aligned" in _expect_einval(rp.unpack, recv[1:], dst)
+    assert "null" in _expect_einval(rp.unpack, 0, dst)
+    bad = list(dst)
+    bad[2] = 0                                                          # a null local tensor
+    _expect_einval(rp.unpack, recv, bad)
+    bad[2] = dst[2]
+    bad[0] = torch.empty(2 << 20, dtype=torch.bfloat16, device="cuda")  # 4 MB for the 1 GB embedding
+    assert dst[0].numel() * 2 > (1 << 30)
+    assert "smaller" in _expect_einval(rp.unpack, recv, bad)
+    _expect_einval(rp.pack, [0] * sp.num_local_tensors, recv)          # wrong role
+    del recv, dst, bad
+    torch.cuda.empty_cache()
+
+
+def test_pack_buffer_checks(plans):
+    tr, ro, rp, sp = plans
+    ws = workspace_for(sp)
+    _expect_einval(sp.pack, [0] * sp.num_local_tensors, torch.empty(16, dtype=torch.uint8, device="cuda"))  # not uploaded
+    sp.upload(ws)
+    src = wb.allocate_locals(tr, 0)
+    send = torch.empty(sp.buffer_bytes + 64, dtype=torch.uint8, device="cuda")
+    _expect_einval(sp.pack, src, send[8:])
+    _expect_einval(sp.pack, src, torch.empty(1 << 20, dtype=torch.uint8, device="cuda"))
+    _expect_einval(sp.pack, src[:-1] + [0], send)
+    del src, send
+    torch.cuda.empty_cache()
+
+
+def test_forward_and_probe_checks():
+    w = WORKLOADS["mixtral_ep8fsdp2_to_ep2"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    rp = wb.Plan(tr, ro, wb.RECEIVER, 0, node_size=1)
+    assert rp.forward_bytes(1) > (64 << 20)
+    ws = workspace_for(rp)
+    rp.upload(ws)
+    small = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    _expect_einval(rp.forward_round, 0, 1, small, small)              # receive buffer too small
+    _expect_einval(rp.forward_round, 0, 3, small, small)              # no such stage
+    x = torch.empty(1024, dtype=torch.bfloat16, device="cuda")
+    _expect_einval(lambda: wb._check(wb.lib.wb_make_ids(x.data_ptr() + 1, wb.DTYPES["bf16"], 100, 1 << 24, 0, 16, None)))
+    _expect_einval(lambda: wb._check(wb.lib.wb_make_ids(x.data_ptr(), wb.DTYPES["bf16"], 100, 1 << 24, 0, 8, None)))
+    idx = torch.empty(16, dtype=torch.int64, device="cuda")
+    val = torch.empty(16, dtype=torch.int32, device="cuda")
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    _expect_einval(lambda: wb._check(wb.lib.wb_diff2(x.data_ptr() + 1, wb.DTYPES["bf16"], 4, 4, idx.data_ptr(),
+                                                     val.data_ptr(), 16, cnt.data_ptr(), None)))
+    _expect_einval(lambda: wb._check(wb.lib.wb_diff2(x.data_ptr(), wb.DTYPES["bf16"], 4, 4, idx.data_ptr(),
+                                                     val.data_ptr(), 16, cnt.data_ptr() + 4, None)))
