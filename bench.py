@@ -571,7 +571,10 @@ def main():
     else:
         dom = "wb::wb_tasks_kernel (unpack)"
     achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
-    traffic = stored_traffic(args.workload, "unpack")
+    # HBM bytes of the launches the roofline times (both launches of an fp8 unpack)
+    parts = [stored_traffic(args.workload, k) for k in (("unpack", "unpack_fp8") if n_blocks and n_tasks else
+                                                        ("unpack_fp8",) if n_blocks else ("unpack",))]
+    traffic = sum(parts) if all(x is not None for x in parts) and not G and nr == 1 and not args.staged else None
     out = {
         "metric": "pack+unpack effective GB/s per GPU (% of HBM peak); wb_plan ms",
         "value": round(value, 1),
