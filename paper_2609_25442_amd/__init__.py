@@ -280,7 +280,8 @@ class Layout:
         return _text(lib.wb_layout_dump, self._h)
 
     def __del__(self):
-        if getattr(self, "_h", None) is not None and self._h.value:
+        # at interpreter teardown the module's globals may already be gone
+        if getattr(self, "_h", None) is not None and self._h.value and _release is not None:
             _release(self)
 
 
@@ -439,7 +440,8 @@ class Plan:
         _check(lib.wb_unpack(self._h, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
     def __del__(self):
-        if getattr(self, "_h", None) is not None and self._h.value:
+        # at interpreter teardown the module's globals may already be gone
+        if getattr(self, "_h", None) is not None and self._h.value and _release is not None:
             _release(self)
 
 
@@ -489,7 +491,8 @@ class Probe:
         _check(lib.wb_probe_scan(self._h, layout._h, rank))
 
     def __del__(self):
-        if getattr(self, "_h", None) is not None and self._h.value:
+        # at interpreter teardown the module's globals may already be gone
+        if getattr(self, "_h", None) is not None and self._h.value and _release is not None:
             _release(self)
 
 

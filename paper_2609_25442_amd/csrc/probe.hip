@@ -204,6 +204,82 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_vec_kernel(const char* __re
   }
 }
 
+constexpr int kFlatUnroll = 8;  // vectors in flight per lane along a one-row field
+
+// One-row fields (flat buffers): with nothing above, D is the row's second
+// difference h. Each workgroup takes kFlatUnroll consecutive tiles of
+// kThreads vectors; lane l of tile u holds vector (tile start + l).
+template <int V>
+__global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __restrict__ src, int64_t cols,
+                                                                 int64_t* __restrict__ index,
+                                                                 int32_t* __restrict__ value, int64_t capacity,
+                                                                 unsigned long long* __restrict__ count) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nvec = cols / V;
+  const int64_t step = int64_t(gridDim.x) * kThreads * kFlatUnroll;
+  for (int64_t cb = int64_t(blockIdx.x) * kThreads * kFlatUnroll; cb < nvec; cb += step) {
+    int x[kFlatUnroll][V];
+    int l1[kFlatUnroll], l2[kFlatUnroll];
+#pragma unroll
+    for (int u = 0; u < kFlatUnroll; ++u) {
+      const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
+      const int64_t j0 = v * V;
+      l1[u] = l2[u] = 0;
+      if (v < nvec) {
+        const uint4 q = *reinterpret_cast<const uint4*>(src + j0 * (16 / V));
+        if (V == 8) {
+          const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            x[u][2 * k] = int(w[k] & 0xFFFFu);
+            x[u][2 * k + 1] = int(w[k] >> 16);
+          }
+        } else {
+          x[u][0] = int(__uint_as_float(q.x));
+          x[u][1] = int(__uint_as_float(q.y));
+          x[u][2] = int(__uint_as_float(q.z));
+          x[u][3] = int(__uint_as_float(q.w));
+        }
+        if (lane == 0 && j0 >= 2) {
+          if (V == 8) {
+            const uint32_t pw = *reinterpret_cast<const uint32_t*>(src + (j0 - 2) * 2);
+            l2[u] = int(pw & 0xFFFFu);
+            l1[u] = int(pw >> 16);
+          } else {
+            const uint2 pw = *reinterpret_cast<const uint2*>(src + (j0 - 2) * 4);
+            l2[u] = int(__uint_as_float(pw.x));
+            l1[u] = int(__uint_as_float(pw.y));
+          }
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < V; ++k) x[u][k] = 0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kFlatUnroll; ++u) {
+      const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
+      if (cb + int64_t(u) * kThreads >= nvec) break;  // uniform over the workgroup
+      int p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
+      if (lane == 0) {
+        p1 = l1[u];
+        p2 = l2[u];
+      }
+      int d[V];
+      d[0] = x[u][0] - 2 * p1 + p2;
+      d[1] = x[u][1] - 2 * x[u][0] + p1;
+#pragma unroll
+      for (int k = 2; k < V; ++k) d[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
+      unsigned any = 0;
+#pragma unroll
+      for (int k = 0; k < V; ++k) any |= (v < nvec && d[k] != 0) ? (1u << k) : 0u;
+      if (__ballot(any != 0) == 0) continue;
+#pragma unroll
+      for (int k = 0; k < V; ++k) emit_entries((any >> k) & 1u, v * V + k, d[k], lane, index, value, capacity, count);
+    }
+  }
+}
+
 __global__ void wb_zero_count_kernel(unsigned long long* count) { *count = 0; }
 
 }  // namespace
@@ -224,6 +300,17 @@ int launch_diff2(const void* src, int dtype, int64_t rows, int64_t cols, int64_t
   if (rows == 0 || cols == 0) return hipGetLastError();
   const int es = dtype == WB_F32 ? 4 : 2;
   const int V = 16 / es;
+  if (rows == 1 && cols % V == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0) {
+    const int64_t chunks = (cols / V + kThreads * kFlatUnroll - 1) / (kThreads * kFlatUnroll);
+    const dim3 grid(static_cast<unsigned>(chunks < 65536 ? chunks : 65536));
+    if (V == 8)
+      hipLaunchKernelGGL(wb_diff2_flat_kernel<8>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), cols,
+                         index, value, capacity, count);
+    else
+      hipLaunchKernelGGL(wb_diff2_flat_kernel<4>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), cols,
+                         index, value, capacity, count);
+    return hipGetLastError();
+  }
   if (cols % V == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0) {
     const int64_t strips = (rows + kVecStrip - 1) / kVecStrip;
     const int64_t tiles = (cols / V + kThreads - 1) / kThreads;

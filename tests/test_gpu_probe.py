@@ -60,7 +60,7 @@ def _to_gpu(codes, dtype):
 
 # vector path (cols a multiple of 8 bf16 / 4 f32 values, aligned) and element path
 SHAPES = [(1, 1), (1, 1000), (1000, 1), (3, 257), (130, 300), (65, 64), (64, 513), (200, 1), (2, 70000),
-          (97, 2048), (33, 4104)]
+          (97, 2048), (33, 4104), (1, 300000), (1, 8), (1, 2056)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
