@@ -151,3 +151,15 @@ def test_quantize_matrix_partial_edges():
     # the 2x1 edge block at (1, 2) is quantised on its own
     c, s = casts.quantize_block(x[128:, 256:])
     assert scales[1, 2] == s and np.array_equal(codes[128:, 256:], c)
+
+
+def test_quantize_divides_rather_than_multiplying_by_the_reciprocal():
+    for xs, ams, by_div, by_rcp in _rows("fp8_division_cases.txt"):
+        x = np.array([int(xs, 16)], dtype=np.uint32).view(np.float32)[0]
+        amax = np.array([int(ams, 16)], dtype=np.uint32).view(np.float32)[0]
+        block = np.array([x, amax], dtype=np.float32)
+        codes, s = casts.quantize_block(block)
+        assert codes[0] == int(by_div), (xs, ams)
+        st = torch.tensor(amax) / torch.tensor(448.0)
+        assert int((torch.tensor(x) / st).to(torch.float8_e4m3fn).view(torch.uint8)) == int(by_div)
+        assert int((torch.tensor(x) * (1.0 / st)).to(torch.float8_e4m3fn).view(torch.uint8)) == int(by_rcp)
