@@ -50,8 +50,11 @@ def roundtrip(otr, oro, values, tr=None, ro=None, label="", staged=False):
     """Pack every trainer rank and unpack every rollout rank on the GPU through
     the C ABI; compare every payload byte with the oracle's pack, check that
     padding between payloads is untouched, and compare every rollout tensor
-    with the oracle's plan-free expectation. With ``staged`` the send and
-    receive buffers live in pinned host memory."""
+    with the oracle's plan-free expectation. ``staged`` puts buffers in pinned
+    host memory: "send" the send buffers (sender staging), "recv" the receive
+    buffers (receiver staging), True both."""
+    stage_send = staged in (True, "send")
+    stage_recv = staged in (True, "recv")
     from wb_cases import to_wb
 
     tr = tr or to_wb(otr)
@@ -68,7 +71,7 @@ def roundtrip(otr, oro, values, tr=None, ro=None, label="", staged=False):
         ws = workspace_for(p)
         p.upload(ws)
         src = [codes_to_gpu(c, lc.dtype) for c, lc in zip(o_locals, otr.ranks[s].locals)]
-        buf = _buffer(p.buffer_bytes, FILL, staged)
+        buf = _buffer(p.buffer_bytes, FILL, stage_send)
         p.pack(src, buf)
         torch.cuda.synchronize()
         got = buf.cpu().numpy()[:p.buffer_bytes]
@@ -85,7 +88,7 @@ def roundtrip(otr, oro, values, tr=None, ro=None, label="", staged=False):
         p = wb.Plan(tr, ro, wb.RECEIVER, d)
         ws = workspace_for(p)
         p.upload(ws)
-        recv = _buffer(p.buffer_bytes, 0, staged)
+        recv = _buffer(p.buffer_bytes, 0, stage_recv)
         for s in range(otr.nranks):
             so, ro_off, nb = p.region(s, d)
             if nb:

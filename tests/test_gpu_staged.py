@@ -16,9 +16,12 @@ from gpu_util import roundtrip
 pytestmark = pytest.mark.gpu
 
 
+@pytest.mark.parametrize("mode", ["send", "recv", "both"])
 @pytest.mark.parametrize("name", ["llama3_8b_fsdp8_to_tp1", "llama3_8b_tp4_to_tp2", "mixtral_ep8fsdp2_to_ep2",
                                   "dsv3_ep64_to_ep8_fp8"])
-def test_host_staged_parity(name):
+def test_host_staged_parity(name, mode):
+    """Sender staging only, receiver staging only, or both (the fourth mode,
+    neither, is the device-resident parity test)."""
     w = scaled(name)
     otr = layout_from_spec(w["model"], w["trainer"])
     oro = layout_from_spec(w["model"], w["rollout"])
@@ -32,4 +35,5 @@ def test_host_staged_parity(name):
         return cache[t]
 
     roundtrip(otr, oro, values, wb.Layout.describe(w["model"], w["trainer"]),
-              wb.Layout.describe(w["model"], w["rollout"]), label=f"staged-{name}", staged=True)
+              wb.Layout.describe(w["model"], w["rollout"]), label=f"staged-{mode}-{name}",
+              staged=True if mode == "both" else mode)
