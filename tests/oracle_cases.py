@@ -94,3 +94,18 @@ def hand_exchange_pair():
                       [Placement(0, 0, 4, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 8, 1, 0, 8)])
     only_x = RankLayout([Local("x", "bf16", 1, 4, 4)], [Placement(0, 0, 4, 0, 4, 0, 0, 4)])
     return Layout(cat, tr), Layout(cat, [both, only_x, RankLayout(list(both.locals), list(both.placements))])
+
+
+def overlapping_rollout_pair():
+    """Rollout ranks holding overlapping but non-identical rectangles of one
+    tensor (rows 0:4 and 2:6 of T), each replicated on two ranks in different
+    nodes of two, and a replicated vector; trainer FSDP-like row halves."""
+    cat = [CkptTensor("T", 6, 4), CkptTensor("v", 1, 6)]
+    tr = [RankLayout([Local("a", "f32", 1, 3, 4), Local("b", "f32", 1, 1, 6)],
+                     [Placement(0, r0, r0 + 3, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 6, 1, 0, 6)])
+          for r0 in (0, 3)]
+    ro = []
+    for r0 in (0, 2, 0, 2):
+        ro.append(RankLayout([Local("x", "bf16", 1, 4, 4), Local("y", "bf16", 1, 1, 6)],
+                             [Placement(0, r0, r0 + 4, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 6, 1, 0, 6)]))
+    return Layout(cat, tr), Layout(cat, ro)

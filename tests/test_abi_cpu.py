@@ -302,3 +302,12 @@ def test_local_tensor_query():
     for i, lc in enumerate(locs):
         assert p.local_tensor(i) == (lc["dtype"], lc["numel"])
     _expect(wb.WB_EINVAL, p.local_tensor, len(locs))
+
+
+@pytest.mark.parametrize("G", [1, 2, 4])
+def test_overlapping_rollout_exchange_equals_oracle(G):
+    from oracle_cases import overlapping_rollout_pair
+    tr, ro = overlapping_rollout_pair()
+    want = dump(build_plan(tr, ro, node_size=G))
+    for d in range(4):
+        assert wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, d, node_size=G).dump() == want
