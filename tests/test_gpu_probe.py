@@ -143,3 +143,26 @@ def test_probe_recovers_declared_layouts(name):
             want = sorted((p.t, p.r0, p.r1, p.c0, p.c1, remap[p.u], p.base, p.ld, p.tr) for p in rk.placements)
             assert sorted(got.placements(k)) == want, (name, side, r)
             assert [x["numel"] for x in got.locals(k)] == [rk.locals[u].numel for u in keep]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,side", [("llama3_8b_fsdp8_to_tp1", "trainer"), ("llama3_8b_fsdp8_to_tp1", "rollout"),
+                                       ("llama3_8b_tp4_to_tp2", "trainer")])
+def test_probe_full_size(name, side):
+    """The benchmark ranks at full size (16 GB identifier checkpoint), probed
+    through the torch loaders: the recovered placements equal the declared."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    w = WORKLOADS[name]
+    rank = w["pack_rank"] if side == "trainer" else w["unpack_rank"]
+    L = layout_from_spec(w["model"], w[side])
+    cat = [(c.name, c.rows, c.cols) for c in L.catalog]
+    say(f"[probe full] {name} {side} rank {rank}")
+    got = wb.probe_layout(cat, w["trainer"]["dtype"], _loaders(w, side, [rank]))
+    rk = L.ranks[rank]
+    keep = [u for u, lc in enumerate(rk.locals) if lc.scales < 0]
+    remap = {u: i for i, u in enumerate(keep)}
+    want = sorted((p.t, p.r0, p.r1, p.c0, p.c1, remap[p.u], p.base, p.ld, p.tr) for p in rk.placements)
+    assert sorted(got.placements(0)) == want
+    del got
+    torch.cuda.empty_cache()
