@@ -297,33 +297,46 @@ def run_probe(args):
                       for (t, r0, r1, c0, c1, u, b, ld, tr) in declared.placements(rank))
         same = sorted(got.placements(0)) == want
         log(f"[probe] {side} rank {rank}: {ms:.0f} ms, recovered == declared: {same}")
-        # the stencil alone, over the loaded tensors of pass 0
+        # the stencil alone: one batched launch over the loaded tensors of pass 0,
+        # and one over all passes held on the device (what the probe above ran
+        # when it held them); the timed call includes its small table upload
         probe = wb.Probe(cat, dtype)
         ckpt = {n: torch.empty((r, c), dtype=wb.torch_dtype(dtype), device="cuda") for n, r, c in cat}
-        for t, (n, r, c) in enumerate(cat):
-            wb.make_ids(ckpt[n], dtype, probe.first_id(t), 0)
-        locs = load(ckpt)
-        cap = 1 << 24
+        held = []
+        for k in range(probe.num_chunks):
+            for t, (n, r, c) in enumerate(cat):
+                wb.make_ids(ckpt[n], dtype, probe.first_id(t), k)
+            held.append([x.clone() for x in load(ckpt)])
+        shapes = [wb._view_shape(x) for x in held[0]]
+        one = [(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(held[0], shapes)]
+        every = [([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)]
+        cap = 1 << 21
         idx = torch.empty(cap, dtype=torch.int64, device="cuda")
-        val = torch.empty(cap, dtype=torch.int32, device="cuda")
-        counts = torch.zeros(len(locs), dtype=torch.int64, device="cuda")
-        nbytes = sum(x.numel() * x.element_size() for x in locs)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        for rep in range(3):
-            ev[0].record()
-            for u, x in enumerate(locs):
-                b, rr, cc = wb._view_shape(x)
-                wb.diff2(x, dtype, b * rr, cc, idx, val, counts[u:u + 1])
-            ev[1].record()
-            torch.cuda.synchronize()
-        stencil_ms = ev[0].elapsed_time(ev[1])
+        val = torch.empty(cap, dtype=torch.int64, device="cuda")
+        count = torch.zeros(1, dtype=torch.int64, device="cuda")
+        nbytes = sum(x.numel() * x.element_size() for x in held[0])
+        stencil = {}
+        for label, fields, npass in (("one_pass", one, 1), ("all_passes", every, probe.num_chunks)):
+            ws = torch.empty(wb.diff2_batch_workspace(fields), dtype=torch.uint8, device="cuda")
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            times = []
+            for rep in range(4):
+                ev[0].record()
+                wb.diff2_batch(fields, idx, val, count, ws)
+                ev[1].record()
+                torch.cuda.synchronize()
+                times.append(ev[0].elapsed_time(ev[1]))
+            best = min(times[1:])
+            rate = nbytes * npass / (best * 1e-3) / 1e9
+            stencil[label] = {"launches": 1, "bytes": nbytes * npass, "entries": int(count.item()),
+                              "table_bytes": ws.numel(), "ms": round(best, 3), "GB/s": round(rate, 1),
+                              "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+            log(f"[probe] {side} diff2 {label}: {best:.3f} ms, {rate:.0f} GB/s, {int(count.item())} entries")
         out["ranks"][side] = {"rank": rank, "probe_ms": round(ms, 1), "recovered_equals_declared": same,
                               "placements": len(want), "local_tensors": len(keep),
-                              "passes": stats[0], "scan_ms": round(stats["scan_s"][0] * 1e3, 1),
-                              "diff2": {"launches": len(locs), "bytes": nbytes, "ms": round(stencil_ms, 3),
-                                        "GB/s": round(nbytes / (stencil_ms * 1e-3) / 1e9, 1),
-                                        "frac_of_hbm_peak": round(nbytes / (stencil_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
-        del locs, ckpt, idx, val, got
+                              "hold_passes": stats["hold_passes"][0], "passes": stats[0],
+                              "scan_ms": round(stats["scan_s"][0] * 1e3, 1), "diff2": stencil}
+        del held, one, every, ckpt, idx, val, got
         torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 

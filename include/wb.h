@@ -380,9 +380,10 @@ int wb_probe_first_id(const wb_probe_t* probe, int32_t t, int64_t* id);
 int wb_probe_add_local(wb_probe_t* probe, const char* name, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
                        int32_t* index);
 /* Host arrays of n entries of pass `chunk` for local tensor `local`: flat
- * element index and diff2 value (as wb_diff2 writes them). Errors: WB_EINVAL
- * (index or chunk out of range). */
-int wb_probe_record(wb_probe_t* probe, int32_t local, int32_t chunk, const int64_t* index, const int32_t* value,
+ * element index and diff2 value (as wb_diff2 writes them, widened to int64),
+ * added times 2^(16 chunk). Entries of wb_diff2_batch over all passes at once
+ * are recorded as chunk 0. Errors: WB_EINVAL (index or chunk out of range). */
+int wb_probe_record(wb_probe_t* probe, int32_t local, int32_t chunk, const int64_t* index, const int64_t* value,
                     int64_t n);
 /* Fill rank `rank` of `layout` (made by wb_layout_create over the same catalog,
  * with no local tensors yet) with the probe's local tensors and the placements
@@ -411,6 +412,40 @@ int wb_make_ids(void* dst, int32_t dtype, int64_t numel, int64_t first_id, int32
  * (null, misaligned, bad dtype or shape). */
 int wb_diff2(const void* src, int32_t dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
              int64_t capacity, uint64_t* count, void* stream);
+/* A field for wb_diff2_batch: `passes` (1 to 3) device arrays data[0..passes)
+ * of dtype WB_BF16 or WB_F32, each seen as [rows, cols] (row-major,
+ * contiguous, element-aligned). Its value at (i, j) is the sum over k of
+ * 2^(16 k) times the chunk held by data[k] (bf16 bit pattern or exact f32
+ * value): with data[k] the loaded tensor after probing pass k, that is the
+ * identifier field itself. rows or cols may be 0 (a field with no entries). */
+typedef struct wb_field {
+  const void* data[3];
+  int32_t dtype;
+  int32_t passes;
+  int64_t rows, cols;
+} wb_field;
+/* Device workspace bytes wb_diff2_batch needs for these n fields (its
+ * tables: 56 bytes per field, then 24 per workgroup of the launch; 0 when no
+ * field has elements). Errors: WB_EINVAL (bad field). */
+int wb_diff2_batch_workspace(const wb_field* fields, int32_t n, size_t* bytes);
+/* diff2 of n fields in one stencil launch (Algorithm 1 runs diff2 over every
+ * loaded tensor after each pass). Because diff2 is linear, a field of several
+ * passes gives the sum over k of 2^(16 k) times diff2 of pass k, formed before
+ * the stencil: the entries that chunk wrap-arounds leave in single passes
+ * cancel inside the launch, and only the identifier field's own entries (at
+ * most 16 per slice copy) come out. Values are int64 (identifiers below 2^48).
+ * An entry's index is its flat position in the concatenation of the fields in
+ * order: field f's element (i, j) is the sum over g < f of rows_g * cols_g,
+ * plus i * cols_f + j. index, value (8-byte aligned), capacity and count as
+ * for wb_diff2 (count is the total over all fields). workspace is device
+ * memory of at least wb_diff2_batch_workspace bytes, 8-byte aligned, owned by
+ * the caller; the call copies the tile table into it on `stream` and waits
+ * for that copy (so it returns after the stream's earlier work), and the
+ * workspace must stay untouched until the launch has run. Errors: WB_EINVAL
+ * (null, misaligned, bad field, workspace too small, more than 2^31 - 1
+ * tiles), WB_EHIP. */
+int wb_diff2_batch(const wb_field* fields, int32_t n, void* workspace, size_t workspace_bytes, int64_t* index,
+                   int64_t* value, int64_t capacity, uint64_t* count, void* stream);
 
 /* Message of the calling thread's last failed call ("" if none). */
 const char* wb_last_error(void);

@@ -60,6 +60,10 @@ class SegmentInfo(ctypes.Structure):
                                        "bytes")]
 
 
+class Field(ctypes.Structure):
+    _fields_ = [("data", c_void_p * 3), ("dtype", c_int32), ("passes", c_int32), ("rows", c_int64), ("cols", c_int64)]
+
+
 class LocalInfo(ctypes.Structure):
     _fields_ = [("name", c_char_p), ("dtype", c_int32), ("quant_block", c_int32), ("batch", c_int64),
                 ("rows", c_int64), ("cols", c_int64), ("scale_index", c_int32), ("scales_index", c_int32)]
@@ -126,6 +130,9 @@ def _load():
         "wb_probe_scan": [c_void_p, L, c_int32],
         "wb_make_ids": [c_void_p, c_int32, c_int64, c_int64, c_int32, c_int32, c_void_p],
         "wb_diff2": [c_void_p, c_int32, c_int64, c_int64, c_void_p, c_void_p, c_int64, c_void_p, c_void_p],
+        "wb_diff2_batch_workspace": [POINTER(Field), c_int32, POINTER(c_size_t)],
+        "wb_diff2_batch": [POINTER(Field), c_int32, c_void_p, c_size_t, c_void_p, c_void_p, c_int64, c_void_p,
+                           c_void_p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -480,11 +487,12 @@ class Probe:
         return v.value
 
     def record(self, local: int, chunk: int, index, value):
-        """index (int64) and value (int32) host arrays (numpy) of one pass."""
+        """index and value host arrays (numpy, taken as int64) of one pass, or
+        of all passes at once as chunk 0."""
         import numpy as np
 
         index = np.ascontiguousarray(index, dtype=np.int64)
-        value = np.ascontiguousarray(value, dtype=np.int32)
+        value = np.ascontiguousarray(value, dtype=np.int64)
         _check(lib.wb_probe_record(self._h, local, chunk, index.ctypes.data, value.ctypes.data, len(index)))
 
     def scan(self, layout: "Layout", rank: int):
@@ -510,6 +518,40 @@ def diff2(src, dtype: str, rows: int, cols: int, index, value, count, stream=Non
                         _stream_handle(stream)))
 
 
+def _field_array(fields):
+    arr = (Field * len(fields))()
+    for f, (ts, dtype, rows, cols) in enumerate(fields):
+        ts = list(ts) if isinstance(ts, (list, tuple)) else [ts]
+        if not 1 <= len(ts) <= 3:
+            raise ValueError("a field holds 1 to 3 passes")
+        arr[f].dtype, arr[f].passes, arr[f].rows, arr[f].cols = DTYPES[dtype], len(ts), rows, cols
+        for c, t in enumerate(ts):
+            arr[f].data[c] = _ptr(t)
+    return arr
+
+
+def diff2_batch_workspace(fields) -> int:
+    """Device workspace bytes of diff2_batch over ``fields``."""
+    arr = _field_array(fields)
+    v = c_size_t()
+    _check(lib.wb_diff2_batch_workspace(arr, len(fields), byref(v)))
+    return v.value
+
+
+def diff2_batch(fields, index, value, count, workspace, stream=None):
+    """Non-zero diff2 entries of many fields in one launch. ``fields`` is a list
+    of (tensors, dtype, rows, cols); ``tensors`` is one tensor or the list of
+    one loaded tensor per probing pass (value sum of 2^(16 k) times pass k).
+    Entries go to the device tensors index (int64, position in the
+    concatenation of the fields) and value (int64); count (uint64 device
+    scalar) gets their number. ``workspace``: a uint8 device tensor of at least
+    diff2_batch_workspace(fields) bytes."""
+    arr = _field_array(fields)
+    nbytes = workspace.numel() if workspace is not None else 0
+    _check(lib.wb_diff2_batch(arr, len(fields), _ptr(workspace) if nbytes else None, nbytes, _ptr(index),
+                              _ptr(value), index.numel(), _ptr(count), _stream_handle(stream)))
+
+
 def _view_shape(t):
     if t.dim() == 1:
         return 1, 1, t.shape[0]
@@ -520,12 +562,49 @@ def _view_shape(t):
     raise ValueError("local tensors must be 1-, 2- or 3-D")
 
 
-def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", stats=None) -> "Layout":
+def _batched_entries(fields, cap, device):
+    """Run diff2_batch over ``fields``, growing the entry arrays until they
+    hold every entry; returns host (index, value) arrays."""
+    import torch
+
+    count = torch.zeros(1, dtype=torch.int64, device=device)
+    ws = torch.empty(max(diff2_batch_workspace(fields), 8), dtype=torch.uint8, device=device)
+    while True:
+        idx = torch.empty(cap, dtype=torch.int64, device=device)
+        val = torch.empty(cap, dtype=torch.int64, device=device)
+        diff2_batch(fields, idx, val, count, ws)
+        n = int(count.item())
+        if n <= cap:
+            return idx[:n].cpu().numpy(), val[:n].cpu().numpy()
+        cap = n
+
+
+def _record_split(probe, chunk, offsets, index, value):
+    """Hand batched entries to the probe, local tensor by local tensor."""
+    import numpy as np
+
+    order = np.argsort(index, kind="stable")
+    index, value = index[order], value[order]
+    cut = np.searchsorted(index, offsets)
+    for u in range(len(offsets) - 1):
+        a, b = cut[u], cut[u + 1]
+        probe.record(u, chunk, index[a:b] - offsets[u], value[a:b])
+
+
+def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", stats=None,
+                 hold_passes=None) -> "Layout":
     """Discover a layout from weight loaders: ``loaders[r](ckpt)`` takes the
     checkpoint as {name: tensor} and returns rank r's local tensors (a list of
     1-, 2- or 3-D tensors, always the same shapes, values copied unchanged).
-    Returns a Layout with one rank per loader. ``stats`` (a dict) receives
-    timings and entry counts when given."""
+    Returns a Layout with one rank per loader.
+
+    With ``hold_passes`` a copy of every pass's loaded tensors stays in device
+    memory and one diff2 launch over all passes runs at the end (the chunk
+    wrap-arounds cancel inside it, so only the identifier field's few entries
+    reach the host); otherwise each pass gets one launch and its entries are
+    recorded before the next load. None picks holding when the passes fit in free
+    device memory with a quarter to spare. ``stats`` (a dict) receives timings
+    and entry counts when given."""
     import time
 
     import numpy as np
@@ -533,11 +612,11 @@ def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", s
 
     tdt = torch_dtype(ckpt_dtype)
     layout = Layout.create(catalog, len(loaders))
-    count = torch.zeros(1, dtype=torch.int64, device=device)
     ckpt = {n: torch.empty((r, c), dtype=tdt, device=device) for n, r, c in catalog}
     for r, load in enumerate(loaders):
         probe = Probe(catalog, ckpt_dtype)
-        shapes = None
+        shapes, held, hold = None, [], hold_passes
+        rec = stats.setdefault(r, []) if stats is not None else None
         for k in range(probe.num_chunks):
             t0 = time.perf_counter()
             for t, (n, rows, cols) in enumerate(catalog):
@@ -550,31 +629,41 @@ def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", s
                 shapes = [_view_shape(x) for x in locs]
                 for u, (b, rr, cc) in enumerate(shapes):
                     probe.add_local(names[r][u] if names else f"local{u}", ckpt_dtype, b, rr, cc)
-            entries = 0
+                offsets = np.cumsum([0] + [b * rr * cc for b, rr, cc in shapes]).astype(np.int64)
+                if hold is None:
+                    need = (probe.num_chunks - 1) * sum(x.numel() * x.element_size() for x in locs)
+                    hold = need * 4 <= torch.cuda.mem_get_info()[0] * 3
             for u, x in enumerate(locs):
                 if x.dtype != tdt or not x.is_contiguous() or _view_shape(x) != shapes[u]:
                     raise ValueError(f"loader of rank {r} returned a changed or non-contiguous tensor {u}")
-                b, rr, cc = shapes[u]
-                cap = max(4096, x.numel() // 512)
-                while True:
-                    idx = torch.empty(cap, dtype=torch.int64, device=device)
-                    val = torch.empty(cap, dtype=torch.int32, device=device)
-                    diff2(x, ckpt_dtype, b * rr, cc, idx, val, count)
-                    n_ent = int(count.item())
-                    if n_ent <= cap:
-                        break
-                    cap = n_ent
-                probe.record(u, k, idx[:n_ent].cpu().numpy(), val[:n_ent].cpu().numpy())
-                entries += n_ent
+            entries = 0
+            if hold:
+                # a loader may write into the same buffers every pass, or hand
+                # back checkpoint tensors, which the next pass overwrites
+                held.append([x.clone() for x in locs] if k + 1 < probe.num_chunks else locs)
+            else:
+                fields = [(x, ckpt_dtype, b * rr, cc) for x, (b, rr, cc) in zip(locs, shapes)]
+                idx, val = _batched_entries(fields, max(1 << 16, int(offsets[-1]) // 8192), device)
+                _record_split(probe, k, offsets, idx, val)
+                entries = len(idx)
             del locs
             t3 = time.perf_counter()
-            if stats is not None:
-                s = stats.setdefault(r, [])
-                s.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries})
+            if rec is not None:
+                rec.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries})
+        if hold:
+            t2 = time.perf_counter()
+            fields = [([held[k][u] for k in range(probe.num_chunks)], ckpt_dtype, b * rr, cc)
+                      for u, (b, rr, cc) in enumerate(shapes)]
+            idx, val = _batched_entries(fields, 1 << 16, device)
+            _record_split(probe, 0, offsets, idx, val)
+            del fields, held
+            if rec is not None:
+                rec.append({"pass": "all", "diff2_s": time.perf_counter() - t2, "entries": len(idx)})
         t4 = time.perf_counter()
         probe.scan(layout, r)
         if stats is not None:
             stats.setdefault("scan_s", []).append(time.perf_counter() - t4)
+            stats.setdefault("hold_passes", []).append(bool(hold))
         del probe
     return layout
 

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstring>
 #include <new>
 #include <string>
@@ -658,7 +659,7 @@ int wb_probe_add_local(wb_probe_t* P, const char* name, int32_t dtype, int64_t b
   });
 }
 
-int wb_probe_record(wb_probe_t* P, int32_t local, int32_t chunk, const int64_t* index, const int32_t* value,
+int wb_probe_record(wb_probe_t* P, int32_t local, int32_t chunk, const int64_t* index, const int64_t* value,
                     int64_t n) {
   return guarded([&]() -> int {
     if (!P) return set_error(WB_EINVAL, "null probe");
@@ -704,6 +705,102 @@ int wb_diff2(const void* src, int32_t dtype, int64_t rows, int64_t cols, int64_t
     if (rc != WB_OK) return rc;
     const int e = wb::launch_diff2(src, dtype, rows, cols, index, value, capacity,
                                    reinterpret_cast<unsigned long long*>(count), stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("diff2 launch: ") + wb::hip_error_string(e));
+    return WB_OK;
+  });
+}
+
+// Check the fields of a batched diff2 call and build its field and tile
+// tables; the device extents of the fields are checked only when `memory` is
+// set. The workspace holds the field table, then (8-byte aligned) the tiles.
+struct Diff2Tables {
+  std::vector<wb::DiffField> fields;
+  std::vector<wb::DiffTile> tiles;
+  size_t tiles_offset() const { return (fields.size() * sizeof(wb::DiffField) + 7) / 8 * 8; }
+  size_t bytes() const { return tiles.empty() ? 0 : tiles_offset() + tiles.size() * sizeof(wb::DiffTile); }
+};
+
+static int diff2_batch_tables(const wb_field* fields, int32_t n, bool memory, Diff2Tables& T) {
+  if (n < 0 || (n > 0 && !fields)) return set_error(WB_EINVAL, "fields is null or n is negative");
+  int64_t base = 0;
+  for (int32_t fi = 0; fi < n; ++fi) {
+    const wb_field& x = fields[fi];
+    const std::string what = "field " + std::to_string(fi);
+    if (x.dtype != WB_F32 && x.dtype != WB_BF16) return set_error(WB_EINVAL, what + ": diff2 needs f32 or bf16");
+    if (x.passes < 1 || x.passes > wb::kMaxPasses)
+      return set_error(WB_EINVAL, what + ": passes must be 1.." + std::to_string(wb::kMaxPasses));
+    if (x.rows < 0 || x.cols < 0 || (x.cols > 0 && x.rows > (int64_t(1) << 61) / x.cols))
+      return set_error(WB_EINVAL, what + ": bad shape");
+    const int64_t numel = x.rows * x.cols;
+    if (base > (int64_t(1) << 61) - numel) return set_error(WB_EINVAL, "fields too large");
+    wb::DiffField f{};
+    f.rows = x.rows;
+    f.cols = x.cols;
+    f.base = base;
+    f.dtype = x.dtype;
+    f.passes = static_cast<uint8_t>(x.passes);
+    const int es = wb::dtype_bytes(x.dtype);
+    for (int c = 0; c < x.passes; ++c) {
+      f.src[c] = x.data[c];
+      if (numel == 0) continue;
+      const std::string d = what + " data[" + std::to_string(c) + "]";
+      if (!x.data[c]) return set_error(WB_EINVAL, d + " is null");
+      if (reinterpret_cast<uintptr_t>(x.data[c]) % es) return set_error(WB_EINVAL, d + " is not element-aligned");
+      if (memory) {
+        const int rc = check_extent(x.data[c], numel * es, d.c_str(), es);
+        if (rc != WB_OK) return rc;
+      }
+    }
+    wb::diff_tiles(fi, f, T.tiles);
+    T.fields.push_back(f);
+    base += numel;
+  }
+  if (T.tiles.size() > size_t(INT32_MAX)) return set_error(WB_EINVAL, "more than 2^31 - 1 tiles");
+  return WB_OK;
+}
+
+int wb_diff2_batch_workspace(const wb_field* fields, int32_t n, size_t* bytes) {
+  return guarded([&]() -> int {
+    if (!bytes) return set_error(WB_EINVAL, "bytes is null");
+    Diff2Tables T;
+    const int rc = diff2_batch_tables(fields, n, false, T);
+    if (rc != WB_OK) return rc;
+    *bytes = T.bytes();
+    return WB_OK;
+  });
+}
+
+int wb_diff2_batch(const wb_field* fields, int32_t n, void* workspace, size_t workspace_bytes, int64_t* index,
+                   int64_t* value, int64_t capacity, uint64_t* count, void* stream) {
+  return guarded([&]() -> int {
+    if (capacity < 0) return set_error(WB_EINVAL, "negative capacity");
+    if (!count || reinterpret_cast<uintptr_t>(count) % 8) return set_error(WB_EINVAL, "count must be 8-byte aligned");
+    int rc = WB_OK;
+    if (capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
+    if (rc == WB_OK && capacity > 0) rc = check_extent(value, capacity * 8, "value", 8);
+    if (rc != WB_OK) return rc;
+    Diff2Tables T;
+    rc = diff2_batch_tables(fields, n, true, T);
+    if (rc != WB_OK) return rc;
+    const size_t need = T.bytes();
+    if (need > workspace_bytes) return set_error(WB_EINVAL, "workspace smaller than wb_diff2_batch_workspace");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    if (need > 0) {
+      rc = check_extent(workspace, static_cast<int64_t>(need), "workspace", 8);
+      if (rc != WB_OK) return rc;
+      std::vector<char> host(need);
+      std::memcpy(host.data(), T.fields.data(), T.fields.size() * sizeof(wb::DiffField));
+      std::memcpy(host.data() + T.tiles_offset(), T.tiles.data(), T.tiles.size() * sizeof(wb::DiffTile));
+      hipError_t e = hipMemcpyAsync(ws, host.data(), need, hipMemcpyHostToDevice, st);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (diff2 tables)");
+      e = hipStreamSynchronize(st);  // the host copy is freed on return
+      if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    }
+    const int e = wb::launch_diff2_batch(reinterpret_cast<const wb::DiffField*>(ws),
+                                         reinterpret_cast<const wb::DiffTile*>(ws + T.tiles_offset()),
+                                         int64_t(T.tiles.size()), index, value, capacity,
+                                         reinterpret_cast<unsigned long long*>(count), stream);
     if (e != 0) return set_error(WB_EHIP, std::string("diff2 launch: ") + wb::hip_error_string(e));
     return WB_OK;
   });

@@ -281,7 +281,7 @@ void probe_init(wb_probe_t& P, const wb_tensor_desc* catalog, int n, int ckpt_dt
   P.nchunks = (bits + P.bits - 1) / P.bits;
 }
 
-void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int32_t* value, int64_t n) {
+void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int64_t* value, int64_t n) {
   if (local < 0 || local >= static_cast<int>(P.locals.size())) fail(WB_EINVAL, "local index out of range");
   if (chunk < 0 || chunk >= P.nchunks) fail(WB_EINVAL, "chunk out of range");
   if (n < 0 || (n > 0 && (!index || !value))) fail(WB_EINVAL, "bad entry arrays");

@@ -2,16 +2,27 @@
 //
 // wb_make_ids_kernel writes one b-bit chunk of every checkpoint element's
 // identifier into a checkpoint tensor, in a form a value-preserving loader
-// copies unchanged: 16-bit and 8-bit dtypes carry the chunk as their bit
-// pattern, fp32 carries it as an exactly representable value.
+// copies unchanged: bf16 carries the chunk as its bit pattern, fp32 as an
+// exactly representable value.
 //
-// wb_diff2_kernel computes the second-order difference of a loaded chunk
+// The diff2 kernels compute the second-order difference of a loaded chunk
 // field (Eq. diff2: the outer product of [1, -2, 1] with itself, the field
-// taken as 0 above and left of the tensor) and appends its non-zero entries
-// to a list. A slice copy leaves at most 16 of them, so the list is short.
+// taken as 0 above and left of the tensor) and append its non-zero entries to
+// a list. A slice copy leaves at most 16 of them, so the list is short. The
+// work is cut into tiles, each one workgroup's share of one field:
+//   ELEM  64 rows x 256 columns, one element per lane (any width, any
+//         element-aligned address);
+//   VEC   32 rows (128 batched) x 256 vectors of 16 bytes (8 bf16 or 4 fp32
+//         values), several rows in flight (cols a multiple of the vector,
+//         16-byte aligned field);
+//   FLAT  one-row fields, 8 x 256 vectors per tile (16 x 256 batched).
+// Single-field launches walk one field's tiles with a strided grid; the
+// batched launch takes one tile per workgroup from a table that covers many
+// fields, so all of a rank's tensors take one launch.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <vector>
 
 #include "wb_internal.hpp"
 
@@ -19,7 +30,10 @@ namespace wb {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kStrip = 64;  // rows per workgroup in the stencil
+constexpr int kStrip = 64;      // rows of an ELEM tile
+constexpr int kVecStrip = 32;   // rows of a VEC tile
+constexpr int kUnroll = 4;      // row vectors in flight per lane (VEC)
+constexpr int kFlatUnroll = 8;  // vectors in flight per lane (FLAT)
 
 __global__ __launch_bounds__(kThreads) void wb_make_ids_kernel(char* dst, int dtype, int64_t numel, int64_t first_id,
                                                                int shift, uint32_t mask) {
@@ -28,259 +42,319 @@ __global__ __launch_bounds__(kThreads) void wb_make_ids_kernel(char* dst, int dt
     const uint32_t v = uint32_t((uint64_t(first_id + n) >> shift) & mask);
     if (dtype == WB_F32)
       reinterpret_cast<float*>(dst)[n] = float(v);
-    else if (dtype == WB_BF16)
-      reinterpret_cast<uint16_t*>(dst)[n] = uint16_t(v);
     else
-      reinterpret_cast<uint8_t*>(dst)[n] = uint8_t(v);
+      reinterpret_cast<uint16_t*>(dst)[n] = uint16_t(v);
+  }
+}
+
+// Where non-zero entries go: slot k of index/value, k from an atomic counter;
+// slots at or past capacity are counted but not written.
+template <typename T>
+struct Sink {
+  int64_t* __restrict__ index;
+  T* __restrict__ value;
+  int64_t capacity;
+  unsigned long long* __restrict__ count;
+};
+
+// The chunk fields a tile reads: element value sum over k < n of p[k] << (16 k).
+// Single-field launches read one pass as int; batched launches recombine up
+// to kMaxPasses passes as int64 (identifiers below 2^48, |diff2| below 2^52).
+template <int P>
+struct Passes {
+  const char* p[P];
+  int n;
+};
+
+// Append the lanes' non-zero entries of one candidate position: one ballot,
+// one atomic add per wavefront.
+template <typename T>
+__device__ __forceinline__ void emit_entries(bool emit, int64_t pos, T d, int lane, const Sink<T>& out) {
+  const unsigned long long m = __ballot(emit);
+  if (m == 0) return;
+  unsigned long long base = 0;
+  const int leader = __ffsll(static_cast<long long>(m)) - 1;
+  if (lane == leader) base = atomicAdd(out.count, static_cast<unsigned long long>(__popcll(m)));
+  base = __shfl(base, leader, 64);
+  if (emit) {
+    const unsigned long long below = lane ? (m & ((1ull << lane) - 1)) : 0ull;
+    const int64_t slot = int64_t(base) + __popcll(below);
+    if (slot < out.capacity) {
+      out.index[slot] = pos;
+      out.value[slot] = d;
+    }
   }
 }
 
 __device__ __forceinline__ int load_chunk(const char* src, int dtype, int64_t k) {
   if (dtype == WB_F32) return int(reinterpret_cast<const float*>(src)[k]);
-  if (dtype == WB_BF16) return int(reinterpret_cast<const uint16_t*>(src)[k]);
-  return int(reinterpret_cast<const uint8_t*>(src)[k]);
+  return int(reinterpret_cast<const uint16_t*>(src)[k]);
 }
 
-// One thread per column, kStrip rows per workgroup (two halo rows above).
-// The column's horizontal second difference h(i) = c(i,j) - 2 c(i,j-1) +
-// c(i,j-2) takes the two left neighbours from the lanes to the left (the
-// first two lanes of a wavefront load theirs); then D = h(i) - 2 h(i-1) + h(i-2).
-__global__ __launch_bounds__(kThreads) void wb_diff2_kernel(const char* __restrict__ src, int dtype, int64_t rows,
-                                                            int64_t cols, int64_t* __restrict__ index,
-                                                            int32_t* __restrict__ value, int64_t capacity,
-                                                            unsigned long long* __restrict__ count) {
+template <typename T, int P>
+__device__ __forceinline__ T load_value(const Passes<P>& s, int dtype, int64_t k) {
+  T v = 0;
+#pragma unroll
+  for (int c = 0; c < P; ++c)
+    if (c < s.n) v += T(load_chunk(s.p[c], dtype, k)) << (16 * c);
+  return v;
+}
+
+// ELEM tile: thread t takes column jb + t over rows [i0, i0 + kStrip), after
+// two halo rows above. The horizontal difference h(i) = c(i,j) - 2 c(i,j-1) +
+// c(i,j-2) takes its left neighbours from the lanes to the left (the first two
+// lanes of a wavefront load theirs); then D = h(i) - 2 h(i-1) + h(i-2).
+template <typename T, int P>
+__device__ __forceinline__ void elem_tile(const Passes<P>& s, int dtype, int64_t rows, int64_t cols, int64_t base,
+                                          int64_t i0, int64_t jb, const Sink<T>& out) {
   const int lane = threadIdx.x & 63;
-  for (int64_t jb = int64_t(blockIdx.x) * kThreads; jb < cols; jb += int64_t(gridDim.x) * kThreads) {
   const int64_t j = jb + threadIdx.x;
   const bool col = j < cols;
-  for (int64_t i0 = int64_t(blockIdx.y) * kStrip; i0 < rows; i0 += int64_t(gridDim.y) * kStrip) {
   const int64_t i1 = i0 + kStrip < rows ? i0 + kStrip : rows;
-  int h1 = 0, h2 = 0;  // h(i-1), h(i-2)
+  T h1 = 0, h2 = 0;  // h(i-1), h(i-2)
   for (int64_t i = (i0 >= 2 ? i0 - 2 : 0); i < i1; ++i) {
     const int64_t rowbase = i * cols;
-    const int c0 = col ? load_chunk(src, dtype, rowbase + j) : 0;
-    int c1 = __shfl_up(c0, 1, 64), c2 = __shfl_up(c0, 2, 64);
-    if (lane == 0) c1 = (col && j >= 1) ? load_chunk(src, dtype, rowbase + j - 1) : 0;
-    if (lane <= 1) c2 = (col && j >= 2) ? load_chunk(src, dtype, rowbase + j - 2) : 0;
+    const T c0 = col ? load_value<T, P>(s, dtype, rowbase + j) : T(0);
+    T c1 = __shfl_up(c0, 1, 64), c2 = __shfl_up(c0, 2, 64);
+    if (lane == 0) c1 = (col && j >= 1) ? load_value<T, P>(s, dtype, rowbase + j - 1) : T(0);
+    if (lane <= 1) c2 = (col && j >= 2) ? load_value<T, P>(s, dtype, rowbase + j - 2) : T(0);
     if (j < 1) c1 = 0;
     if (j < 2) c2 = 0;
-    const int h = c0 - 2 * c1 + c2;
-    const int d = h - 2 * h1 + h2;
+    const T h = c0 - 2 * c1 + c2;
+    const T d = h - 2 * h1 + h2;
     h2 = h1;
     h1 = h;
-    const bool emit = col && i >= i0 && d != 0;
-    const unsigned long long m = __ballot(emit);
-    if (m == 0) continue;
-    unsigned long long base = 0;
-    const int leader = __ffsll(static_cast<long long>(m)) - 1;
-    if (lane == leader) base = atomicAdd(count, static_cast<unsigned long long>(__popcll(m)));
-    base = __shfl(base, leader, 64);
-    if (emit) {
-      const unsigned long long below = lane ? (m & ((1ull << lane) - 1)) : 0ull;
-      const int64_t slot = int64_t(base) + __popcll(below);
-      if (slot < capacity) {
-        index[slot] = rowbase + j;
-        value[slot] = d;
-      }
-    }
-  }
-  }
+    emit_entries<T>(col && i >= i0 && d != 0, base + rowbase + j, d, lane, out);
   }
 }
 
-// Append the lanes' non-zero entries of one candidate position: one ballot,
-// one atomic add per wavefront.
-__device__ __forceinline__ void emit_entries(bool emit, int64_t pos, int d, int lane, int64_t* __restrict__ index,
-                                             int32_t* __restrict__ value, int64_t capacity,
-                                             unsigned long long* __restrict__ count) {
-  const unsigned long long m = __ballot(emit);
-  if (m == 0) return;
-  unsigned long long base = 0;
-  const int leader = __ffsll(static_cast<long long>(m)) - 1;
-  if (lane == leader) base = atomicAdd(count, static_cast<unsigned long long>(__popcll(m)));
-  base = __shfl(base, leader, 64);
-  if (emit) {
-    const unsigned long long below = lane ? (m & ((1ull << lane) - 1)) : 0ull;
-    const int64_t slot = int64_t(base) + __popcll(below);
-    if (slot < capacity) {
-      index[slot] = pos;
-      value[slot] = d;
+// Add the V chunk values of one 16-byte vector, shifted, to x.
+template <int V, typename T>
+__device__ __forceinline__ void add_vec(const uint4 q, int shift, T* x) {
+  if (V == 8) {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[2 * k] += T(w[k] & 0xFFFFu) << shift;
+      x[2 * k + 1] += T(w[k] >> 16) << shift;
     }
+  } else {
+    x[0] += T(int(__uint_as_float(q.x))) << shift;
+    x[1] += T(int(__uint_as_float(q.y))) << shift;
+    x[2] += T(int(__uint_as_float(q.z))) << shift;
+    x[3] += T(int(__uint_as_float(q.w))) << shift;
   }
 }
 
-constexpr int kVecStrip = 32;  // rows per workgroup in the vector stencil
-constexpr int kUnroll = 4;     // row vectors in flight per lane
+// Add the values at columns j0 - 1 (l1) and j0 - 2 (l2) of a row, j0 >= 2.
+template <int V, typename T>
+__device__ __forceinline__ void add_left_pair(const char* row, int64_t j0, int shift, T& l1, T& l2) {
+  if (V == 8) {
+    const uint32_t pw = *reinterpret_cast<const uint32_t*>(row + (j0 - 2) * 2);
+    l2 += T(pw & 0xFFFFu) << shift;
+    l1 += T(pw >> 16) << shift;
+  } else {
+    const uint2 pw = *reinterpret_cast<const uint2*>(row + (j0 - 2) * 4);
+    l2 += T(int(__uint_as_float(pw.x))) << shift;
+    l1 += T(int(__uint_as_float(pw.y))) << shift;
+  }
+}
 
-// V columns per lane from one 16-byte load (8 bf16 or 4 fp32 values), rows
-// loaded kUnroll at a time. The two columns left of a lane's vector are the
-// previous lane's last two (the first lane of each wavefront loads them). Same
-// arithmetic as wb_diff2_kernel; needs cols % V == 0 and a 16-byte aligned src.
-template <int V>
-__global__ __launch_bounds__(kThreads) void wb_diff2_vec_kernel(const char* __restrict__ src, int64_t rows,
-                                                                int64_t cols, int64_t* __restrict__ index,
-                                                                int32_t* __restrict__ value, int64_t capacity,
-                                                                unsigned long long* __restrict__ count) {
+// Row i's vector at column j0 (x) and, for the first lane of a wavefront,
+// the two values left of it, summed over the passes.
+template <int V, typename T, int P>
+__device__ __forceinline__ void load_row_vec(const Passes<P>& s, int64_t rowoff, int64_t j0, bool left, T* x, T& l1,
+                                             T& l2) {
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    if (c >= s.n) break;
+    const char* row = s.p[c] + rowoff;
+    add_vec<V, T>(*reinterpret_cast<const uint4*>(row + j0 * (16 / V)), 16 * c, x);
+    if (left) add_left_pair<V, T>(row, j0, 16 * c, l1, l2);
+  }
+}
+
+// VEC tile: thread t takes the V columns of vector vb + t over rows [i0, i0 +
+// S), after two halo rows, U rows in flight. The two columns left of a
+// lane's vector are the previous lane's last two (the first lane of each
+// wavefront loads them). Same arithmetic as the ELEM tile.
+template <int V, typename T, int P, int U, int S>
+__device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
+                                         int64_t vb, const Sink<T>& out) {
   const int lane = threadIdx.x & 63;
   const int64_t nvec = cols / V;
-  for (int64_t vb = int64_t(blockIdx.x) * kThreads; vb < nvec; vb += int64_t(gridDim.x) * kThreads) {
-    const int64_t v = vb + threadIdx.x;
-    const bool live = v < nvec;
-    const int64_t j0 = v * V;
-    for (int64_t i0 = int64_t(blockIdx.y) * kVecStrip; i0 < rows; i0 += int64_t(gridDim.y) * kVecStrip) {
-      const int64_t i1 = i0 + kVecStrip < rows ? i0 + kVecStrip : rows;
-      int h1[V], h2[V];
+  const int64_t v = vb + threadIdx.x;
+  const bool live = v < nvec;
+  const int64_t j0 = v * V;
+  const int64_t i1 = i0 + S < rows ? i0 + S : rows;
+  T h1[V], h2[V];
 #pragma unroll
-      for (int k = 0; k < V; ++k) h1[k] = h2[k] = 0;
-      for (int64_t ib = (i0 >= 2 ? i0 - 2 : 0); ib < i1; ib += kUnroll) {
-        int x[kUnroll][V];
-        int l1[kUnroll], l2[kUnroll];  // columns j0 - 1 and j0 - 2 of the first lane
+  for (int k = 0; k < V; ++k) h1[k] = h2[k] = 0;
+  for (int64_t ib = (i0 >= 2 ? i0 - 2 : 0); ib < i1; ib += U) {
+    T x[U][V];
+    T l1[U], l2[U];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          const int64_t i = ib + u;
-          l1[u] = l2[u] = 0;
-          if (live && i < i1) {
-            const char* row = src + i * cols * (16 / V);
-            const uint4 q = *reinterpret_cast<const uint4*>(row + j0 * (16 / V));
-            if (V == 8) {
-              const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-              for (int k = 0; k < 4; ++k) {
-                x[u][2 * k] = int(w[k] & 0xFFFFu);
-                x[u][2 * k + 1] = int(w[k] >> 16);
-              }
-            } else {
-              x[u][0] = int(__uint_as_float(q.x));
-              x[u][1] = int(__uint_as_float(q.y));
-              x[u][2] = int(__uint_as_float(q.z));
-              x[u][3] = int(__uint_as_float(q.w));
-            }
-            if (lane == 0 && j0 >= 2) {
-              if (V == 8) {
-                const uint32_t pw = *reinterpret_cast<const uint32_t*>(row + (j0 - 2) * 2);
-                l2[u] = int(pw & 0xFFFFu);
-                l1[u] = int(pw >> 16);
-              } else {
-                const uint2 pw = *reinterpret_cast<const uint2*>(row + (j0 - 2) * 4);
-                l2[u] = int(__uint_as_float(pw.x));
-                l1[u] = int(__uint_as_float(pw.y));
-              }
-            }
-          } else {
-#pragma unroll
-            for (int k = 0; k < V; ++k) x[u][k] = 0;
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          const int64_t i = ib + u;
-          if (i >= i1) break;  // uniform: every lane of the workgroup has the same rows
-          int p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
-          if (lane == 0) {
-            p1 = l1[u];
-            p2 = l2[u];
-          }
-          int h[V];
-          h[0] = x[u][0] - 2 * p1 + p2;
-          h[1] = x[u][1] - 2 * x[u][0] + p1;
-#pragma unroll
-          for (int k = 2; k < V; ++k) h[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
-          int d[V];
-          unsigned any = 0;
-#pragma unroll
-          for (int k = 0; k < V; ++k) {
-            d[k] = h[k] - 2 * h1[k] + h2[k];
-            h2[k] = h1[k];
-            h1[k] = h[k];
-            any |= (live && i >= i0 && d[k] != 0) ? (1u << k) : 0u;
-          }
-          if (__ballot(any != 0) == 0) continue;
-#pragma unroll
-          for (int k = 0; k < V; ++k)
-            emit_entries((any >> k) & 1u, i * cols + j0 + k, d[k], lane, index, value, capacity, count);
-        }
-      }
-    }
-  }
-}
-
-constexpr int kFlatUnroll = 8;  // vectors in flight per lane along a one-row field
-
-// One-row fields (flat buffers): with nothing above, D is the row's second
-// difference h. Each workgroup takes kFlatUnroll consecutive tiles of
-// kThreads vectors; lane l of tile u holds vector (tile start + l).
-template <int V>
-__global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __restrict__ src, int64_t cols,
-                                                                 int64_t* __restrict__ index,
-                                                                 int32_t* __restrict__ value, int64_t capacity,
-                                                                 unsigned long long* __restrict__ count) {
-  const int lane = threadIdx.x & 63;
-  const int64_t nvec = cols / V;
-  const int64_t step = int64_t(gridDim.x) * kThreads * kFlatUnroll;
-  for (int64_t cb = int64_t(blockIdx.x) * kThreads * kFlatUnroll; cb < nvec; cb += step) {
-    int x[kFlatUnroll][V];
-    int l1[kFlatUnroll], l2[kFlatUnroll];
-#pragma unroll
-    for (int u = 0; u < kFlatUnroll; ++u) {
-      const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
-      const int64_t j0 = v * V;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = ib + u;
       l1[u] = l2[u] = 0;
-      if (v < nvec) {
-        const uint4 q = *reinterpret_cast<const uint4*>(src + j0 * (16 / V));
-        if (V == 8) {
-          const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            x[u][2 * k] = int(w[k] & 0xFFFFu);
-            x[u][2 * k + 1] = int(w[k] >> 16);
-          }
-        } else {
-          x[u][0] = int(__uint_as_float(q.x));
-          x[u][1] = int(__uint_as_float(q.y));
-          x[u][2] = int(__uint_as_float(q.z));
-          x[u][3] = int(__uint_as_float(q.w));
-        }
-        if (lane == 0 && j0 >= 2) {
-          if (V == 8) {
-            const uint32_t pw = *reinterpret_cast<const uint32_t*>(src + (j0 - 2) * 2);
-            l2[u] = int(pw & 0xFFFFu);
-            l1[u] = int(pw >> 16);
-          } else {
-            const uint2 pw = *reinterpret_cast<const uint2*>(src + (j0 - 2) * 4);
-            l2[u] = int(__uint_as_float(pw.x));
-            l1[u] = int(__uint_as_float(pw.y));
-          }
-        }
-      } else {
-#pragma unroll
-        for (int k = 0; k < V; ++k) x[u][k] = 0;
-      }
+      for (int k = 0; k < V; ++k) x[u][k] = 0;
+      if (live && i < i1) load_row_vec<V, T, P>(s, i * cols * (16 / V), j0, lane == 0 && j0 >= 2, x[u], l1[u], l2[u]);
     }
 #pragma unroll
-    for (int u = 0; u < kFlatUnroll; ++u) {
-      const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
-      if (cb + int64_t(u) * kThreads >= nvec) break;  // uniform over the workgroup
-      int p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = ib + u;
+      if (i >= i1) break;  // uniform: every lane of the workgroup has the same rows
+      T p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
       if (lane == 0) {
         p1 = l1[u];
         p2 = l2[u];
       }
-      int d[V];
-      d[0] = x[u][0] - 2 * p1 + p2;
-      d[1] = x[u][1] - 2 * x[u][0] + p1;
+      T h[V];
+      h[0] = x[u][0] - 2 * p1 + p2;
+      h[1] = x[u][1] - 2 * x[u][0] + p1;
 #pragma unroll
-      for (int k = 2; k < V; ++k) d[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
+      for (int k = 2; k < V; ++k) h[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
+      T d[V];
       unsigned any = 0;
 #pragma unroll
-      for (int k = 0; k < V; ++k) any |= (v < nvec && d[k] != 0) ? (1u << k) : 0u;
+      for (int k = 0; k < V; ++k) {
+        d[k] = h[k] - 2 * h1[k] + h2[k];
+        h2[k] = h1[k];
+        h1[k] = h[k];
+        any |= (live && i >= i0 && d[k] != 0) ? (1u << k) : 0u;
+      }
       if (__ballot(any != 0) == 0) continue;
 #pragma unroll
-      for (int k = 0; k < V; ++k) emit_entries((any >> k) & 1u, v * V + k, d[k], lane, index, value, capacity, count);
+      for (int k = 0; k < V; ++k) emit_entries<T>((any >> k) & 1u, base + i * cols + j0 + k, d[k], lane, out);
     }
   }
 }
 
+// FLAT tile of a one-row field: with nothing above, D is the row's second
+// difference. Lane l of sub-tile u takes vector cb + u * kThreads + l.
+template <int V, typename T, int P, int U>
+__device__ __forceinline__ void flat_tile(const Passes<P>& s, int64_t cols, int64_t base, int64_t cb,
+                                          const Sink<T>& out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nvec = cols / V;
+  T x[U][V];
+  T l1[U], l2[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
+    l1[u] = l2[u] = 0;
+#pragma unroll
+    for (int k = 0; k < V; ++k) x[u][k] = 0;
+    if (v < nvec) load_row_vec<V, T, P>(s, 0, v * V, lane == 0 && v * V >= 2, x[u], l1[u], l2[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t v = cb + int64_t(u) * kThreads + threadIdx.x;
+    if (cb + int64_t(u) * kThreads >= nvec) break;  // uniform over the workgroup
+    T p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
+    if (lane == 0) {
+      p1 = l1[u];
+      p2 = l2[u];
+    }
+    T d[V];
+    d[0] = x[u][0] - 2 * p1 + p2;
+    d[1] = x[u][1] - 2 * x[u][0] + p1;
+#pragma unroll
+    for (int k = 2; k < V; ++k) d[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
+    unsigned any = 0;
+#pragma unroll
+    for (int k = 0; k < V; ++k) any |= (v < nvec && d[k] != 0) ? (1u << k) : 0u;
+    if (__ballot(any != 0) == 0) continue;
+#pragma unroll
+    for (int k = 0; k < V; ++k) emit_entries<T>((any >> k) & 1u, base + v * V + k, d[k], lane, out);
+  }
+}
+
+// Single-field launches: one pass, int arithmetic, a strided grid over the
+// field's tiles.
+
+__global__ __launch_bounds__(kThreads) void wb_diff2_kernel(const char* __restrict__ src, int dtype, int64_t rows,
+                                                            int64_t cols, Sink<int> out) {
+  const Passes<1> s{{src}, 1};
+  for (int64_t jb = int64_t(blockIdx.x) * kThreads; jb < cols; jb += int64_t(gridDim.x) * kThreads)
+    for (int64_t i0 = int64_t(blockIdx.y) * kStrip; i0 < rows; i0 += int64_t(gridDim.y) * kStrip)
+      elem_tile<int, 1>(s, dtype, rows, cols, 0, i0, jb, out);
+}
+
+template <int V>
+__global__ __launch_bounds__(kThreads) void wb_diff2_vec_kernel(const char* __restrict__ src, int64_t rows,
+                                                                int64_t cols, Sink<int> out) {
+  const Passes<1> s{{src}, 1};
+  const int64_t nvec = cols / V;
+  for (int64_t vb = int64_t(blockIdx.x) * kThreads; vb < nvec; vb += int64_t(gridDim.x) * kThreads)
+    for (int64_t i0 = int64_t(blockIdx.y) * kVecStrip; i0 < rows; i0 += int64_t(gridDim.y) * kVecStrip)
+      vec_tile<V, int, 1, kUnroll, kVecStrip>(s, rows, cols, 0, i0, vb, out);
+}
+
+template <int V>
+__global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __restrict__ src, int64_t cols,
+                                                                 Sink<int> out) {
+  const Passes<1> s{{src}, 1};
+  const int64_t nvec = cols / V;
+  const int64_t step = int64_t(gridDim.x) * kThreads * kFlatUnroll;
+  for (int64_t cb = int64_t(blockIdx.x) * kThreads * kFlatUnroll; cb < nvec; cb += step)
+    flat_tile<V, int, 1, kFlatUnroll>(s, cols, 0, cb, out);
+}
+
+// Batched launch: workgroup b takes tile b of the table; int64 arithmetic
+// over up to kMaxPasses passes, fewer values in flight per lane, taller VEC
+// tiles and FLAT tiles of several sub-tiles (fewer, larger table rows).
+constexpr int kBatchUnroll = 2;
+constexpr int kBatchVecStrip = 128;
+constexpr int kBatchFlatUnroll = 4;
+constexpr int kBatchFlatSub = 4;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
+
+__global__ __launch_bounds__(kThreads) void wb_diff2_batch_kernel(const DiffField* __restrict__ fields,
+                                                                  const DiffTile* __restrict__ tiles,
+                                                                  Sink<int64_t> out) {
+  const DiffTile t = tiles[blockIdx.x];
+  const DiffField& f = fields[t.field];
+  Passes<kMaxPasses> s;
+#pragma unroll
+  for (int c = 0; c < kMaxPasses; ++c) s.p[c] = static_cast<const char*>(f.src[c]);
+  s.n = f.passes;
+  if (f.kind == DIFF_FLAT) {
+    for (int q = 0; q < kBatchFlatSub; ++q) {
+      const int64_t cb = t.j0 + int64_t(q) * kBatchFlatUnroll * kThreads;
+      if (f.dtype == WB_F32)
+        flat_tile<4, int64_t, kMaxPasses, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
+      else
+        flat_tile<8, int64_t, kMaxPasses, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
+    }
+  } else if (f.kind == DIFF_VEC) {
+    if (f.dtype == WB_F32)
+      vec_tile<4, int64_t, kMaxPasses, kBatchUnroll, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+    else
+      vec_tile<8, int64_t, kMaxPasses, kBatchUnroll, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+  } else {
+    elem_tile<int64_t, kMaxPasses>(s, f.dtype, f.rows, f.cols, f.base, t.i0, t.j0, out);
+  }
+}
+
 __global__ void wb_zero_count_kernel(unsigned long long* count) { *count = 0; }
+
+// VEC and FLAT tiles need whole 16-byte vectors in every pass.
+int tile_kind(const void* const* src, int passes, int dtype, int64_t rows, int64_t cols) {
+  const int V = dtype == WB_F32 ? 4 : 8;
+  if (cols % V != 0) return DIFF_ELEM;
+  for (int c = 0; c < passes; ++c)
+    if (reinterpret_cast<uintptr_t>(src[c]) % 16 != 0) return DIFF_ELEM;
+  return rows == 1 ? DIFF_FLAT : DIFF_VEC;
+}
+
+// A 2-D grid over (x tiles, y strips), about 64 K workgroups at most; each
+// workgroup loops over further tiles.
+dim3 strided_grid(int64_t xtiles, int64_t strips) {
+  const int64_t y = strips < 65535 ? strips : 65535;
+  const int64_t xcap = (65536 + y - 1) / y;
+  return dim3(static_cast<unsigned>(xtiles < xcap ? xtiles : xcap), static_cast<unsigned>(y));
+}
 
 }  // namespace
 
@@ -298,41 +372,67 @@ int launch_diff2(const void* src, int dtype, int64_t rows, int64_t cols, int64_t
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipLaunchKernelGGL(wb_zero_count_kernel, dim3(1), dim3(1), 0, st, count);
   if (rows == 0 || cols == 0) return hipGetLastError();
-  const int es = dtype == WB_F32 ? 4 : 2;
-  const int V = 16 / es;
-  if (rows == 1 && cols % V == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0) {
-    const int64_t chunks = (cols / V + kThreads * kFlatUnroll - 1) / (kThreads * kFlatUnroll);
-    const dim3 grid(static_cast<unsigned>(chunks < 65536 ? chunks : 65536));
-    if (V == 8)
-      hipLaunchKernelGGL(wb_diff2_flat_kernel<8>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), cols,
-                         index, value, capacity, count);
-    else
-      hipLaunchKernelGGL(wb_diff2_flat_kernel<4>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), cols,
-                         index, value, capacity, count);
-    return hipGetLastError();
+  const Sink<int> out{index, value, capacity, count};
+  const char* s = static_cast<const char*>(src);
+  const bool f32 = dtype == WB_F32;
+  const int V = f32 ? 4 : 8;
+  switch (tile_kind(&src, 1, dtype, rows, cols)) {
+    case DIFF_FLAT: {
+      const int64_t tiles = (cols / V + kThreads * kFlatUnroll - 1) / (kThreads * kFlatUnroll);
+      const dim3 grid(static_cast<unsigned>(tiles < 65536 ? tiles : 65536));
+      if (f32)
+        hipLaunchKernelGGL(wb_diff2_flat_kernel<4>, grid, dim3(kThreads), 0, st, s, cols, out);
+      else
+        hipLaunchKernelGGL(wb_diff2_flat_kernel<8>, grid, dim3(kThreads), 0, st, s, cols, out);
+      break;
+    }
+    case DIFF_VEC: {
+      const dim3 grid = strided_grid((cols / V + kThreads - 1) / kThreads, (rows + kVecStrip - 1) / kVecStrip);
+      if (f32)
+        hipLaunchKernelGGL(wb_diff2_vec_kernel<4>, grid, dim3(kThreads), 0, st, s, rows, cols, out);
+      else
+        hipLaunchKernelGGL(wb_diff2_vec_kernel<8>, grid, dim3(kThreads), 0, st, s, rows, cols, out);
+      break;
+    }
+    default: {
+      const dim3 grid = strided_grid((cols + kThreads - 1) / kThreads, (rows + kStrip - 1) / kStrip);
+      hipLaunchKernelGGL(wb_diff2_kernel, grid, dim3(kThreads), 0, st, s, dtype, rows, cols, out);
+    }
   }
-  if (cols % V == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0) {
-    const int64_t strips = (rows + kVecStrip - 1) / kVecStrip;
-    const int64_t tiles = (cols / V + kThreads - 1) / kThreads;
-    const int64_t ytiles = strips < 65535 ? strips : 65535;
-    const int64_t xtiles = tiles < (65536 + ytiles - 1) / ytiles ? tiles : (65536 + ytiles - 1) / ytiles;
-    const dim3 grid(static_cast<unsigned>(xtiles), static_cast<unsigned>(ytiles));
-    if (V == 8)
-      hipLaunchKernelGGL(wb_diff2_vec_kernel<8>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), rows,
-                         cols, index, value, capacity, count);
-    else
-      hipLaunchKernelGGL(wb_diff2_vec_kernel<4>, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), rows,
-                         cols, index, value, capacity, count);
-    return hipGetLastError();
+  return hipGetLastError();
+}
+
+void diff_tiles(int32_t fi, DiffField& f, std::vector<DiffTile>& out) {
+  f.kind = static_cast<uint8_t>(tile_kind(f.src, f.passes, f.dtype, f.rows, f.cols));
+  if (f.rows == 0 || f.cols == 0) return;
+  const int64_t nvec = f.cols / (f.dtype == WB_F32 ? 4 : 8);
+  int64_t istep = kStrip, jstep = kThreads, jend = f.cols;
+  if (f.kind == DIFF_FLAT) {
+    istep = 1;
+    jstep = int64_t(kThreads) * kBatchFlatUnroll * kBatchFlatSub;
+    jend = nvec;
+  } else if (f.kind == DIFF_VEC) {
+    istep = kBatchVecStrip;
+    jend = nvec;
   }
-  const int64_t strips = (rows + kStrip - 1) / kStrip;
-  const int64_t tiles = (cols + kThreads - 1) / kThreads;
-  const int64_t ytiles = strips < 65535 ? strips : 65535;
-  // about 64 K workgroups at most; each loops over further column tiles
-  const int64_t xtiles = tiles < (65536 + ytiles - 1) / ytiles ? tiles : (65536 + ytiles - 1) / ytiles;
-  const dim3 grid(static_cast<unsigned>(xtiles), static_cast<unsigned>(ytiles));
-  hipLaunchKernelGGL(wb_diff2_kernel, grid, dim3(kThreads), 0, st, static_cast<const char*>(src), dtype, rows, cols,
-                     index, value, capacity, count);
+  DiffTile t{};
+  t.field = fi;
+  for (int64_t i0 = 0; i0 < f.rows; i0 += istep)
+    for (int64_t j0 = 0; j0 < jend; j0 += jstep) {
+      t.i0 = i0;
+      t.j0 = j0;
+      out.push_back(t);
+    }
+}
+
+int launch_diff2_batch(const DiffField* fields, const DiffTile* tiles, int64_t ntiles, int64_t* index, int64_t* value,
+                       int64_t capacity, unsigned long long* count, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(wb_zero_count_kernel, dim3(1), dim3(1), 0, st, count);
+  if (ntiles == 0) return hipGetLastError();
+  const Sink<int64_t> out{index, value, capacity, count};
+  hipLaunchKernelGGL(wb_diff2_batch_kernel, dim3(static_cast<unsigned>(ntiles)), dim3(kThreads), 0, st, fields, tiles,
+                     out);
   return hipGetLastError();
 }
 

@@ -165,6 +165,27 @@ static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
 enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
 
+// A field of a batched diff2 launch: rows x cols values, value at (i, j) the
+// sum over k < passes of src[k][i * cols + j] << (16 k); its element 0 is
+// entry index base of the output. kind says how its tiles read it.
+constexpr int kMaxPasses = 3;
+enum DiffKind : uint8_t { DIFF_ELEM = 0, DIFF_VEC = 1, DIFF_FLAT = 2 };
+struct DiffField {
+  const void* src[kMaxPasses];
+  int64_t rows, cols, base;
+  int32_t dtype;
+  uint8_t kind, passes;
+  uint16_t pad;
+};
+static_assert(sizeof(DiffField) == 56, "DiffField layout");
+// One workgroup's share: the tile of field `field` starting at row i0 and
+// column (ELEM) or 16-byte vector (VEC, FLAT) j0.
+struct DiffTile {
+  int32_t field, pad;
+  int64_t i0, j0;
+};
+static_assert(sizeof(DiffTile) == 24, "DiffTile layout");
+
 // A local tensor of a probed rank and its recombined diff2 entries.
 struct ProbeLocal {
   std::string name;
@@ -230,10 +251,15 @@ int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const
 const char* hip_error_string(int err);
 // probe.cpp
 void probe_init(wb_probe_t& P, const wb_tensor_desc* catalog, int n, int ckpt_dtype);
-void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int32_t* value, int64_t n);
+void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int64_t* value, int64_t n);
 void probe_scan(const wb_probe_t& P, wb_layout_t& out, int rank);
 // probe.hip
 int launch_make_ids(void* dst, int dtype, int64_t numel, int64_t first_id, int shift, uint32_t mask, void* stream);
 int launch_diff2(const void* src, int dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
                  int64_t capacity, unsigned long long* count, void* stream);
+// appends the tiles of one field (element 0 at entry index base) to out
+// fills f.kind and appends the tiles of field f (index fi) to out
+void diff_tiles(int32_t fi, DiffField& f, std::vector<DiffTile>& out);
+int launch_diff2_batch(const DiffField* fields, const DiffTile* tiles, int64_t ntiles, int64_t* index, int64_t* value,
+                       int64_t capacity, unsigned long long* count, void* stream);
 }  // namespace wb

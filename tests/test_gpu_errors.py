@@ -105,3 +105,20 @@ def test_forward_and_probe_checks():
                                                      val.data_ptr(), 16, cnt.data_ptr(), None)))
     _expect_einval(lambda: wb._check(wb.lib.wb_diff2(x.data_ptr(), wb.DTYPES["bf16"], 4, 4, idx.data_ptr(),
                                                      val.data_ptr(), 16, cnt.data_ptr() + 4, None)))
+    f = [([x, x], "bf16", 16, 64)]
+    arr = wb._field_array(f)
+    need = wb.diff2_batch_workspace(f)
+    ws = torch.empty(need + 64, dtype=torch.uint8, device="cuda")
+    v64 = torch.empty(16, dtype=torch.int64, device="cuda")
+
+    def batch(ws_ptr, ws_bytes, value_ptr, count_ptr, fields=arr):
+        return wb._check(wb.lib.wb_diff2_batch(fields, 1, ws_ptr, ws_bytes, idx.data_ptr(), value_ptr, 16, count_ptr,
+                                               None))
+
+    assert "workspace" in _expect_einval(batch, ws.data_ptr(), need - 8, v64.data_ptr(), cnt.data_ptr())
+    _expect_einval(batch, ws.data_ptr() + 4, need, v64.data_ptr(), cnt.data_ptr())        # misaligned workspace
+    _expect_einval(batch, ws.data_ptr(), need, v64.data_ptr() + 4, cnt.data_ptr())        # misaligned values
+    _expect_einval(batch, ws.data_ptr(), need, v64.data_ptr(), cnt.data_ptr() + 4)        # misaligned count
+    bad = wb._field_array([([x.data_ptr() + 1, x.data_ptr()], "bf16", 16, 64)])
+    assert "aligned" in _expect_einval(batch, ws.data_ptr(), need, v64.data_ptr(), cnt.data_ptr(), bad)
+    torch.cuda.synchronize()

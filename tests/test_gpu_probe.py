@@ -118,14 +118,109 @@ def test_diff2_capacity_overflow_reports_the_count():
         assert want[(int(i) // 90, int(i) % 90)] == int(v)
 
 
+def _batch(fields, cap):
+    """Run wb_diff2_batch; returns (count, {index: value})."""
+    idx = torch.full((cap,), -1, dtype=torch.int64, device="cuda")
+    val = torch.zeros(cap, dtype=torch.int64, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ws = torch.empty(max(wb.diff2_batch_workspace(fields), 8), dtype=torch.uint8, device="cuda")
+    wb.diff2_batch(fields, idx, val, count, ws)
+    torch.cuda.synchronize()
+    n = int(count.item())
+    m = min(n, cap)
+    got = dict(zip(idx[:m].cpu().numpy().tolist(), val[:m].cpu().numpy().tolist()))
+    assert len(got) == m
+    return n, got
+
+
+def _expected(fields_np):
+    """Oracle entries of a batch: diff2 of every field's value (sum of 2^(16 k)
+    times pass k), at the field's offset in the concatenation."""
+    want, off = {}, 0
+    for passes, R, C in fields_np:
+        A = sum((p.astype(np.int64) << (16 * k)) for k, p in enumerate(passes))
+        for (i, j), v in nonzeros(diff2(np.asarray(A, dtype=np.int64).reshape(R, C))).items():
+            want[off + i * C + j] = v
+        off += R * C
+    return want
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", ["random", "slices"])
+def test_diff2_batch_one_pass_matches_oracle(dtype, kind):
+    """Every shape above in one launch, plus empty fields and an unaligned view
+    (element tiles): entries at each field's offset in the concatenation."""
+    rng = np.random.default_rng(11)
+    shapes = SHAPES + [(0, 5), (4, 0), (40, 512)]
+    fields, fields_np, keep = [], [], []
+    for n, (R, C) in enumerate(shapes):
+        F = _field(rng, R, C, kind) if R * C else np.zeros((R, C), dtype=np.int64)
+        if n == len(shapes) - 1:   # one element into its allocation
+            big = _to_gpu(np.concatenate([[7], F.ravel(), [9]]), dtype)
+            x = big[1:1 + R * C]
+            keep.append(big)
+        else:
+            x = _to_gpu(F, dtype)
+        fields.append((x, dtype, R, C))
+        fields_np.append(([F], R, C))
+    say(f"[diff2 batch] {dtype} {kind} {len(fields)} fields")
+    want = _expected(fields_np)
+    n, got = _batch(fields, sum(R * C for R, C in shapes) + 16)
+    assert n == len(want)
+    assert got == want
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("passes", [2, 3])
+def test_diff2_batch_recombines_passes(dtype, passes):
+    """Fields given as several passes: random chunks (every entry survives,
+    values up to 2^52), and the chunks of real identifier slices, whose
+    wrap-around entries cancel inside the launch so that only diff2 of the
+    identifier field itself comes out."""
+    rng = np.random.default_rng(12 + passes)
+    fields, fields_np = [], []
+    for R, C in SHAPES:
+        if rng.random() < 0.5:
+            chunks = [rng.integers(0, 1 << 16, size=(R, C)) for _ in range(passes)]
+        else:
+            A = np.zeros((R, C), dtype=np.int64)
+            for _ in range(3):
+                a = int(rng.integers(0, R)); b = int(rng.integers(a + 1, R + 1))
+                c = int(rng.integers(0, C)); d = int(rng.integers(c + 1, C + 1))
+                base = int(rng.integers(1 << 24, 1 << (16 * passes - 2)))
+                i = np.arange(a, b)[:, None]; j = np.arange(c, d)[None, :]
+                A[a:b, c:d] = base + i * int(rng.integers(1, 5000)) + j
+            chunks = [id_chunk(A, k, 16) for k in range(passes)]
+            # the chunk fields alone have many more entries than the identifiers
+            assert sum(len(nonzeros(diff2(ch))) for ch in chunks) >= len(nonzeros(diff2(A)))
+        fields.append(([_to_gpu(ch, dtype) for ch in chunks], dtype, R, C))
+        fields_np.append((chunks, R, C))
+    say(f"[diff2 batch] {dtype} passes={passes}")
+    want = _expected(fields_np)
+    n, got = _batch(fields, sum(R * C for R, C in SHAPES) + 16)
+    assert n == len(want)
+    assert got == want
+
+
+def test_diff2_batch_capacity_overflow_reports_the_count():
+    rng = np.random.default_rng(13)
+    F = [rng.integers(0, 1 << 16, size=(50, 90)) for _ in range(2)]
+    fields = [([_to_gpu(f, "bf16") for f in F], "bf16", 50, 90), (_to_gpu(F[0], "bf16"), "bf16", 50, 90)]
+    want = _expected([(F, 50, 90), ([F[0]], 50, 90)])
+    n, got = _batch(fields, 10)
+    assert n == len(want)
+    assert len(got) == 10 and all(want[i] == v for i, v in got.items())
+
+
 def _loaders(w, side, ranks):
     par = w[side]
     fn = ref.STYLES[par["style"]]
     return [lambda T, r=r: [x.contiguous() for x in fn(w["model"], par, T, r) if x is not None] for r in ranks]
 
 
+@pytest.mark.parametrize("hold", [True, False])
 @pytest.mark.parametrize("name", ORDER)
-def test_probe_recovers_declared_layouts(name):
+def test_probe_recovers_declared_layouts(name, hold):
     w = scaled(name)
     shapes = ref.ckpt_shapes(w["model"])
     for side in ("trainer", "rollout"):
@@ -133,9 +228,11 @@ def test_probe_recovers_declared_layouts(name):
         cat = [(c.name, c.rows, c.cols) for c in L.catalog]
         assert all(shapes[n] == (r, c) for n, r, c in cat)
         ranks = sorted({0, L.nranks - 1})
-        say(f"[probe] {name} {side} ranks {ranks}")
+        say(f"[probe] {name} {side} ranks {ranks} hold_passes={hold}")
         dtype = w["trainer"]["dtype"]
-        got = wb.probe_layout(cat, dtype, _loaders(w, side, ranks))
+        stats = {}
+        got = wb.probe_layout(cat, dtype, _loaders(w, side, ranks), stats=stats, hold_passes=hold)
+        assert stats["hold_passes"] == [hold] * len(ranks)
         for k, r in enumerate(ranks):
             rk = L.ranks[r]
             keep = [u for u, lc in enumerate(rk.locals) if lc.scales < 0]
@@ -146,19 +243,22 @@ def test_probe_recovers_declared_layouts(name):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("name,side", [("llama3_8b_fsdp8_to_tp1", "trainer"), ("llama3_8b_fsdp8_to_tp1", "rollout"),
-                                       ("llama3_8b_tp4_to_tp2", "trainer")])
-def test_probe_full_size(name, side):
+@pytest.mark.parametrize("name,side,hold", [("llama3_8b_fsdp8_to_tp1", "trainer", True),
+                                            ("llama3_8b_fsdp8_to_tp1", "rollout", True),
+                                            ("llama3_8b_fsdp8_to_tp1", "rollout", False),
+                                            ("llama3_8b_tp4_to_tp2", "trainer", True)])
+def test_probe_full_size(name, side, hold):
     """The benchmark ranks at full size (16 GB identifier checkpoint), probed
-    through the torch loaders: the recovered placements equal the declared."""
+    through the torch loaders, with the passes held on the device or recorded
+    one by one: the recovered placements equal the declared."""
     from synthetic_checkpoint.workloads import WORKLOADS
 
     w = WORKLOADS[name]
     rank = w["pack_rank"] if side == "trainer" else w["unpack_rank"]
     L = layout_from_spec(w["model"], w[side])
     cat = [(c.name, c.rows, c.cols) for c in L.catalog]
-    say(f"[probe full] {name} {side} rank {rank}")
-    got = wb.probe_layout(cat, w["trainer"]["dtype"], _loaders(w, side, [rank]))
+    say(f"[probe full] {name} {side} rank {rank} hold_passes={hold}")
+    got = wb.probe_layout(cat, w["trainer"]["dtype"], _loaders(w, side, [rank]), hold_passes=hold)
     rk = L.ranks[rank]
     keep = [u for u, lc in enumerate(rk.locals) if lc.scales < 0]
     remap = {u: i for i, u in enumerate(keep)}
