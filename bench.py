@@ -172,11 +172,10 @@ def _launch_grids(w):
     ro = wb.Layout.describe(w["model"], w["rollout"])
     rp = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"])
     sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
-    rt, rb, _ = rp.work_counts()
-    st, _, _ = sp.work_counts()
-    return {"pack": (st * 256, "wb_tasks_kernel", sp.traffic()),
-            "unpack": (rt * 256, "wb_tasks_kernel", rp.kernel_traffic(0)),
-            "unpack_fp8": (rb * 256, "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
+    # rocprofv3 reports Grid_Size(_X) in threads: x workgroups of 256
+    return {"pack": (sp.launch_grid(0)[0] * 256, "wb_tasks_kernel", sp.traffic()),
+            "unpack": (rp.launch_grid(0)[0] * 256, "wb_tasks_kernel", rp.kernel_traffic(0)),
+            "unpack_fp8": (rp.launch_grid(1)[0] * 256, "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
 
 
 def summarize_counters(workload, fetch_csv, write_csv):

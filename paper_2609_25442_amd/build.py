@@ -37,13 +37,13 @@ def _run(cmd):
 
 def build(verbose: bool = False, out: str = OUT, defines=()) -> str:
     """Compile and link libwb.so at ``out``; ``defines`` are extra -D flags for
-    the kernels (tuning knobs such as WB_UNROLL)."""
+    the host and device sources (tuning knobs such as WB_CHUNK_PER_LANE)."""
     bdir = os.path.join(ROOT, "_build", os.path.basename(out) + ".d")
     os.makedirs(bdir, exist_ok=True)
     objs = []
     for s in HOST_SOURCES:
         o = os.path.join(bdir, s + ".o")
-        _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, s), "-o", o])
+        _run(["g++", *HOST_FLAGS, *["-D" + d for d in defines], "-c", os.path.join(CSRC, s), "-o", o])
         objs.append(o)
     for s in DEVICE_SOURCES:
         o = os.path.join(bdir, s + ".o")

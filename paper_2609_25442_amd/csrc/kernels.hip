@@ -7,7 +7,12 @@
 //  * wb_tasks_kernel  -- copy/cast work items: 16-byte vectorised row copies,
 //    fp32 -> bf16 (v_cvt_pk_bf16_f32, round to nearest even), bf16 -> fp32,
 //    an element-wise fallback for unaligned or odd cases, and 64 x 64 tiles
-//    transposed through LDS where a trainer stores a shard transposed.
+//    transposed through LDS where a trainer stores a shard transposed. The
+//    vector kinds are spread over several workgroups per item: each takes one
+//    chunk of kChunkVecs vectors, issues all of its loads, then all of its
+//    stores, and exits (no loop, so no wait on the completion of earlier
+//    stores before the next loads, which caps a looping copy well below the
+//    rate of these one-shot workgroups on gfx950).
 //  * wb_qblock_kernel -- one fp8 E4M3FN block (<= 128 x 128) per workgroup,
 //    gathered from its wire pieces into registers: amax by wavefront
 //    shuffles plus LDS across the four waves, s = amax / 448 (IEEE division),
@@ -23,20 +28,23 @@
 namespace wb {
 namespace {
 
-// Tuning knobs (build-time): 16-byte vectors in flight per lane, and whether
-// loads / stores carry the non-temporal hint (every byte is touched once).
-#ifndef WB_UNROLL
-#define WB_UNROLL 4
-#endif
+// Tuning knobs (build-time): whether loads / stores carry the non-temporal
+// hint (every byte is touched once), and dynamic LDS reserved per copy
+// workgroup (a cap on workgroups per CU). The chunk size is in wb_internal.hpp.
 #ifndef WB_NT_LOAD
 #define WB_NT_LOAD 1
 #endif
 #ifndef WB_NT_STORE
 #define WB_NT_STORE 1
 #endif
+#ifndef WB_TASK_DYN_LDS
+#define WB_TASK_DYN_LDS 0
+#endif
+#ifndef WB_QBLOCK_DYN_LDS
+#define WB_QBLOCK_DYN_LDS 0
+#endif
 
-constexpr int kThreads = 256;
-constexpr int kUnroll = WB_UNROLL;
+constexpr int kThreads = kChunkThreads;
 
 template <class T>
 __device__ __forceinline__ T ld(const T* p) {
@@ -93,95 +101,94 @@ struct Walker {
   }
 };
 
-// 16-byte row copy; cols, strides and offsets in bytes.
-__device__ void run_copy16(const Task& t, const char* src, char* dst) {
-  const uint32_t vpr = t.cols >> 4;
-  if (t.rows == 1) {
-    const u32x4* s = reinterpret_cast<const u32x4*>(src);
-    u32x4* d = reinterpret_cast<u32x4*>(dst);
-    uint32_t i = threadIdx.x;
-    for (; i + (kUnroll - 1) * kThreads < vpr; i += kUnroll * kThreads) {
-      u32x4 v[kUnroll];
+// Vectors [q0, q1) of a rows x vpr block in row-major order: lane l takes
+// q0 + l + k * kThreads for k < kChunkPerLane. Each pointer is null where the
+// lane has no vector.
+struct ChunkWalk {
+  uint32_t r[kChunkPerLane], c[kChunkPerLane];
+  bool on[kChunkPerLane];
+  __device__ ChunkWalk(uint32_t q0, uint32_t q1, uint32_t vpr) {
+    Walker w(q0 + threadIdx.x, vpr);
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) v[k] = ld(s + i + k * kThreads);
-#pragma unroll
-      for (int k = 0; k < kUnroll; ++k) st(v[k], d + i + k * kThreads);
+    for (int k = 0; k < kChunkPerLane; ++k) {
+      on[k] = q0 + threadIdx.x + k * kThreads < q1;
+      r[k] = w.r;
+      c[k] = w.c;
+      w.step();
     }
-    for (; i < vpr; i += kThreads) st(ld(s + i), d + i);
+  }
+};
+
+// 16-byte row copy of one chunk; cols, strides and offsets in bytes.
+__device__ void run_copy16(const Task& t, const char* src, char* dst, uint32_t q0) {
+  const uint32_t vpr = t.cols >> 4;
+  const uint32_t total = t.rows * vpr;
+  if (q0 >= total) return;
+  const uint32_t q1 = min(total, q0 + uint32_t(kChunkVecs));
+  u32x4 v[kChunkPerLane];
+  if (t.rows == 1) {
+    const u32x4* s = reinterpret_cast<const u32x4*>(src) + q0 + threadIdx.x;
+    u32x4* d = reinterpret_cast<u32x4*>(dst) + q0 + threadIdx.x;
+    const uint32_t m = q1 - q0;
+#pragma unroll
+    for (int k = 0; k < kChunkPerLane; ++k)
+      if (threadIdx.x + k * kThreads < m) v[k] = ld(s + k * kThreads);
+#pragma unroll
+    for (int k = 0; k < kChunkPerLane; ++k)
+      if (threadIdx.x + k * kThreads < m) st(v[k], d + k * kThreads);
     return;
   }
-  const uint64_t total = uint64_t(t.rows) * vpr;
-  Walker w(threadIdx.x, vpr);
-  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
-    u32x4 v[kUnroll];
-    u32x4* dp[kUnroll];
+  const ChunkWalk w(q0, q1, vpr);
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      dp[k] = nullptr;
-      if (q + uint64_t(k) * kThreads < total) {
-        const u32x4* sp = reinterpret_cast<const u32x4*>(src + uint64_t(w.r) * t.src_ld) + w.c;
-        dp[k] = reinterpret_cast<u32x4*>(dst + uint64_t(w.r) * t.dst_ld) + w.c;
-        v[k] = ld(sp);
-      }
-      w.step();
-    }
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k]) v[k] = ld(reinterpret_cast<const u32x4*>(src + uint64_t(w.r[k]) * t.src_ld) + w.c[k]);
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) st(v[k], dp[k]);
-  }
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k]) st(v[k], reinterpret_cast<u32x4*>(dst + uint64_t(w.r[k]) * t.dst_ld) + w.c[k]);
 }
 
-// fp32 -> bf16, 8 elements per vector; strides in elements.
-__device__ void run_f32_bf16(const Task& t, const char* src, char* dst) {
+// fp32 -> bf16 of one chunk of output vectors (8 elements each); strides in
+// elements.
+__device__ void run_f32_bf16(const Task& t, const char* src, char* dst, uint32_t q0) {
   const uint32_t vpr = t.cols >> 3;
-  const uint64_t total = uint64_t(t.rows) * vpr;
-  Walker w(threadIdx.x, vpr);
-  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
-    f32x4 a[kUnroll], b[kUnroll];
-    u32x4* dp[kUnroll];
+  const uint32_t total = t.rows * vpr;
+  if (q0 >= total) return;
+  const ChunkWalk w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
+  f32x4 a[kChunkPerLane], b[kChunkPerLane];
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      dp[k] = nullptr;
-      if (q + uint64_t(k) * kThreads < total) {
-        const f32x4* sp = reinterpret_cast<const f32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 4);
-        dp[k] = reinterpret_cast<u32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 2);
-        a[k] = ld(sp);
-        b[k] = ld(sp + 1);
-      }
-      w.step();
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k]) {
+      const f32x4* sp = reinterpret_cast<const f32x4*>(src + (uint64_t(w.r[k]) * t.src_ld + uint64_t(w.c[k]) * 8) * 4);
+      a[k] = ld(sp);
+      b[k] = ld(sp + 1);
     }
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) st(cvt8_f32_bf16(a[k], b[k]), dp[k]);
-  }
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k])
+      st(cvt8_f32_bf16(a[k], b[k]),
+         reinterpret_cast<u32x4*>(dst + (uint64_t(w.r[k]) * t.dst_ld + uint64_t(w.c[k]) * 8) * 2));
 }
 
-// bf16 -> fp32, 8 elements per vector; strides in elements.
-__device__ void run_bf16_f32(const Task& t, const char* src, char* dst) {
+// bf16 -> fp32 of one chunk of input vectors (8 elements each); strides in
+// elements.
+__device__ void run_bf16_f32(const Task& t, const char* src, char* dst, uint32_t q0) {
   const uint32_t vpr = t.cols >> 3;
-  const uint64_t total = uint64_t(t.rows) * vpr;
-  Walker w(threadIdx.x, vpr);
-  for (uint64_t q = threadIdx.x; q < total; q += kUnroll * kThreads) {
-    u32x4 v[kUnroll];
-    f32x4* dp[kUnroll];
+  const uint32_t total = t.rows * vpr;
+  if (q0 >= total) return;
+  const ChunkWalk w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
+  u32x4 v[kChunkPerLane];
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      dp[k] = nullptr;
-      if (q + uint64_t(k) * kThreads < total) {
-        const u32x4* sp = reinterpret_cast<const u32x4*>(src + (uint64_t(w.r) * t.src_ld + uint64_t(w.c) * 8) * 2);
-        dp[k] = reinterpret_cast<f32x4*>(dst + (uint64_t(w.r) * t.dst_ld + uint64_t(w.c) * 8) * 4);
-        v[k] = ld(sp);
-      }
-      w.step();
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k])
+      v[k] = ld(reinterpret_cast<const u32x4*>(src + (uint64_t(w.r[k]) * t.src_ld + uint64_t(w.c[k]) * 8) * 2));
+#pragma unroll
+  for (int k = 0; k < kChunkPerLane; ++k)
+    if (w.on[k]) {
+      const u32x4 x = v[k];
+      f32x4* dp = reinterpret_cast<f32x4*>(dst + (uint64_t(w.r[k]) * t.dst_ld + uint64_t(w.c[k]) * 8) * 4);
+      st(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, dp);
+      st(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, dp + 1);
     }
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) {
-        const u32x4 x = v[k];
-        st(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, dp[k]);
-        st(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, dp[k] + 1);
-      }
-  }
 }
 
 // Raw bits of one element, widened to 32 bits.
@@ -263,19 +270,26 @@ __device__ __forceinline__ const char* base_of(uint16_t idx, const uint64_t* ptr
   return idx == 0 ? buf : idx == kAuxBuffer ? aux : reinterpret_cast<const char*>(ptrs[idx]);
 }
 
+// Workgroup b takes chunk b mod 2^shift of work item b >> shift; a grid wider
+// than kMaxGridX workgroups is folded into rows of gridDim.x.
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
                                                             const uint64_t* __restrict__ ptrs, const char* buf,
-                                                            const char* aux) {
-  const Task t = tasks[blockIdx.x];
+                                                            const char* aux, uint32_t ntasks, uint32_t shift) {
+  const uint64_t b = uint64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+  const uint64_t ti = b >> shift;
+  if (ti >= ntasks) return;
+  const uint32_t chunk = uint32_t(b) & ((1u << shift) - 1u);
+  const Task t = tasks[ti];
   const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
   char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
+  const uint32_t q0 = chunk * uint32_t(kChunkVecs);
   switch (t.kind) {
-    case TASK_COPY16: run_copy16(t, src, dst); break;
-    case TASK_F32_BF16: run_f32_bf16(t, src, dst); break;
-    case TASK_BF16_F32: run_bf16_f32(t, src, dst); break;
-    case TASK_SCALAR: run_scalar(t, src, dst); break;
-    case TASK_TRANSPOSE: run_transpose(t, src, dst); break;
-    case TASK_TRANSPOSE16: run_transpose16(t, src, dst); break;
+    case TASK_COPY16: run_copy16(t, src, dst, q0); break;
+    case TASK_F32_BF16: run_f32_bf16(t, src, dst, q0); break;
+    case TASK_BF16_F32: run_bf16_f32(t, src, dst, q0); break;
+    case TASK_SCALAR: if (chunk == 0) run_scalar(t, src, dst); break;
+    case TASK_TRANSPOSE: if (chunk == 0) run_transpose(t, src, dst); break;
+    case TASK_TRANSPOSE16: if (chunk == 0) run_transpose16(t, src, dst); break;
     default: break;
   }
 }
@@ -433,17 +447,31 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, const void* aux, void* stream) {
+void task_grid(uint32_t n, uint32_t shift, uint32_t* gx, uint32_t* gy) {
+  const uint64_t total = uint64_t(n) << shift;
+  if (total <= kMaxGridX) {
+    *gx = static_cast<uint32_t>(total);
+    *gy = 1;
+  } else {
+    *gx = kMaxGridX;
+    *gy = static_cast<uint32_t>((total + kMaxGridX - 1) / kMaxGridX);
+  }
+}
+
+int launch_tasks(const Task* tasks, uint32_t n, uint32_t shift, const uint64_t* ptrs, const void* buf,
+                 const void* aux, void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_tasks_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), tasks, ptrs,
-                     static_cast<const char*>(buf), static_cast<const char*>(aux));
+  uint32_t gx, gy;
+  task_grid(n, shift, &gx, &gy);
+  hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS, static_cast<hipStream_t>(stream),
+                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, shift);
   return hipGetLastError();
 }
 
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_qblock_kernel, dim3(n), dim3(kThreads), 0, static_cast<hipStream_t>(stream), blocks, pieces,
+  hipLaunchKernelGGL(wb_qblock_kernel, dim3(n), dim3(kThreads), WB_QBLOCK_DYN_LDS, static_cast<hipStream_t>(stream), blocks, pieces,
                      ptrs, static_cast<const char*>(buf));
   return hipGetLastError();
 }

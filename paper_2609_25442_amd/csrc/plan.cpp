@@ -224,7 +224,7 @@ bool cast_supported(int sdt, int ddt) {
 int64_t env_task_bytes() {
   const char* s = std::getenv("WB_TASK_BYTES");
   const int64_t v = s ? std::atoll(s) : 0;
-  return v >= 1024 ? v : (int64_t(1) << 18);
+  return v >= 1024 && v <= (int64_t(1) << 30) ? v : (int64_t(1) << 18);
 }
 
 // The dtype a segment's bytes travel in: that of the trainer placement they
@@ -462,6 +462,9 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   if (!ranges) fail(WB_EINVAL, "internal: round ranges");
   auto check_task = [&](const Task& t) {
     if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
+    // the kernel counts a work item's vectors and chunk offsets in 32 bits
+    if (uint64_t(t.rows) * t.cols >= (uint64_t(1) << 31) || task_chunks(t) > (1u << P.task_shift))
+      fail(WB_EINVAL, "internal: work item too large for its launch");
     const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
     switch (t.kind) {
       case TASK_COPY16:
@@ -918,6 +921,10 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   P.role = role;
   P.rank = rank;
   build_rank_view(trainer, rollout, P);
+  uint32_t most = 1;  // workgroups of the copy kernel per work item
+  for (const Task& t : P.tasks) most = std::max(most, task_chunks(t));
+  P.task_shift = 0;
+  while ((1u << P.task_shift) < most) ++P.task_shift;
   check_work(P, role == WB_SENDER ? trainer.ranks[rank] : rollout.ranks[rank]);
 }
 

@@ -136,6 +136,28 @@ struct Task {
 };
 static_assert(sizeof(Task) == 48, "Task layout");
 
+// The copy kernel runs 2^shift workgroups of kChunkThreads threads per work
+// item; a vector-kind item is cut into chunks of kChunkVecs 16-byte vectors
+// (kChunkPerLane per lane), one per workgroup, the other kinds run in the
+// item's first workgroup. Grids wider than kMaxGridX workgroups fold into a
+// second dimension.
+#ifndef WB_CHUNK_PER_LANE
+#define WB_CHUNK_PER_LANE 1
+#endif
+constexpr int kChunkThreads = 256;
+constexpr int kChunkPerLane = WB_CHUNK_PER_LANE;
+constexpr uint32_t kChunkVecs = uint32_t(kChunkThreads) * kChunkPerLane;
+constexpr uint32_t kMaxGridX = 1u << 22;
+
+// Workgroups a work item needs (host side of the rule above).
+inline uint32_t task_chunks(const Task& t) {
+  uint64_t vecs = 0;
+  if (t.kind == TASK_COPY16) vecs = uint64_t(t.rows) * (t.cols >> 4);
+  else if (t.kind == TASK_F32_BF16 || t.kind == TASK_BF16_F32) vecs = uint64_t(t.rows) * (t.cols >> 3);
+  else return 1;
+  return static_cast<uint32_t>(vecs == 0 ? 1 : (vecs + kChunkVecs - 1) / kChunkVecs);
+}
+
 // One fp8 destination block and the wire pieces that fill it. Blocks filled by
 // a single 16-byte aligned bf16 piece (QB_SINGLE) carry its source address
 // here, so the kernel needs no piece lookups for them.
@@ -216,6 +238,7 @@ struct wb_plan_t {
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
+  uint32_t task_shift = 0;              // log2 of the copy kernel's workgroups per work item
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
@@ -245,7 +268,9 @@ std::string dump_plan(const wb_plan_t& P);
 // ptrs[1 + u] is local tensor u; work items with index 0 use buf, with index
 // kAuxBuffer aux (the second buffer of a forward launch).
 constexpr uint16_t kAuxBuffer = 0xFFFF;
-int launch_tasks(const Task* tasks, uint32_t n, const uint64_t* ptrs, const void* buf, const void* aux, void* stream);
+void task_grid(uint32_t n, uint32_t shift, uint32_t* gx, uint32_t* gy);
+int launch_tasks(const Task* tasks, uint32_t n, uint32_t shift, const uint64_t* ptrs, const void* buf,
+                 const void* aux, void* stream);
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream);
 const char* hip_error_string(int err);
