@@ -321,6 +321,56 @@ __device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
 
 constexpr int kLdsPieces = 32;
 
+// q = E4M3FN(RN(x / s)) of this thread's 8 x 8 elements, stored as 8-byte
+// rows (or bytes at a ragged right edge).
+//
+// kFast: RN(x / s) without a per-element division. With s = m * 2^E (m in
+// [1, 2)) take x' = x * 2^-E, r' = RN(1 / m), q0 = RN(x' r'), e = x' - q0 m
+// (exact, by FMA) and q = RN(q0 + e r'). For |q| >= 2^-10, the smallest
+// magnitude that does not round to zero in E4M3, all of this stays in the
+// normal range; the sign is copied from x because x' can underflow to a zero
+// whose sign the correction loses. Since |x| <= amax, |q| <= 448.00003 rounds
+// to at most 448 in E4M3, so no clamp is needed (the exhaustive bf16 check
+// covers it). Otherwise: IEEE division, clamped to +-448 (a no-op that keeps
+// the conversion away from its overflow path whatever the source).
+template <bool kFast>
+__device__ __forceinline__ void quantise_store(const float (&v)[8][8], const QBlock& b, int rows, int cols, int rb,
+                                               int cg, float s, uint8_t* q8) {
+  const uint32_t sbits = __float_as_uint(s);
+  const float pw = __uint_as_float(uint32_t(254 - int((sbits >> 23) & 0xFF)) << 23);  // 2^-E
+  const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);             // m
+  const float rp = 1.0f / sp;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int r = rb + 16 * k;
+    if (r >= rows || cg >= cols) continue;
+    float q[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      if (kFast) {
+        const float xp = v[k][m] * pw;
+        const float q0 = xp * rp;
+        const float e = fmaf(-q0, sp, xp);
+        q[m] = __builtin_copysignf(fmaf(e, rp, q0), v[k][m]);
+      } else {
+        q[m] = __builtin_amdgcn_fmed3f(v[k][m] / s, -448.0f, 448.0f);
+      }
+    }
+    uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
+    uint32_t hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
+    uint8_t* dst = q8 + uint64_t(r) * b.dst_ld + cg;
+    if ((b.flags & QB_VEC_STORE) && cg + 8 <= cols) {
+      st(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
+    } else {
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+        if (cg + m < cols) dst[m] = static_cast<uint8_t>((m < 4 ? lo : hi) >> (8 * (m & 3)));
+    }
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
@@ -397,53 +447,15 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   amax = fmaxf(fmaxf(wave_max[0], wave_max[1]), fmaxf(wave_max[2], wave_max[3]));
 
   const float s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
-  // RN(x / s): with s = m * 2^E (m in [1, 2)) take x' = x * 2^-E and s' = m,
-  // r' = RN(1 / s'), q0 = RN(x' r'), e = x' - q0 s' (exact, by FMA),
-  // q = RN(q0 + e r'). For |q| >= 2^-10, the smallest magnitude that does not
-  // round to zero in E4M3, all of this stays in the normal range. A block
-  // whose scale is subnormal uses IEEE division per element.
-  const uint32_t sbits = __float_as_uint(s);
-  const int sexp = int((sbits >> 23) & 0xFF);
   // the fast path is verified exhaustively for every bf16 (x, amax) pair; fp32
-  // sources take IEEE division
-  const bool fast = sexp != 0 && (b.flags & QB_BF16_SOURCE);
-  const float pw = __uint_as_float(uint32_t(254 - sexp) << 23);  // 2^-(sexp - 127)
-  const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);
-  const float rp = 1.0f / sp;
+  // sources and blocks with a subnormal scale take IEEE division. The branch is
+  // uniform over the workgroup and taken once, outside the element loops.
+  const int sexp = int((__float_as_uint(s) >> 23) & 0xFF);
   uint8_t* q8 = reinterpret_cast<uint8_t*>(ptrs[b.dst_idx]) + b.dst_off;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int r = rb + 16 * k;
-    if (r >= rows || cg >= cols) continue;
-    float q[8];
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      float qq;
-      if (fast) {
-        const float xp = v[k][m] * pw;
-        const float q0 = xp * rp;
-        const float e = fmaf(-q0, sp, xp);
-        // x' can underflow to a zero whose sign the correction loses; x / s
-        // always carries the sign of x
-        qq = __builtin_copysignf(fmaf(e, rp, q0), v[k][m]);
-      } else {
-        qq = v[k][m] / s;
-      }
-      q[m] = __builtin_amdgcn_fmed3f(qq, -448.0f, 448.0f);
-    }
-    uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
-    lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
-    uint32_t hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
-    hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
-    uint8_t* dst = q8 + uint64_t(r) * b.dst_ld + cg;
-    if ((b.flags & QB_VEC_STORE) && cg + 8 <= cols) {
-      st(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
-    } else {
-#pragma unroll
-      for (int m = 0; m < 8; ++m)
-        if (cg + m < cols) dst[m] = static_cast<uint8_t>((m < 4 ? lo : hi) >> (8 * (m & 3)));
-    }
-  }
+  if (sexp != 0 && (b.flags & QB_BF16_SOURCE))
+    quantise_store<true>(v, b, rows, cols, rb, cg, s, q8);
+  else
+    quantise_store<false>(v, b, rows, cols, rb, cg, s, q8);
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
