@@ -172,10 +172,13 @@ def _launch_grids(w):
     ro = wb.Layout.describe(w["model"], w["rollout"])
     rp = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"])
     sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
-    # rocprofv3 reports Grid_Size(_X) in threads: x workgroups of 256
-    return {"pack": (sp.launch_grid(0)[0] * 256, "wb_tasks_kernel", sp.traffic()),
-            "unpack": (rp.launch_grid(0)[0] * 256, "wb_tasks_kernel", rp.kernel_traffic(0)),
-            "unpack_fp8": (rp.launch_grid(1)[0] * 256, "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
+    def threads_x(plan, launch):  # rocprofv3 reports Grid_Size(_X) in threads
+        x, _, t = plan.launch_grid(launch)
+        return x * t
+
+    return {"pack": (threads_x(sp, 0), "wb_tasks_kernel", sp.traffic()),
+            "unpack": (threads_x(rp, 0), "wb_tasks_kernel", rp.kernel_traffic(0)),
+            "unpack_fp8": (threads_x(rp, 1), "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
 
 
 def summarize_counters(workload, fetch_csv, write_csv):

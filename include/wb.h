@@ -245,14 +245,16 @@ int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* w
 int wb_plan_kernel_traffic(const wb_plan_t* plan, int32_t launch, int64_t* read_bytes, int64_t* write_bytes);
 /* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
 int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
-/* Grid (workgroups in x and y; 256 threads each) of one launch of one round:
- * launch 0 the copy/cast kernel of wb_pack_round / wb_unpack_round, 1 the fp8
- * block kernel, 2 and 3 the forward packings of exchange stages 1 and 2. A
- * copy/cast work item takes several workgroups (one per chunk of its vectors),
- * so the copy grid is a multiple of the work-item count. Both are 0 for a
- * launch that enqueues nothing. WB_EINVAL for a null argument, a launch
- * outside 0..3 or a round out of range. */
-int wb_plan_launch_grid(const wb_plan_t* plan, int32_t launch, int32_t round, uint32_t* grid_x, uint32_t* grid_y);
+/* Grid (workgroups in x and y) and workgroup size (threads) of one launch of
+ * one round: launch 0 the copy/cast kernel of wb_pack_round / wb_unpack_round,
+ * 1 the fp8 block kernel, 2 and 3 the forward packings of exchange stages 1
+ * and 2. A copy/cast work item takes several workgroups (one per chunk of its
+ * vectors), so the copy grid is a multiple of the work-item count; the fp8
+ * grid has one workgroup per block. The grid is 0 x 0 for a launch that
+ * enqueues nothing. WB_EINVAL for a null argument, a launch outside 0..3 or a
+ * round out of range. */
+int wb_plan_launch_grid(const wb_plan_t* plan, int32_t launch, int32_t round, uint32_t* grid_x, uint32_t* grid_y,
+                        uint32_t* threads);
 /* Canonical text form of the global plan (one line per segment). */
 int wb_plan_dump(const wb_plan_t* plan, char* buf, size_t cap, size_t* needed);
 

@@ -109,7 +109,7 @@ def _load():
         "wb_plan_workspace_bytes": [P, POINTER(c_int64)],
         "wb_plan_traffic_bytes": [P, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_work_counts": [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
-        "wb_plan_launch_grid": [P, c_int32, c_int32, POINTER(c_uint32), POINTER(c_uint32)],
+        "wb_plan_launch_grid": [P, c_int32, c_int32, POINTER(c_uint32), POINTER(c_uint32), POINTER(c_uint32)],
         "wb_plan_kernel_traffic": [P, c_int32, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_dump": [P, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
         "wb_plan_upload": [P, c_void_p, c_size_t, c_void_p],
@@ -430,11 +430,12 @@ class Plan:
         return a.value, b.value, c.value
 
     def launch_grid(self, launch=0, round=0):
-        """(workgroups in x, in y) of one launch of one round: 0 copy/cast,
-        1 fp8 blocks, 2 and 3 the forward packings of exchange stages 1 and 2."""
-        x, y = c_uint32(), c_uint32()
-        _check(lib.wb_plan_launch_grid(self._h, launch, round, byref(x), byref(y)))
-        return x.value, y.value
+        """(workgroups in x, in y, threads per workgroup) of one launch of one
+        round: 0 copy/cast, 1 fp8 blocks, 2 and 3 the forward packings of
+        exchange stages 1 and 2."""
+        x, y, t = c_uint32(), c_uint32(), c_uint32()
+        _check(lib.wb_plan_launch_grid(self._h, launch, round, byref(x), byref(y), byref(t)))
+        return x.value, y.value, t.value
 
     def dump(self) -> str:
         return _text(lib.wb_plan_dump, self._h)

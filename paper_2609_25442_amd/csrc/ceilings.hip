@@ -1,8 +1,9 @@
 // Practical HBM ceilings of this GPU for 16-byte vector streams: read-only,
-// write-only and copy (each workgroup copying one contiguous 256 KiB chunk, as
-// the packing and assembly work items do), over 8 GiB buffers, best of five.
-// Prints one JSON object. Used to put the resharding kernels' bandwidth next
-// to what a plain stream reaches on the same part.
+// write-only, copy with one contiguous 256 KiB chunk per workgroup looping over
+// it, copy with one-shot 4 KiB workgroups (one load and one store per lane, the
+// packing and assembly kernels' pattern), and hipMemcpy, over 8 GiB buffers,
+// best of five. Prints one JSON object. Used to put the resharding kernels'
+// bandwidth next to what a plain stream reaches on the same part.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -54,6 +55,11 @@ __global__ void copy_chunks(const u32x4* __restrict__ s, u32x4* __restrict__ d, 
   for (; i < b; i += blockDim.x) d[i] = s[i];
 }
 
+__global__ void copy_oneshot(const u32x4* __restrict__ s, u32x4* __restrict__ d) {
+  const uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+}
+
 int main() {
   const uint64_t bytes = 8ull << 30, n = bytes / 16;
   const int read_grid = 512, write_grid = 16384, threads = 256;
@@ -67,8 +73,8 @@ int main() {
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
-  double gbs[4];
-  for (int which = 0; which < 4; ++which) {
+  double gbs[5];
+  for (int which = 0; which < 5; ++which) {
     float best = 1e30f;
     for (int r = 0; r < 6; ++r) {
       CHECK(hipEventRecord(e0));
@@ -76,6 +82,7 @@ int main() {
       if (which == 1) write_stream<<<write_grid, threads>>>(d, n);
       if (which == 2) copy_chunks<<<int((n + per - 1) / per), threads>>>(s, d, n, per);
       if (which == 3) CHECK(hipMemcpyAsync(d, s, bytes, hipMemcpyDeviceToDevice, 0));
+      if (which == 4) copy_oneshot<<<int(n / threads), threads>>>(s, d);
       CHECK(hipEventRecord(e1));
       CHECK(hipEventSynchronize(e1));
       float ms;
@@ -85,7 +92,8 @@ int main() {
     gbs[which] = (which >= 2 ? 2.0 : 1.0) * double(bytes) / (best * 1e-3) / 1e9;
   }
   std::printf("{\"read_GBps\": %.1f, \"write_GBps\": %.1f, \"copy_GBps\": %.1f, \"hipMemcpy_GBps\": %.1f, "
-              "\"bytes\": %llu}\n", gbs[0], gbs[1], gbs[2], gbs[3], (unsigned long long)bytes);
+              "\"copy_oneshot_GBps\": %.1f, \"bytes\": %llu}\n", gbs[0], gbs[1], gbs[2], gbs[3], gbs[4],
+              (unsigned long long)bytes);
   CHECK(hipFree(s));
   CHECK(hipFree(d));
   CHECK(hipFree(out));

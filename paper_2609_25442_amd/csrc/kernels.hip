@@ -270,15 +270,18 @@ __device__ __forceinline__ const char* base_of(uint16_t idx, const uint64_t* ptr
   return idx == 0 ? buf : idx == kAuxBuffer ? aux : reinterpret_cast<const char*>(ptrs[idx]);
 }
 
-// Workgroup b takes chunk b mod 2^shift of work item b >> shift; a grid wider
-// than kMaxGridX workgroups is folded into rows of gridDim.x.
+// Workgroup b < nchunked * 2^shift takes chunk b mod 2^shift of work item
+// b >> shift; the following workgroups take one single-workgroup item each. A
+// grid wider than kMaxGridX workgroups is folded into rows of gridDim.x.
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
                                                             const uint64_t* __restrict__ ptrs, const char* buf,
-                                                            const char* aux, uint32_t ntasks, uint32_t shift) {
+                                                            const char* aux, uint32_t ntasks, uint32_t nchunked,
+                                                            uint32_t shift) {
   const uint64_t b = uint64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-  const uint64_t ti = b >> shift;
+  const uint64_t cw = uint64_t(nchunked) << shift;
+  const uint64_t ti = b < cw ? b >> shift : nchunked + (b - cw);
   if (ti >= ntasks) return;
-  const uint32_t chunk = uint32_t(b) & ((1u << shift) - 1u);
+  const uint32_t chunk = b < cw ? uint32_t(b) & ((1u << shift) - 1u) : 0u;
   const Task t = tasks[ti];
   const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
   char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
@@ -321,8 +324,8 @@ __device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
 
 constexpr int kLdsPieces = 32;
 
-// q = E4M3FN(RN(x / s)) of this thread's 8 x 8 elements, stored as 8-byte
-// rows (or bytes at a ragged right edge).
+// q = E4M3FN(RN(x / s)) of this thread's R x 8 elements (rows rb + k * 128 / R),
+// stored as 8-byte rows (or bytes at a ragged right edge).
 //
 // kFast: RN(x / s) without a per-element division. With s = m * 2^E (m in
 // [1, 2)) take x' = x * 2^-E, r' = RN(1 / m), q0 = RN(x' r'), e = x' - q0 m
@@ -333,16 +336,16 @@ constexpr int kLdsPieces = 32;
 // to at most 448 in E4M3, so no clamp is needed (the exhaustive bf16 check
 // covers it). Otherwise: IEEE division, clamped to +-448 (a no-op that keeps
 // the conversion away from its overflow path whatever the source).
-template <bool kFast>
-__device__ __forceinline__ void quantise_store(const float (&v)[8][8], const QBlock& b, int rows, int cols, int rb,
+template <bool kFast, int R>
+__device__ __forceinline__ void quantise_store(const float (&v)[R][8], const QBlock& b, int rows, int cols, int rb,
                                                int cg, float s, uint8_t* q8) {
   const uint32_t sbits = __float_as_uint(s);
   const float pw = __uint_as_float(uint32_t(254 - int((sbits >> 23) & 0xFF)) << 23);  // 2^-E
   const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);             // m
   const float rp = 1.0f / sp;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int r = rb + 16 * k;
+  for (int k = 0; k < R; ++k) {
+    const int r = rb + (128 / R) * k;
     if (r >= rows || cg >= cols) continue;
     float q[8];
 #pragma unroll
@@ -373,42 +376,46 @@ __device__ __forceinline__ void quantise_store(const float (&v)[8][8], const QBl
 
 }  // namespace
 
-__global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
-                                                             const QPiece* __restrict__ pieces,
-                                                             const uint64_t* __restrict__ ptrs, const char* recv) {
-  __shared__ float wave_max[kThreads / 64];
+// One block per workgroup of 16 * 128 / R threads: thread t holds columns
+// 8 (t mod 16) .. + 7 of rows t / 16 + k * 128 / R, k < R.
+template <int R>
+__global__ __launch_bounds__(16 * 128 / R) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
+                                                                 const QPiece* __restrict__ pieces,
+                                                                 const uint64_t* __restrict__ ptrs, const char* recv) {
+  constexpr int T = 16 * 128 / R;
+  __shared__ float wave_max[T / 64];
   __shared__ QPiece lds_pcs[kLdsPieces];
   const QBlock b = blocks[blockIdx.x];
   const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
   const int cg = (threadIdx.x & 15) * 8;  // first of this thread's 8 columns
-  const int rb = threadIdx.x >> 4;        // rows rb, rb + 16, ..., rb + 112
-  float v[8][8];
+  const int rb = threadIdx.x >> 4;        // rows rb, rb + 128 / R, ...
+  float v[R][8];
   if (b.flags & QB_SINGLE) {
-    // one aligned bf16 piece covers the block: eight independent 16-byte loads
+    // one aligned bf16 piece covers the block: R independent 16-byte loads
     const char* base = recv + b.src_off + uint64_t(cg) * 2;
-    u32x4 raw[8];
+    u32x4 raw[R];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int r = rb + 16 * k;
+    for (int k = 0; k < R; ++k) {
+      const int r = rb + (128 / R) * k;
       raw[k] = u32x4{0u, 0u, 0u, 0u};
       if (r < rows && cg < cols) raw[k] = ld(reinterpret_cast<const u32x4*>(base + uint64_t(r) * b.src_ld * 2));
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) unpack8(raw[k], v[k]);
+    for (int k = 0; k < R; ++k) unpack8(raw[k], v[k]);
   } else {
     // several pieces (or an unaligned / fp32 one): stage the piece list in LDS,
     // resolve each row chunk's source first, then issue the loads
     const int n = b.npieces;
     const QPiece* pcs = pieces + b.piece0;
     if (n <= kLdsPieces) {
-      for (int i = threadIdx.x; i < n; i += kThreads) lds_pcs[i] = pcs[i];
+      for (int i = threadIdx.x; i < n; i += T) lds_pcs[i] = pcs[i];
       __syncthreads();
       pcs = lds_pcs;
     }
-    const char* src[8];
+    const char* src[R];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int r = rb + 16 * k;
+    for (int k = 0; k < R; ++k) {
+      const int r = rb + (128 / R) * k;
       src[k] = nullptr;
       if (r >= rows || cg >= cols) continue;
       for (int i = 0; i < n; ++i) {
@@ -420,16 +427,16 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
         }
       }
     }
-    u32x4 raw[8];
+    u32x4 raw[R];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < R; ++k) {
       raw[k] = u32x4{0u, 0u, 0u, 0u};
       if (src[k]) raw[k] = ld(reinterpret_cast<const u32x4*>(src[k]));
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < R; ++k) {
       unpack8(raw[k], v[k]);
-      const int r = rb + 16 * k;
+      const int r = rb + (128 / R) * k;
       if (!src[k] && r < rows && cg < cols) {
 #pragma unroll
         for (int m = 0; m < 8; ++m) v[k][m] = cg + m < cols ? gather_one(pcs, n, recv, r, cg + m) : 0.0f;
@@ -438,13 +445,15 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   }
   float amax = 0.0f;
 #pragma unroll
-  for (int k = 0; k < 8; ++k)
+  for (int k = 0; k < R; ++k)
 #pragma unroll
     for (int m = 0; m < 8; ++m) amax = fmaxf(amax, fabsf(v[k][m]));
   for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
   if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = amax;
   __syncthreads();
-  amax = fmaxf(fmaxf(wave_max[0], wave_max[1]), fmaxf(wave_max[2], wave_max[3]));
+  amax = wave_max[0];
+#pragma unroll
+  for (int w = 1; w < T / 64; ++w) amax = fmaxf(amax, wave_max[w]);
 
   const float s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
   // the fast path is verified exhaustively for every bf16 (x, amax) pair; fp32
@@ -453,14 +462,14 @@ __global__ __launch_bounds__(kThreads) void wb_qblock_kernel(const QBlock* __res
   const int sexp = int((__float_as_uint(s) >> 23) & 0xFF);
   uint8_t* q8 = reinterpret_cast<uint8_t*>(ptrs[b.dst_idx]) + b.dst_off;
   if (sexp != 0 && (b.flags & QB_BF16_SOURCE))
-    quantise_store<true>(v, b, rows, cols, rb, cg, s, q8);
+    quantise_store<true, R>(v, b, rows, cols, rb, cg, s, q8);
   else
-    quantise_store<false>(v, b, rows, cols, rb, cg, s, q8);
+    quantise_store<false, R>(v, b, rows, cols, rb, cg, s, q8);
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
-void task_grid(uint32_t n, uint32_t shift, uint32_t* gx, uint32_t* gy) {
-  const uint64_t total = uint64_t(n) << shift;
+void task_grid(uint32_t n, uint32_t nchunked, uint32_t shift, uint32_t* gx, uint32_t* gy) {
+  const uint64_t total = (uint64_t(nchunked) << shift) + (n - nchunked);
   if (total <= kMaxGridX) {
     *gx = static_cast<uint32_t>(total);
     *gy = 1;
@@ -470,21 +479,21 @@ void task_grid(uint32_t n, uint32_t shift, uint32_t* gx, uint32_t* gy) {
   }
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, uint32_t shift, const uint64_t* ptrs, const void* buf,
-                 const void* aux, void* stream) {
+int launch_tasks(const Task* tasks, uint32_t n, uint32_t nchunked, uint32_t shift, const uint64_t* ptrs,
+                 const void* buf, const void* aux, void* stream) {
   if (n == 0) return hipSuccess;
   uint32_t gx, gy;
-  task_grid(n, shift, &gx, &gy);
+  task_grid(n, nchunked, shift, &gx, &gy);
   hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS, static_cast<hipStream_t>(stream),
-                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, shift);
+                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, nchunked, shift);
   return hipGetLastError();
 }
 
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_qblock_kernel, dim3(n), dim3(kThreads), WB_QBLOCK_DYN_LDS, static_cast<hipStream_t>(stream), blocks, pieces,
-                     ptrs, static_cast<const char*>(buf));
+  hipLaunchKernelGGL(wb_qblock_kernel<kQBlockRows>, dim3(n), dim3(kQBlockThreads), WB_QBLOCK_DYN_LDS,
+                     static_cast<hipStream_t>(stream), blocks, pieces, ptrs, static_cast<const char*>(buf));
   return hipGetLastError();
 }
 

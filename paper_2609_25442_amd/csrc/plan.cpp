@@ -503,6 +503,13 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   const RoundWire& W = P.rounds[k];
   size[0] = P.role == WB_SENDER ? W.st[0].send_bytes[P.rank] : W.recv_total[P.rank];
   aux_size = 0;
+  auto check_order = [&](uint32_t a, uint32_t b, uint32_t nchunked) {
+    if (nchunked > b - a) fail(WB_EINVAL, "internal: chunked work item count");
+    for (uint32_t ti = a; ti < b; ++ti)
+      if (task_chunked(P.tasks[ti]) != (ti < a + nchunked)) fail(WB_EINVAL, "internal: work item order");
+  };
+  check_order(P.round_tasks[k], P.round_tasks[k + 1], P.round_chunked[k]);
+  for (int st = 0; st < 2; ++st) check_order(P.round_fwd[st][k], P.round_fwd[st][k + 1], P.fwd_chunked[st][k]);
   for (uint32_t ti = P.round_tasks[k]; ti < P.round_tasks[k + 1]; ++ti) {
     if (P.tasks[ti].src_idx == kAuxBuffer || P.tasks[ti].dst_idx == kAuxBuffer)
       fail(WB_EINVAL, "internal: pack or unpack work item on the forward buffer");
@@ -921,7 +928,19 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   P.role = role;
   P.rank = rank;
   build_rank_view(trainer, rollout, P);
-  uint32_t most = 1;  // workgroups of the copy kernel per work item
+  // each launch range: chunked items first (in planner order), then the rest
+  auto partition = [&](uint32_t a, uint32_t b) {
+    const auto mid = std::stable_partition(P.tasks.begin() + a, P.tasks.begin() + b, task_chunked);
+    return static_cast<uint32_t>(mid - (P.tasks.begin() + a));
+  };
+  const size_t nr = P.rounds.size();
+  P.round_chunked.assign(nr, 0);
+  for (auto& f : P.fwd_chunked) f.assign(nr, 0);
+  for (size_t k = 0; k < nr; ++k) {
+    P.round_chunked[k] = partition(P.round_tasks[k], P.round_tasks[k + 1]);
+    for (int st = 0; st < 2; ++st) P.fwd_chunked[st][k] = partition(P.round_fwd[st][k], P.round_fwd[st][k + 1]);
+  }
+  uint32_t most = 1;  // workgroups of the copy kernel per chunked work item
   for (const Task& t : P.tasks) most = std::max(most, task_chunks(t));
   P.task_shift = 0;
   while ((1u << P.task_shift) < most) ++P.task_shift;

@@ -136,11 +136,11 @@ struct Task {
 };
 static_assert(sizeof(Task) == 48, "Task layout");
 
-// The copy kernel runs 2^shift workgroups of kChunkThreads threads per work
-// item; a vector-kind item is cut into chunks of kChunkVecs 16-byte vectors
-// (kChunkPerLane per lane), one per workgroup, the other kinds run in the
-// item's first workgroup. Grids wider than kMaxGridX workgroups fold into a
-// second dimension.
+// Copy kernel launch: the vector kinds (chunked items) come first in each
+// launch's range of work items and take 2^shift workgroups of kChunkThreads
+// threads each, one per chunk of kChunkVecs 16-byte vectors (kChunkPerLane per
+// lane); the other kinds follow with one workgroup each. Grids wider than
+// kMaxGridX workgroups fold into a second dimension.
 #ifndef WB_CHUNK_PER_LANE
 #define WB_CHUNK_PER_LANE 1
 #endif
@@ -148,6 +148,10 @@ constexpr int kChunkThreads = 256;
 constexpr int kChunkPerLane = WB_CHUNK_PER_LANE;
 constexpr uint32_t kChunkVecs = uint32_t(kChunkThreads) * kChunkPerLane;
 constexpr uint32_t kMaxGridX = 1u << 22;
+
+inline bool task_chunked(const Task& t) {
+  return t.kind == TASK_COPY16 || t.kind == TASK_F32_BF16 || t.kind == TASK_BF16_F32;
+}
 
 // Workgroups a work item needs (host side of the rule above).
 inline uint32_t task_chunks(const Task& t) {
@@ -186,6 +190,15 @@ struct QPiece {
 static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
 enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
+
+// The fp8 block kernel runs one block per workgroup; each thread holds
+// kQBlockRows rows of 8 columns.
+#ifndef WB_QBLOCK_ROWS
+#define WB_QBLOCK_ROWS 8
+#endif
+constexpr int kQBlockRows = WB_QBLOCK_ROWS;
+constexpr int kQBlockThreads = 16 * 128 / kQBlockRows;
+static_assert(kQBlockRows == 2 || kQBlockRows == 4 || kQBlockRows == 8, "rows per thread");
 
 // A field of a batched diff2 launch: rows x cols values, value at (i, j) the
 // sum over k < passes of src[k][i * cols + j] << (16 k); its element 0 is
@@ -238,7 +251,9 @@ struct wb_plan_t {
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
-  uint32_t task_shift = 0;              // log2 of the copy kernel's workgroups per work item
+  uint32_t task_shift = 0;              // log2 of the copy kernel's workgroups per chunked work item
+  std::vector<uint32_t> round_chunked;  // [k]: chunked items at the start of round k's pack/unpack range
+  std::vector<uint32_t> fwd_chunked[2]; // the same for the forward range of stage 1 + i, round k
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
@@ -268,9 +283,10 @@ std::string dump_plan(const wb_plan_t& P);
 // ptrs[1 + u] is local tensor u; work items with index 0 use buf, with index
 // kAuxBuffer aux (the second buffer of a forward launch).
 constexpr uint16_t kAuxBuffer = 0xFFFF;
-void task_grid(uint32_t n, uint32_t shift, uint32_t* gx, uint32_t* gy);
-int launch_tasks(const Task* tasks, uint32_t n, uint32_t shift, const uint64_t* ptrs, const void* buf,
-                 const void* aux, void* stream);
+// n work items, the first nchunked of them chunked
+void task_grid(uint32_t n, uint32_t nchunked, uint32_t shift, uint32_t* gx, uint32_t* gy);
+int launch_tasks(const Task* tasks, uint32_t n, uint32_t nchunked, uint32_t shift, const uint64_t* ptrs,
+                 const void* buf, const void* aux, void* stream);
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream);
 const char* hip_error_string(int err);
