@@ -325,23 +325,28 @@ __device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
 constexpr int kLdsPieces = 32;
 
 // q = E4M3FN(RN(x / s)) of this thread's R x 8 elements (rows rb + k * 128 / R),
-// stored as 8-byte rows (or bytes at a ragged right edge).
+// stored as 8-byte rows (or bytes at a ragged right edge). Three ways to get
+// RN(x / s), chosen once per block:
 //
-// kFast: RN(x / s) without a per-element division. With s = m * 2^E (m in
-// [1, 2)) take x' = x * 2^-E, r' = RN(1 / m), q0 = RN(x' r'), e = x' - q0 m
-// (exact, by FMA) and q = RN(q0 + e r'). For |q| >= 2^-10, the smallest
-// magnitude that does not round to zero in E4M3, all of this stays in the
-// normal range; the sign is copied from x because x' can underflow to a zero
-// whose sign the correction loses. Since |x| <= amax, |q| <= 448.00003 rounds
-// to at most 448 in E4M3, so no clamp is needed (the exhaustive bf16 check
-// covers it). Otherwise: IEEE division, clamped to +-448 (a no-op that keeps
-// the conversion away from its overflow path whatever the source).
-template <bool kFast, int R>
+// kMode 2 (s = m 2^E with -90 <= E <= 100): r = RN(1 / s), q0 = RN(x r),
+//   e = x - q0 s (exact, by FMA), q = RN(q0 + e r). A quotient that can round
+//   to a non-zero E4M3 value has |x / s| >= 2^-10, so q0 >= 2^-10, e is at
+//   least 2^(E - 33) in magnitude and every intermediate is a normal number;
+//   r stays normal for E <= 100.
+// kMode 1 (any normal s): the same on x' = x 2^-E and m, which keeps the
+//   intermediates normal whatever E.
+// In both the sign is copied from x: a quotient that rounds to zero can lose
+//   it in the correction. Since |x| <= amax, |q| <= 448.00003 rounds to at most
+//   448 in E4M3, so no clamp is needed. Both are verified exhaustively for
+//   every bf16 (x, amax) pair.
+// kMode 0 (fp32 sources, subnormal s): IEEE division, clamped to +-448 (a no-op
+//   that keeps the conversion away from its overflow path whatever the source).
+template <int kMode, int R>
 __device__ __forceinline__ void quantise_store(const float (&v)[R][8], const QBlock& b, int rows, int cols, int rb,
                                                int cg, float s, uint8_t* q8) {
   const uint32_t sbits = __float_as_uint(s);
   const float pw = __uint_as_float(uint32_t(254 - int((sbits >> 23) & 0xFF)) << 23);  // 2^-E
-  const float sp = __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u);             // m
+  const float sp = kMode == 1 ? __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u) : s;  // m, or s
   const float rp = 1.0f / sp;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
@@ -350,8 +355,8 @@ __device__ __forceinline__ void quantise_store(const float (&v)[R][8], const QBl
     float q[8];
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
-      if (kFast) {
-        const float xp = v[k][m] * pw;
+      if (kMode != 0) {
+        const float xp = kMode == 1 ? v[k][m] * pw : v[k][m];
         const float q0 = xp * rp;
         const float e = fmaf(-q0, sp, xp);
         q[m] = __builtin_copysignf(fmaf(e, rp, q0), v[k][m]);
@@ -456,15 +461,16 @@ __global__ __launch_bounds__(16 * 128 / R) void wb_qblock_kernel(const QBlock* _
   for (int w = 1; w < T / 64; ++w) amax = fmaxf(amax, wave_max[w]);
 
   const float s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
-  // the fast path is verified exhaustively for every bf16 (x, amax) pair; fp32
-  // sources and blocks with a subnormal scale take IEEE division. The branch is
-  // uniform over the workgroup and taken once, outside the element loops.
-  const int sexp = int((__float_as_uint(s) >> 23) & 0xFF);
+  // the branch is uniform over the workgroup and taken once, outside the
+  // element loops
+  const int sexp = int((__float_as_uint(s) >> 23) & 0xFF);  // E + 127
   uint8_t* q8 = reinterpret_cast<uint8_t*>(ptrs[b.dst_idx]) + b.dst_off;
-  if (sexp != 0 && (b.flags & QB_BF16_SOURCE))
-    quantise_store<true, R>(v, b, rows, cols, rb, cg, s, q8);
+  if (!(b.flags & QB_BF16_SOURCE) || sexp == 0)
+    quantise_store<0, R>(v, b, rows, cols, rb, cg, s, q8);
+  else if (sexp >= 127 - 90 && sexp <= 127 + 100)
+    quantise_store<2, R>(v, b, rows, cols, rb, cg, s, q8);
   else
-    quantise_store<false, R>(v, b, rows, cols, rb, cg, s, q8);
+    quantise_store<1, R>(v, b, rows, cols, rb, cg, s, q8);
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
