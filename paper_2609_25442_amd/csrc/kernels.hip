@@ -2,17 +2,18 @@
 // a packing kernel coalesces a round's tensors into per-receiver buffers in
 // checkpoint format; an assembly kernel scatters them into the inference
 // tensors). Both are batched across tensors: one launch walks a flat table of
-// work items, one 256-thread workgroup per item.
+// work items, each spread over one or more workgroups.
 //
 //  * wb_tasks_kernel  -- copy/cast work items: 16-byte vectorised row copies,
 //    fp32 -> bf16 (v_cvt_pk_bf16_f32, round to nearest even), bf16 -> fp32,
 //    an element-wise fallback for unaligned or odd cases, and 64 x 64 tiles
-//    transposed through LDS where a trainer stores a shard transposed. The
-//    vector kinds are spread over several workgroups per item: each takes one
-//    chunk of kChunkVecs vectors, issues all of its loads, then all of its
-//    stores, and exits (no loop, so no wait on the completion of earlier
-//    stores before the next loads, which caps a looping copy well below the
-//    rate of these one-shot workgroups on gfx950).
+//    transposed through LDS where a trainer stores a shard transposed. Work
+//    items are spread over several one-wave workgroups: a vector kind takes
+//    one per chunk of kChunkVecs vectors, each issuing all of its loads, then
+//    all of its stores, and exiting (no loop, so no wait on the completion of
+//    earlier stores before the next loads, which caps a looping copy well
+//    below the rate of these one-shot workgroups on gfx950); a transpose
+//    takes one per 64 x 64 (registers) or 32 x 32 (LDS) tile.
 //  * wb_qblock_kernel -- one fp8 E4M3FN block (<= 128 x 128) per workgroup,
 //    gathered from its wire pieces into registers: amax by wavefront
 //    shuffles plus LDS across the four waves, s = amax / 448 (IEEE division),
@@ -223,28 +224,34 @@ __device__ void run_scalar(const Task& t, const char* src, char* dst) {
   }
 }
 
-// dst[c][r] = cvt(src[r][c]) for one tile of up to 64 x 64, through LDS.
-__device__ void run_transpose(const Task& t, const char* src, char* dst) {
-  __shared__ uint32_t tile[64][65];
+// dst[c][r] = cvt(src[r][c]) for quarter `part` (32 x 32) of a tile of up to
+// 64 x 64, through LDS (padded rows: conflict-free column reads).
+__device__ void run_transpose(const Task& t, const char* src, char* dst, uint32_t part) {
+  __shared__ uint32_t tile[32][33];
+  const uint32_t r0 = (part >> 1) * 32, c0 = (part & 1) * 32;
+  if (r0 >= t.rows || c0 >= t.cols) return;  // uniform over the workgroup
   const int ss = dt_bytes(t.sdt), ds = dt_bytes(t.ddt);
-  const uint32_t R = t.rows, C = t.cols;
-  for (uint32_t i = threadIdx.x; i < 64 * 64; i += kThreads) {
-    const uint32_t r = i >> 6, c = i & 63;
+  const uint32_t R = min(32u, t.rows - r0), C = min(32u, t.cols - c0);
+  src += (uint64_t(r0) * t.src_ld + c0) * ss;
+  dst += (uint64_t(c0) * t.dst_ld + r0) * ds;
+  for (uint32_t i = threadIdx.x; i < 32 * 32; i += kThreads) {
+    const uint32_t r = i >> 5, c = i & 31;
     if (r < R && c < C) tile[r][c] = load_bits(src + (uint64_t(r) * t.src_ld + c) * ss, t.sdt);
   }
   __syncthreads();
-  for (uint32_t i = threadIdx.x; i < 64 * 64; i += kThreads) {
-    const uint32_t c = i >> 6, r = i & 63;
+  for (uint32_t i = threadIdx.x; i < 32 * 32; i += kThreads) {
+    const uint32_t c = i >> 5, r = i & 31;
     if (r < R && c < C) store_converted(dst + (uint64_t(c) * t.dst_ld + r) * ds, tile[r][c], t.sdt, t.ddt);
   }
 }
 
 // dst[c][r] = src[r][c] for 2-byte elements, 64 rows x (64..256) columns: each
-// wave takes one 64 x 64 tile, each lane an 8 x 8 sub-tile that it loads as
-// eight 16-byte rows, transposes in registers and stores as eight 16-byte rows.
-// Lanes 8i..8i+7 cover one 128-byte span of a row on both sides.
-__device__ void run_transpose16(const Task& t, const char* src, char* dst) {
-  const uint32_t w = threadIdx.x >> 6, l = threadIdx.x & 63;
+// wave takes one 64 x 64 tile (tile `w` of the item), each lane an 8 x 8
+// sub-tile that it loads as eight 16-byte rows, transposes in registers and
+// stores as eight 16-byte rows. Lanes 8i..8i+7 cover one 128-byte span of a
+// row on both sides.
+__device__ void run_transpose16(const Task& t, const char* src, char* dst, uint32_t w) {
+  const uint32_t l = threadIdx.x & 63;
   if (w * 64 >= t.cols) return;
   const uint32_t c0 = w * 64 + 8 * (l & 7), r0 = 8 * (l >> 3);
   u32x4 a[8];
@@ -270,18 +277,28 @@ __device__ __forceinline__ const char* base_of(uint16_t idx, const uint64_t* ptr
   return idx == 0 ? buf : idx == kAuxBuffer ? aux : reinterpret_cast<const char*>(ptrs[idx]);
 }
 
-// Workgroup b < nchunked * 2^shift takes chunk b mod 2^shift of work item
-// b >> shift; the following workgroups take one single-workgroup item each. A
-// grid wider than kMaxGridX workgroups is folded into rows of gridDim.x.
+// Workgroups are laid out class by class: item i of class 0 takes workgroups
+// [i, i + 1) * 2^s0, chunk = b mod 2^s0; then class 1 the same with s1; then
+// one workgroup per class-2 item. A grid wider than kMaxGridX workgroups is
+// folded into rows of gridDim.x.
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
                                                             const uint64_t* __restrict__ ptrs, const char* buf,
-                                                            const char* aux, uint32_t ntasks, uint32_t nchunked,
-                                                            uint32_t shift) {
-  const uint64_t b = uint64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-  const uint64_t cw = uint64_t(nchunked) << shift;
-  const uint64_t ti = b < cw ? b >> shift : nchunked + (b - cw);
+                                                            const char* aux, uint32_t ntasks, uint32_t n0,
+                                                            uint32_t n1, uint32_t s0, uint32_t s1) {
+  uint64_t b = uint64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+  const uint64_t w0 = uint64_t(n0) << s0, w1 = uint64_t(n1) << s1;
+  uint64_t ti;
+  uint32_t chunk = 0;
+  if (b < w0) {
+    ti = b >> s0;
+    chunk = uint32_t(b) & ((1u << s0) - 1u);
+  } else if ((b -= w0) < w1) {
+    ti = n0 + (b >> s1);
+    chunk = uint32_t(b) & ((1u << s1) - 1u);
+  } else {
+    ti = uint64_t(n0) + n1 + (b - w1);
+  }
   if (ti >= ntasks) return;
-  const uint32_t chunk = b < cw ? uint32_t(b) & ((1u << shift) - 1u) : 0u;
   const Task t = tasks[ti];
   const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
   char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
@@ -291,8 +308,8 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
     case TASK_F32_BF16: run_f32_bf16(t, src, dst, q0); break;
     case TASK_BF16_F32: run_bf16_f32(t, src, dst, q0); break;
     case TASK_SCALAR: if (chunk == 0) run_scalar(t, src, dst); break;
-    case TASK_TRANSPOSE: if (chunk == 0) run_transpose(t, src, dst); break;
-    case TASK_TRANSPOSE16: if (chunk == 0) run_transpose16(t, src, dst); break;
+    case TASK_TRANSPOSE: run_transpose(t, src, dst, chunk); break;
+    case TASK_TRANSPOSE16: run_transpose16(t, src, dst, chunk * (kThreads / 64) + (threadIdx.x >> 6)); break;
     default: break;
   }
 }
@@ -474,24 +491,26 @@ __global__ __launch_bounds__(16 * 128 / R) void wb_qblock_kernel(const QBlock* _
   if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
 }
 
-void task_grid(uint32_t n, uint32_t nchunked, uint32_t shift, uint32_t* gx, uint32_t* gy) {
-  const uint64_t total = (uint64_t(nchunked) << shift) + (n - nchunked);
+void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy) {
+  const uint64_t total =
+      (uint64_t(sp.n[0]) << sh.s[0]) + (uint64_t(sp.n[1]) << sh.s[1]) + (n - sp.n[0] - sp.n[1]);
   if (total <= kMaxGridX) {
     *gx = static_cast<uint32_t>(total);
     *gy = 1;
-  } else {
-    *gx = kMaxGridX;
+  } else {  // fewest rows, then the narrowest rows: fewer than gy idle workgroups
     *gy = static_cast<uint32_t>((total + kMaxGridX - 1) / kMaxGridX);
+    *gx = static_cast<uint32_t>((total + *gy - 1) / *gy);
   }
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, uint32_t nchunked, uint32_t shift, const uint64_t* ptrs,
+int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskShift& sh, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream) {
   if (n == 0) return hipSuccess;
   uint32_t gx, gy;
-  task_grid(n, nchunked, shift, &gx, &gy);
+  task_grid(n, sp, sh, &gx, &gy);
   hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS, static_cast<hipStream_t>(stream),
-                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, nchunked, shift);
+                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, sp.n[0], sp.n[1],
+                     sh.s[0], sh.s[1]);
   return hipGetLastError();
 }
 

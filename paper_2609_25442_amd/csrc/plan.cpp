@@ -463,7 +463,8 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   auto check_task = [&](const Task& t) {
     if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
     // the kernel counts a work item's vectors and chunk offsets in 32 bits
-    if (uint64_t(t.rows) * t.cols >= (uint64_t(1) << 31) || task_chunks(t) > (1u << P.task_shift))
+    const int cls = task_class(t);
+    if (uint64_t(t.rows) * t.cols >= (uint64_t(1) << 31) || (cls < 2 && task_chunks(t) > (1u << P.task_shift.s[cls])))
       fail(WB_EINVAL, "internal: work item too large for its launch");
     const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
     switch (t.kind) {
@@ -503,13 +504,15 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   const RoundWire& W = P.rounds[k];
   size[0] = P.role == WB_SENDER ? W.st[0].send_bytes[P.rank] : W.recv_total[P.rank];
   aux_size = 0;
-  auto check_order = [&](uint32_t a, uint32_t b, uint32_t nchunked) {
-    if (nchunked > b - a) fail(WB_EINVAL, "internal: chunked work item count");
-    for (uint32_t ti = a; ti < b; ++ti)
-      if (task_chunked(P.tasks[ti]) != (ti < a + nchunked)) fail(WB_EINVAL, "internal: work item order");
+  auto check_order = [&](uint32_t a, uint32_t b, const TaskSplit& sp) {
+    if (uint64_t(sp.n[0]) + sp.n[1] > b - a) fail(WB_EINVAL, "internal: work item class sizes");
+    for (uint32_t ti = a; ti < b; ++ti) {
+      const int want = ti < a + sp.n[0] ? 0 : ti < a + sp.n[0] + sp.n[1] ? 1 : 2;
+      if (task_class(P.tasks[ti]) != want) fail(WB_EINVAL, "internal: work item order");
+    }
   };
-  check_order(P.round_tasks[k], P.round_tasks[k + 1], P.round_chunked[k]);
-  for (int st = 0; st < 2; ++st) check_order(P.round_fwd[st][k], P.round_fwd[st][k + 1], P.fwd_chunked[st][k]);
+  check_order(P.round_tasks[k], P.round_tasks[k + 1], P.round_split[k]);
+  for (int st = 0; st < 2; ++st) check_order(P.round_fwd[st][k], P.round_fwd[st][k + 1], P.fwd_split[st][k]);
   for (uint32_t ti = P.round_tasks[k]; ti < P.round_tasks[k + 1]; ++ti) {
     if (P.tasks[ti].src_idx == kAuxBuffer || P.tasks[ti].dst_idx == kAuxBuffer)
       fail(WB_EINVAL, "internal: pack or unpack work item on the forward buffer");
@@ -928,22 +931,32 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   P.role = role;
   P.rank = rank;
   build_rank_view(trainer, rollout, P);
-  // each launch range: chunked items first (in planner order), then the rest
+  // each launch range ordered by work item class (planner order within a class)
   auto partition = [&](uint32_t a, uint32_t b) {
-    const auto mid = std::stable_partition(P.tasks.begin() + a, P.tasks.begin() + b, task_chunked);
-    return static_cast<uint32_t>(mid - (P.tasks.begin() + a));
+    const auto first = P.tasks.begin() + a, last = P.tasks.begin() + b;
+    const auto mid0 = std::stable_partition(first, last, [](const Task& t) { return task_class(t) == 0; });
+    const auto mid1 = std::stable_partition(mid0, last, [](const Task& t) { return task_class(t) == 1; });
+    TaskSplit sp;
+    sp.n[0] = static_cast<uint32_t>(mid0 - first);
+    sp.n[1] = static_cast<uint32_t>(mid1 - mid0);
+    return sp;
   };
   const size_t nr = P.rounds.size();
-  P.round_chunked.assign(nr, 0);
-  for (auto& f : P.fwd_chunked) f.assign(nr, 0);
+  P.round_split.assign(nr, TaskSplit{});
+  for (auto& f : P.fwd_split) f.assign(nr, TaskSplit{});
   for (size_t k = 0; k < nr; ++k) {
-    P.round_chunked[k] = partition(P.round_tasks[k], P.round_tasks[k + 1]);
-    for (int st = 0; st < 2; ++st) P.fwd_chunked[st][k] = partition(P.round_fwd[st][k], P.round_fwd[st][k + 1]);
+    P.round_split[k] = partition(P.round_tasks[k], P.round_tasks[k + 1]);
+    for (int st = 0; st < 2; ++st) P.fwd_split[st][k] = partition(P.round_fwd[st][k], P.round_fwd[st][k + 1]);
   }
-  uint32_t most = 1;  // workgroups of the copy kernel per chunked work item
-  for (const Task& t : P.tasks) most = std::max(most, task_chunks(t));
-  P.task_shift = 0;
-  while ((1u << P.task_shift) < most) ++P.task_shift;
+  uint32_t most[2] = {1, 1};  // workgroups of the copy kernel per item of classes 0 and 1
+  for (const Task& t : P.tasks) {
+    const int cls = task_class(t);
+    if (cls < 2) most[cls] = std::max(most[cls], task_chunks(t));
+  }
+  for (int c = 0; c < 2; ++c) {
+    P.task_shift.s[c] = 0;
+    while ((1u << P.task_shift.s[c]) < most[c]) ++P.task_shift.s[c];
+  }
   check_work(P, role == WB_SENDER ? trainer.ranks[rank] : rollout.ranks[rank]);
 }
 

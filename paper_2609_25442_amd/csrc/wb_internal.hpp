@@ -136,31 +136,56 @@ struct Task {
 };
 static_assert(sizeof(Task) == 48, "Task layout");
 
-// Copy kernel launch: the vector kinds (chunked items) come first in each
-// launch's range of work items and take 2^shift workgroups of kChunkThreads
-// threads each, one per chunk of kChunkVecs 16-byte vectors (kChunkPerLane per
-// lane); the other kinds follow with one workgroup each. Grids wider than
-// kMaxGridX workgroups fold into a second dimension.
+// Copy kernel launch. Each launch's range of work items is ordered by class:
+// class 0 (the vector kinds) takes 2^shift[0] workgroups of kChunkThreads
+// threads (a multiple of 64: one wave by default) per item, one per chunk of
+// kChunkVecs 16-byte vectors (kChunkPerLane per lane); class 1 (transposes)
+// takes 2^shift[1] per item, TASK_TRANSPOSE16 one per kChunkThreads / 64 tiles
+// of 64 x 64 and TASK_TRANSPOSE one per 32 x 32 quarter of its tile; class 2
+// (element-wise) one workgroup per item. Grids wider than kMaxGridX
+// workgroups fold into a second dimension.
+#ifndef WB_CHUNK_THREADS
+#define WB_CHUNK_THREADS 64
+#endif
 #ifndef WB_CHUNK_PER_LANE
 #define WB_CHUNK_PER_LANE 1
 #endif
-constexpr int kChunkThreads = 256;
+constexpr int kChunkThreads = WB_CHUNK_THREADS;
 constexpr int kChunkPerLane = WB_CHUNK_PER_LANE;
 constexpr uint32_t kChunkVecs = uint32_t(kChunkThreads) * kChunkPerLane;
 constexpr uint32_t kMaxGridX = 1u << 22;
+static_assert(kChunkThreads % 64 == 0 && kChunkThreads <= 256, "copy workgroup size");
 
-inline bool task_chunked(const Task& t) {
-  return t.kind == TASK_COPY16 || t.kind == TASK_F32_BF16 || t.kind == TASK_BF16_F32;
+inline int task_class(const Task& t) {
+  if (t.kind == TASK_TRANSPOSE || t.kind == TASK_TRANSPOSE16) return 1;
+  return t.kind == TASK_SCALAR ? 2 : 0;
 }
 
 // Workgroups a work item needs (host side of the rule above).
 inline uint32_t task_chunks(const Task& t) {
   uint64_t vecs = 0;
-  if (t.kind == TASK_COPY16) vecs = uint64_t(t.rows) * (t.cols >> 4);
-  else if (t.kind == TASK_F32_BF16 || t.kind == TASK_BF16_F32) vecs = uint64_t(t.rows) * (t.cols >> 3);
-  else return 1;
+  switch (t.kind) {
+    case TASK_COPY16: vecs = uint64_t(t.rows) * (t.cols >> 4); break;
+    case TASK_F32_BF16:
+    case TASK_BF16_F32: vecs = uint64_t(t.rows) * (t.cols >> 3); break;
+    case TASK_TRANSPOSE16: {
+      const uint32_t per = kChunkThreads / 64, tiles = (t.cols + 63) / 64;
+      return (tiles + per - 1) / per;
+    }
+    case TASK_TRANSPOSE: return 4;
+    default: return 1;
+  }
   return static_cast<uint32_t>(vecs == 0 ? 1 : (vecs + kChunkVecs - 1) / kChunkVecs);
 }
+
+// Items of classes 0 and 1 at the start of one launch's range (class 2 follows)
+// and the plan-wide log2 workgroups per item of each class.
+struct TaskSplit {
+  uint32_t n[2] = {0, 0};
+};
+struct TaskShift {
+  uint32_t s[2] = {0, 0};
+};
 
 // One fp8 destination block and the wire pieces that fill it. Blocks filled by
 // a single 16-byte aligned bf16 piece (QB_SINGLE) carry its source address
@@ -251,9 +276,9 @@ struct wb_plan_t {
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
-  uint32_t task_shift = 0;              // log2 of the copy kernel's workgroups per chunked work item
-  std::vector<uint32_t> round_chunked;  // [k]: chunked items at the start of round k's pack/unpack range
-  std::vector<uint32_t> fwd_chunked[2]; // the same for the forward range of stage 1 + i, round k
+  wb::TaskShift task_shift;             // log2 of the copy kernel's workgroups per item of classes 0 and 1
+  std::vector<wb::TaskSplit> round_split;  // [k]: class sizes of round k's pack/unpack range
+  std::vector<wb::TaskSplit> fwd_split[2]; // the same for the forward range of stage 1 + i, round k
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
@@ -283,9 +308,9 @@ std::string dump_plan(const wb_plan_t& P);
 // ptrs[1 + u] is local tensor u; work items with index 0 use buf, with index
 // kAuxBuffer aux (the second buffer of a forward launch).
 constexpr uint16_t kAuxBuffer = 0xFFFF;
-// n work items, the first nchunked of them chunked
-void task_grid(uint32_t n, uint32_t nchunked, uint32_t shift, uint32_t* gx, uint32_t* gy);
-int launch_tasks(const Task* tasks, uint32_t n, uint32_t nchunked, uint32_t shift, const uint64_t* ptrs,
+// n work items ordered by class, split as in `sp`
+void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy);
+int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskShift& sh, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream);
 int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
                    void* stream);
