@@ -489,7 +489,7 @@ int wb_plan_launch_grid(const wb_plan_t* P, int32_t launch, int32_t round, uint3
   *threads = launch == 1 ? wb::kQBlockThreads : wb::kChunkThreads;
   if (launch == 1) {
     const uint32_t n = P->round_qblocks[round + 1] - P->round_qblocks[round];
-    if (n) *gx = n, *gy = 1;
+    if (n) *gx = wb::qblock_workgroups(n, P->round_qsingle[round]), *gy = 1;
     return WB_OK;
   }
   const std::vector<uint32_t>& r = launch == 0 ? P->round_tasks : P->round_fwd[launch - 2];
@@ -576,7 +576,8 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
   if (e != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(e));
   const auto* blocks = reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks);
   e = wb::launch_qblocks(blocks + P->round_qblocks[round], P->round_qblocks[round + 1] - P->round_qblocks[round],
-                         reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table, buf, stream);
+                         P->round_qsingle[round], reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table,
+                         buf, stream);
   if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
   return WB_OK;
 }

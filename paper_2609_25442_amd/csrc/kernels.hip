@@ -14,9 +14,11 @@
 //    earlier stores before the next loads, which caps a looping copy well
 //    below the rate of these one-shot workgroups on gfx950); a transpose
 //    takes one per 64 x 64 (registers) or 32 x 32 (LDS) tile.
-//  * wb_qblock_kernel -- one fp8 E4M3FN block (<= 128 x 128) per workgroup,
-//    gathered from its wire pieces into registers: amax by wavefront
-//    shuffles plus LDS across the four waves, s = amax / 448 (IEEE division),
+//  * wb_qblock_kernel -- fp8 E4M3FN blocks (<= 128 x 128): two single-piece
+//    bf16 blocks per workgroup (a row of the pair is one 512-byte load span),
+//    other blocks one per workgroup, gathered from their wire pieces; blocks
+//    held in registers, amax by wavefront shuffles plus LDS across the four
+//    waves, s = amax / 448 (IEEE division),
 //    q = RN(x / s) computed with one reciprocal per block and a remainder
 //    correction for bf16 sources (exact in the range that reaches E4M3;
 //    checked for every bf16 input pair), IEEE division otherwise, then
@@ -341,52 +343,68 @@ __device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
 
 constexpr int kLdsPieces = 32;
 
-// q = E4M3FN(RN(x / s)) of this thread's R x 8 elements (rows rb + k * 128 / R),
-// stored as 8-byte rows (or bytes at a ragged right edge). Three ways to get
-// RN(x / s), chosen once per block:
+// The block's scale s = amax / 448 (IEEE division; 1 for an all-zero block)
+// and the quantities RN(x / s) is computed from, s = m 2^E (m in [1, 2)):
 //
-// kMode 2 (s = m 2^E with -90 <= E <= 100): r = RN(1 / s), q0 = RN(x r),
+// mode 2 (bf16 source, -90 <= E <= 100): r = RN(1 / s), q0 = RN(x r),
 //   e = x - q0 s (exact, by FMA), q = RN(q0 + e r). A quotient that can round
 //   to a non-zero E4M3 value has |x / s| >= 2^-10, so q0 >= 2^-10, e is at
 //   least 2^(E - 33) in magnitude and every intermediate is a normal number;
 //   r stays normal for E <= 100.
-// kMode 1 (any normal s): the same on x' = x 2^-E and m, which keeps the
-//   intermediates normal whatever E.
+// mode 1 (bf16 source, any other normal s): the same on x' = x 2^-E and m,
+//   which keeps the intermediates normal whatever E.
 // In both the sign is copied from x: a quotient that rounds to zero can lose
 //   it in the correction. Since |x| <= amax, |q| <= 448.00003 rounds to at most
 //   448 in E4M3, so no clamp is needed. Both are verified exhaustively for
 //   every bf16 (x, amax) pair.
-// kMode 0 (fp32 sources, subnormal s): IEEE division, clamped to +-448 (a no-op
+// mode 0 (fp32 sources, subnormal s): IEEE division, clamped to +-448 (a no-op
 //   that keeps the conversion away from its overflow path whatever the source).
-template <int kMode, int R>
-__device__ __forceinline__ void quantise_store(const float (&v)[R][8], const QBlock& b, int rows, int cols, int rb,
-                                               int cg, float s, uint8_t* q8) {
-  const uint32_t sbits = __float_as_uint(s);
-  const float pw = __uint_as_float(uint32_t(254 - int((sbits >> 23) & 0xFF)) << 23);  // 2^-E
-  const float sp = kMode == 1 ? __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u) : s;  // m, or s
-  const float rp = 1.0f / sp;
+struct QScale {
+  float s, sp, rp, pw;
+  int mode;
+};
+
+__device__ __forceinline__ QScale make_scale(float amax, bool bf16_source) {
+  QScale q;
+  q.s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
+  const uint32_t sbits = __float_as_uint(q.s);
+  const int sexp = int((sbits >> 23) & 0xFF);  // E + 127
+  q.mode = (!bf16_source || sexp == 0) ? 0 : (sexp >= 127 - 90 && sexp <= 127 + 100) ? 2 : 1;
+  q.pw = __uint_as_float(uint32_t(254 - sexp) << 23);  // 2^-E
+  q.sp = q.mode == 1 ? __uint_as_float((sbits & 0x007FFFFFu) | 0x3F800000u) : q.s;  // m, or s
+  q.rp = 1.0f / q.sp;
+  return q;
+}
+
+template <int kMode>
+__device__ __forceinline__ float quotient(float x, const QScale& q) {
+  if (kMode == 0) return __builtin_amdgcn_fmed3f(x / q.s, -448.0f, 448.0f);
+  const float xp = kMode == 1 ? x * q.pw : x;
+  const float q0 = xp * q.rp;
+  const float e = fmaf(-q0, q.sp, xp);
+  return __builtin_copysignf(fmaf(e, q.rp, q0), x);
+}
+
+// E4M3FN(RN(x / s)) of this thread's R rows of 8 columns (rows rb + kStep k),
+// row k's values produced by row(k, v); 8-byte stores, or bytes at a ragged
+// right edge or an unaligned destination.
+template <int kMode, int R, int kStep, class Row>
+__device__ __forceinline__ void quantise_store(Row row, const QScale& qs, int rows, int cols, int rb, int cg,
+                                               uint8_t* q8, uint32_t dst_ld, bool vec) {
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    const int r = rb + (128 / R) * k;
+    const int r = rb + kStep * k;
     if (r >= rows || cg >= cols) continue;
-    float q[8];
+    float v[8], q[8];
+    row(k, v);
 #pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      if (kMode != 0) {
-        const float xp = kMode == 1 ? v[k][m] * pw : v[k][m];
-        const float q0 = xp * rp;
-        const float e = fmaf(-q0, sp, xp);
-        q[m] = __builtin_copysignf(fmaf(e, rp, q0), v[k][m]);
-      } else {
-        q[m] = __builtin_amdgcn_fmed3f(v[k][m] / s, -448.0f, 448.0f);
-      }
-    }
+    for (int m = 0; m < 8; ++m) q[m] = quotient<kMode>(v[m], qs);
     uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
     lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
     uint32_t hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
     hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
-    uint8_t* dst = q8 + uint64_t(r) * b.dst_ld + cg;
-    if ((b.flags & QB_VEC_STORE) && cg + 8 <= cols) {
+    uint8_t* dst = q8 + uint64_t(r) * dst_ld + cg;
+    if (vec && cg + 8 <= cols) {
       st(u32x2{lo, hi}, reinterpret_cast<u32x2*>(dst));
     } else {
 #pragma unroll
@@ -396,73 +414,174 @@ __device__ __forceinline__ void quantise_store(const float (&v)[R][8], const QBl
   }
 }
 
-}  // namespace
+template <int R, int kStep, class Row>
+__device__ __forceinline__ void quantise_block(Row row, const QScale& qs, int rows, int cols, int rb, int cg,
+                                               uint8_t* q8, uint32_t dst_ld, bool vec) {
+  // the mode is uniform over the block, so this branch is taken once, outside
+  // the element loops
+  if (qs.mode == 2)
+    quantise_store<2, R, kStep>(row, qs, rows, cols, rb, cg, q8, dst_ld, vec);
+  else if (qs.mode == 1)
+    quantise_store<1, R, kStep>(row, qs, rows, cols, rb, cg, q8, dst_ld, vec);
+  else
+    quantise_store<0, R, kStep>(row, qs, rows, cols, rb, cg, q8, dst_ld, vec);
+}
 
-// One block per workgroup of 16 * 128 / R threads: thread t holds columns
-// 8 (t mod 16) .. + 7 of rows t / 16 + k * 128 / R, k < R.
-template <int R>
-__global__ __launch_bounds__(16 * 128 / R) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
-                                                                 const QPiece* __restrict__ pieces,
-                                                                 const uint64_t* __restrict__ ptrs, const char* recv) {
-  constexpr int T = 16 * 128 / R;
-  __shared__ float wave_max[T / 64];
-  __shared__ QPiece lds_pcs[kLdsPieces];
-  const QBlock b = blocks[blockIdx.x];
-  const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
-  const int cg = (threadIdx.x & 15) * 8;  // first of this thread's 8 columns
-  const int rb = threadIdx.x >> 4;        // rows rb, rb + 128 / R, ...
-  float v[R][8];
-  if (b.flags & QB_SINGLE) {
-    // one aligned bf16 piece covers the block: R independent 16-byte loads
-    const char* base = recv + b.src_off + uint64_t(cg) * 2;
-    u32x4 raw[R];
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
+// Takes the word by value: __builtin_bit_cast applied to a vector element
+// expression (v.y) reads the vector's first element in this compiler.
+__device__ __forceinline__ u16x2 as_u16x2(uint32_t w) { return __builtin_bit_cast(u16x2, w); }
+
+// Per-lane view of one of the two blocks of a pair.
+struct PairLane {
+  const char* src;   // this lane's first element (row rb, column cg)
+  uint64_t src_ld2;  // wire row stride in bytes
+  uint8_t* q8;       // fp8 block origin
+  uint32_t dst_ld;
+  int rows, cols;
+  bool vec;
+};
+
+// Blocks i0 and i0 + 1 (absent when i0 + 1 == nsingle), both QB_SINGLE. In
+// each half-wave, lanes 0..15 take block i0 and lanes 16..31 block i0 + 1, so a
+// load instruction reads 512 contiguous bytes of each of two rows when the two
+// blocks are neighbours on the wire; thread t holds columns 8 (t mod 16) .. + 7
+// of rows t / 32 + 8 k, k < 16, as raw bf16. kFull: both blocks present,
+// 128 x 128 and with 8-byte stores, so no load or store needs a predicate.
+template <bool kFull>
+__device__ __forceinline__ void qblock_pair_run(const PairLane& L, int h, bool on, const QBlock& b0,
+                                                const QBlock& b1, const uint64_t* __restrict__ ptrs) {
+  constexpr int R = 16, kStep = 8;
+  static_assert(kQBlockThreads == 32 * kStep, "pair mapping");
+  __shared__ uint32_t wave_max[kQBlockThreads / 64][2];
+  const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 5;
+  u32x4 raw[R];
+  if (kFull) {
+    const char* p = L.src;
 #pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const int r = rb + (128 / R) * k;
-      raw[k] = u32x4{0u, 0u, 0u, 0u};
-      if (r < rows && cg < cols) raw[k] = ld(reinterpret_cast<const u32x4*>(base + uint64_t(r) * b.src_ld * 2));
-    }
-#pragma unroll
-    for (int k = 0; k < R; ++k) unpack8(raw[k], v[k]);
+    for (int k = 0; k < R; ++k, p += kStep * L.src_ld2) raw[k] = ld(reinterpret_cast<const u32x4*>(p));
   } else {
-    // several pieces (or an unaligned / fp32 one): stage the piece list in LDS,
-    // resolve each row chunk's source first, then issue the loads
-    const int n = b.npieces;
-    const QPiece* pcs = pieces + b.piece0;
-    if (n <= kLdsPieces) {
-      for (int i = threadIdx.x; i < n; i += T) lds_pcs[i] = pcs[i];
-      __syncthreads();
-      pcs = lds_pcs;
-    }
-    const char* src[R];
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-      const int r = rb + (128 / R) * k;
-      src[k] = nullptr;
-      if (r >= rows || cg >= cols) continue;
-      for (int i = 0; i < n; ++i) {
-        const QPiece& p = pcs[i];
-        if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) {
-          const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
-          if (p.sdt == WB_BF16 && (reinterpret_cast<uintptr_t>(a) & 15) == 0) src[k] = a;
-          break;
-        }
-      }
-    }
-    u32x4 raw[R];
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
+      const int r = rb + kStep * k;
       raw[k] = u32x4{0u, 0u, 0u, 0u};
-      if (src[k]) raw[k] = ld(reinterpret_cast<const u32x4*>(src[k]));
+      if (r < L.rows && cg < L.cols)
+        raw[k] = ld(reinterpret_cast<const u32x4*>(L.src + uint64_t(kStep * k) * L.src_ld2));
     }
+  }
+  // amax: finite bf16 magnitudes order as their bit patterns with the sign
+  // cleared (two per word, packed 16-bit maxima)
+  u16x2 acc = {0, 0};
 #pragma unroll
-    for (int k = 0; k < R; ++k) {
-      unpack8(raw[k], v[k]);
-      const int r = rb + (128 / R) * k;
-      if (!src[k] && r < rows && cg < cols) {
+  for (int k = 0; k < R; ++k) {
+    const u32x4 a = raw[k] & 0x7FFF7FFFu;
+    acc = __builtin_elementwise_max(acc, as_u16x2(a.x));
+    acc = __builtin_elementwise_max(acc, as_u16x2(a.y));
+    acc = __builtin_elementwise_max(acc, as_u16x2(a.z));
+    acc = __builtin_elementwise_max(acc, as_u16x2(a.w));
+  }
+  uint32_t m = max(uint32_t(acc.x), uint32_t(acc.y));
+  // lanes of one block: xor 1..8 within a 16-lane group, xor 32 across the
+  // half-waves
+  m = max(m, uint32_t(__shfl_xor(int(m), 1)));
+  m = max(m, uint32_t(__shfl_xor(int(m), 2)));
+  m = max(m, uint32_t(__shfl_xor(int(m), 4)));
+  m = max(m, uint32_t(__shfl_xor(int(m), 8)));
+  m = max(m, uint32_t(__shfl_xor(int(m), 32)));
+  if ((threadIdx.x & 47) == 0) wave_max[threadIdx.x >> 6][h] = m;  // lanes 0 and 16
+  __syncthreads();
+  m = wave_max[0][h];
 #pragma unroll
-        for (int m = 0; m < 8; ++m) v[k][m] = cg + m < cols ? gather_one(pcs, n, recv, r, cg + m) : 0.0f;
+  for (int w = 1; w < kQBlockThreads / 64; ++w) m = max(m, wave_max[w][h]);
+  const QScale qs = make_scale(__uint_as_float(m << 16), true);
+  // rows and columns past the edge are skipped by the store loop; in the full
+  // case there are none
+  const int rows = kFull ? 128 : L.rows, cols = kFull ? 128 : L.cols;
+  quantise_block<R, kStep>([&](int k, float* v) { unpack8(raw[k], v); }, qs, rows, cols, rb, cg, L.q8, L.dst_ld,
+                           kFull || L.vec);
+  const QBlock& b = h ? b1 : b0;
+  if (on && (threadIdx.x & ~16u) == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = qs.s;
+}
+
+__device__ void qblock_pair(const QBlock* __restrict__ blocks, uint32_t i0, uint32_t nsingle,
+                            const uint64_t* __restrict__ ptrs, const char* recv) {
+  // both descriptors are read at workgroup-uniform addresses; each lane then
+  // selects its block's fields
+  const bool has1 = i0 + 1 < nsingle;
+  const QBlock b0 = blocks[i0];
+  const QBlock b1 = blocks[has1 ? i0 + 1 : i0];
+  const int h = (threadIdx.x >> 4) & 1;
+  const bool on = h == 0 || has1;
+  const QBlock& b = h ? b1 : b0;
+  const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 5;
+  PairLane L;
+  L.src_ld2 = uint64_t(b.src_ld) * 2;
+  L.src = recv + b.src_off + uint64_t(cg) * 2 + uint64_t(rb) * L.src_ld2;
+  L.dst_ld = b.dst_ld;
+  uint8_t* const q0 = reinterpret_cast<uint8_t*>(ptrs[b0.dst_idx]) + b0.dst_off;
+  uint8_t* const q1 = reinterpret_cast<uint8_t*>(ptrs[b1.dst_idx]) + b1.dst_off;
+  L.q8 = h ? q1 : q0;
+  L.rows = on ? b.rows_m1 + 1 : 0;
+  L.cols = b.cols_m1 + 1;
+  L.vec = (b.flags & QB_VEC_STORE) != 0;
+  const bool full = has1 && b0.rows_m1 == 127 && b0.cols_m1 == 127 && b1.rows_m1 == 127 && b1.cols_m1 == 127 &&
+                    (b0.flags & b1.flags & QB_VEC_STORE);
+  if (full)
+    qblock_pair_run<true>(L, h, on, b0, b1, ptrs);
+  else
+    qblock_pair_run<false>(L, h, on, b0, b1, ptrs);
+}
+
+// One block of any kind (several wire pieces, unaligned or fp32 ones): thread t
+// holds columns 8 (t mod 16) .. + 7 of rows t / 16 + 16 k, k < 8, as fp32,
+// gathered from the pieces.
+__device__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, const uint64_t* __restrict__ ptrs,
+                           const char* recv) {
+  constexpr int R = 8, kStep = 16;
+  static_assert(kQBlockThreads == 16 * kStep, "block mapping");
+  __shared__ float wave_max[kQBlockThreads / 64];
+  __shared__ QPiece lds_pcs[kLdsPieces];
+  const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
+  const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 4;
+  // stage the piece list in LDS, resolve each row chunk's source first, then
+  // issue the loads
+  const int n = b.npieces;
+  const QPiece* pcs = pieces + b.piece0;
+  if (n <= kLdsPieces) {
+    for (int i = threadIdx.x; i < n; i += kQBlockThreads) lds_pcs[i] = pcs[i];
+    __syncthreads();
+    pcs = lds_pcs;
+  }
+  const char* src[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int r = rb + kStep * k;
+    src[k] = nullptr;
+    if (r >= rows || cg >= cols) continue;
+    for (int i = 0; i < n; ++i) {
+      const QPiece& p = pcs[i];
+      if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) {
+        const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
+        if (p.sdt == WB_BF16 && (reinterpret_cast<uintptr_t>(a) & 15) == 0) src[k] = a;
+        break;
       }
+    }
+  }
+  u32x4 raw[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    raw[k] = u32x4{0u, 0u, 0u, 0u};
+    if (src[k]) raw[k] = ld(reinterpret_cast<const u32x4*>(src[k]));
+  }
+  float v[R][8];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    unpack8(raw[k], v[k]);
+    const int r = rb + kStep * k;
+    if (!src[k] && r < rows && cg < cols) {
+#pragma unroll
+      for (int m = 0; m < 8; ++m) v[k][m] = cg + m < cols ? gather_one(pcs, n, recv, r, cg + m) : 0.0f;
     }
   }
   float amax = 0.0f;
@@ -475,20 +594,33 @@ __global__ __launch_bounds__(16 * 128 / R) void wb_qblock_kernel(const QBlock* _
   __syncthreads();
   amax = wave_max[0];
 #pragma unroll
-  for (int w = 1; w < T / 64; ++w) amax = fmaxf(amax, wave_max[w]);
-
-  const float s = amax > 0.0f ? amax / 448.0f : 1.0f;  // IEEE fp32 division
-  // the branch is uniform over the workgroup and taken once, outside the
-  // element loops
-  const int sexp = int((__float_as_uint(s) >> 23) & 0xFF);  // E + 127
+  for (int w = 1; w < kQBlockThreads / 64; ++w) amax = fmaxf(amax, wave_max[w]);
+  const QScale qs = make_scale(amax, (b.flags & QB_BF16_SOURCE) != 0);
   uint8_t* q8 = reinterpret_cast<uint8_t*>(ptrs[b.dst_idx]) + b.dst_off;
-  if (!(b.flags & QB_BF16_SOURCE) || sexp == 0)
-    quantise_store<0, R>(v, b, rows, cols, rb, cg, s, q8);
-  else if (sexp >= 127 - 90 && sexp <= 127 + 100)
-    quantise_store<2, R>(v, b, rows, cols, rb, cg, s, q8);
-  else
-    quantise_store<1, R>(v, b, rows, cols, rb, cg, s, q8);
-  if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = s;
+  quantise_block<R, kStep>(
+      [&](int k, float* out) {
+#pragma unroll
+        for (int m = 0; m < 8; ++m) out[m] = v[k][m];
+      },
+      qs, rows, cols, rb, cg, q8, b.dst_ld, (b.flags & QB_VEC_STORE) != 0);
+  if (threadIdx.x == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = qs.s;
+}
+
+}  // namespace
+
+// Workgroup w < ceil(nsingle / 2) takes the QB_SINGLE blocks 2w and 2w + 1;
+// the following workgroups one other block each.
+__global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
+                                                                   const QPiece* __restrict__ pieces,
+                                                                   const uint64_t* __restrict__ ptrs,
+                                                                   const char* recv, uint32_t n, uint32_t nsingle) {
+  const uint32_t npair = (nsingle + 1) / 2;
+  if (blockIdx.x < npair) {
+    qblock_pair(blocks, 2 * blockIdx.x, nsingle, ptrs, recv);
+  } else {
+    const uint32_t i = nsingle + (blockIdx.x - npair);
+    if (i < n) qblock_one(blocks[i], pieces, ptrs, recv);
+  }
 }
 
 void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy) {
@@ -514,11 +646,12 @@ int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskS
   return hipGetLastError();
 }
 
-int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
-                   void* stream) {
+int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
+                   const void* buf, void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_qblock_kernel<kQBlockRows>, dim3(n), dim3(kQBlockThreads), WB_QBLOCK_DYN_LDS,
-                     static_cast<hipStream_t>(stream), blocks, pieces, ptrs, static_cast<const char*>(buf));
+  hipLaunchKernelGGL(wb_qblock_kernel, dim3(qblock_workgroups(n, nsingle)), dim3(kQBlockThreads), WB_QBLOCK_DYN_LDS,
+                     static_cast<hipStream_t>(stream), blocks, pieces, ptrs, static_cast<const char*>(buf), n,
+                     nsingle);
   return hipGetLastError();
 }
 

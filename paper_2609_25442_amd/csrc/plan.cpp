@@ -242,6 +242,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   for (const Segment& g : P.segs) by_round[g.round].push_back(&g);
   P.round_tasks.assign(nrounds + 1, 0);
   P.round_qblocks.assign(nrounds + 1, 0);
+  P.round_qsingle.assign(nrounds, 0);
   if (P.role == WB_SENDER) {
     const Rank& R = trainer.ranks[P.rank];
     P.n_locals = static_cast<int>(R.locals.size());
@@ -432,6 +433,13 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     for (int64_t i = 0; i < nblocks; ++i) sorted.push_back(P.qblocks[at[i]]);
     P.qblocks.swap(sorted);
   }
+  // within a round, the single-piece blocks first (block order within each
+  // class, so consecutive single-piece blocks are mostly horizontal neighbours)
+  for (int k = 0; k < nrounds; ++k) {
+    const auto first = P.qblocks.begin() + P.round_qblocks[k], last = P.qblocks.begin() + P.round_qblocks[k + 1];
+    const auto mid = std::stable_partition(first, last, [](const QBlock& b) { return (b.flags & QB_SINGLE) != 0; });
+    P.round_qsingle[k] = static_cast<uint32_t>(mid - first);
+  }
 }
 
 // Every byte a work item touches lies inside its buffer, and vector work items
@@ -527,8 +535,12 @@ void check_work(const wb_plan_t& P, const Rank& R) {
       check_task(t);
     }
   }
+  if (P.round_qsingle.size() != nr || P.round_qsingle[k] > P.round_qblocks[k + 1] - P.round_qblocks[k])
+    fail(WB_EINVAL, "internal: single-piece fp8 block count");
   for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
     const QBlock& b = P.qblocks[bi];
+    if (((b.flags & QB_SINGLE) != 0) != (bi < P.round_qblocks[k] + P.round_qsingle[k]))
+      fail(WB_EINVAL, "internal: fp8 block order");
     const uint64_t rows = b.rows_m1 + 1u, cols = b.cols_m1 + 1u;
     inside(b.dst_idx, b.dst_off, (rows - 1) * b.dst_ld + cols, "fp8 block");
     inside(b.scale_idx, uint64_t(b.scale_off) * 4, 4, "fp8 scale");

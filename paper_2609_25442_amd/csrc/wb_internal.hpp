@@ -216,14 +216,13 @@ static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
 enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
 
-// The fp8 block kernel runs one block per workgroup; each thread holds
-// kQBlockRows rows of 8 columns.
-#ifndef WB_QBLOCK_ROWS
-#define WB_QBLOCK_ROWS 8
-#endif
-constexpr int kQBlockRows = WB_QBLOCK_ROWS;
-constexpr int kQBlockThreads = 16 * 128 / kQBlockRows;
-static_assert(kQBlockRows == 2 || kQBlockRows == 4 || kQBlockRows == 8, "rows per thread");
+// The fp8 block kernel runs kQBlockThreads threads per workgroup. Each launch's
+// range of blocks starts with its QB_SINGLE blocks, taken two per workgroup
+// (horizontal neighbours in block order, so one row of the pair is 512
+// contiguous bytes of the wire), 16 rows of 8 columns per thread; the other
+// blocks follow, one per workgroup, 8 rows of 8 columns per thread.
+constexpr int kQBlockThreads = 256;
+inline uint32_t qblock_workgroups(uint32_t n, uint32_t nsingle) { return (nsingle + 1) / 2 + (n - nsingle); }
 
 // A field of a batched diff2 launch: rows x cols values, value at (i, j) the
 // sum over k < passes of src[k][i * cols + j] << (16 k); its element 0 is
@@ -282,6 +281,7 @@ struct wb_plan_t {
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
+  std::vector<uint32_t> round_qsingle;  // [k]: QB_SINGLE blocks at the start of round k's block range
   std::vector<uint32_t> round_fwd[2];   // forward work of exchange stage 1 + i, round k: [k] .. [k + 1]
   int64_t fwd_bytes[2] = {0, 0};        // bytes this rank forwards in each exchange stage (all rounds)
   // copies of the two layouts used for dumps and queries
@@ -312,8 +312,9 @@ constexpr uint16_t kAuxBuffer = 0xFFFF;
 void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy);
 int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskShift& sh, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream);
-int launch_qblocks(const QBlock* blocks, uint32_t n, const QPiece* pieces, const uint64_t* ptrs, const void* buf,
-                   void* stream);
+// n blocks, the first nsingle of them QB_SINGLE
+int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
+                   const void* buf, void* stream);
 const char* hip_error_string(int err);
 // probe.cpp
 void probe_init(wb_probe_t& P, const wb_tensor_desc* catalog, int n, int ckpt_dtype);

@@ -80,21 +80,58 @@ def test_bf16_to_f32_all_codes():
 
 def _domain_chunk(a0, a1):
     """Blocks of 16384 bf16 codes: for each amax code a in [a0, a1), four blocks
-    holding every code c with |c| <= a (others zero), each led by +a."""
+    holding every code c with |c| <= a (others zero) and +a, rotated."""
     a = torch.arange(a0, a1, dtype=torch.int32, device="cuda")
     c = torch.arange(0, 1 << 16, dtype=torch.int32, device="cuda")
     keep = (c & 0x7FFF)[None, :] <= a[:, None]
     x = torch.where(keep, c[None, :], torch.zeros_like(c)[None, :])
     x = x.view(-1, 16384)
     x[:, 0] = a.repeat_interleave(4)
+    # rotate each block by its own offset, so that the amax (and every other
+    # code) sits at a different row, column, lane and word from block to block
+    nb = x.shape[0]
+    shift = (torch.arange(nb, device="cuda") * 4099 + a0 * 61) % 16384
+    idx = (torch.arange(16384, device="cuda")[None, :] + shift[:, None]) % 16384
+    x = torch.gather(x, 1, idx)
     return x.to(torch.int16).view(torch.bfloat16).reshape(-1, 128)
 
 
-def test_fp8_quantiser_all_pairs():
+def _split_fp8_plan(rows, split):
+    """rows x 128 bf16 held by `split` trainer ranks, one column slab each, so
+    every 128 x 128 destination block is filled from `split` wire pieces (the
+    fp8 kernel's general path; one piece takes its single-piece path)."""
+    if split == 1:
+        p, ws = _one_tensor_plan(rows, 128, "bf16", "f8e4m3", block=128)
+        return p, ws, lambda x: x
+    w = 128 // split
+    tr = wb.Layout.create([("X", rows, 128)], split)
+    for r in range(split):
+        tr.add_local(r, "x", "bf16", 1, rows, w)
+        tr.add_placement(r, 0, 0, rows, r * w, (r + 1) * w, 0, 0, w)
+    ro = wb.Layout.create([("X", rows, 128)], 1)
+    ro.add_local(0, "y", "f8e4m3", 1, rows, 128, 128)
+    ro.add_placement(0, 0, 0, rows, 0, 128, 0, 0, 128)
+    p = wb.Plan(tr, ro, wb.RECEIVER, 0)
+    ws = workspace_for(p)
+    p.upload(ws)
+    recv = torch.empty(p.buffer_bytes, dtype=torch.uint8, device="cuda")
+    regions = [p.region(s, 0) for s in range(split)]
+
+    def to_wire(x):
+        for s, (_, off, nb) in enumerate(regions):
+            assert nb == rows * w * 2
+            recv[off:off + nb].view(torch.bfloat16).view(rows, w).copy_(x[:, s * w:(s + 1) * w])
+        return recv
+
+    return p, ws, to_wire
+
+
+@pytest.mark.parametrize("split", [1, 2])
+def test_fp8_quantiser_all_pairs(split):
     amax_max = 0x7F7F + 1
     per = 2048                                    # amax codes per launch -> 8192 blocks
     rows = per * 4 * 128
-    p, ws = _one_tensor_plan(rows, 128, "bf16", "f8e4m3", block=128)
+    p, ws, to_wire = _split_fp8_plan(rows, split)
     q = torch.empty(rows, 128, dtype=torch.float8_e4m3fn, device="cuda")
     s = torch.empty(rows // 128, 1, dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(7)
@@ -105,7 +142,7 @@ def test_fp8_quantiser_all_pairs():
         x = _domain_chunk(a0, a1)
         if x.shape[0] < rows:
             x = torch.cat([x, torch.zeros(rows - x.shape[0], 128, dtype=torch.bfloat16, device="cuda")])
-        p.unpack(x, [q, s])
+        p.unpack(to_wire(x), [q, s])
         xf = x.float().view(-1, 16384)
         amax = xf.abs().amax(dim=1)
         # divide by a tensor: torch turns division by a CPU scalar into a
@@ -131,7 +168,7 @@ def test_fp8_quantiser_all_pairs():
     # all-zero blocks (scale 1) and signed zeros
     x = torch.zeros(rows, 128, dtype=torch.bfloat16, device="cuda")
     x.view(-1, 16384)[1::2] = -0.0
-    p.unpack(x, [q, s])
+    p.unpack(to_wire(x), [q, s])
     assert bool((s == 1.0).all())
     qb = q.view(torch.uint8).view(-1, 16384)
     assert bool((qb[0::2] == 0).all()) and bool((qb[1::2] == 0x80).all())

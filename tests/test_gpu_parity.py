@@ -16,6 +16,7 @@ from synthetic_checkpoint.workloads import ORDER, scaled
 
 from gpu_util import roundtrip, say
 from oracle_cases import hand_replicated_pair, random_model, random_par
+from wb_cases import to_wb
 
 pytestmark = pytest.mark.gpu
 
@@ -99,3 +100,31 @@ def test_transposed_trainer_shards(rows, cols, split):
     tr = Layout(cat, ranks)
     ro = Layout(cat, [RankLayout([Local("x", "bf16", 1, rows, cols)], [Placement(0, 0, rows, 0, cols, 0, 0, cols)])])
     roundtrip(tr, ro, _values(cat, "bf16"), label=f"transposed-{rows}x{cols}/{split}")
+
+
+def test_fp8_paired_and_general_blocks():
+    """fp8 blocks of one launch on both kernel paths: 19 single-piece blocks
+    (taken two per workgroup, the last one alone; pairs that straddle tensors
+    and block rows; ragged right and bottom edges) and blocks filled from two
+    wire pieces or from an unaligned one (one per workgroup)."""
+    cat = [CkptTensor("T", 300, 392), CkptTensor("V", 130, 264), CkptTensor("W", 128, 128), CkptTensor("U", 200, 136)]
+    r0 = RankLayout([Local("t0", "bf16", 1, 256, 392), Local("v", "bf16", 1, 130, 264), Local("u0", "bf16", 1, 200, 60)],
+                    [Placement(0, 0, 256, 0, 392, 0, 0, 392), Placement(1, 0, 130, 0, 264, 1, 0, 264),
+                     Placement(3, 0, 200, 0, 60, 2, 0, 60)])
+    r1 = RankLayout([Local("t1", "bf16", 1, 44, 392), Local("w", "bf16", 1, 128, 128), Local("u1", "bf16", 1, 200, 76)],
+                    [Placement(0, 256, 300, 0, 392, 0, 0, 392), Placement(2, 0, 128, 0, 128, 1, 0, 128),
+                     Placement(3, 0, 200, 60, 136, 2, 0, 76)])
+    tr = Layout(cat, [r0, r1])
+    locs, pls = [], []
+    for t, c in enumerate(cat):
+        nbr, nbc = -(-c.rows // 128), -(-c.cols // 128)
+        u = len(locs)
+        locs += [Local("q" + c.name, "f8e4m3", 1, c.rows, c.cols, 128, scale=u + 1),
+                 Local("s" + c.name, "f32", 1, nbr, nbc, scales=u)]
+        pls.append(Placement(t, 0, c.rows, 0, c.cols, u, 0, c.cols))
+    ro = Layout(cat, [RankLayout(locs, pls)])
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
+    nb = p.work_counts()[1]
+    gx = p.launch_grid(1)[0]
+    assert nb == 12 + 6 + 1 + 4 and gx == (19 + 1) // 2 + 4, (nb, gx)
+    roundtrip(tr, ro, _values(cat, "bf16"), label="fp8-paths")
