@@ -104,16 +104,16 @@ struct Walker {
   }
 };
 
-// Vectors [q0, q1) of a rows x vpr block in row-major order: lane l takes
-// q0 + l + k * kThreads for k < kChunkPerLane. Each pointer is null where the
-// lane has no vector.
+// Units [q0, q1) of a rows x vpr block in row-major order: lane l takes
+// q0 + l + k * kThreads for k < N; on[k] says whether that unit exists.
+template <int N = kChunkPerLane>
 struct ChunkWalk {
-  uint32_t r[kChunkPerLane], c[kChunkPerLane];
-  bool on[kChunkPerLane];
+  uint32_t r[N], c[N];
+  bool on[N];
   __device__ ChunkWalk(uint32_t q0, uint32_t q1, uint32_t vpr) {
     Walker w(q0 + threadIdx.x, vpr);
 #pragma unroll
-    for (int k = 0; k < kChunkPerLane; ++k) {
+    for (int k = 0; k < N; ++k) {
       on[k] = q0 + threadIdx.x + k * kThreads < q1;
       r[k] = w.r;
       c[k] = w.c;
@@ -141,7 +141,7 @@ __device__ void run_copy16(const Task& t, const char* src, char* dst, uint32_t q
       if (threadIdx.x + k * kThreads < m) st(v[k], d + k * kThreads);
     return;
   }
-  const ChunkWalk w(q0, q1, vpr);
+  const ChunkWalk<> w(q0, q1, vpr);
 #pragma unroll
   for (int k = 0; k < kChunkPerLane; ++k)
     if (w.on[k]) v[k] = ld(reinterpret_cast<const u32x4*>(src + uint64_t(w.r[k]) * t.src_ld) + w.c[k]);
@@ -150,26 +150,26 @@ __device__ void run_copy16(const Task& t, const char* src, char* dst, uint32_t q
     if (w.on[k]) st(v[k], reinterpret_cast<u32x4*>(dst + uint64_t(w.r[k]) * t.dst_ld) + w.c[k]);
 }
 
-// fp32 -> bf16 of one chunk of output vectors (8 elements each); strides in
-// elements.
-__device__ void run_f32_bf16(const Task& t, const char* src, char* dst, uint32_t q0) {
-  const uint32_t vpr = t.cols >> 3;
+// fp32 -> bf16 of one chunk of 2 kThreads units of 4 elements (chunk c starts
+// at unit 2 c kThreads): lane l converts units l and l + kThreads, so each load
+// instruction of the wave reads 64 consecutive 16-byte vectors of a row; two
+// 8-byte stores. Strides in elements.
+__device__ void run_f32_bf16(const Task& t, const char* src, char* dst, uint32_t chunk) {
+  const uint32_t vpr = t.cols >> 2;
   const uint32_t total = t.rows * vpr;
+  const uint32_t q0 = chunk * 2 * uint32_t(kThreads);
   if (q0 >= total) return;
-  const ChunkWalk w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
-  f32x4 a[kChunkPerLane], b[kChunkPerLane];
+  const ChunkWalk<2> w(q0, min(total, q0 + 2 * uint32_t(kThreads)), vpr);
+  f32x4 a[2];
 #pragma unroll
-  for (int k = 0; k < kChunkPerLane; ++k)
-    if (w.on[k]) {
-      const f32x4* sp = reinterpret_cast<const f32x4*>(src + (uint64_t(w.r[k]) * t.src_ld + uint64_t(w.c[k]) * 8) * 4);
-      a[k] = ld(sp);
-      b[k] = ld(sp + 1);
-    }
-#pragma unroll
-  for (int k = 0; k < kChunkPerLane; ++k)
+  for (int k = 0; k < 2; ++k)
     if (w.on[k])
-      st(cvt8_f32_bf16(a[k], b[k]),
-         reinterpret_cast<u32x4*>(dst + (uint64_t(w.r[k]) * t.dst_ld + uint64_t(w.c[k]) * 8) * 2));
+      a[k] = ld(reinterpret_cast<const f32x4*>(src + (uint64_t(w.r[k]) * t.src_ld + uint64_t(w.c[k]) * 4) * 4));
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+    if (w.on[k])
+      st(u32x2{pack_bf16x2(a[k].x, a[k].y), pack_bf16x2(a[k].z, a[k].w)},
+         reinterpret_cast<u32x2*>(dst + (uint64_t(w.r[k]) * t.dst_ld + uint64_t(w.c[k]) * 4) * 2));
 }
 
 // bf16 -> fp32 of one chunk of input vectors (8 elements each); strides in
@@ -178,7 +178,7 @@ __device__ void run_bf16_f32(const Task& t, const char* src, char* dst, uint32_t
   const uint32_t vpr = t.cols >> 3;
   const uint32_t total = t.rows * vpr;
   if (q0 >= total) return;
-  const ChunkWalk w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
+  const ChunkWalk<> w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
   u32x4 v[kChunkPerLane];
 #pragma unroll
   for (int k = 0; k < kChunkPerLane; ++k)
@@ -307,7 +307,7 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
   const uint32_t q0 = chunk * uint32_t(kChunkVecs);
   switch (t.kind) {
     case TASK_COPY16: run_copy16(t, src, dst, q0); break;
-    case TASK_F32_BF16: run_f32_bf16(t, src, dst, q0); break;
+    case TASK_F32_BF16: run_f32_bf16(t, src, dst, chunk); break;
     case TASK_BF16_F32: run_bf16_f32(t, src, dst, q0); break;
     case TASK_SCALAR: if (chunk == 0) run_scalar(t, src, dst); break;
     case TASK_TRANSPOSE: run_transpose(t, src, dst, chunk); break;

@@ -166,7 +166,10 @@ inline uint32_t task_chunks(const Task& t) {
   uint64_t vecs = 0;
   switch (t.kind) {
     case TASK_COPY16: vecs = uint64_t(t.rows) * (t.cols >> 4); break;
-    case TASK_F32_BF16:
+    case TASK_F32_BF16: {  // units of 4 elements, 2 kChunkThreads per chunk
+      const uint64_t units = uint64_t(t.rows) * (t.cols >> 2), per = 2 * uint64_t(kChunkThreads);
+      return static_cast<uint32_t>(units == 0 ? 1 : (units + per - 1) / per);
+    }
     case TASK_BF16_F32: vecs = uint64_t(t.rows) * (t.cols >> 3); break;
     case TASK_TRANSPOSE16: {
       const uint32_t per = kChunkThreads / 64, tiles = (t.cols + 63) / 64;
