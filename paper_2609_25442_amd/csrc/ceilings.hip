@@ -1,9 +1,12 @@
 // Practical HBM ceilings of this GPU for 16-byte vector streams: read-only,
 // write-only, copy with one contiguous 256 KiB chunk per workgroup looping over
-// it, copy with one-shot 4 KiB workgroups (one load and one store per lane, the
-// packing and assembly kernels' pattern), and hipMemcpy, over 8 GiB buffers,
-// best of five. Prints one JSON object. Used to put the resharding kernels'
-// bandwidth next to what a plain stream reaches on the same part.
+// it, hipMemcpy, copy with one-shot one-wave workgroups (one load and one store
+// per lane, the copy kernel's pattern), and a one-shot stream that reads two
+// bytes per byte written (each lane loads two vectors one wave apart and
+// stores one: the read/write mix of the fp32 -> bf16 and fp8 assembly), over
+// 8 GiB buffers, best of five. Prints one JSON object. Used to put the
+// resharding kernels' bandwidth next to what a plain stream reaches on the
+// same part.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -60,6 +63,13 @@ __global__ void copy_oneshot(const u32x4* __restrict__ s, u32x4* __restrict__ d)
   __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
+// vectors 2 b T + l and 2 b T + T + l in, one vector out (T = blockDim.x)
+__global__ void read2_write1_oneshot(const u32x4* __restrict__ s, u32x4* __restrict__ d) {
+  const uint64_t i = uint64_t(blockIdx.x) * 2 * blockDim.x + threadIdx.x;
+  const u32x4 a = __builtin_nontemporal_load(s + i), b = __builtin_nontemporal_load(s + i + blockDim.x);
+  __builtin_nontemporal_store(a ^ b, d + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x);
+}
+
 int main() {
   const uint64_t bytes = 8ull << 30, n = bytes / 16;
   const int read_grid = 512, write_grid = 16384, threads = 256;
@@ -73,8 +83,8 @@ int main() {
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
-  double gbs[5];
-  for (int which = 0; which < 5; ++which) {
+  double gbs[6];
+  for (int which = 0; which < 6; ++which) {
     float best = 1e30f;
     for (int r = 0; r < 6; ++r) {
       CHECK(hipEventRecord(e0));
@@ -82,18 +92,20 @@ int main() {
       if (which == 1) write_stream<<<write_grid, threads>>>(d, n);
       if (which == 2) copy_chunks<<<int((n + per - 1) / per), threads>>>(s, d, n, per);
       if (which == 3) CHECK(hipMemcpyAsync(d, s, bytes, hipMemcpyDeviceToDevice, 0));
-      if (which == 4) copy_oneshot<<<int(n / threads), threads>>>(s, d);
+      if (which == 4) copy_oneshot<<<int(n / 64), 64>>>(s, d);
+      if (which == 5) read2_write1_oneshot<<<int(n / 2 / 64), 64>>>(s, d);  // reads n vectors, writes n / 2
       CHECK(hipEventRecord(e1));
       CHECK(hipEventSynchronize(e1));
       float ms;
       CHECK(hipEventElapsedTime(&ms, e0, e1));
       if (r > 0 && ms < best) best = ms;  // first run warms up
     }
-    gbs[which] = (which >= 2 ? 2.0 : 1.0) * double(bytes) / (best * 1e-3) / 1e9;
+    const double moved = which == 5 ? 1.5 : which >= 2 ? 2.0 : 1.0;  // bytes read + written per buffer byte
+    gbs[which] = moved * double(bytes) / (best * 1e-3) / 1e9;
   }
   std::printf("{\"read_GBps\": %.1f, \"write_GBps\": %.1f, \"copy_GBps\": %.1f, \"hipMemcpy_GBps\": %.1f, "
-              "\"copy_oneshot_GBps\": %.1f, \"bytes\": %llu}\n", gbs[0], gbs[1], gbs[2], gbs[3], gbs[4],
-              (unsigned long long)bytes);
+              "\"copy_oneshot_GBps\": %.1f, \"read2_write1_oneshot_GBps\": %.1f, \"bytes\": %llu}\n", gbs[0], gbs[1],
+              gbs[2], gbs[3], gbs[4], gbs[5], (unsigned long long)bytes);
   CHECK(hipFree(s));
   CHECK(hipFree(d));
   CHECK(hipFree(out));

@@ -341,7 +341,7 @@ __device__ __forceinline__ void unpack8(const u32x4 x, float* v) {
   v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
 }
 
-constexpr int kLdsPieces = 32;
+constexpr int kLdsPieces = 128;
 
 // The block's scale s = amax / 448 (IEEE division; 1 for an all-zero block)
 // and the quantities RN(x / s) is computed from, s = m 2^E (m in [1, 2)):
@@ -542,16 +542,28 @@ __device__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, c
   static_assert(kQBlockThreads == 16 * kStep, "block mapping");
   __shared__ float wave_max[kQBlockThreads / 64];
   __shared__ QPiece lds_pcs[kLdsPieces];
+  __shared__ uint8_t row_piece[128];
   const int rows = b.rows_m1 + 1, cols = b.cols_m1 + 1;
   const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 4;
-  // stage the piece list in LDS, resolve each row chunk's source first, then
-  // issue the loads
+  // stage the piece list in LDS with a row -> piece table for the pieces that
+  // span the block's full width (row bands: the common case, a replicated
+  // tensor split by rows among its senders); resolve each row chunk's source
+  // first (the table, else a search of the list), then issue the loads
   const int n = b.npieces;
   const QPiece* pcs = pieces + b.piece0;
+  bool table = false;
   if (n <= kLdsPieces) {
     for (int i = threadIdx.x; i < n; i += kQBlockThreads) lds_pcs[i] = pcs[i];
+    for (int r = threadIdx.x; r < 128; r += kQBlockThreads) row_piece[r] = 0xFF;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += kQBlockThreads) {
+      const QPiece& p = lds_pcs[i];
+      if (p.c0 == 0 && p.c1m1 == cols - 1)
+        for (int r = p.r0; r <= p.r1m1; ++r) row_piece[r] = static_cast<uint8_t>(i);
+    }
     __syncthreads();
     pcs = lds_pcs;
+    table = true;
   }
   const char* src[R];
 #pragma unroll
@@ -559,13 +571,16 @@ __device__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, c
     const int r = rb + kStep * k;
     src[k] = nullptr;
     if (r >= rows || cg >= cols) continue;
-    for (int i = 0; i < n; ++i) {
-      const QPiece& p = pcs[i];
-      if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) {
-        const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
-        if (p.sdt == WB_BF16 && (reinterpret_cast<uintptr_t>(a) & 15) == 0) src[k] = a;
-        break;
+    int i = table ? row_piece[r] : 0xFF;
+    if (i == 0xFF)
+      for (i = 0; i < n; ++i) {
+        const QPiece& p = pcs[i];
+        if (r >= p.r0 && r <= p.r1m1 && cg >= p.c0 && cg + 7 <= p.c1m1) break;
       }
+    if (i < n) {
+      const QPiece& p = pcs[i];
+      const char* a = recv + p.src_off + (uint64_t(r - p.r0) * p.src_ld + (cg - p.c0)) * 2;
+      if (p.sdt == WB_BF16 && cg + 7 <= p.c1m1 && (reinterpret_cast<uintptr_t>(a) & 15) == 0) src[k] = a;
     }
   }
   u32x4 raw[R];
