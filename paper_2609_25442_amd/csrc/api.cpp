@@ -496,7 +496,7 @@ int wb_plan_launch_grid(const wb_plan_t* P, int32_t launch, int32_t round, uint3
   const std::vector<wb::TaskSplit>& c = launch == 0 ? P->round_split : P->fwd_split[launch - 2];
   if (r.size() != P->rounds.size() + 1 || c.size() != P->rounds.size()) return WB_OK;
   const uint32_t n = r[round + 1] - r[round];
-  if (n) wb::task_grid(n, c[round], P->task_shift, gx, gy);
+  if (n) wb::task_grid(n, c[round], gx, gy);
   return WB_OK;
 }
 
@@ -572,7 +572,7 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
   const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
   const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
   int e = wb::launch_tasks(tasks + P->round_tasks[round], P->round_tasks[round + 1] - P->round_tasks[round],
-                           P->round_split[round], P->task_shift, table, buf, nullptr, stream);
+                           P->round_split[round], table, buf, nullptr, stream);
   if (e != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(e));
   const auto* blocks = reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks);
   e = wb::launch_qblocks(blocks + P->round_qblocks[round], P->round_qblocks[round + 1] - P->round_qblocks[round],
@@ -610,7 +610,7 @@ int wb_forward_round(wb_plan_t* P, int32_t round, int32_t stage, const void* rec
     if (rc != WB_OK) return rc;
     const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
     const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
-    const int e = wb::launch_tasks(tasks + a, b - a, P->fwd_split[stage - 1][round], P->task_shift, table,
+    const int e = wb::launch_tasks(tasks + a, b - a, P->fwd_split[stage - 1][round], table,
                                    recv_buf, fwd_buf, stream);
     if (e != 0) return set_error(WB_EHIP, std::string("forward launch: ") + wb::hip_error_string(e));
     return WB_OK;

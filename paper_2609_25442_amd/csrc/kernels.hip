@@ -638,9 +638,9 @@ __global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock*
   }
 }
 
-void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy) {
+void task_grid(uint32_t n, const TaskSplit& sp, uint32_t* gx, uint32_t* gy) {
   const uint64_t total =
-      (uint64_t(sp.n[0]) << sh.s[0]) + (uint64_t(sp.n[1]) << sh.s[1]) + (n - sp.n[0] - sp.n[1]);
+      (uint64_t(sp.n[0]) << sp.s[0]) + (uint64_t(sp.n[1]) << sp.s[1]) + (n - sp.n[0] - sp.n[1]);
   if (total <= kMaxGridX) {
     *gx = static_cast<uint32_t>(total);
     *gy = 1;
@@ -650,14 +650,14 @@ void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* g
   }
 }
 
-int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskShift& sh, const uint64_t* ptrs,
-                 const void* buf, const void* aux, void* stream) {
+int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint64_t* ptrs, const void* buf,
+                 const void* aux, void* stream) {
   if (n == 0) return hipSuccess;
   uint32_t gx, gy;
-  task_grid(n, sp, sh, &gx, &gy);
+  task_grid(n, sp, &gx, &gy);
   hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS, static_cast<hipStream_t>(stream),
                      tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, sp.n[0], sp.n[1],
-                     sh.s[0], sh.s[1]);
+                     sp.s[0], sp.s[1]);
   return hipGetLastError();
 }
 

@@ -471,9 +471,7 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   auto check_task = [&](const Task& t) {
     if (t.rows == 0 || t.cols == 0) fail(WB_EINVAL, "internal: empty work item");
     // the kernel counts a work item's vectors and chunk offsets in 32 bits
-    const int cls = task_class(t);
-    if (uint64_t(t.rows) * t.cols >= (uint64_t(1) << 31) || (cls < 2 && task_chunks(t) > (1u << P.task_shift.s[cls])))
-      fail(WB_EINVAL, "internal: work item too large for its launch");
+    if (uint64_t(t.rows) * t.cols >= (uint64_t(1) << 31)) fail(WB_EINVAL, "internal: work item too large");
     const uint64_t ss = dtype_bytes(t.sdt), ds = dtype_bytes(t.ddt);
     switch (t.kind) {
       case TASK_COPY16:
@@ -514,9 +512,13 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   aux_size = 0;
   auto check_order = [&](uint32_t a, uint32_t b, const TaskSplit& sp) {
     if (uint64_t(sp.n[0]) + sp.n[1] > b - a) fail(WB_EINVAL, "internal: work item class sizes");
+    if (sp.s[0] > 24 || sp.s[1] > 24) fail(WB_EINVAL, "internal: work item class shift");
     for (uint32_t ti = a; ti < b; ++ti) {
       const int want = ti < a + sp.n[0] ? 0 : ti < a + sp.n[0] + sp.n[1] ? 1 : 2;
       if (task_class(P.tasks[ti]) != want) fail(WB_EINVAL, "internal: work item order");
+      // every chunk of an item has a workgroup
+      if (want < 2 && task_chunks(P.tasks[ti]) > (1u << sp.s[want]))
+        fail(WB_EINVAL, "internal: work item too large for its launch");
     }
   };
   check_order(P.round_tasks[k], P.round_tasks[k + 1], P.round_split[k]);
@@ -951,6 +953,11 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
     TaskSplit sp;
     sp.n[0] = static_cast<uint32_t>(mid0 - first);
     sp.n[1] = static_cast<uint32_t>(mid1 - mid0);
+    for (int c = 0; c < 2; ++c) {
+      uint32_t most = 1;  // workgroups of the copy kernel per item of class c in this launch
+      for (auto it = c == 0 ? first : mid0; it != (c == 0 ? mid0 : mid1); ++it) most = std::max(most, task_chunks(*it));
+      while ((1u << sp.s[c]) < most) ++sp.s[c];
+    }
     return sp;
   };
   const size_t nr = P.rounds.size();
@@ -959,15 +966,6 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   for (size_t k = 0; k < nr; ++k) {
     P.round_split[k] = partition(P.round_tasks[k], P.round_tasks[k + 1]);
     for (int st = 0; st < 2; ++st) P.fwd_split[st][k] = partition(P.round_fwd[st][k], P.round_fwd[st][k + 1]);
-  }
-  uint32_t most[2] = {1, 1};  // workgroups of the copy kernel per item of classes 0 and 1
-  for (const Task& t : P.tasks) {
-    const int cls = task_class(t);
-    if (cls < 2) most[cls] = std::max(most[cls], task_chunks(t));
-  }
-  for (int c = 0; c < 2; ++c) {
-    P.task_shift.s[c] = 0;
-    while ((1u << P.task_shift.s[c]) < most[c]) ++P.task_shift.s[c];
   }
   check_work(P, role == WB_SENDER ? trainer.ranks[rank] : rollout.ranks[rank]);
 }

@@ -137,7 +137,7 @@ struct Task {
 static_assert(sizeof(Task) == 48, "Task layout");
 
 // Copy kernel launch. Each launch's range of work items is ordered by class:
-// class 0 (the vector kinds) takes 2^shift[0] workgroups of kChunkThreads
+// class 0 (the vector kinds) takes 2^s[0] workgroups of kChunkThreads
 // threads (a multiple of 64: one wave by default) per item, one per chunk of
 // kChunkVecs 16-byte vectors (kChunkPerLane per lane); class 1 (transposes)
 // takes 2^shift[1] per item, TASK_TRANSPOSE16 one per kChunkThreads / 64 tiles
@@ -181,12 +181,10 @@ inline uint32_t task_chunks(const Task& t) {
   return static_cast<uint32_t>(vecs == 0 ? 1 : (vecs + kChunkVecs - 1) / kChunkVecs);
 }
 
-// Items of classes 0 and 1 at the start of one launch's range (class 2 follows)
-// and the plan-wide log2 workgroups per item of each class.
+// One launch's range: items of classes 0 and 1 at its start (class 2 follows)
+// and log2 of the workgroups per item of each class (fits its longest item).
 struct TaskSplit {
   uint32_t n[2] = {0, 0};
-};
-struct TaskShift {
   uint32_t s[2] = {0, 0};
 };
 
@@ -278,7 +276,6 @@ struct wb_plan_t {
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
-  wb::TaskShift task_shift;             // log2 of the copy kernel's workgroups per item of classes 0 and 1
   std::vector<wb::TaskSplit> round_split;  // [k]: class sizes of round k's pack/unpack range
   std::vector<wb::TaskSplit> fwd_split[2]; // the same for the forward range of stage 1 + i, round k
   std::vector<wb::QBlock> qblocks;      // grouped by round
@@ -312,8 +309,8 @@ std::string dump_plan(const wb_plan_t& P);
 // kAuxBuffer aux (the second buffer of a forward launch).
 constexpr uint16_t kAuxBuffer = 0xFFFF;
 // n work items ordered by class, split as in `sp`
-void task_grid(uint32_t n, const TaskSplit& sp, const TaskShift& sh, uint32_t* gx, uint32_t* gy);
-int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const TaskShift& sh, const uint64_t* ptrs,
+void task_grid(uint32_t n, const TaskSplit& sp, uint32_t* gx, uint32_t* gy);
+int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream);
 // n blocks, the first nsingle of them QB_SINGLE
 int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
