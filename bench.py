@@ -172,9 +172,11 @@ def _launch_grids(w):
     ro = wb.Layout.describe(w["model"], w["rollout"])
     rp = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"])
     sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
-    def threads_x(plan, launch):  # rocprofv3 reports Grid_Size(_X) in threads
-        x, _, t = plan.launch_grid(launch)
-        return x * t
+    def threads_x(plan, launch):
+        # rocprofv3 reports grid sizes in threads: the kernel trace per
+        # dimension (Grid_Size_X), the counter collection the product (Grid_Size)
+        x, y, t = plan.launch_grid(launch)
+        return x * t, x * max(y, 1) * t
 
     return {"pack": (threads_x(sp, 0), "wb_tasks_kernel", sp.traffic()),
             "unpack": (threads_x(rp, 0), "wb_tasks_kernel", rp.kernel_traffic(0)),
@@ -199,9 +201,9 @@ def summarize_counters(workload, fetch_csv, write_csv):
         factor = statistics.mean(copies) * 1024 / copy_bytes
         out["calibration"][counter] = {"copy_bytes": copy_bytes, "copy_kib": statistics.mean(copies),
                                        "factor": round(factor, 5)}
-        for label, (grid, kname, _) in grids.items():
+        for label, ((_, total), kname, _) in grids.items():
             vals = [float(r["Counter_Value"]) for r in rows
-                    if kname in r["Kernel_Name"] and int(r["Grid_Size"]) == grid and grid > 0]
+                    if kname in r["Kernel_Name"] and int(r["Grid_Size"]) == total and total > 0]
             if vals:
                 per.setdefault(label, {})[counter] = (statistics.mean(vals), len(vals), factor)
     for label, c in per.items():
@@ -225,9 +227,9 @@ def summarize_trace(workload, trace_csv):
     grids, recv_bytes = _launch_grids(WORKLOADS[workload])
     rows = _read_csv(trace_csv)
     res = {}
-    for label, (grid, kname, alg) in grids.items():
+    for label, ((gx, _), kname, alg) in grids.items():
         ds = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows
-              if kname in r["Kernel_Name"] and int(r["Grid_Size_X"]) == grid and grid > 0]
+              if kname in r["Kernel_Name"] and int(r["Grid_Size_X"]) == gx and gx > 0]
         if ds:
             res[label] = {"launches": len(ds), "avg_us": round(statistics.mean(ds) / 1e3, 2),
                           "min_us": round(min(ds) / 1e3, 2), "max_us": round(max(ds) / 1e3, 2),
