@@ -10,8 +10,10 @@ senders' regions). Other workloads: --workload NAME.
 Prints one JSON line: effective GB/s of the step (algorithmic bytes: each
 element read once in the source dtype and written once in the destination
 dtype, plus fp8 scales), the HBM roofline of the dominant kernel from HIP
-events on the launch stream, wb_plan time, and the CPU oracle timed on a
-bounded sample of the same workload.
+events on the launch stream, wb_plan time, this GPU's stream ceilings
+(measured first, in a child process) with the dominant kernel's fraction of the
+one-shot stream of its read/write mix, and the CPU oracle timed on a bounded
+sample of the same workload.
 """
 
 from __future__ import annotations
@@ -241,6 +243,15 @@ def summarize_trace(workload, trace_csv):
     return res
 
 
+def run_ceilings():
+    """This GPU's stream ceilings (paper_2609_25442_amd/wb_ceilings, a separate
+    process: 2 x 8 GiB of device memory while it runs)."""
+    import subprocess
+
+    exe = os.path.join(ROOT, "paper_2609_25442_amd", "wb_ceilings")
+    return subprocess.run([exe], capture_output=True, text=True, timeout=300)
+
+
 def run_plan_stress():
     """Host planning time on a DeepSeek-V3-like catalog of 58 MoE layers
     (44,776 checkpoint tensors), EP64 bf16 trainer -> EP8 fp8 rollout: median of
@@ -352,6 +363,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip measuring this GPU's stream ceilings before the benchmark")
     ap.add_argument("--round-budget", type=int, default=0,
                     help="bytes per rank per round (0: one round); each step packs and unpacks every round")
     ap.add_argument("--node-size", type=int, default=0,
@@ -376,10 +389,7 @@ def main():
         print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
         return
     if args.ceilings:
-        import subprocess
-
-        exe = os.path.join(ROOT, "paper_2609_25442_amd", "wb_ceilings")
-        r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+        r = run_ceilings()
         sys.stderr.write(r.stderr)
         print(r.stdout.strip())
         sys.exit(r.returncode)
@@ -398,6 +408,17 @@ def main():
     if args.plan_stress:
         run_plan_stress()
         return
+
+    # the practical ceilings of this machine, measured before the benchmark
+    # allocates anything, for reading the roofline fraction against
+    ceilings = None
+    if not args.no_ceilings and not args.staged:
+        r = run_ceilings()
+        if r.returncode == 0:
+            ceilings = json.loads(r.stdout.strip().splitlines()[-1])
+            ceilings.pop("bytes", None)
+        else:
+            log(f"[bench] stream ceilings failed ({r.returncode}): {r.stderr.strip()[-300:]}")
 
     import torch
 
@@ -620,6 +641,12 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
     }
+    if ceilings:
+        # the one-shot stream with the dominant kernel's read/write mix: a same-
+        # dtype copy reads one byte per byte written, a cast assembly two
+        mix = "copy_oneshot_GBps" if ur < 1.5 * uw else "read2_write1_oneshot_GBps"
+        out["stream_ceilings"] = dict(ceilings, matching=mix,
+                                      frac_of_matching=round(achieved / ceilings[mix], 4) if ceilings.get(mix) else None)
     if fwds:
         out["forward"] = {f"stage{st}": {"bytes": fwd_bytes[st], "ms": round(fwd_ms[st], 4) if st in fwd_ms else None,
                                          "GB/s": round(fwd_bytes[st] / (fwd_ms[st] * 1e-3) / 1e9, 1)
