@@ -4,7 +4,7 @@ The paper uses the full checkpoint as the bridge between trainer and rollout
 parameters: every element has one position in it, and a worker's source map
 says which checkpoint elements it holds. Here a checkpoint is an ordered list
 of tensors of at most two dimensions ([rows, cols]; vectors are [1, n]).
-Names and order are this build's reading (the paper assumes a real checkpoint
+Names and order are the reading taken here (the paper assumes a real checkpoint
 and prints none); parity depends only on shapes and order.
 
 Families:

@@ -9,7 +9,7 @@ transposition. A *placement* is one such slice-copy:
     local[u][base + (i - r0) * ld + (j - c0)] = T_t[i, j]     (not transposed)
     local[u][base + (j - c0) * ld + (i - r0)] = T_t[i, j]     (transposed)
 
-The paper recovers placements by probing the loader; this build declares them
+The paper recovers placements by probing the loader; here they are declared
 (``describe_layout``) for the layouts its workloads use. A layout covers every
 rank of one side (all trainer ranks, or all rollout ranks).
 

@@ -7,7 +7,7 @@ distinct slices, one per replica, so the trainers together send one copy and
 no replica becomes a single-source bottleneck). Without rule 6 each rollout
 rank receives everything it needs from the trainers; with it, replicated
 rollout tensors are also split and completed by two exchange stages.
-The canonical choices below are this build's reading; the paper fixes none of
+The canonical choices below are the reading taken here; the paper fixes none of
 them:
 
 1. Trainer *groups*: placements of one checkpoint tensor with identical
