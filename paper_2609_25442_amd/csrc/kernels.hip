@@ -247,15 +247,15 @@ __device__ void run_transpose(const Task& t, const char* src, char* dst, uint32_
   }
 }
 
-// dst[c][r] = src[r][c] for 2-byte elements, 64 rows x (64..256) columns: each
-// wave takes one 64 x 64 tile (tile `w` of the item), each lane an 8 x 8
-// sub-tile that it loads as eight 16-byte rows, transposes in registers and
-// stores as eight 16-byte rows. Lanes 8i..8i+7 cover one 128-byte span of a
-// row on both sides.
+// dst[c][r] = src[r][c] for 2-byte elements, (64..256) rows x 64 columns: each
+// wave takes one 64 x 64 tile (tile `w` of the item, counted down the rows),
+// each lane an 8 x 8 sub-tile that it loads as eight 16-byte rows, transposes
+// in registers and stores as eight 16-byte rows. Lanes 8i..8i+7 cover one
+// 128-byte span of a row on both sides.
 __device__ void run_transpose16(const Task& t, const char* src, char* dst, uint32_t w) {
   const uint32_t l = threadIdx.x & 63;
-  if (w * 64 >= t.cols) return;
-  const uint32_t c0 = w * 64 + 8 * (l & 7), r0 = 8 * (l >> 3);
+  if (w * 64 >= t.rows) return;
+  const uint32_t c0 = 8 * (l & 7), r0 = w * 64 + 8 * (l >> 3);
   u32x4 a[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)

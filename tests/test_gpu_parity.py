@@ -87,11 +87,13 @@ def test_generator_matches_on_gpu():
             assert np.array_equal(bits, sc.values_numpy(t, np.arange(r * c), dt))
 
 
-@pytest.mark.parametrize("rows,cols,split", [(520, 200, 1), (640, 264, 2), (130, 77, 1), (1024, 512, 3)])
+@pytest.mark.parametrize("rows,cols,split", [(520, 200, 1), (640, 264, 2), (130, 77, 1), (1024, 512, 3), (384, 1100, 2)])
 def test_transposed_trainer_shards(rows, cols, split):
     """Trainer ranks hold column slabs of T stored transposed (row-parallel
     shards); the rollout wants T row-major in one tensor. Large aligned slabs
-    take the register-transpose path, ragged edges and odd widths the tiles."""
+    take the register-transpose path (items of up to 256 slab rows: 384 x 1100
+    in two slabs gives 550-row slabs, two full items and a ragged band per
+    64-column strip), ragged edges and odd widths the tiles."""
     cat = [CkptTensor("T", rows, cols)]
     cuts = [cols * k // split for k in range(split + 1)]
     ranks = []
