@@ -41,6 +41,11 @@ class CkptTensor:
     rows: int
     cols: int
 
+    def __post_init__(self):
+        # a checkpoint tensor holds at least one element (vectors are [1, n])
+        if self.rows < 1 or self.cols < 1:
+            raise ValueError(f"checkpoint tensor {self.name!r} needs a positive shape, got {self.rows} x {self.cols}")
+
     @property
     def numel(self) -> int:
         return self.rows * self.cols

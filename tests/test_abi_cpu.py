@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 
 import paper_2609_25442_amd as wb
-from oracle.layout import describe_layout, layout_from_spec
+from oracle.catalog import CkptTensor
+from oracle.layout import Layout, Local, Placement, RankLayout, describe_layout, layout_from_spec
 from oracle.plan import build_plan, dump, dump_layout
 from synthetic_checkpoint.workloads import ORDER, WORKLOADS, scaled
 
@@ -346,3 +347,30 @@ def test_overlapping_rollout_exchange_equals_oracle(G):
     want = dump(build_plan(tr, ro, node_size=G))
     for d in range(4):
         assert wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, d, node_size=G).dump() == want
+
+
+def test_degenerate_layouts_are_refused_by_both_sides():
+    """A zero-sized checkpoint tensor and a rollout rank needing elements no
+    trainer holds are errors for the library (WB_EINVAL) and for the oracle
+    (ValueError); a trainer rank that holds nothing gets an empty plan with an
+    empty grid."""
+    with pytest.raises(wb.WbError) as e:
+        wb.Layout.create([("Z", 0, 8), ("A", 4, 8)], 1)
+    assert e.value.code == wb.WB_EINVAL
+    with pytest.raises(ValueError):
+        CkptTensor("Z", 0, 8)
+    cat = [CkptTensor("A", 4, 4)]
+    tr = Layout(cat, [RankLayout([Local("a", "bf16", 1, 2, 4)], [Placement(0, 0, 2, 0, 4, 0, 0, 4)])])
+    ro = Layout(cat, [RankLayout([Local("a", "bf16", 1, 4, 4)], [Placement(0, 0, 4, 0, 4, 0, 0, 4)])])
+    _expect(wb.WB_EINVAL, wb.Plan, to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
+    with pytest.raises(ValueError):
+        build_plan(tr, ro)
+    cat = [CkptTensor("A", 1, 1)]
+    tr = Layout(cat, [RankLayout([Local("a", "bf16", 1, 1, 1)], [Placement(0, 0, 1, 0, 1, 0, 0, 1)]),
+                      RankLayout([], [])])
+    ro = Layout(cat, [RankLayout([Local("a", "bf16", 1, 1, 1)], [Placement(0, 0, 1, 0, 1, 0, 0, 1)])])
+    s1 = wb.Plan(to_wb(tr), to_wb(ro), wb.SENDER, 1)
+    assert s1.buffer_bytes == 0 and s1.work_counts() == (0, 0, 0) and s1.launch_grid(0)[:2] == (0, 0)
+    r0 = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
+    assert r0.work_counts()[0] == 1 and r0.traffic() == (2, 2)
+    assert build_plan(tr, ro).send_bytes[1] == 0

@@ -130,3 +130,44 @@ def test_fp8_paired_and_general_blocks():
     gx = p.launch_grid(1)[0]
     assert nb == 12 + 6 + 1 + 4 and gx == (19 + 1) // 2 + 4, (nb, gx)
     roundtrip(tr, ro, _values(cat, "bf16"), label="fp8-paths")
+
+
+def _tiny_catalog_layouts(tdtype, rdtype, block=0):
+    """[A 1 x 1, B 1 x 3, C 3 x 1, Z 2 x 2] held by two trainer ranks (B split
+    by columns, rank 1 holding none of A and Z), wanted whole by one rollout
+    rank in ``rdtype`` (fp8 with one block per tensor when ``block``)."""
+    cat = [CkptTensor("A", 1, 1), CkptTensor("B", 1, 3), CkptTensor("C", 3, 1), CkptTensor("Z", 2, 2)]
+    r0 = RankLayout([Local("a", tdtype, 1, 1, 1), Local("b0", tdtype, 1, 1, 2), Local("z", tdtype, 1, 2, 2)],
+                    [Placement(0, 0, 1, 0, 1, 0, 0, 1), Placement(1, 0, 1, 0, 2, 1, 0, 2),
+                     Placement(3, 0, 2, 0, 2, 2, 0, 2)])
+    r1 = RankLayout([Local("c", tdtype, 1, 3, 1), Local("b1", tdtype, 1, 1, 1)],
+                    [Placement(2, 0, 3, 0, 1, 0, 0, 1), Placement(1, 0, 1, 2, 3, 1, 0, 1)])
+    locs, pls = [], []
+    for t, c in enumerate(cat):
+        u = len(locs)
+        if block:
+            locs += [Local("q" + c.name, rdtype, 1, c.rows, c.cols, block, scale=u + 1),
+                     Local("s" + c.name, "f32", 1, 1, 1, scales=u)]
+        else:
+            locs.append(Local(c.name.lower(), rdtype, 1, c.rows, c.cols))
+        pls.append(Placement(t, 0, c.rows, 0, c.cols, u, 0, c.cols))
+    return cat, Layout(cat, [r0, r1]), Layout(cat, [RankLayout(locs, pls)])
+
+
+@pytest.mark.parametrize("tdtype,rdtype,block", [("bf16", "bf16", 0), ("f32", "bf16", 0), ("bf16", "f8e4m3", 128),
+                                                 ("f32", "f8e4m3", 128)])
+def test_single_elements_and_zero_blocks(tdtype, rdtype, block):
+    """Degenerate shapes through each cast path: 1 x 1, 1 x 3 and 3 x 1 tensors
+    and a 2 x 2 block of signed zeros. As fp8, every tensor is one partial
+    block: a one-element block quantises to +-448 exactly with s = |x| / 448,
+    and the all-zero block takes s = 1 and keeps each zero's sign."""
+    cat, tr, ro = _tiny_catalog_layouts(tdtype, rdtype, block)
+    base = _values(cat, tdtype)
+    neg0 = 0x80000000 if tdtype == "f32" else 0x8000
+
+    def values(t):
+        if cat[t].name != "Z":
+            return base(t)
+        return np.array([[0, neg0], [neg0, 0]], dtype=np.uint32 if tdtype == "f32" else np.uint16)
+
+    roundtrip(tr, ro, values, label=f"tiny-{tdtype}-{rdtype}")
