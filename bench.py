@@ -566,11 +566,19 @@ def main():
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
     fwd_ms = {}
+    spread = {}
     if nr == 1:
-        pack_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in events)
+        pack_steps = [e[0].elapsed_time(e[1]) for e in events]
+        unpack_steps = [e[-2].elapsed_time(e[-1]) for e in events]
+        pack_ms = statistics.mean(pack_steps)
         for st in fwds:
             fwd_ms[st] = statistics.mean(e[st].elapsed_time(e[1 + st]) for e in events)
-        unpack_ms = statistics.mean(e[-2].elapsed_time(e[-1]) for e in events)
+        unpack_ms = statistics.mean(unpack_steps)
+        # per-step spread of the two launches (the mean is what the line reports)
+        for name, xs in (("pack", pack_steps), ("unpack", unpack_steps)):
+            spread[name] = {"ms_min": round(min(xs), 4), "ms_median": round(statistics.median(xs), 4),
+                            "ms_max": round(max(xs), 4)}
+        log("unpack ms per step: " + " ".join(f"{x:.3f}" for x in unpack_steps))
     else:
         # per-kernel times of a round-based step: one more pass timing the
         # packs and the unpacks of all rounds separately
@@ -633,8 +641,10 @@ def main():
                    "rounds": nr, "round_budget": rb, "pipeline": bool(args.pipeline), "node_size": G},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "plan_ms": plan_ms,
-        "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes},
-        "unpack": {"ms": round(unpack_ms, 4), "GB/s": round(achieved, 1), "bytes": unpack_bytes},
+        "pack": {"ms": round(pack_ms, 4), "GB/s": round(pack_bytes / (pack_ms * 1e-3) / 1e9, 1), "bytes": pack_bytes,
+                 **spread.get("pack", {})},
+        "unpack": {"ms": round(unpack_ms, 4), "GB/s": round(achieved, 1), "bytes": unpack_bytes,
+                   **spread.get("unpack", {})},
         "device_copy": {"GB/s": round(2 * csrc.numel() / (copy_ms * 1e-3) / 1e9, 1), "bytes": 2 * csrc.numel(),
                         "what": "torch copy_ of (up to 16 GiB of) the receive buffer: hipMemcpy device to device"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
