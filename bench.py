@@ -409,7 +409,7 @@ def main():
         run_plan_stress()
         return
 
-    # the practical ceilings of this machine, measured before the benchmark
+    # the practical ceilings of this GPU, measured before the benchmark
     # allocates anything, for reading the roofline fraction against
     ceilings = None
     if not args.no_ceilings and not args.staged:
