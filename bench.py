@@ -435,11 +435,13 @@ def main():
     ro = wb.Layout.describe(w["model"], w["rollout"])
     plan_ms = {}
     for label, role, rank in (("unpack", wb.RECEIVER, d), ("pack", wb.SENDER, s0)):
+        # median of 20 plans (global plan plus rank view), fewer if they pass 3 s
         ts = []
-        for _ in range(5):
+        while len(ts) < 20 and (len(ts) < 3 or sum(ts) < 3000):
             t0 = time.perf_counter()
             p = wb.Plan(tr, ro, role, rank)
             ts.append((time.perf_counter() - t0) * 1e3)
+            del p
         plan_ms[label] = round(statistics.median(ts), 2)
     rb, G = args.round_budget, args.node_size
     rplan = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=rb, node_size=G)
