@@ -338,47 +338,65 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     }
   }
   if (nblocks == 0) return;
-  // pieces: count per block, prefix, fill (canonical segment order within a block)
+  // Blocks are built in id order (locals, then batch, block row, block column).
+  // A block filled whole by one aligned bf16 wire piece (QB_SINGLE) keeps that
+  // piece's address in its own descriptor, which is all the pair path reads,
+  // and takes no piece-table entry; the other blocks list their pieces (count
+  // per block, prefix, fill; canonical segment order within a block). Every
+  // piece adds to its block's covered area, so a block with a whole piece and
+  // any other one fails the exact-cover check.
+  P.qblocks.assign(nblocks, QBlock{});
   std::vector<uint32_t> count(nblocks + 1, 0);
-  auto for_blocks = [&](const Span& sp, auto&& fn) {
-    const Placement& q = R.pls[sp.g->dst_pl];
-    const Local& dl = R.locals[q.u];
-    const int64_t B = dl.block, nbr = (dl.rows + B - 1) / B, nbc = (dl.cols + B - 1) / B;
-    const int64_t Rr = sp.g->x.rows(), C = sp.g->x.cols();
-    for (int64_t bi = sp.row0 / B; bi <= (sp.row0 + Rr - 1) / B; ++bi)
-      for (int64_t bj = sp.col0 / B; bj <= (sp.col0 + C - 1) / B; ++bj)
-        fn(block_base[q.u] + (sp.e * nbr + bi) * nbc + bj, bi, bj, B);
-  };
-  for (const Span& sp : qspans) for_blocks(sp, [&](int64_t id, int64_t, int64_t, int64_t) { ++count[id + 1]; });
-  for (int64_t i = 0; i < nblocks; ++i) count[i + 1] += count[i];
-  P.qpieces.resize(count[nblocks]);
-  std::vector<uint32_t> fill(count.begin(), count.end() - 1);
   std::vector<int64_t> area(nblocks, 0);
   std::vector<int> block_round(nblocks, -1);
-  for (const Span& sp : qspans) {
+  auto for_pieces = [&](const Span& sp, auto&& fn) {
     const Segment& g = *sp.g;
+    const Placement& q = R.pls[g.dst_pl];
+    const Local& dl = R.locals[q.u];
     const int sdt = wire_dtype(trainer, P.segs, g), ss = dtype_bytes(sdt);
+    const int64_t B = dl.block, nbr = (dl.rows + B - 1) / B, nbc = (dl.cols + B - 1) / B;
     const int64_t Rr = g.x.rows(), C = g.x.cols();
-    for_blocks(sp, [&](int64_t id, int64_t bi, int64_t bj, int64_t B) {
-      const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
-      const int64_t b0 = std::max(sp.col0, bj * B), b1 = std::min(sp.col0 + C, (bj + 1) * B);
-      QPiece pc{};
-      pc.src_off = g.recv_off + uint64_t(((a0 - sp.row0) * C + (b0 - sp.col0)) * ss);
-      pc.src_ld = static_cast<uint32_t>(C);
-      pc.r0 = static_cast<uint8_t>(a0 - bi * B);
-      pc.r1m1 = static_cast<uint8_t>(a1 - bi * B - 1);
-      pc.c0 = static_cast<uint8_t>(b0 - bj * B);
-      pc.c1m1 = static_cast<uint8_t>(b1 - bj * B - 1);
-      pc.sdt = static_cast<uint8_t>(sdt);
-      P.qpieces[fill[id]++] = pc;
-      area[id] += (a1 - a0) * (b1 - b0);
-      if (block_round[id] >= 0 && block_round[id] != g.round) fail(WB_EINVAL, "internal: fp8 block spans rounds");
-      block_round[id] = g.round;
+    for (int64_t bi = sp.row0 / B; bi <= (sp.row0 + Rr - 1) / B; ++bi)
+      for (int64_t bj = sp.col0 / B; bj <= (sp.col0 + C - 1) / B; ++bj) {
+        const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
+        const int64_t b0 = std::max(sp.col0, bj * B), b1 = std::min(sp.col0 + C, (bj + 1) * B);
+        const int64_t rows = std::min(B, dl.rows - bi * B), cols = std::min(B, dl.cols - bj * B);
+        QPiece pc{};
+        pc.src_off = g.recv_off + uint64_t(((a0 - sp.row0) * C + (b0 - sp.col0)) * ss);
+        pc.src_ld = static_cast<uint32_t>(C);
+        pc.r0 = static_cast<uint8_t>(a0 - bi * B);
+        pc.r1m1 = static_cast<uint8_t>(a1 - bi * B - 1);
+        pc.c0 = static_cast<uint8_t>(b0 - bj * B);
+        pc.c1m1 = static_cast<uint8_t>(b1 - bj * B - 1);
+        pc.sdt = static_cast<uint8_t>(sdt);
+        const bool single = sdt == WB_BF16 && a0 == bi * B && b0 == bj * B && a1 - a0 == rows && b1 - b0 == cols &&
+                            cols % 8 == 0 && pc.src_off % 16 == 0 && (uint64_t(C) * 2) % 16 == 0;
+        fn(block_base[q.u] + (sp.e * nbr + bi) * nbc + bj, pc, single, (a1 - a0) * (b1 - b0));
+      }
+  };
+  for (const Span& sp : qspans)
+    for_pieces(sp, [&](int64_t id, const QPiece& pc, bool single, int64_t a) {
+      area[id] += a;
+      if (block_round[id] >= 0 && block_round[id] != sp.g->round) fail(WB_EINVAL, "internal: fp8 block spans rounds");
+      block_round[id] = sp.g->round;
+      if (single) {
+        QBlock& b = P.qblocks[id];
+        b.flags |= QB_SINGLE;
+        b.src_off = pc.src_off;
+        b.src_ld = pc.src_ld;
+      } else {
+        ++count[id + 1];
+      }
     });
+  for (int64_t i = 0; i < nblocks; ++i) count[i + 1] += count[i];
+  P.qpieces.resize(count[nblocks]);
+  {
+    std::vector<uint32_t> fill(count.begin(), count.end() - 1);
+    for (const Span& sp : qspans)
+      for_pieces(sp, [&](int64_t id, const QPiece& pc, bool single, int64_t) {
+        if (!single) P.qpieces[fill[id]++] = pc;
+      });
   }
-  // blocks are built in id order (locals, then batch, block row, block column)
-  P.qblocks.clear();
-  P.qblocks.reserve(nblocks);
   for (size_t u = 0; u < R.locals.size(); ++u) {
     const Local& l = R.locals[u];
     if (l.block <= 0) continue;
@@ -390,7 +408,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           const int64_t rows = std::min(B, l.rows - bi * B), cols = std::min(B, l.cols - bj * B);
           if (area[id] != rows * cols) fail(WB_EINVAL, "fp8 block of " + l.name + " is not exactly covered");
           if (count[id + 1] - count[id] > 65535) fail(WB_EUNSUPPORTED, "too many pieces in one fp8 block");
-          QBlock b{};
+          QBlock& b = P.qblocks[id];
           b.dst_off = uint64_t((e * l.rows + bi * B) * l.cols + bj * B);
           b.piece0 = count[id];
           b.npieces = static_cast<uint16_t>(count[id + 1] - count[id]);
@@ -400,21 +418,10 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           b.scale_idx = static_cast<uint16_t>(1 + l.scale);
           b.rows_m1 = static_cast<uint8_t>(rows - 1);
           b.cols_m1 = static_cast<uint8_t>(cols - 1);
-          b.flags = (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) ? QB_VEC_STORE : 0;
+          if (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) b.flags |= QB_VEC_STORE;
           bool bf16 = true;
           for (uint32_t i = count[id]; i < count[id + 1]; ++i) bf16 = bf16 && P.qpieces[i].sdt == WB_BF16;
           if (bf16) b.flags |= QB_BF16_SOURCE;
-          if (b.npieces == 1) {
-            const QPiece& q = P.qpieces[b.piece0];
-            if (bf16 && q.r0 == 0 && q.c0 == 0 && q.r1m1 == rows - 1 && q.c1m1 == cols - 1 && cols % 8 == 0 &&
-                q.src_off % 16 == 0 && (uint64_t(q.src_ld) * 2) % 16 == 0) {
-              b.flags |= QB_SINGLE;
-              b.src_off = q.src_off;
-              b.src_ld = q.src_ld;
-            }
-          }
-          if (static_cast<int64_t>(P.qblocks.size()) != id) fail(WB_EINVAL, "internal: fp8 block order");
-          P.qblocks.push_back(b);
         }
   }
   // group the blocks by round, canonical block order within a round (a
@@ -552,7 +559,7 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         fail(WB_EINVAL, "internal: misaligned single-piece fp8 block");
       inside(0, b.src_off, ((rows - 1) * b.src_ld + cols) * 2, "fp8 single-piece source");
     }
-    if (uint64_t(b.piece0) + b.npieces > P.qpieces.size() || b.npieces == 0)
+    if (uint64_t(b.piece0) + b.npieces > P.qpieces.size() || (b.npieces == 0) != ((b.flags & QB_SINGLE) != 0))
       fail(WB_EINVAL, "internal: fp8 block pieces out of range");
     for (uint32_t i = b.piece0; i < b.piece0 + b.npieces; ++i) {
       const QPiece& q = P.qpieces[i];

@@ -190,12 +190,13 @@ struct TaskSplit {
 
 // One fp8 destination block and the wire pieces that fill it. Blocks filled by
 // a single 16-byte aligned bf16 piece (QB_SINGLE) carry its source address
-// here, so the kernel needs no piece lookups for them.
+// here and have no piece-table entry, so the kernel needs no piece lookups
+// for them.
 struct QBlock {
   uint64_t dst_off;     // bytes from the fp8 tensor to the block origin
   uint64_t src_off;     // QB_SINGLE: bytes from recv_buf to the block's first element
   uint32_t src_ld;      // QB_SINGLE: wire row length in elements
-  uint32_t piece0;      // first piece
+  uint32_t piece0;      // first piece (npieces is 0 for QB_SINGLE blocks)
   uint32_t dst_ld;      // row stride of the fp8 matrix (elements = bytes)
   uint32_t scale_off;   // element index of the block's scale
   uint16_t npieces, dst_idx, scale_idx;
