@@ -655,8 +655,14 @@ def main():
     }
     if ceilings:
         # the one-shot stream with the dominant kernel's read/write mix: a same-
-        # dtype copy reads one byte per byte written, a cast assembly two
-        mix = "copy_oneshot_GBps" if ur < 1.5 * uw else "read2_write1_oneshot_GBps"
+        # dtype copy reads one byte per byte written, a cast assembly two (the
+        # faster of the two 2 : 1 shapes: one 16-byte store per lane, or two
+        # 8-byte halves one wave apart as the cast kernels store)
+        if ur < 1.5 * uw:
+            mix = "copy_oneshot_GBps"
+        else:
+            mix = max(("read2_write1_oneshot_GBps", "read2_write1_halves_oneshot_GBps"),
+                      key=lambda k: ceilings.get(k) or 0.0)
         out["stream_ceilings"] = dict(ceilings, matching=mix,
                                       frac_of_matching=round(achieved / ceilings[mix], 4) if ceilings.get(mix) else None)
     if fwds:

@@ -13,6 +13,7 @@
 #include <cstdio>
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #define CHECK(x)                                                                   \
   do {                                                                             \
@@ -70,6 +71,16 @@ __global__ void read2_write1_oneshot(const u32x4* __restrict__ s, u32x4* __restr
   __builtin_nontemporal_store(a ^ b, d + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x);
 }
 
+// the memory shape of the fp32 -> bf16 and fp8 assemblies: vectors 2 b T + l
+// and 2 b T + T + l in, an 8-byte half of each out at the same two positions
+// of an array of halves
+__global__ void read2_write1_halves_oneshot(const u32x4* __restrict__ s, u32x2* __restrict__ d) {
+  const uint64_t i = uint64_t(blockIdx.x) * 2 * blockDim.x + threadIdx.x;
+  const u32x4 a = __builtin_nontemporal_load(s + i), b = __builtin_nontemporal_load(s + i + blockDim.x);
+  __builtin_nontemporal_store(u32x2{a.x ^ a.z, a.y ^ a.w}, d + i);
+  __builtin_nontemporal_store(u32x2{b.x ^ b.z, b.y ^ b.w}, d + i + blockDim.x);
+}
+
 int main() {
   const uint64_t bytes = 8ull << 30, n = bytes / 16;
   const int read_grid = 512, write_grid = 16384, threads = 256;
@@ -83,8 +94,8 @@ int main() {
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
-  double gbs[6];
-  for (int which = 0; which < 6; ++which) {
+  double gbs[7];
+  for (int which = 0; which < 7; ++which) {
     float best = 1e30f;
     for (int r = 0; r < 6; ++r) {
       CHECK(hipEventRecord(e0));
@@ -94,18 +105,20 @@ int main() {
       if (which == 3) CHECK(hipMemcpyAsync(d, s, bytes, hipMemcpyDeviceToDevice, 0));
       if (which == 4) copy_oneshot<<<int(n / 64), 64>>>(s, d);
       if (which == 5) read2_write1_oneshot<<<int(n / 2 / 64), 64>>>(s, d);  // reads n vectors, writes n / 2
+      if (which == 6) read2_write1_halves_oneshot<<<int(n / 2 / 64), 64>>>(s, reinterpret_cast<u32x2*>(d));
       CHECK(hipEventRecord(e1));
       CHECK(hipEventSynchronize(e1));
       float ms;
       CHECK(hipEventElapsedTime(&ms, e0, e1));
       if (r > 0 && ms < best) best = ms;  // first run warms up
     }
-    const double moved = which == 5 ? 1.5 : which >= 2 ? 2.0 : 1.0;  // bytes read + written per buffer byte
+    const double moved = which >= 5 ? 1.5 : which >= 2 ? 2.0 : 1.0;  // bytes read + written per buffer byte
     gbs[which] = moved * double(bytes) / (best * 1e-3) / 1e9;
   }
   std::printf("{\"read_GBps\": %.1f, \"write_GBps\": %.1f, \"copy_GBps\": %.1f, \"hipMemcpy_GBps\": %.1f, "
-              "\"copy_oneshot_GBps\": %.1f, \"read2_write1_oneshot_GBps\": %.1f, \"bytes\": %llu}\n", gbs[0], gbs[1],
-              gbs[2], gbs[3], gbs[4], gbs[5], (unsigned long long)bytes);
+              "\"copy_oneshot_GBps\": %.1f, \"read2_write1_oneshot_GBps\": %.1f, "
+              "\"read2_write1_halves_oneshot_GBps\": %.1f, \"bytes\": %llu}\n",
+              gbs[0], gbs[1], gbs[2], gbs[3], gbs[4], gbs[5], gbs[6], (unsigned long long)bytes);
   CHECK(hipFree(s));
   CHECK(hipFree(d));
   CHECK(hipFree(out));

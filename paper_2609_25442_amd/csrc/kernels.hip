@@ -159,8 +159,21 @@ __device__ void run_f32_bf16(const Task& t, const char* src, char* dst, uint32_t
   const uint32_t total = t.rows * vpr;
   const uint32_t q0 = chunk * 2 * uint32_t(kThreads);
   if (q0 >= total) return;
-  const ChunkWalk<2> w(q0, min(total, q0 + 2 * uint32_t(kThreads)), vpr);
+  const uint32_t q1 = min(total, q0 + 2 * uint32_t(kThreads));
   f32x4 a[2];
+  if (t.rows == 1) {  // one run: unit q is input vector q and output half q
+    const f32x4* s = reinterpret_cast<const f32x4*>(src) + q0 + threadIdx.x;
+    u32x2* d = reinterpret_cast<u32x2*>(dst) + q0 + threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+      if (q0 + threadIdx.x + k * kThreads < q1) a[k] = ld(s + k * kThreads);
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+      if (q0 + threadIdx.x + k * kThreads < q1)
+        st(u32x2{pack_bf16x2(a[k].x, a[k].y), pack_bf16x2(a[k].z, a[k].w)}, d + k * kThreads);
+    return;
+  }
+  const ChunkWalk<2> w(q0, q1, vpr);
 #pragma unroll
   for (int k = 0; k < 2; ++k)
     if (w.on[k])
@@ -178,8 +191,24 @@ __device__ void run_bf16_f32(const Task& t, const char* src, char* dst, uint32_t
   const uint32_t vpr = t.cols >> 3;
   const uint32_t total = t.rows * vpr;
   if (q0 >= total) return;
-  const ChunkWalk<> w(q0, min(total, q0 + uint32_t(kChunkVecs)), vpr);
+  const uint32_t q1 = min(total, q0 + uint32_t(kChunkVecs));
   u32x4 v[kChunkPerLane];
+  if (t.rows == 1) {  // one run: input vector q becomes output vectors 2q and 2q + 1
+    const u32x4* s = reinterpret_cast<const u32x4*>(src) + q0 + threadIdx.x;
+    f32x4* d = reinterpret_cast<f32x4*>(dst) + 2 * (q0 + threadIdx.x);
+#pragma unroll
+    for (int k = 0; k < kChunkPerLane; ++k)
+      if (q0 + threadIdx.x + k * kThreads < q1) v[k] = ld(s + k * kThreads);
+#pragma unroll
+    for (int k = 0; k < kChunkPerLane; ++k)
+      if (q0 + threadIdx.x + k * kThreads < q1) {
+        const u32x4 x = v[k];
+        st(f32x4{bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y)}, d + 2 * k * kThreads);
+        st(f32x4{bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)}, d + 2 * k * kThreads + 1);
+      }
+    return;
+  }
+  const ChunkWalk<> w(q0, q1, vpr);
 #pragma unroll
   for (int k = 0; k < kChunkPerLane; ++k)
     if (w.on[k])
