@@ -374,3 +374,31 @@ def test_degenerate_layouts_are_refused_by_both_sides():
     r0 = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
     assert r0.work_counts()[0] == 1 and r0.traffic() == (2, 2)
     assert build_plan(tr, ro).send_bytes[1] == 0
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_work_item_size_changes_only_the_grid(name, monkeypatch):
+    """WB_TASK_BYTES only re-cuts the kernels' work: the canonical plan, the
+    buffer sizes and each launch's algorithmic bytes are the same for 1 KiB,
+    4 KiB, the default and 1 GiB items, and every grid has a workgroup for each
+    chunk of its longest item class (the planner's bounds proof runs on every
+    plan)."""
+    w = scaled(name)
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    seen = None
+    items = {}
+    for tb in ("1024", "4096", "", str(1 << 30)):
+        monkeypatch.setenv("WB_TASK_BYTES", tb)
+        rp = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"])
+        sp = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
+        items[tb] = rp.work_counts()[0]
+        facts = (rp.dump(), rp.buffer_bytes, sp.buffer_bytes, rp.kernel_traffic(0), rp.kernel_traffic(1),
+                 sp.kernel_traffic(0))
+        assert seen is None or facts == seen, (name, tb)
+        seen = facts
+        for p in (rp, sp):
+            x, y, _ = p.launch_grid(0)
+            n = p.work_counts()[0]
+            assert (x * y >= n) if n else (x, y) == (0, 0)
+    assert items["1024"] > items[""]  # the setting reached the planner

@@ -171,3 +171,20 @@ def test_single_elements_and_zero_blocks(tdtype, rdtype, block):
         return np.array([[0, neg0], [neg0, 0]], dtype=np.uint32 if tdtype == "f32" else np.uint16)
 
     roundtrip(tr, ro, values, label=f"tiny-{tdtype}-{rdtype}")
+
+
+@pytest.mark.parametrize("task_bytes", [1024, 4096, 1 << 30])
+@pytest.mark.parametrize("name", ORDER)
+def test_work_item_size_leaves_results_unchanged(name, task_bytes, monkeypatch):
+    """The planner cuts contiguous runs into work items of WB_TASK_BYTES
+    (default 256 KiB) and each launch maps workgroups to items by class shifts
+    fitted to its longest item. One-chunk items (1 KiB), ragged multi-chunk
+    items (4 KiB) and one item per run (1 GiB: the longest shifts and the most
+    idle workgroups) give the oracle's bytes on every scaled workload."""
+    monkeypatch.setenv("WB_TASK_BYTES", str(task_bytes))
+    w = scaled(name)
+    otr = layout_from_spec(w["model"], w["trainer"])
+    oro = layout_from_spec(w["model"], w["rollout"])
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    roundtrip(otr, oro, _values(otr.catalog, w["trainer"]["dtype"]), tr, ro, label=f"{name}/{task_bytes}")
