@@ -33,8 +33,21 @@ def random_model(rng) -> ModelShapes:
                        num_experts=int(rng.choice([2, 4, 8])), num_shared_experts=1)
 
 
-def random_par(rng, m: ModelShapes, side: str) -> Parallelism:
-    """A random parallelism valid for model m (trainer or rollout side)."""
+def random_medium_model(rng) -> ModelShapes:
+    """Like random_model, with shapes that span several 16-byte vectors,
+    64 x 64 transpose tiles and 128 x 128 fp8 blocks, and ragged tails."""
+    fam = ["dense", "mixtral", "moe_only"][int(rng.integers(0, 3))]
+    nkv = int(rng.choice([1, 2, 4]))
+    qpg = int(rng.choice([1, 2]))
+    return ModelShapes(fam, num_layers=int(rng.integers(1, 3)), hidden=int(rng.choice([128, 200, 256, 384])),
+                       num_heads=nkv * qpg, num_kv_heads=nkv, head_dim=int(rng.choice([32, 64])),
+                       ffn=int(rng.choice([256, 320, 512])), vocab=int(rng.choice([256, 500])),
+                       num_experts=int(rng.choice([2, 4])), num_shared_experts=1)
+
+
+def random_par(rng, m: ModelShapes, side: str, blocks=(4, 8)) -> Parallelism:
+    """A random parallelism valid for model m (trainer or rollout side); fp8
+    rollouts take a block edge from ``blocks``."""
     dtype = ["f32", "bf16"][int(rng.integers(0, 2))]
     while True:
         style = ["fsdp_flat", "megatron"][int(rng.integers(0, 2))] if side == "trainer" else "serving"
@@ -50,7 +63,7 @@ def random_par(rng, m: ModelShapes, side: str) -> Parallelism:
             else:
                 q = "f8e4m3" if rng.integers(0, 3) == 0 else ""
                 p = Parallelism(style, "bf16" if q else dtype, tp=tp, ep=ep, dp=dp, quant=q,
-                                quant_block=int(rng.choice([4, 8])))
+                                quant_block=int(rng.choice(list(blocks))))
             describe_layout(m, p)
             return p
         except ValueError:

@@ -15,7 +15,7 @@ from oracle.layout import Layout, Local, Placement, RankLayout, describe_layout,
 from synthetic_checkpoint.workloads import ORDER, scaled
 
 from gpu_util import roundtrip, say
-from oracle_cases import hand_replicated_pair, random_model, random_par
+from oracle_cases import hand_replicated_pair, random_medium_model, random_model, random_par
 from wb_cases import to_wb
 
 pytestmark = pytest.mark.gpu
@@ -50,6 +50,20 @@ def test_random_tiny_layout_parity(seed):
     oro = describe_layout(m, random_par(rng, m, "rollout"))
     dtype = otr.ranks[0].locals[0].dtype
     roundtrip(otr, oro, _values(otr.catalog, dtype), label=f"random{seed}")
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_medium_layout_parity(seed):
+    """Random models with hidden sizes of 128 to 384 under random trainer and
+    rollout parallelism: vector copies and casts, register-transposed slabs,
+    fp8 blocks of 64 and 128 (two-block and general paths), odd flat-shard
+    boundaries and ragged tails, each through every rank."""
+    rng = np.random.default_rng(2000 + seed)
+    m = random_medium_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout", blocks=(64, 128)))
+    dtype = otr.ranks[0].locals[0].dtype
+    roundtrip(otr, oro, _values(otr.catalog, dtype), label=f"random-medium{seed}")
 
 
 def test_hand_layout_with_transposed_destination():
