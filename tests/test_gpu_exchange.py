@@ -17,7 +17,7 @@ from oracle.transfer import pack as o_pack
 from synthetic_checkpoint.workloads import ORDER, scaled
 
 from gpu_util import FILL, codes_to_gpu, gpu_to_codes, say, workspace_for
-from oracle_cases import random_model, random_par
+from oracle_cases import random_medium_model, random_model, random_par
 from wb_cases import to_wb
 
 pytestmark = pytest.mark.gpu
@@ -141,6 +141,20 @@ def test_random_three_stage(seed):
     G = int(rng.integers(1, oro.nranks + 1))
     budget = int(rng.choice([0, 400]))
     three_stage(otr, oro, _values(otr), G, budget, label=f"random {seed} G={G} budget={budget}")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_medium_three_stage(seed):
+    """The same on random models with hidden sizes of 128 to 384 (vector work
+    items, transposed slabs, fp8 blocks of 64 and 128), in one round or in 1 MiB
+    rounds."""
+    rng = np.random.default_rng(2900 + seed)
+    m = random_medium_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout", blocks=(64, 128)))
+    G = int(rng.integers(1, oro.nranks + 1))
+    budget = int(rng.choice([0, 1 << 20]))
+    three_stage(otr, oro, _values(otr), G, budget, label=f"random-medium {seed} G={G} budget={budget}")
 
 
 def test_figure5_dp4_three_stage():
