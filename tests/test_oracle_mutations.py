@@ -120,6 +120,24 @@ def _wire_align_128(mine, ns, nd):
 _orig_wire = plan._wire
 
 
+def _quantize_flattened(lc, staged):
+    # blocks tiled over the flattened [batch * rows, cols] matrix (scales kept right)
+    x = staged.view(np.float32)
+    codes, _ = casts.quantize_matrix(x.reshape(lc.batch * lc.rows, lc.cols), lc.block)
+    scales = [casts.quantize_matrix(m, lc.block)[1] for m in x.reshape(lc.batch, lc.rows, lc.cols)]
+    return codes.ravel(), np.stack(scales).ravel().view(np.uint32)
+
+
+def _quantize_scales_transposed(lc, staged):
+    # each expert's scales written [bj][bi]
+    out_c, out_s = [], []
+    for m in staged.view(np.float32).reshape(lc.batch, lc.rows, lc.cols):
+        c, s = casts.quantize_matrix(m, lc.block)
+        out_c.append(c)
+        out_s.append(np.ascontiguousarray(s.T))
+    return np.stack(out_c).ravel(), np.concatenate([s.ravel() for s in out_s]).view(np.uint32)
+
+
 MUTANTS = {
     # casts
     "bf16 truncates": (casts, "f32_to_bf16", _truncating_bf16, [T_casts.test_hand_worked_rounding_cases]),
@@ -128,6 +146,12 @@ MUTANTS = {
     "fp8 divides by multiplying the reciprocal": (casts, "quantize_block", _quantize_by_reciprocal,
                                                   [T_casts.test_quantize_divides_rather_than_multiplying_by_the_reciprocal]),
     "fp8 ties round up": (casts, "f64_to_e4m3", _e4m3_ties_up, [T_casts.test_hand_worked_rounding_cases]),
+    "stacked fp8 tiled over the flattened experts": (transfer, "_quantize_local", _quantize_flattened,
+                                                      [lambda: T_transfer.test_stacked_fp8_blocks_tile_each_expert(
+                                                          272, 328, 128, "bf16")]),
+    "stacked fp8 scales written [e][bj][bi]": (transfer, "_quantize_local", _quantize_scales_transposed,
+                                               [lambda: T_transfer.test_stacked_fp8_blocks_tile_each_expert(
+                                                   130, 200, 64, "bf16")]),
     # placements
     "transposed placement read as plain": (transfer, "local_index", _ignores_transpose,
                                            [lambda: T_layout.test_layout_matches_torch_slicing(
