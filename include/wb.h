@@ -26,7 +26,10 @@
  *     released with the matching *_destroy call.
  *   - "stream" arguments are hipStream_t values passed as void* (NULL is the
  *     null stream). Device pointers must be device memory or pinned host memory
- *     addressable from the current HIP device, and 16-byte aligned.
+ *     addressable from the current HIP device, and 16-byte aligned. Calls that
+ *     launch work refuse (WB_EINVAL, before anything is enqueued) null and
+ *     misaligned pointers, pageable host memory and unknown addresses, and
+ *     device allocations smaller than the call needs.
  *   - The library never allocates device memory. It allocates host memory and,
  *     for the pointer tables of wb_pack/wb_unpack, a small pinned host buffer.
  */

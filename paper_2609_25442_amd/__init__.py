@@ -201,6 +201,33 @@ def _ptr(x) -> int:
     return x if isinstance(x, int) else x.data_ptr()
 
 
+# torch dtypes that hold each library dtype's codes (the value type, or an
+# integer view of the same width)
+_CODE_TYPES = {"f32": ("float32", "int32", "uint32"), "bf16": ("bfloat16", "int16", "uint16"),
+               "f8e4m3": ("float8_e4m3fn", "uint8", "int8")}
+
+
+def _einval(msg: str):
+    raise WbError(WB_EINVAL, msg)
+
+
+def _check_memory(x, what: str):
+    """A tensor handed to a kernel: contiguous, on the GPU or in pinned host
+    memory. Raw pointers (ints) are left to the library's own checks."""
+    if isinstance(x, int) or x is None:
+        return
+    if not x.is_contiguous():
+        _einval(f"{what} is not contiguous")
+    if not (x.is_cuda or x.is_pinned()):
+        _einval(f"{what} is neither device memory nor pinned host memory")
+
+
+def _check_buffer(x, nbytes: int, what: str):
+    _check_memory(x, what)
+    if not isinstance(x, int) and x is not None and x.numel() * x.element_size() < nbytes:
+        _einval(f"{what} is smaller than the plan needs ({x.numel() * x.element_size()} < {nbytes} bytes)")
+
+
 class Layout:
     """All ranks of one side: a checkpoint catalog and per-rank local tensors
     and placements."""
@@ -305,6 +332,7 @@ class Plan:
         _live.add(self)
         self.role, self.rank = role, rank
         self._workspace = None
+        self._locals = None
 
     def _i64(self, fn):
         v = c_int64()
@@ -351,11 +379,33 @@ class Plan:
         _check(lib.wb_plan_round_region(self._h, rnd, sender, receiver, byref(s), byref(r), byref(b)))
         return s.value, r.value, b.value
 
+    def _check_locals(self, xs, what: str):
+        """The pointer table of a pack or unpack: one tensor (or raw pointer)
+        per local tensor of the rank, each of the plan's dtype and size."""
+        if self._locals is None:
+            self._locals = [self.local_tensor(i) for i in range(self.num_local_tensors)]
+        if len(xs) != len(self._locals):
+            _einval(f"{what}: {len(xs)} tensors given, the plan's rank has {len(self._locals)} local tensors")
+        for i, (x, (dt, numel)) in enumerate(zip(xs, self._locals)):
+            if isinstance(x, int) or x is None:
+                continue
+            name = str(x.dtype).replace("torch.", "")
+            if name not in _CODE_TYPES[dt]:
+                _einval(f"{what} {i} has dtype {name}; the plan's local tensor is {dt}")
+            if x.numel() != numel:
+                _einval(f"{what} {i} has {x.numel()} elements: "
+                        f"{'smaller' if x.numel() < numel else 'larger'} than the plan's {numel}")
+            _check_memory(x, f"{what} {i}")
+
     def pack_round(self, rnd, src, send_buf, stream=None):
+        self._check_locals(src, "local tensor")
+        _check_buffer(send_buf, self.round_buffer_bytes(rnd), "send_buf")
         ptrs = (c_void_p * max(1, len(src)))(*[_ptr(x) for x in src])
         _check(lib.wb_pack_round(self._h, rnd, ptrs, _ptr(send_buf), _stream_handle(stream)))
 
     def unpack_round(self, rnd, recv_buf, dst, stream=None):
+        self._check_locals(dst, "local tensor")
+        _check_buffer(recv_buf, self.round_buffer_bytes(rnd), "recv_buf")
         ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
         _check(lib.wb_unpack_round(self._h, rnd, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
@@ -387,6 +437,8 @@ class Plan:
         return v.value
 
     def forward_round(self, rnd, stage, recv_buf, fwd_buf, stream=None):
+        _check_buffer(recv_buf, self.round_buffer_bytes(rnd), "recv_buf")
+        _check_buffer(fwd_buf, self.forward_bytes(stage, rnd), "fwd_buf")
         _check(lib.wb_forward_round(self._h, rnd, stage, _ptr(recv_buf), _ptr(fwd_buf) if fwd_buf is not None else 0,
                                     _stream_handle(stream)))
 
@@ -443,15 +495,20 @@ class Plan:
     def upload(self, workspace, stream=None):
         """Copy the work tables into ``workspace`` (a device tensor or pointer of
         at least ``workspace_bytes`` bytes); the plan keeps a reference to it."""
+        _check_memory(workspace, "workspace")
         nbytes = workspace.numel() * workspace.element_size() if hasattr(workspace, "numel") else self.workspace_bytes
         _check(lib.wb_plan_upload(self._h, _ptr(workspace), nbytes, _stream_handle(stream)))
         self._workspace = workspace
 
     def pack(self, src, send_buf, stream=None):
+        self._check_locals(src, "local tensor")
+        _check_buffer(send_buf, self.buffer_bytes, "send_buf")
         ptrs = (c_void_p * max(1, len(src)))(*[_ptr(x) for x in src])
         _check(lib.wb_pack(self._h, ptrs, _ptr(send_buf), _stream_handle(stream)))
 
     def unpack(self, recv_buf, dst, stream=None):
+        self._check_locals(dst, "local tensor")
+        _check_buffer(recv_buf, self.buffer_bytes, "recv_buf")
         ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
         _check(lib.wb_unpack(self._h, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 

@@ -46,13 +46,21 @@ int copy_text(const std::string& s, char* buf, size_t cap, size_t* needed) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Refuse a pointer whose device allocation is smaller than what the kernels
-// will touch. Memory the runtime cannot size (e.g. pinned host memory) is
-// accepted as given.
+// Refuse a pointer the GPU cannot address (pageable host memory, or an
+// address the runtime does not know) and one whose device allocation is
+// smaller than what the kernels will touch. Pinned host memory is accepted;
+// the runtime does not size it.
 int check_extent(const void* p, int64_t bytes, const char* what, int align = 16) {
   if (!p) return set_error(WB_EINVAL, std::string(what) + " is null");
   if (reinterpret_cast<uintptr_t>(p) % align != 0)
     return set_error(WB_EINVAL, std::string(what) + " is not " + std::to_string(align) + "-byte aligned");
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return set_error(WB_EINVAL, std::string(what) + " is not memory the GPU can address (device or pinned host)");
+  }
+  if (attr.type == hipMemoryTypeUnregistered)
+    return set_error(WB_EINVAL, std::string(what) + " is pageable host memory: the kernels need device or pinned host memory");
   hipDeviceptr_t base = nullptr;
   size_t size = 0;
   if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
@@ -721,7 +729,8 @@ int wb_diff2(const void* src, int32_t dtype, int64_t rows, int64_t cols, int64_t
     if (dtype != WB_F32 && dtype != WB_BF16) return set_error(WB_EINVAL, "diff2 needs an f32 or bf16 field");
     if (rows < 1 || cols < 1 || capacity < 0) return set_error(WB_EINVAL, "bad shape or capacity");
     if (!count || reinterpret_cast<uintptr_t>(count) % 8) return set_error(WB_EINVAL, "count must be 8-byte aligned");
-    int rc = check_extent(src, rows * cols * wb::dtype_bytes(dtype), "src", wb::dtype_bytes(dtype));
+    int rc = check_extent(count, 8, "count", 8);
+    if (rc == WB_OK) rc = check_extent(src, rows * cols * wb::dtype_bytes(dtype), "src", wb::dtype_bytes(dtype));
     if (rc == WB_OK && capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
     if (rc == WB_OK && capacity > 0) rc = check_extent(value, capacity * 4, "value", 4);
     if (rc != WB_OK) return rc;
@@ -797,8 +806,8 @@ int wb_diff2_batch(const wb_field* fields, int32_t n, void* workspace, size_t wo
   return guarded([&]() -> int {
     if (capacity < 0) return set_error(WB_EINVAL, "negative capacity");
     if (!count || reinterpret_cast<uintptr_t>(count) % 8) return set_error(WB_EINVAL, "count must be 8-byte aligned");
-    int rc = WB_OK;
-    if (capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
+    int rc = check_extent(count, 8, "count", 8);
+    if (rc == WB_OK && capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
     if (rc == WB_OK && capacity > 0) rc = check_extent(value, capacity * 8, "value", 8);
     if (rc != WB_OK) return rc;
     Diff2Tables T;

@@ -402,3 +402,38 @@ def test_work_item_size_changes_only_the_grid(name, monkeypatch):
             n = p.work_counts()[0]
             assert (x * y >= n) if n else (x, y) == (0, 0)
     assert items["1024"] > items[""]  # the setting reached the planner
+
+
+def test_binding_refuses_bad_tensors_before_the_library():
+    """The binding checks every tensor of a pack or unpack against the plan
+    (count, dtype, element count, contiguity, device or pinned memory) and the
+    buffers' size before anything reaches the library: all refused here on a
+    machine without a GPU, so nothing could have been launched."""
+    import torch
+
+    tr, ro = hand_replicated_pair()
+    T, R = to_wb(tr), to_wb(ro)
+    rp = wb.Plan(T, R, wb.RECEIVER, 1)
+    sp = wb.Plan(T, R, wb.SENDER, 0)
+    dst = [torch.empty(12, dtype=torch.bfloat16), torch.empty(5, dtype=torch.bfloat16)]
+    recv = torch.empty(rp.buffer_bytes, dtype=torch.uint8)
+
+    def refused(fn, *a, word):
+        with pytest.raises(wb.WbError) as e:
+            fn(*a)
+        assert e.value.code == wb.WB_EINVAL and word in str(e.value), str(e.value)
+
+    refused(rp.unpack, recv, dst[:1], word="2 local tensors")
+    refused(rp.unpack, recv, dst, word="pinned")                                   # pageable host tensors
+    refused(rp.unpack, recv, [dst[0].float(), dst[1]], word="dtype float32")
+    refused(rp.unpack, recv, [torch.empty(11, dtype=torch.bfloat16), dst[1]], word="smaller")
+    refused(rp.unpack, recv, [torch.empty(13, dtype=torch.int16), dst[1]], word="larger")
+    refused(rp.unpack, recv, [torch.empty(6, 4, dtype=torch.bfloat16)[:, ::2], dst[1]], word="contiguous")
+    refused(rp.unpack_round, 0, recv, dst[:1], word="2 local tensors")
+    # raw pointers pass to the library, which refuses the unuploaded plan
+    refused(rp.unpack, 0, [0, 0], 0, word="uploaded")
+    src = [torch.empty(24, dtype=torch.float32), torch.empty(10, dtype=torch.float32)]
+    refused(sp.pack, src, torch.empty(sp.buffer_bytes, dtype=torch.uint8), word="pinned")
+    refused(sp.pack, [0, 0], torch.empty(sp.buffer_bytes - 1, dtype=torch.uint8), word="pinned")
+    refused(sp.pack_round, 0, [0, 0, 0], 0, word="2 local tensors")
+    refused(sp.upload, torch.empty(sp.workspace_bytes, dtype=torch.uint8), word="pinned")

@@ -73,7 +73,10 @@ def test_unpack_buffer_checks(plans):
 def test_pack_buffer_checks(plans):
     tr, ro, rp, sp = plans
     ws = workspace_for(sp)
-    _expect_einval(sp.pack, [0] * sp.num_local_tensors, torch.empty(16, dtype=torch.uint8, device="cuda"))  # not uploaded
+    # not uploaded (through the C ABI: the binding would refuse the small buffer first)
+    ptrs = (wb.c_void_p * sp.num_local_tensors)()
+    buf = torch.empty(16, dtype=torch.uint8, device="cuda")
+    assert "uploaded" in _expect_einval(lambda: wb._check(wb.lib.wb_pack(sp._h, ptrs, buf.data_ptr(), None)))
     sp.upload(ws)
     src = wb.allocate_locals(tr, 0)
     send = torch.empty(sp.buffer_bytes + 64, dtype=torch.uint8, device="cuda")
@@ -122,3 +125,48 @@ def test_forward_and_probe_checks():
     bad = wb._field_array([([x.data_ptr() + 1, x.data_ptr()], "bf16", 16, 64)])
     assert "aligned" in _expect_einval(batch, ws.data_ptr(), need, v64.data_ptr(), cnt.data_ptr(), bad)
     torch.cuda.synchronize()
+
+
+def _hip_pointer_type(ptr: int):
+    """The HIP runtime's own classification of an address (hipPointerGetAttributes:
+    None on an error, else the hipMemoryType; 0 is unregistered host memory)."""
+    import ctypes
+
+    class Attr(ctypes.Structure):
+        _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int), ("devicePointer", ctypes.c_void_p),
+                    ("hostPointer", ctypes.c_void_p), ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    a = Attr()
+    rc = hip.hipPointerGetAttributes(ctypes.byref(a), ctypes.c_void_p(ptr))
+    if rc != 0:
+        hip.hipGetLastError()
+        return None
+    return a.type
+
+
+def test_pageable_host_memory_refused(plans):
+    """Pageable host memory given as raw pointers is refused on the host before
+    any launch. The runtime must classify it as the library's check expects
+    (an error or type 0) before the library is handed it."""
+    tr, ro, rp, sp = plans
+    host = torch.empty(1 << 20, dtype=torch.uint8)            # pageable
+    pinned = torch.empty(1 << 20, dtype=torch.uint8, pin_memory=True)
+    assert _hip_pointer_type(pinned.data_ptr()) == 1            # hipMemoryTypeHost
+    kind = _hip_pointer_type(host.data_ptr())
+    if kind not in (None, 0):
+        pytest.skip(f"runtime reports pageable memory as type {kind}")
+    msg = _expect_einval(lambda: wb._check(wb.lib.wb_make_ids(host.data_ptr(), wb.DTYPES["bf16"], 100, 1 << 24, 0, 16,
+                                                              None)))
+    assert "pageable" in msg or "address" in msg
+    ws = workspace_for(rp)
+    rp.upload(ws)
+    dst = wb.allocate_locals(ro, 0)
+    ptrs = (wb.c_void_p * len(dst))(*[t.data_ptr() for t in dst])
+    msg = _expect_einval(lambda: wb._check(wb.lib.wb_unpack(rp._h, host.data_ptr(), ptrs, None)))
+    assert "recv_buf" in msg and ("pageable" in msg or "address" in msg)
+    # the binding refuses pageable tensors itself
+    assert "pinned" in _expect_einval(rp.unpack, host, dst)
+    del dst
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
