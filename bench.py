@@ -2,18 +2,21 @@
 
 One step = pack of one trainer rank's shards (wb_pack) followed by the
 assembly of one rollout rank's tensors (wb_unpack), on synthetic seeded
-parameters already resident in HBM, for the Llama-3-8B-shaped workload
-(trainer FSDP=8 flat bf16 shards -> rollout TP=1 bf16 with fused qkv and
-gate_up; pack trainer rank 0, unpack the full rollout replica from the eight
-senders' regions). Other workloads: --workload NAME.
+parameters already resident in HBM. The headline workload is the largest
+one that fits one GPU, Mixtral-8x7B-shaped (trainer EP=8 x FSDP=2 flat fp32
+shards -> rollout EP=2 bf16 with stacked experts; pack trainer rank 0,
+unpack rollout rank 0 from the sixteen senders' regions: 169 GB per step).
+Other workloads: --workload NAME.
 
 Prints one JSON line: effective GB/s of the step (algorithmic bytes: each
 element read once in the source dtype and written once in the destination
 dtype, plus fp8 scales), the HBM roofline of the dominant kernel from HIP
 events on the launch stream, wb_plan time, this GPU's stream ceilings
 (measured first, in a child process) with the dominant kernel's fraction of the
-one-shot stream of its read/write mix, and the CPU oracle timed on a bounded
-sample of the same workload.
+one-shot stream of its read/write mix, the CPU oracle timed on bounded
+samples of the same workload (unpack and pack), and ``per_config``: every
+workload timed in the same run (fewer steps each), its pack and unpack rates,
+roofline fraction and plan time.
 """
 
 from __future__ import annotations
@@ -30,7 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
-DEFAULT_WORKLOAD = "llama3_8b_fsdp8_to_tp1"
+DEFAULT_WORKLOAD = "mixtral_ep8fsdp2_to_ep2"
 
 
 def log(*a):
@@ -70,30 +73,44 @@ def work_fingerprint(workload):
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload, kernel):
+def stored_traffic(workload, kernel, why=None):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source."""
+    taken on the current kernel source (else None, with the reason appended to
+    the list ``why`` when given)."""
     path = os.path.join(ROOT, "profiles", f"traffic-{workload}.txt")
     if not os.path.exists(path):
+        if why is not None:
+            why.append(f"no profiles/traffic-{workload}.txt")
         return None
     rec = json.load(open(path))
-    if rec.get("work_fingerprint") != work_fingerprint(workload) or kernel not in rec.get("kernels", {}):
+    fp = work_fingerprint(workload)
+    if rec.get("work_fingerprint") != fp or kernel not in rec.get("kernels", {}):
+        if why is not None:
+            why.append(f"{kernel}: stored fingerprint {rec.get('work_fingerprint')} != current {fp}"
+                       if rec.get("work_fingerprint") != fp else f"{kernel}: not in the stored counters")
         return None
     return rec["kernels"][kernel]["hbm_bytes_per_launch"]
 
 
-def cpu_baseline(w, recv_host_fn, budget_s=15.0, max_tensor_bytes=256 << 20, wall_cap_s=90.0):
-    """The oracle as it stands, on a time-bounded sample of the workload: its
-    planner, then its element-by-element unpack of the receiver's tensors, one
-    destination tensor at a time in layout order (every segment that feeds
-    the tensor, then its blockwise quantisation when it is fp8), until the
-    unpack calls have taken ``budget_s`` seconds (or ``wall_cap_s`` of wall
-    time have passed). Tensors above ``max_tensor_bytes`` (embeddings and
-    output heads) are left out of the sample: the oracle's index arrays for
-    them take gigabytes. Each segment's wire bytes are copied back to back into
-    one reused, pre-touched host buffer by ``recv_host_fn(offset, nbytes, out)``
+def cpu_baseline(w, recv_host_fn, src_host_fn, unpack_budget_s=12.0, pack_budget_s=8.0,
+                 max_tensor_bytes=256 << 20, wall_cap_s=90.0):
+    """The oracle as it stands, on time-bounded samples of the workload: its
+    planner, its element-by-element unpack of the receiver's tensors and its
+    pack of the sender's segments.
+
+    Unpack: one destination tensor at a time in layout order (every segment
+    that feeds it, then its blockwise quantisation when it is fp8) until the
+    unpack calls have taken ``unpack_budget_s`` seconds (or ``wall_cap_s`` of
+    wall time have passed). Tensors above ``max_tensor_bytes`` (embeddings and
+    output heads) are left out: the oracle's index arrays for them take
+    gigabytes. Each segment's wire bytes are copied back to back into one
+    reused, pre-touched host buffer by ``recv_host_fn(offset, nbytes, out)``
     (the segments re-based onto it), so the rate counts the oracle and not
-    first-touch page faults."""
+    first-touch page faults.
+
+    Pack: the sender's segments in send-buffer order, one oracle pack call
+    per segment (re-based to offset 0), until ``pack_budget_s``; the local
+    tensors they read are fetched once by ``src_host_fn(u)`` (not timed)."""
     import dataclasses
 
     import numpy as np
@@ -101,6 +118,7 @@ def cpu_baseline(w, recv_host_fn, budget_s=15.0, max_tensor_bytes=256 << 20, wal
     from oracle.layout import DTYPE_BYTES, Layout
     from oracle.layout import layout_from_spec
     from oracle.plan import build_plan
+    from oracle.transfer import pack as o_pack
     from oracle.transfer import unpack as o_unpack
 
     t0 = time.perf_counter()
@@ -148,13 +166,47 @@ def cpu_baseline(w, recv_host_fn, budget_s=15.0, max_tensor_bytes=256 << 20, wal
         n_t += 1
         n_seg += len(segs)
         log(f"[cpu_baseline] {lc.name}: {n_t} tensors, {done_bytes / 1e9:.2f} GB in {spent:.1f} s")
-        if spent >= budget_s or time.perf_counter() - wall0 >= wall_cap_s:
+        if spent >= unpack_budget_s or time.perf_counter() - wall0 >= wall_cap_s:
             break
-    return {"value": round(done_bytes / spent / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    del buf
+    # pack: the sender's segments in send order
+    s0 = w["pack_rank"]
+    mine = sorted((g for g in oplan.segments if g.s == s0 and g.stage == 0), key=lambda g: g.send_off)
+    trk = otr.ranks[s0]
+    host = [np.zeros(0, dtype=np.uint8)] * len(trk.locals)
+    p_bytes, p_spent, p_seg, fetched = 0, 0.0, 0, set()
+    wall1 = time.perf_counter()
+    for g in mine:
+        u = trk.placements[g.src_pl].u
+        if u not in fetched:
+            host = list(host)
+            host[u] = src_host_fn(u)
+            fetched.add(u)
+        sub = dataclasses.replace(oplan, segments=[dataclasses.replace(g, send_off=0)], rounds=None,
+                                  send_bytes=[g.nbytes if r == s0 else 0 for r in range(otr.nranks)])
+        t1 = time.perf_counter()
+        o_pack(sub, s0, host)
+        p_spent += time.perf_counter() - t1
+        p_bytes += 2 * g.nbytes
+        p_seg += 1
+        if p_spent >= pack_budget_s or time.perf_counter() - wall1 >= wall_cap_s:
+            break
+    log(f"[cpu_baseline] pack: {p_seg} segments, {p_bytes / 1e9:.2f} GB in {p_spent:.1f} s")
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = None
+    total = done_bytes + p_bytes
+    return {"value": round(total / (spent + p_spent) / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"oracle unpack of the first {n_t} rollout tensors of rank {d} of at most "
                       f"{max_tensor_bytes >> 20} MiB ({skipped} larger ones left out; {n_seg} segments, "
-                      f"{done_bytes / 1e9:.2f} GB read+written) in {spent:.1f} s, single-threaded numpy; "
-                      f"oracle plan {plan_ms:.0f} ms",
+                      f"{done_bytes / 1e9:.2f} GB read+written in {spent:.1f} s) and oracle pack of the first "
+                      f"{p_seg} of trainer rank {s0}'s {len(mine)} segments ({p_bytes / 1e9:.2f} GB read+written "
+                      f"in {p_spent:.1f} s), single-threaded numpy; oracle plan {plan_ms:.0f} ms",
+            "unpack": {"GB/s": round(done_bytes / spent / 1e9, 4), "bytes": done_bytes, "s": round(spent, 2)},
+            "pack": {"GB/s": round(p_bytes / p_spent / 1e9, 4) if p_spent else None, "bytes": p_bytes,
+                     "s": round(p_spent, 2)},
+            "host_cpu_count": os.cpu_count(), "host_affinity_cpus": affinity,
             "plan_ms": round(plan_ms, 1)}
 
 
@@ -356,77 +408,17 @@ def run_probe(args):
     print(json.dumps(out), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-ceilings", action="store_true",
-                    help="skip measuring this GPU's stream ceilings before the benchmark")
-    ap.add_argument("--round-budget", type=int, default=0,
-                    help="bytes per rank per round (0: one round); each step packs and unpacks every round")
-    ap.add_argument("--node-size", type=int, default=0,
-                    help="rollout ranks per node: plan with rollout de-duplication and the two exchange stages; "
-                         "each step also runs the unpack rank's forward packings")
-    ap.add_argument("--pipeline", action="store_true",
-                    help="with rounds: pack round k+1 on one stream while round k is assembled on another")
-    ap.add_argument("--plan-stress", action="store_true",
-                    help="wb_plan time on a 58-MoE-layer DeepSeek-V3-like catalog (44,776 tensors, EP64 -> EP8 fp8)")
-    ap.add_argument("--probe", action="store_true",
-                    help="discover the trainer and rollout ranks' layouts by probing torch loaders (diff2 kernels)")
-    ap.add_argument("--staged", action="store_true",
-                    help="send and receive buffers in pinned host memory (PCIe-bound; not the headline value)")
-    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="print HBM traffic per launch from two rocprofv3 --pmc runs of this benchmark")
-    ap.add_argument("--ceilings", action="store_true",
-                    help="print this GPU's read, write and copy stream ceilings (paper_2609_25442_amd/wb_ceilings)")
-    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
-                    help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
-    args = ap.parse_args()
-    if args.summarize_counters:
-        print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
-        return
-    if args.ceilings:
-        r = run_ceilings()
-        sys.stderr.write(r.stderr)
-        print(r.stdout.strip())
-        sys.exit(r.returncode)
-    if args.summarize_trace:
-        print(json.dumps(summarize_trace(args.workload, args.summarize_trace), indent=1))
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the resharding hot path here runs on a single MI355X "
-              "(pack of one trainer rank, unpack of one rollout rank); --gpus above 1 is not supported.",
-              file=sys.stderr)
-        sys.exit(2)
-
-    if args.probe:
-        run_probe(args)
-        return
-    if args.plan_stress:
-        run_plan_stress()
-        return
-
-    # the practical ceilings of this GPU, measured before the benchmark
-    # allocates anything, for reading the roofline fraction against
-    ceilings = None
-    if not args.no_ceilings and not args.staged:
-        r = run_ceilings()
-        if r.returncode == 0:
-            ceilings = json.loads(r.stdout.strip().splitlines()[-1])
-            ceilings.pop("bytes", None)
-        else:
-            log(f"[bench] stream ceilings failed ({r.returncode}): {r.stderr.strip()[-300:]}")
-
+def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
+    """Build one workload's inputs in HBM, time ``steps`` steps after
+    ``warmup``, and return its JSON record (with the CPU oracle's samples
+    when ``with_cpu``). Frees the workload's device memory before returning."""
     import torch
 
     import paper_2609_25442_amd as wb
     import synthetic_checkpoint as sc
     from synthetic_checkpoint.workloads import WORKLOADS
 
-    w = WORKLOADS[args.workload]
+    w = WORKLOADS[name]
     src_dtype = w["trainer"]["dtype"]
     s0, d = w["pack_rank"], w["unpack_rank"]
     torch.cuda.set_device(0)
@@ -451,7 +443,7 @@ def main():
     sws = torch.empty(splan.workspace_bytes, dtype=torch.uint8, device="cuda")
     rplan.upload(rws)
     splan.upload(sws)
-    log(f"[bench] {args.workload}: plan ms {plan_ms}; recv {rplan.buffer_bytes / 1e9:.2f} GB")
+    log(f"[bench] {name}: plan ms {plan_ms}; recv {rplan.buffer_bytes / 1e9:.2f} GB")
 
     # inputs: every sender's region for the receiver, through real packs. With
     # rounds, each round has its receive buffer (what the network delivers) and
@@ -556,17 +548,17 @@ def main():
                 rplan.forward_round(k, st, recvs[k], fwds[st], stream)
             rplan.unpack_round(k, recvs[k], dst, stream)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 + len(fwds))] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 + len(fwds))] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
+    ms_per_step = elapsed * 1e3 / steps
     fwd_ms = {}
     spread = {}
     if nr == 1:
@@ -620,7 +612,8 @@ def main():
         dom = "wb::wb_tasks_kernel (unpack)"
     achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
     # HBM bytes of the launches the roofline times (both launches of an fp8 unpack)
-    parts = [stored_traffic(args.workload, k) for k in (("unpack", "unpack_fp8") if n_blocks and n_tasks else
+    why = []
+    parts = [stored_traffic(name, k, why) for k in (("unpack", "unpack_fp8") if n_blocks and n_tasks else
                                                         ("unpack_fp8",) if n_blocks else ("unpack",))]
     traffic = sum(parts) if all(x is not None for x in parts) and not G and nr == 1 and not args.staged else None
     out = {
@@ -628,8 +621,8 @@ def main():
         "value": round(value, 1),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -637,7 +630,7 @@ def main():
         "dtype": src_dtype if src_dtype == w["rollout"]["dtype"] and not w["rollout"].get("quant")
         else f"{src_dtype}->{w['rollout'].get('quant') or w['rollout']['dtype']}",
         "data": "synthetic",
-        "config": {"workload": args.workload, "trainer": w["trainer"], "rollout": w["rollout"],
+        "config": {"workload": name, "trainer": w["trainer"], "rollout": w["rollout"],
                    "pack_rank": s0, "unpack_rank": d, "bytes_per_step": pack_bytes + unpack_bytes,
                    "buffers": "pinned host (PCIe)" if args.staged else "device",
                    "rounds": nr, "round_budget": rb, "pipeline": bool(args.pipeline), "node_size": G},
@@ -651,7 +644,12 @@ def main():
                         "what": "torch copy_ of (up to 16 GiB of) the receive buffer: hipMemcpy device to device"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic,
+                     "traffic_source": (f"stored: profiles/traffic-{name}.txt, two rocprofv3 --pmc runs (FETCH_SIZE, "
+                                        "then WRITE_SIZE) of this benchmark scaled by a device copy of known size; "
+                                        "used only while the kernels' source and the plans' launch grids match its "
+                                        "fingerprint") if traffic is not None else
+                     ("; ".join(why) or "not the one-round device-buffer step the counters were taken on")},
     }
     if ceilings:
         # the one-shot stream with the dominant kernel's read/write mix: a same-
@@ -670,12 +668,123 @@ def main():
                                          "GB/s": round(fwd_bytes[st] / (fwd_ms[st] * 1e-3) / 1e9, 1)
                                          if fwd_ms.get(st) else None} for st in fwds}
         out["config"]["bytes_per_step"] = pack_bytes + sum(fwd_bytes.values()) + unpack_bytes
-    if not args.no_cpu_baseline and nr == 1 and not G:
+    if with_cpu and nr == 1 and not G:
+        import numpy as np
+
         def recv_host(off, nb, out):
             torch.from_numpy(out[:nb]).copy_(recv[off:off + nb])
-        out["cpu_baseline"] = cpu_baseline(w, recv_host)
-    print(json.dumps(out), flush=True)
 
+        def src_host(u):
+            x = src0[u].reshape(-1)
+            return x.view(torch.int32 if x.element_size() == 4 else torch.int16).cpu().numpy().view(
+                np.uint32 if x.element_size() == 4 else np.uint16)
+
+        out["cpu_baseline"] = cpu_baseline(w, recv_host, src_host)
+    # free the workload's device memory before the next one
+    locs = buf = p = ws = None
+    del recvs, sends, recv, send0, fwds, src0, dst, rws, sws, rplan, splan, csrc
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+
+def per_config_entry(rec):
+    """The part of a workload's record that the headline line repeats for
+    every workload."""
+    ent = {"value_GBps": rec["value"], "pct_of_hbm_peak": rec["pct_of_hbm_peak"], "ms_per_step": rec["ms_per_step"],
+           "steps": rec["steps"], "dtype": rec["dtype"], "bytes_per_step": rec["config"]["bytes_per_step"],
+           "pack": {k: rec["pack"][k] for k in ("ms", "GB/s", "bytes")},
+           "unpack": {k: rec["unpack"][k] for k in ("ms", "GB/s", "bytes")},
+           "roofline_kernel": rec["roofline"]["kernel"], "roofline_frac": rec["roofline"]["frac"],
+           "pack_frac": round(rec["pack"]["GB/s"] / HBM_PEAK_GBS, 4),
+           "plan_ms": rec["plan_ms"], "stored_traffic_applies": rec["roofline"]["traffic"] is not None,
+           "traffic": rec["roofline"]["traffic"]}
+    sc = rec.get("stream_ceilings")
+    if sc:
+        ent["frac_of_matching_ceiling"] = sc.get("frac_of_matching")
+    return ent
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="time only --workload (by default every workload is timed after it, fewer steps each)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip measuring this GPU's stream ceilings before the benchmark")
+    ap.add_argument("--round-budget", type=int, default=0,
+                    help="bytes per rank per round (0: one round); each step packs and unpacks every round")
+    ap.add_argument("--node-size", type=int, default=0,
+                    help="rollout ranks per node: plan with rollout de-duplication and the two exchange stages; "
+                         "each step also runs the unpack rank's forward packings")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="with rounds: pack round k+1 on one stream while round k is assembled on another")
+    ap.add_argument("--plan-stress", action="store_true",
+                    help="wb_plan time on a 58-MoE-layer DeepSeek-V3-like catalog (44,776 tensors, EP64 -> EP8 fp8)")
+    ap.add_argument("--probe", action="store_true",
+                    help="discover the trainer and rollout ranks' layouts by probing torch loaders (diff2 kernels)")
+    ap.add_argument("--staged", action="store_true",
+                    help="send and receive buffers in pinned host memory (PCIe-bound; not the headline value)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print HBM traffic per launch from two rocprofv3 --pmc runs of this benchmark")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="print this GPU's read, write and copy stream ceilings (paper_2609_25442_amd/wb_ceilings)")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
+    args = ap.parse_args()
+    if args.summarize_counters:
+        print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
+        return
+    if args.ceilings:
+        r = run_ceilings()
+        sys.stderr.write(r.stderr)
+        print(r.stdout.strip())
+        sys.exit(r.returncode)
+    if args.summarize_trace:
+        print(json.dumps(summarize_trace(args.workload, args.summarize_trace), indent=1))
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the resharding hot path here runs on a single MI355X "
+              "(pack of one trainer rank, unpack of one rollout rank); --gpus above 1 is not supported.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    if args.probe:
+        run_probe(args)
+        return
+    if args.plan_stress:
+        run_plan_stress()
+        return
+
+    # the practical ceilings of this GPU, measured before the benchmark
+    # allocates anything, for reading the roofline fraction against
+    ceilings = None
+    if not args.no_ceilings and not args.staged:
+        r = run_ceilings()
+        if r.returncode == 0:
+            ceilings = json.loads(r.stdout.strip().splitlines()[-1])
+            ceilings.pop("bytes", None)
+        else:
+            log(f"[bench] stream ceilings failed ({r.returncode}): {r.stderr.strip()[-300:]}")
+
+    out = run_workload(args, args.workload, args.steps, args.warmup, ceilings, with_cpu=not args.no_cpu_baseline)
+    plain = not (args.round_budget or args.node_size or args.pipeline or args.staged)
+    if plain and not args.no_per_config:
+        # every workload in the same run: its pack and unpack rates and roofline
+        from synthetic_checkpoint.workloads import ORDER
+
+        per = {}
+        for other in ORDER:
+            rec = out if other == args.workload else run_workload(args, other, min(args.steps, 10), 2, ceilings)
+            per[other] = per_config_entry(rec)
+            log(f"[bench] {other}: {per[other]['value_GBps']} GB/s, unpack frac {per[other]['roofline_frac']}")
+        out["per_config"] = per
+    print(json.dumps(out), flush=True)
 
 if __name__ == "__main__":
     main()
