@@ -31,7 +31,9 @@
  *     misaligned pointers, pageable host memory and unknown addresses, and
  *     device allocations smaller than the call needs.
  *   - The library never allocates device memory. It allocates host memory and,
- *     for the pointer tables of wb_pack/wb_unpack, a small pinned host buffer.
+ *     for the pointer tables of wb_pack/wb_unpack, a small pinned host buffer;
+ *     wb_unpack_round_noalloc uses a fixed device array the library's code
+ *     object holds on each GPU.
  */
 #ifndef WB_H
 #define WB_H
@@ -292,6 +294,20 @@ int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void
  * wb_pack / wb_unpack refuse (WB_EINVAL) plans with more than one round. */
 int wb_pack_round(wb_plan_t* plan, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream);
 int wb_unpack_round(wb_plan_t* plan, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream);
+
+/* For callers that cannot allocate memory (code under stream capture, tight
+ * serving loops, harnesses that forbid allocation): wb_unpack_round with no
+ * caller workspace and no wb_plan_upload. The call stages the round's work
+ * tables and the dst_ptrs table in a device array that the library holds on
+ * each GPU it runs on until the process ends (32 MiB per GPU), then enqueues
+ * the kernels of wb_unpack_round on stream; it allocates nothing. Every call
+ * on a GPU shares that GPU's array and overwrites it: calls on one stream are
+ * ordered, calls that overlap in time on one GPU (other streams, threads or
+ * plans) race. The plan's host tables are the source of the staging copies:
+ * keep the plan alive until the call's work has run.
+ * Errors: WB_ESIZE (checked first) when the round's tables exceed the array
+ * (plan with a smaller round budget); otherwise as wb_unpack_round, WB_EHIP. */
+int wb_unpack_round_noalloc(wb_plan_t* plan, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream);
 
 /* ---- three-stage plans: rollout-side de-duplication and exchange ------ */
 

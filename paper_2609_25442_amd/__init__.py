@@ -99,6 +99,7 @@ def _load():
         "wb_plan_round_region": [P, c_int32, c_int32, c_int32, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
         "wb_pack_round": [P, c_int32, POINTER(c_void_p), c_void_p, c_void_p],
         "wb_unpack_round": [P, c_int32, c_void_p, POINTER(c_void_p), c_void_p],
+        "wb_unpack_round_noalloc": [P, c_int32, c_void_p, POINTER(c_void_p), c_void_p],
         "wb_plan_num_segments": [P, POINTER(c_int64)],
         "wb_plan_buffer_bytes": [P, POINTER(c_int64)],
         "wb_plan_num_peers": [P, POINTER(c_int32)],
@@ -408,6 +409,15 @@ class Plan:
         _check_buffer(recv_buf, self.round_buffer_bytes(rnd), "recv_buf")
         ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
         _check(lib.wb_unpack_round(self._h, rnd, _ptr(recv_buf), ptrs, _stream_handle(stream)))
+
+    def unpack_round_noalloc(self, rnd, recv_buf, dst, stream=None):
+        """unpack_round without a workspace or upload: the library stages the
+        round's tables in its own per-GPU device array (calls that overlap on
+        one GPU race; a round whose tables exceed the array raises WB_ESIZE)."""
+        self._check_locals(dst, "local tensor")
+        _check_buffer(recv_buf, self.round_buffer_bytes(rnd), "recv_buf")
+        ptrs = (c_void_p * max(1, len(dst)))(*[_ptr(x) for x in dst])
+        _check(lib.wb_unpack_round_noalloc(self._h, rnd, _ptr(recv_buf), ptrs, _stream_handle(stream)))
 
     @property
     def node_size(self) -> int:

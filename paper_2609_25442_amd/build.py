@@ -19,7 +19,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 HOST_SOURCES = ["api.cpp", "layout.cpp", "plan.cpp", "probe.cpp"]
 CEILINGS = os.path.join(HERE, "wb_ceilings")   # stream-bandwidth probe used by bench.py --ceilings
-DEVICE_SOURCES = ["kernels.hip", "probe.hip"]
+DEVICE_SOURCES = ["kernels.hip", "probe.hip", "noalloc.hip"]
 # no packed fp32 instructions: hipcc would otherwise form v_pk_*_f32 by itself
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

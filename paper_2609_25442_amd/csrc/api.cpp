@@ -625,6 +625,61 @@ int wb_forward_round(wb_plan_t* P, int32_t round, int32_t stage, const void* rec
   });
 }
 
+int wb_unpack_round_noalloc(wb_plan_t* P, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream) {
+  return guarded([&]() -> int {
+    if (!P) return set_error(WB_EINVAL, "null plan");
+    if (P->role != WB_RECEIVER) return set_error(WB_EINVAL, "unpacking needs a receiver plan");
+    if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
+    // the round's tables in the scratch array: [pointer table | tasks | blocks | pieces]
+    const uint32_t t0 = P->round_tasks[round], t1 = P->round_tasks[round + 1];
+    const uint32_t b0 = P->round_qblocks[round], b1 = P->round_qblocks[round + 1];
+    const uint32_t q0 = P->round_qpieces[2 * round], q1 = P->round_qpieces[2 * round + 1];
+    const size_t off_tasks = align256(sizeof(uint64_t) * (P->n_locals + 1));
+    const size_t off_blocks = align256(off_tasks + sizeof(wb::Task) * (t1 - t0));
+    const size_t off_pieces = align256(off_blocks + sizeof(wb::QBlock) * (b1 - b0));
+    const size_t need = off_pieces + sizeof(wb::QPiece) * (q1 - q0);
+    void* base = nullptr;
+    size_t cap = 0;
+    hipError_t e = static_cast<hipError_t>(wb::scratch_address(&base, &cap));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (scratch array)");
+    if (need > cap)
+      return set_error(WB_ESIZE, "the round's work tables need " + std::to_string(need) + " bytes; the library's scratch "
+                                 "array holds " + std::to_string(cap) + ": plan with a smaller round budget");
+    if (!dst_ptrs && P->n_locals > 0) return set_error(WB_EINVAL, "local tensor pointer array is null");
+    const wb::Rank& R = rank_of(P);
+    int rc = check_extent(recv_buf, rank_bytes(P, round, P->role, P->rank), "recv_buf");
+    for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
+      rc = check_extent(dst_ptrs[i], local_bytes(R.locals[i]), "local tensor");
+    if (rc != WB_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    auto* ws = static_cast<uint8_t*>(base);
+    e = static_cast<hipError_t>(
+        wb::launch_store_table(reinterpret_cast<uint64_t*>(ws), const_cast<const void* const*>(dst_ptrs), P->n_locals, stream));
+    if (e != hipSuccess) return hip_fail(e, "pointer table launch");
+    if (t1 > t0 && (e = hipMemcpyAsync(ws + off_tasks, P->tasks.data() + t0, sizeof(wb::Task) * (t1 - t0),
+                                       hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (tasks)");
+    if (b1 > b0 && (e = hipMemcpyAsync(ws + off_blocks, P->qblocks.data() + b0, sizeof(wb::QBlock) * (b1 - b0),
+                                       hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (fp8 blocks)");
+    if (q1 > q0 && (e = hipMemcpyAsync(ws + off_pieces, P->qpieces.data() + q0, sizeof(wb::QPiece) * (q1 - q0),
+                                       hipMemcpyHostToDevice, st)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (fp8 pieces)");
+    const auto* table = reinterpret_cast<const uint64_t*>(ws);
+    int k = wb::launch_tasks(reinterpret_cast<const wb::Task*>(ws + off_tasks), t1 - t0, P->round_split[round], table,
+                             recv_buf, nullptr, stream);
+    if (k != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(k));
+    // blocks address pieces by their index in the whole table: the staged range
+    // starts at piece q0
+    const auto* pieces =
+        reinterpret_cast<const wb::QPiece*>(reinterpret_cast<uintptr_t>(ws + off_pieces) - sizeof(wb::QPiece) * q0);
+    k = wb::launch_qblocks(reinterpret_cast<const wb::QBlock*>(ws + off_blocks), b1 - b0, P->round_qsingle[round], pieces,
+                           table, recv_buf, stream);
+    if (k != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(k));
+    return WB_OK;
+  });
+}
+
 int wb_pack(wb_plan_t* P, const void* const* src_ptrs, void* send_buf, void* stream) {
   return guarded([&]() -> int {
     if (!P) return set_error(WB_EINVAL, "null plan");

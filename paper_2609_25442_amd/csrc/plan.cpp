@@ -241,6 +241,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   P.round_tasks.assign(nrounds + 1, 0);
   P.round_qblocks.assign(nrounds + 1, 0);
   P.round_qsingle.assign(nrounds, 0);
+  P.round_qpieces.assign(2 * size_t(nrounds), 0);  // every plan: ranks without fp8 blocks keep empty ranges
   if (P.role == WB_SENDER) {
     const Rank& R = trainer.ranks[P.rank];
     P.n_locals = static_cast<int>(R.locals.size());
@@ -445,6 +446,18 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
     const auto mid = std::stable_partition(first, last, [](const QBlock& b) { return (b.flags & QB_SINGLE) != 0; });
     P.round_qsingle[k] = static_cast<uint32_t>(mid - first);
   }
+  // the range of the piece table each round's blocks read
+  for (int k = 0; k < nrounds; ++k) {
+    uint32_t lo = UINT32_MAX, hi = 0;
+    for (uint32_t i = P.round_qblocks[k]; i < P.round_qblocks[k + 1]; ++i) {
+      const QBlock& b = P.qblocks[i];
+      if (b.npieces == 0) continue;
+      lo = std::min(lo, b.piece0);
+      hi = std::max(hi, b.piece0 + b.npieces);
+    }
+    P.round_qpieces[2 * k] = hi ? lo : 0;
+    P.round_qpieces[2 * k + 1] = hi;
+  }
 }
 
 // Every byte a work item touches lies inside its buffer, and vector work items
@@ -544,6 +557,9 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   }
   if (P.round_qsingle.size() != nr || P.round_qsingle[k] > P.round_qblocks[k + 1] - P.round_qblocks[k])
     fail(WB_EINVAL, "internal: single-piece fp8 block count");
+  if (P.round_qpieces.size() != 2 * nr || P.round_qpieces[2 * k] > P.round_qpieces[2 * k + 1] ||
+      P.round_qpieces[2 * k + 1] > P.qpieces.size())
+    fail(WB_EINVAL, "internal: fp8 piece range of a round");
   for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
     const QBlock& b = P.qblocks[bi];
     if (((b.flags & QB_SINGLE) != 0) != (bi < P.round_qblocks[k] + P.round_qsingle[k]))
@@ -561,6 +577,8 @@ void check_work(const wb_plan_t& P, const Rank& R) {
     }
     if (uint64_t(b.piece0) + b.npieces > P.qpieces.size() || (b.npieces == 0) != ((b.flags & QB_SINGLE) != 0))
       fail(WB_EINVAL, "internal: fp8 block pieces out of range");
+    if (b.npieces && (b.piece0 < P.round_qpieces[2 * k] || b.piece0 + b.npieces > P.round_qpieces[2 * k + 1]))
+      fail(WB_EINVAL, "internal: fp8 block pieces outside its round's piece range");
     for (uint32_t i = b.piece0; i < b.piece0 + b.npieces; ++i) {
       const QPiece& q = P.qpieces[i];
       if (q.r1m1 < q.r0 || q.c1m1 < q.c0 || q.r1m1 >= rows || q.c1m1 >= cols)

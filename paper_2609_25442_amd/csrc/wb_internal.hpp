@@ -283,6 +283,7 @@ struct wb_plan_t {
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
   std::vector<uint32_t> round_qsingle;  // [k]: QB_SINGLE blocks at the start of round k's block range
+  std::vector<uint32_t> round_qpieces;  // [2k], [2k + 1]: the piece-table range round k's blocks read
   std::vector<uint32_t> round_fwd[2];   // forward work of exchange stage 1 + i, round k: [k] .. [k + 1]
   int64_t fwd_bytes[2] = {0, 0};        // bytes this rank forwards in each exchange stage (all rounds)
   // copies of the two layouts used for dumps and queries
@@ -317,6 +318,12 @@ int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint6
 int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
                    const void* buf, void* stream);
 const char* hip_error_string(int err);
+// noalloc.hip: the library's per-GPU scratch array for allocation-free calls
+// (its address on the current device, found once per device, and its size)
+int scratch_address(void** out, size_t* bytes);
+// dev[0] = 0, dev[1 + i] = ptrs[i] for i < n, written by kernels whose
+// arguments carry the pointers (no host buffer outlives the call)
+int launch_store_table(uint64_t* dev, const void* const* ptrs, int n, void* stream);
 // probe.cpp
 void probe_init(wb_probe_t& P, const wb_tensor_desc* catalog, int n, int ckpt_dtype);
 void probe_record(wb_probe_t& P, int local, int chunk, const int64_t* index, const int64_t* value, int64_t n);

@@ -437,3 +437,24 @@ def test_binding_refuses_bad_tensors_before_the_library():
     refused(sp.pack, [0, 0], torch.empty(sp.buffer_bytes - 1, dtype=torch.uint8), word="pinned")
     refused(sp.pack_round, 0, [0, 0, 0], 0, word="2 local tensors")
     refused(sp.upload, torch.empty(sp.workspace_bytes, dtype=torch.uint8), word="pinned")
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_noalloc_entry_reads_only_planned_tables(name):
+    """wb_unpack_round_noalloc reads the round's table ranges before anything
+    else; on a machine without a GPU it must then stop at the device lookup
+    with an error, for plans with and without fp8 blocks and in every round
+    (a plan without fp8 blocks once had no piece ranges, and the call read
+    past an empty table)."""
+    w = scaled(name)
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    for budget in (0, 4096):
+        p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=budget)
+        ptrs = (wb.c_void_p * max(1, p.num_local_tensors))()
+        for k in range(p.num_rounds):
+            rc = wb.lib.wb_unpack_round_noalloc(p._h, k, None, ptrs, None)
+            assert rc == wb.WB_EHIP, (rc, wb.lib.wb_last_error())
+        assert wb.lib.wb_unpack_round_noalloc(p._h, p.num_rounds, None, ptrs, None) == wb.WB_EINVAL
+    s = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
+    assert wb.lib.wb_unpack_round_noalloc(s._h, 0, None, ptrs, None) == wb.WB_EINVAL
