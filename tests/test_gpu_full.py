@@ -10,9 +10,20 @@ packed for real and its region copied into the receive buffer; then:
   checkpoint slice built with torch on the GPU (torch's fp32 -> bf16 cast; for
   fp8 tensors torch's blockwise amax / 448, x / s, E4M3FN formula), so no
   element is left unwritten;
+* unpack output against the oracle, every element of every tensor that is
+  not fp8: the oracle's placement formula (local_index) evaluated on index
+  tensors on the GPU gives each element's position, and its value is the
+  checkpoint element (copies) or the oracle's fp32 -> bf16 rounding, which is
+  elementwise and so is evaluated once per distinct fp32 value of the tensor;
+* fp8 tensors against the oracle: every expert matrix of every layer
+  (routed w13 and w2, the shared expert's) staged through the oracle's
+  placement formula and quantised by the oracle's quantize_matrix in a pool
+  of host processes, codes and scales compared in full;
 * sampled elements and whole fp8 blocks are computed one by one by the CPU
-  oracle from the seeded generator and compared.
+  oracle from the numpy generator and compared.
 """
+
+import os
 
 import numpy as np
 import pytest
@@ -100,6 +111,112 @@ def _check_unpack_full(oro, d, dst, cat, src_dtype):
         q, s = _torch_quant(st, lc)
         assert torch.equal(dst[u].view(-1).view(torch.uint8), q.view(-1).view(torch.uint8)), f"{lc.name} codes"
         assert torch.equal(dst[lc.scale].view(-1).view(torch.int32), s.reshape(-1).view(torch.int32)), f"{lc.name} scales"
+
+
+class _OracleCast:
+    """The oracle's elementwise cast applied to GPU tensors of codes: each
+    distinct code is cast once by the oracle on the host, and the results are
+    kept (sorted by code) and gathered back on the GPU."""
+
+    def __init__(self, src, dst, device="cuda"):
+        if (src, dst) == ("f32", "bf16"):
+            self.fn = casts.f32_to_bf16
+        elif (src, dst) == ("bf16", "f32"):
+            self.fn = casts.bf16_to_f32
+        else:
+            raise ValueError(f"no cast {src} -> {dst}")
+        self.src, self.dst = src, dst
+        self.keys = torch.empty(0, dtype=SIGNED[src][1], device=device)
+        self.vals = torch.empty(0, dtype=SIGNED[dst][1], device=device)
+
+    def __call__(self, codes):
+        uniq = torch.unique(codes.reshape(-1))
+        new = uniq[~torch.isin(uniq, self.keys)]
+        if new.numel():
+            out = self.fn(new.cpu().numpy().view(CODE_DTYPE[self.src]))
+            out = torch.from_numpy(np.ascontiguousarray(out).view(SIGNED[self.dst][0])).to(self.keys.device)
+            keys = torch.cat([self.keys, new])
+            order = torch.argsort(keys)
+            self.keys, self.vals = keys[order], torch.cat([self.vals, out])[order]
+        return self.vals[torch.searchsorted(self.keys, codes.reshape(-1))].view(codes.shape)
+
+
+def _oracle_index(p, device="cuda"):
+    """Flat local positions of a placement's rectangle by the oracle's formula,
+    evaluated on GPU index tensors."""
+    i = torch.arange(p.r0, p.r1, dtype=torch.int64, device=device)[:, None]
+    j = torch.arange(p.c0, p.c1, dtype=torch.int64, device=device)[None, :]
+    return local_index(p, i, j)
+
+
+def _check_unpack_oracle(oro, d, dst, cat, src_dtype, device="cuda"):
+    """Every element of every non-fp8 rollout tensor against the oracle (the
+    placements cover each tensor exactly, so this is every element)."""
+    rk = oro.ranks[d]
+    by_t = {}
+    for p in rk.placements:
+        if not rk.locals[p.u].block:
+            by_t.setdefault(p.t, []).append(p)
+    n = 0
+    cast = {}
+    for t, pls in sorted(by_t.items()):
+        T = sc.values_torch(t, cat[t].rows, cat[t].cols, src_dtype, device=device).view(cat[t].rows, cat[t].cols)
+        T = T.view(SIGNED[src_dtype][1])
+        for p in pls:
+            lc = rk.locals[p.u]
+            want = T[p.r0:p.r1, p.c0:p.c1].contiguous()
+            if lc.dtype != src_dtype:
+                want = cast.setdefault(lc.dtype, _OracleCast(src_dtype, lc.dtype, device))(want)
+            got = dst[p.u].reshape(-1).view(SIGNED[lc.dtype][1])[_oracle_index(p, device)]
+            if not torch.equal(got, want):
+                bad = torch.nonzero(got != want)[:5].tolist()
+                raise AssertionError(f"{lc.name}: placement of tensor {t} rows {p.r0}:{p.r1} cols {p.c0}:{p.c1}: "
+                                     f"first mismatches at {bad}")
+            n += p.numel
+        del T
+    return n
+
+
+def _check_fp8_oracle(oro, d, dst, cat, src_dtype, prefixes, workers, device="cuda"):
+    """Every fp8 tensor whose name starts with one of ``prefixes`` (one layer
+    each, taken in turn to bound host memory) against the oracle: each batch
+    matrix staged in fp32 through the oracle's placement formula, quantised by
+    casts.quantize_matrix in host processes, codes and scales compared in
+    full. Returns the number of matrices compared."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+
+    rk = oro.ranks[d]
+    done = 0
+    with cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as pool:
+        for prefix in prefixes:
+            futs = []
+            for u, lc in enumerate(rk.locals):
+                if not lc.block or not lc.name.startswith(prefix):
+                    continue
+                staged = torch.zeros(lc.numel, dtype=torch.float32, device=device)
+                for p in rk.placements:
+                    if p.u == u:
+                        x = sc.values_torch(p.t, cat[p.t].rows, cat[p.t].cols, src_dtype, device=device,
+                                            start=p.r0 * cat[p.t].cols, count=(p.r1 - p.r0) * cat[p.t].cols)
+                        staged[_oracle_index(p, device)] = x.view(p.r1 - p.r0, cat[p.t].cols)[:, p.c0:p.c1].float()
+                staged = staged.view(lc.batch, lc.rows, lc.cols)
+                for e in range(lc.batch):
+                    futs.append((u, e, pool.submit(casts.quantize_matrix, staged[e].cpu().numpy(), lc.block)))
+                del staged
+            assert futs, f"no fp8 tensors under {prefix}"
+            for u, e, f in futs:
+                codes, scales = f.result()
+                lc = rk.locals[u]
+                got = dst[u][e] if lc.batch > 1 else dst[u]
+                got = got.reshape(-1).view(torch.uint8).cpu().numpy()
+                assert np.array_equal(got, codes.ravel()), f"{lc.name}[{e}] codes differ from the oracle"
+                sl = dst[lc.scale][e] if lc.batch > 1 else dst[lc.scale]
+                assert np.array_equal(sl.reshape(-1).view(torch.int32).cpu().numpy(),
+                                      np.ascontiguousarray(scales).ravel().view(np.int32)), f"{lc.name}[{e}] scales"
+            done += len(futs)
+            say(f"  {prefix}: {len(futs)} fp8 matrices equal the oracle's")
+    return done
 
 
 def _oracle_value(t, i, j, cat, src_dtype):
@@ -201,6 +318,15 @@ def test_full_size_workload(name):
     torch.cuda.synchronize()
     say(f"[{name}] full check against torch")
     _check_unpack_full(oro, d, dst, cat, src_dtype)
+    say(f"[{name}] every non-fp8 element against the oracle")
+    n = _check_unpack_oracle(oro, d, dst, cat, src_dtype)
+    say(f"[{name}] {n} elements equal the oracle's")
+    if any(lc.block for lc in oro.ranks[d].locals):
+        workers = max(1, min(15, (os.cpu_count() or 2) - 1))
+        nl = w["model"]["num_layers"]
+        say(f"[{name}] fp8 tensors of all {nl} layers against the oracle ({workers} host processes)")
+        m = _check_fp8_oracle(oro, d, dst, cat, src_dtype, [f"layers.{k}." for k in range(nl)], workers)
+        say(f"[{name}] {m} fp8 matrices equal the oracle's")
     say(f"[{name}] sampled check against the oracle")
     _check_unpack_sampled(oro, d, dst, cat, src_dtype, np.random.default_rng(11))
     del recv, dst
