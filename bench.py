@@ -603,18 +603,17 @@ def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
     copy_ms = c0.elapsed_time(c1) / 3
     del scratch
 
-    n_tasks, n_blocks, _ = rplan.work_counts()
-    if n_blocks and n_tasks:
-        dom = "wb::wb_qblock_kernel + wb::wb_tasks_kernel (one wb_unpack, timed together)"
-    elif n_blocks:
-        dom = "wb::wb_qblock_kernel (unpack)"
-    else:
-        dom = "wb::wb_tasks_kernel (unpack)"
+    # the launches of one wb_unpack, all timed together: the copy/cast kernel
+    # and the fp8 block kernels that have work
+    launches = [(k, lab, kern) for k, lab, kern in
+                ((0, "unpack", "wb::wb_tasks_kernel"), (1, "unpack_fp8", "wb::wb_qblock_kernel"))
+                if rplan.launch_grid(k)[0]]
+    dom = " + ".join(kern for _, _, kern in launches) + (
+        " (one wb_unpack, timed together)" if len(launches) > 1 else " (unpack)")
     achieved = unpack_bytes / (unpack_ms * 1e-3) / 1e9
-    # HBM bytes of the launches the roofline times (both launches of an fp8 unpack)
+    # HBM bytes of the launches the roofline times (every launch of the unpack)
     why = []
-    parts = [stored_traffic(name, k, why) for k in (("unpack", "unpack_fp8") if n_blocks and n_tasks else
-                                                        ("unpack_fp8",) if n_blocks else ("unpack",))]
+    parts = [stored_traffic(name, lab, why) for _, lab, _ in launches]
     traffic = sum(parts) if all(x is not None for x in parts) and not G and nr == 1 and not args.staged else None
     out = {
         "metric": "pack+unpack effective GB/s per GPU (% of HBM peak); wb_plan ms",

@@ -255,9 +255,10 @@ int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, 
  * 1 the fp8 block kernel, 2 and 3 the forward packings of exchange stages 1
  * and 2. A copy/cast work item takes several workgroups (one per chunk of its
  * vectors), so the copy grid is a multiple of the work-item count; the fp8
- * grid has one workgroup per block. The grid is 0 x 0 for a launch that
- * enqueues nothing. WB_EINVAL for a null argument, a launch outside 0..3 or a
- * round out of range. */
+ * grid has one workgroup per pair of pairable blocks (single-piece blocks and
+ * blocks of full-width row bands) and one per other block. The grid is 0 x 0
+ * for a launch that enqueues nothing. WB_EINVAL for a null argument, a launch
+ * outside 0..3 or a round out of range. */
 int wb_plan_launch_grid(const wb_plan_t* plan, int32_t launch, int32_t round, uint32_t* grid_x, uint32_t* grid_y,
                         uint32_t* threads);
 /* Canonical text form of the global plan (one line per segment). */

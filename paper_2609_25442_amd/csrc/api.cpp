@@ -497,7 +497,7 @@ int wb_plan_launch_grid(const wb_plan_t* P, int32_t launch, int32_t round, uint3
   *threads = launch == 1 ? wb::kQBlockThreads : wb::kChunkThreads;
   if (launch == 1) {
     const uint32_t n = P->round_qblocks[round + 1] - P->round_qblocks[round];
-    if (n) *gx = wb::qblock_workgroups(n, P->round_qsingle[round]), *gy = 1;
+    if (n) *gx = wb::qblock_workgroups(n, P->round_qfull[round], P->round_qsingle[round]), *gy = 1;
     return WB_OK;
   }
   const std::vector<uint32_t>& r = launch == 0 ? P->round_tasks : P->round_fwd[launch - 2];
@@ -584,7 +584,7 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
   if (e != 0) return set_error(WB_EHIP, std::string("copy launch: ") + wb::hip_error_string(e));
   const auto* blocks = reinterpret_cast<const wb::QBlock*>(P->ws + P->off_qblocks);
   e = wb::launch_qblocks(blocks + P->round_qblocks[round], P->round_qblocks[round + 1] - P->round_qblocks[round],
-                         P->round_qsingle[round], reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table,
+                         P->round_qfull[round], P->round_qsingle[round], reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table,
                          buf, stream);
   if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
   return WB_OK;
@@ -673,7 +673,8 @@ int wb_unpack_round_noalloc(wb_plan_t* P, int32_t round, const void* recv_buf, v
     // starts at piece q0
     const auto* pieces =
         reinterpret_cast<const wb::QPiece*>(reinterpret_cast<uintptr_t>(ws + off_pieces) - sizeof(wb::QPiece) * q0);
-    k = wb::launch_qblocks(reinterpret_cast<const wb::QBlock*>(ws + off_blocks), b1 - b0, P->round_qsingle[round], pieces,
+    k = wb::launch_qblocks(reinterpret_cast<const wb::QBlock*>(ws + off_blocks), b1 - b0, P->round_qfull[round],
+                           P->round_qsingle[round], pieces,
                            table, recv_buf, stream);
     if (k != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(k));
     return WB_OK;

@@ -43,8 +43,12 @@ namespace {
 #ifndef WB_TASK_DYN_LDS
 #define WB_TASK_DYN_LDS 0
 #endif
+// The fp8 block kernel reserves enough dynamic LDS to hold two workgroups per
+// CU (two waves per SIMD): more resident workgroups, each gathering 128 rows
+// at once, were slower (measured) and the cap leaves the kernel the registers
+// of every block class without costing occupancy.
 #ifndef WB_QBLOCK_DYN_LDS
-#define WB_QBLOCK_DYN_LDS 0
+#define WB_QBLOCK_DYN_LDS 65536
 #endif
 
 constexpr int kThreads = kChunkThreads;
@@ -472,21 +476,49 @@ struct PairLane {
   bool vec;
 };
 
-// Blocks i0 and i0 + 1 (absent when i0 + 1 == nsingle), both QB_SINGLE. In
+// Blocks i0 and i0 + 1 (absent when i0 + 1 == nsingle), both pairable. In
 // each half-wave, lanes 0..15 take block i0 and lanes 16..31 block i0 + 1, so a
 // load instruction reads 512 contiguous bytes of each of two rows when the two
 // blocks are neighbours on the wire; thread t holds columns 8 (t mod 16) .. + 7
 // of rows t / 32 + 8 k, k < 16, as raw bf16. kFull: both blocks present,
 // 128 x 128 and with 8-byte stores, so no load or store needs a predicate.
-template <bool kFull>
-__device__ __forceinline__ void qblock_pair_run(const PairLane& L, int h, bool on, const QBlock& b0,
-                                                const QBlock& b1, const uint64_t* __restrict__ ptrs) {
+// kBands: at least one block of the pair is QB_BANDS; each row's source is
+// base + r * ld2 of the band that holds it (band tables of both blocks are
+// workgroup-uniform, so they stay in scalar registers and each lane selects);
+// otherwise every row follows the single piece's stride.
+struct PairBands {
+  uint64_t base[2][kMaxBands];  // recv + band offset - first row * pitch (bytes)
+  uint32_t ld2[2][kMaxBands];   // band pitch in bytes
+  uint32_t start[2][kMaxBands]; // first row; bands past the block's last: 256
+};
+
+template <bool kFull, bool kBands>
+__device__ __forceinline__ void qblock_pair_run(const PairLane& L, const PairBands* S, int h, bool on,
+                                                const QBlock& b0, const QBlock& b1, const uint64_t* __restrict__ ptrs) {
   constexpr int R = 16, kStep = 8;
   static_assert(kQBlockThreads == 32 * kStep, "pair mapping");
+  static_assert(kMaxBands == 4, "band selection");
   __shared__ uint32_t wave_max[kQBlockThreads / 64][2];
   const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 5;
   u32x4 raw[R];
-  if (kFull) {
+  if (kBands) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      const uint32_t r = rb + kStep * k;
+      raw[k] = u32x4{0u, 0u, 0u, 0u};
+      if (kFull || (int(r) < L.rows && cg < L.cols)) {
+        uint64_t base = h ? S->base[1][0] : S->base[0][0];
+        uint32_t ld2 = h ? S->ld2[1][0] : S->ld2[0][0];
+#pragma unroll
+        for (int j = 1; j < kMaxBands; ++j)
+          if (r >= (h ? S->start[1][j] : S->start[0][j])) {
+            base = h ? S->base[1][j] : S->base[0][j];
+            ld2 = h ? S->ld2[1][j] : S->ld2[0][j];
+          }
+        raw[k] = ld(reinterpret_cast<const u32x4*>(base + uint64_t(r) * ld2 + uint64_t(cg) * 2));
+      }
+    }
+  } else if (kFull) {
     const char* p = L.src;
 #pragma unroll
     for (int k = 0; k < R; ++k, p += kStep * L.src_ld2) raw[k] = ld(reinterpret_cast<const u32x4*>(p));
@@ -533,15 +565,9 @@ __device__ __forceinline__ void qblock_pair_run(const PairLane& L, int h, bool o
   if (on && (threadIdx.x & ~16u) == 0) reinterpret_cast<float*>(ptrs[b.scale_idx])[b.scale_off] = qs.s;
 }
 
-__device__ void qblock_pair(const QBlock* __restrict__ blocks, uint32_t i0, uint32_t nsingle,
-                            const uint64_t* __restrict__ ptrs, const char* recv) {
-  // both descriptors are read at workgroup-uniform addresses; each lane then
-  // selects its block's fields
-  const bool has1 = i0 + 1 < nsingle;
-  const QBlock b0 = blocks[i0];
-  const QBlock b1 = blocks[has1 ? i0 + 1 : i0];
-  const int h = (threadIdx.x >> 4) & 1;
-  const bool on = h == 0 || has1;
+// This lane's view of the block it works on in a pair (h: 0 or 1).
+__device__ __forceinline__ PairLane pair_lane(const QBlock& b0, const QBlock& b1, int h, bool on,
+                                              const uint64_t* __restrict__ ptrs, const char* recv) {
   const QBlock& b = h ? b1 : b0;
   const int cg = (threadIdx.x & 15) * 8, rb = threadIdx.x >> 5;
   PairLane L;
@@ -554,18 +580,74 @@ __device__ void qblock_pair(const QBlock* __restrict__ blocks, uint32_t i0, uint
   L.rows = on ? b.rows_m1 + 1 : 0;
   L.cols = b.cols_m1 + 1;
   L.vec = (b.flags & QB_VEC_STORE) != 0;
+  return L;
+}
+
+// Blocks i0 and i0 + 1, both QB_SINGLE, 128 x 128, 8-byte stores (the
+// planner's full pairs): no predicates, one quotient form per block.
+__device__ __forceinline__ void qblock_pair_full(const QBlock* __restrict__ blocks, uint32_t i0, const uint64_t* __restrict__ ptrs,
+                                 const char* recv) {
+  const QBlock b0 = blocks[i0];
+  const QBlock b1 = blocks[i0 + 1];
+  const int h = (threadIdx.x >> 4) & 1;
+  qblock_pair_run<true, false>(pair_lane(b0, b1, h, true, ptrs, recv), nullptr, h, true, b0, b1, ptrs);
+}
+
+// Blocks i0 and i0 + 1 (absent when i0 + 1 == n), both pairable, any extent.
+__device__ __forceinline__ void qblock_pair(const QBlock* __restrict__ blocks, uint32_t i0, uint32_t n,
+                            const QPiece* __restrict__ pieces, const uint64_t* __restrict__ ptrs, const char* recv) {
+  // both descriptors are read at workgroup-uniform addresses; each lane then
+  // selects its block's fields
+  const bool has1 = i0 + 1 < n;
+  const QBlock b0 = blocks[i0];
+  const QBlock b1 = blocks[has1 ? i0 + 1 : i0];
+  const int h = (threadIdx.x >> 4) & 1;
+  const bool on = h == 0 || has1;
+  const PairLane L = pair_lane(b0, b1, h, on, ptrs, recv);
   const bool full = has1 && b0.rows_m1 == 127 && b0.cols_m1 == 127 && b1.rows_m1 == 127 && b1.cols_m1 == 127 &&
                     (b0.flags & b1.flags & QB_VEC_STORE);
-  if (full)
-    qblock_pair_run<true>(L, h, on, b0, b1, ptrs);
-  else
-    qblock_pair_run<false>(L, h, on, b0, b1, ptrs);
+  const bool bands = ((b0.flags | b1.flags) & QB_BANDS) != 0;  // uniform over the workgroup
+  if (bands) {
+    PairBands S;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const QBlock& tb = hh ? b1 : b0;
+#pragma unroll
+      for (int j = 0; j < kMaxBands; ++j) {
+        S.base[hh][j] = 0;
+        S.ld2[hh][j] = 0;
+        S.start[hh][j] = 256;
+      }
+      if (tb.flags & QB_BANDS) {
+#pragma unroll
+        for (int j = 0; j < kMaxBands; ++j)
+          if (j < tb.npieces) {
+            const QPiece q = pieces[tb.piece0 + j];
+            S.ld2[hh][j] = q.src_ld * 2;
+            S.base[hh][j] = reinterpret_cast<uint64_t>(recv) + q.src_off - uint64_t(q.r0) * S.ld2[hh][j];
+            S.start[hh][j] = q.r0;
+          }
+      } else {
+        S.ld2[hh][0] = tb.src_ld * 2;
+        S.base[hh][0] = reinterpret_cast<uint64_t>(recv) + tb.src_off;
+        S.start[hh][0] = 0;
+      }
+    }
+    if (full)
+      qblock_pair_run<true, true>(L, &S, h, on, b0, b1, ptrs);
+    else
+      qblock_pair_run<false, true>(L, &S, h, on, b0, b1, ptrs);
+  } else if (full) {
+    qblock_pair_run<true, false>(L, nullptr, h, on, b0, b1, ptrs);
+  } else {
+    qblock_pair_run<false, false>(L, nullptr, h, on, b0, b1, ptrs);
+  }
 }
 
 // One block of any kind (several wire pieces, unaligned or fp32 ones): thread t
 // holds columns 8 (t mod 16) .. + 7 of rows t / 16 + 16 k, k < 8, as fp32,
 // gathered from the pieces.
-__device__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, const uint64_t* __restrict__ ptrs,
+__device__ __forceinline__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, const uint64_t* __restrict__ ptrs,
                            const char* recv) {
   constexpr int R = 8, kStep = 16;
   static_assert(kQBlockThreads == 16 * kStep, "block mapping");
@@ -652,17 +734,23 @@ __device__ void qblock_one(const QBlock& b, const QPiece* __restrict__ pieces, c
 
 }  // namespace
 
-// Workgroup w < ceil(nsingle / 2) takes the QB_SINGLE blocks 2w and 2w + 1;
-// the following workgroups one other block each.
+// The fp8 blocks of a launch range come in three classes, taken by one launch
+// (the slower classes overlap the bulk instead of trailing it in launches of
+// their own): workgroup w < nfull / 2 takes the full pair 2w, 2w + 1; the next
+// ones the other pairable blocks two at a time (the second absent past npair);
+// the rest one block each.
 __global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
                                                                    const QPiece* __restrict__ pieces,
                                                                    const uint64_t* __restrict__ ptrs,
-                                                                   const char* recv, uint32_t n, uint32_t nsingle) {
-  const uint32_t npair = (nsingle + 1) / 2;
-  if (blockIdx.x < npair) {
-    qblock_pair(blocks, 2 * blockIdx.x, nsingle, ptrs, recv);
+                                                                   const char* recv, uint32_t n, uint32_t nfull,
+                                                                   uint32_t npair) {
+  const uint32_t g0 = nfull / 2, g1 = (npair - nfull + 1) / 2;
+  if (blockIdx.x < g0) {
+    qblock_pair_full(blocks, 2 * blockIdx.x, ptrs, recv);
+  } else if (blockIdx.x < g0 + g1) {
+    qblock_pair(blocks + nfull, 2 * (blockIdx.x - g0), npair - nfull, pieces, ptrs, recv);
   } else {
-    const uint32_t i = nsingle + (blockIdx.x - npair);
+    const uint32_t i = npair + (blockIdx.x - g0 - g1);
     if (i < n) qblock_one(blocks[i], pieces, ptrs, recv);
   }
 }
@@ -690,12 +778,12 @@ int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint6
   return hipGetLastError();
 }
 
-int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
-                   const void* buf, void* stream) {
+int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nfull, uint32_t npair, const QPiece* pieces,
+                   const uint64_t* ptrs, const void* buf, void* stream) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(wb_qblock_kernel, dim3(qblock_workgroups(n, nsingle)), dim3(kQBlockThreads), WB_QBLOCK_DYN_LDS,
-                     static_cast<hipStream_t>(stream), blocks, pieces, ptrs, static_cast<const char*>(buf), n,
-                     nsingle);
+  hipLaunchKernelGGL(wb_qblock_kernel, dim3(qblock_workgroups(n, nfull, npair)), dim3(kQBlockThreads),
+                     WB_QBLOCK_DYN_LDS, static_cast<hipStream_t>(stream), blocks, pieces, ptrs,
+                     static_cast<const char*>(buf), n, nfull, npair);
   return hipGetLastError();
 }
 

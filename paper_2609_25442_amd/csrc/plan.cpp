@@ -241,6 +241,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   P.round_tasks.assign(nrounds + 1, 0);
   P.round_qblocks.assign(nrounds + 1, 0);
   P.round_qsingle.assign(nrounds, 0);
+  P.round_qfull.assign(nrounds, 0);
   P.round_qpieces.assign(2 * size_t(nrounds), 0);  // every plan: ranks without fp8 blocks keep empty ranges
   if (P.role == WB_SENDER) {
     const Rank& R = trainer.ranks[P.rank];
@@ -423,6 +424,18 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
           bool bf16 = true;
           for (uint32_t i = count[id]; i < count[id + 1]; ++i) bf16 = bf16 && P.qpieces[i].sdt == WB_BF16;
           if (bf16) b.flags |= QB_BF16_SOURCE;
+          // row bands: every piece spans the block's width, 16-byte aligned
+          // rows; sorted by first row they tile the block from row 0
+          const uint32_t np = count[id + 1] - count[id];
+          if (bf16 && np >= 2 && np <= uint32_t(kMaxBands) && cols % 8 == 0) {
+            QPiece* pc = P.qpieces.data() + count[id];
+            std::sort(pc, pc + np, [](const QPiece& a, const QPiece& c) { return a.r0 < c.r0; });
+            bool bands = true;
+            for (uint32_t i = 0; i < np; ++i)
+              bands = bands && pc[i].c0 == 0 && pc[i].c1m1 == cols - 1 && pc[i].src_off % 16 == 0 &&
+                      (uint64_t(pc[i].src_ld) * 2) % 16 == 0 && pc[i].r0 == (i ? pc[i - 1].r1m1 + 1 : 0);
+            if (bands && pc[np - 1].r1m1 == rows - 1) b.flags |= QB_BANDS;
+          }
         }
   }
   // group the blocks by round, canonical block order within a round (a
@@ -443,8 +456,12 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   // class, so consecutive single-piece blocks are mostly horizontal neighbours)
   for (int k = 0; k < nrounds; ++k) {
     const auto first = P.qblocks.begin() + P.round_qblocks[k], last = P.qblocks.begin() + P.round_qblocks[k + 1];
-    const auto mid = std::stable_partition(first, last, [](const QBlock& b) { return (b.flags & QB_SINGLE) != 0; });
+    const auto mid = std::stable_partition(first, last, qblock_pairable);
     P.round_qsingle[k] = static_cast<uint32_t>(mid - first);
+    // full pairs first among the pairable blocks (an odd one out stays with
+    // the other pairable blocks)
+    const auto fmid = std::stable_partition(first, mid, qblock_full_single);
+    P.round_qfull[k] = static_cast<uint32_t>(fmid - first) & ~1u;
   }
   // the range of the piece table each round's blocks read
   for (int k = 0; k < nrounds; ++k) {
@@ -557,12 +574,15 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   }
   if (P.round_qsingle.size() != nr || P.round_qsingle[k] > P.round_qblocks[k + 1] - P.round_qblocks[k])
     fail(WB_EINVAL, "internal: single-piece fp8 block count");
+  if (P.round_qfull.size() != nr || P.round_qfull[k] % 2 || P.round_qfull[k] > P.round_qsingle[k])
+    fail(WB_EINVAL, "internal: full fp8 pair count");
   if (P.round_qpieces.size() != 2 * nr || P.round_qpieces[2 * k] > P.round_qpieces[2 * k + 1] ||
       P.round_qpieces[2 * k + 1] > P.qpieces.size())
     fail(WB_EINVAL, "internal: fp8 piece range of a round");
   for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
     const QBlock& b = P.qblocks[bi];
-    if (((b.flags & QB_SINGLE) != 0) != (bi < P.round_qblocks[k] + P.round_qsingle[k]))
+    if (qblock_pairable(b) != (bi < P.round_qblocks[k] + P.round_qsingle[k]) ||
+        (bi < P.round_qblocks[k] + P.round_qfull[k] && !qblock_full_single(b)))
       fail(WB_EINVAL, "internal: fp8 block order");
     const uint64_t rows = b.rows_m1 + 1u, cols = b.cols_m1 + 1u;
     inside(b.dst_idx, b.dst_off, (rows - 1) * b.dst_ld + cols, "fp8 block");
@@ -579,6 +599,16 @@ void check_work(const wb_plan_t& P, const Rank& R) {
       fail(WB_EINVAL, "internal: fp8 block pieces out of range");
     if (b.npieces && (b.piece0 < P.round_qpieces[2 * k] || b.piece0 + b.npieces > P.round_qpieces[2 * k + 1]))
       fail(WB_EINVAL, "internal: fp8 block pieces outside its round's piece range");
+    if (b.flags & QB_BANDS) {
+      if ((b.flags & QB_SINGLE) || b.npieces < 2 || b.npieces > kMaxBands || cols % 8 || !(b.flags & QB_BF16_SOURCE))
+        fail(WB_EINVAL, "internal: fp8 band block");
+      for (uint32_t i = 0; i < b.npieces; ++i) {
+        const QPiece& q = P.qpieces[b.piece0 + i];
+        if (q.sdt != WB_BF16 || q.c0 != 0 || q.c1m1 != cols - 1 || q.src_off % 16 || (uint64_t(q.src_ld) * 2) % 16 ||
+            q.r0 != (i ? P.qpieces[b.piece0 + i - 1].r1m1 + 1u : 0u) || (i + 1 == b.npieces && q.r1m1 != rows - 1))
+          fail(WB_EINVAL, "internal: fp8 bands do not tile their block");
+      }
+    }
     for (uint32_t i = b.piece0; i < b.piece0 + b.npieces; ++i) {
       const QPiece& q = P.qpieces[i];
       if (q.r1m1 < q.r0 || q.c1m1 < q.c0 || q.r1m1 >= rows || q.c1m1 >= cols)

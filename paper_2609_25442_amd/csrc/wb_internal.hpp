@@ -216,15 +216,27 @@ struct QPiece {
 };
 static_assert(sizeof(QPiece) == 24, "QPiece layout");
 
-enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4 };
+// QB_BANDS: a block filled by 2..kMaxBands full-width, aligned bf16 row bands
+// (its pieces, sorted by first row); such blocks take the pair path too, each
+// row loaded from the band that holds it.
+enum QBlockFlags : uint8_t { QB_VEC_STORE = 1, QB_BF16_SOURCE = 2, QB_SINGLE = 4, QB_BANDS = 8 };
+constexpr int kMaxBands = 4;
+inline bool qblock_pairable(const QBlock& b) { return (b.flags & (QB_SINGLE | QB_BANDS)) != 0; }
+inline bool qblock_full_single(const QBlock& b) {
+  return (b.flags & QB_SINGLE) && (b.flags & QB_VEC_STORE) && b.rows_m1 == 127 && b.cols_m1 == 127;
+}
 
-// The fp8 block kernel runs kQBlockThreads threads per workgroup. Each launch's
-// range of blocks starts with its QB_SINGLE blocks, taken two per workgroup
-// (horizontal neighbours in block order, so one row of the pair is 512
-// contiguous bytes of the wire), 16 rows of 8 columns per thread; the other
-// blocks follow, one per workgroup, 8 rows of 8 columns per thread.
+// The fp8 block kernel runs kQBlockThreads threads per workgroup. Each launch
+// range of blocks starts with its full pairs (nfull, even: QB_SINGLE blocks of
+// 128 x 128 with 8-byte stores), then the other pairable blocks (QB_SINGLE or
+// QB_BANDS) up to npair, each pair taken by one workgroup (horizontal
+// neighbours in block order, so one row of the pair is 512 contiguous bytes
+// of the wire), 16 rows of 8 columns per thread; the other blocks follow, one
+// per workgroup, 8 rows of 8 columns per thread.
 constexpr int kQBlockThreads = 256;
-inline uint32_t qblock_workgroups(uint32_t n, uint32_t nsingle) { return (nsingle + 1) / 2 + (n - nsingle); }
+inline uint32_t qblock_workgroups(uint32_t n, uint32_t nfull, uint32_t npair) {
+  return nfull / 2 + (npair - nfull + 1) / 2 + (n - npair);
+}
 
 // A field of a batched diff2 launch: rows x cols values, value at (i, j) the
 // sum over k < passes of src[k][i * cols + j] << (16 k); its element 0 is
@@ -282,7 +294,8 @@ struct wb_plan_t {
   std::vector<wb::QBlock> qblocks;      // grouped by round
   std::vector<wb::QPiece> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
-  std::vector<uint32_t> round_qsingle;  // [k]: QB_SINGLE blocks at the start of round k's block range
+  std::vector<uint32_t> round_qfull;    // [k]: blocks of full pairs at the start of round k's block range (even)
+  std::vector<uint32_t> round_qsingle;  // [k]: pairable blocks (full pairs, QB_SINGLE, QB_BANDS) at its start
   std::vector<uint32_t> round_qpieces;  // [2k], [2k + 1]: the piece-table range round k's blocks read
   std::vector<uint32_t> round_fwd[2];   // forward work of exchange stage 1 + i, round k: [k] .. [k + 1]
   int64_t fwd_bytes[2] = {0, 0};        // bytes this rank forwards in each exchange stage (all rounds)
@@ -314,9 +327,9 @@ constexpr uint16_t kAuxBuffer = 0xFFFF;
 void task_grid(uint32_t n, const TaskSplit& sp, uint32_t* gx, uint32_t* gy);
 int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream);
-// n blocks, the first nsingle of them QB_SINGLE
-int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nsingle, const QPiece* pieces, const uint64_t* ptrs,
-                   const void* buf, void* stream);
+// n blocks: nfull in full pairs, then pairable ones up to npair, then the rest
+int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nfull, uint32_t npair, const QPiece* pieces,
+                   const uint64_t* ptrs, const void* buf, void* stream);
 const char* hip_error_string(int err);
 // noalloc.hip: the library's per-GPU scratch array for allocation-free calls
 // (its address on the current device, found once per device, and its size)

@@ -120,14 +120,17 @@ def test_copy_launch_grid_is_dense(name):
         assert items <= wgs < (256 << 10) // chunk * items + y
         assert (r + wr) / wgs >= chunk, (name, role, wgs, r + wr)
     fx, fy, ft = p.launch_grid(1)
-    # fp8 blocks: single-piece ones two per workgroup, the others one each
+    # fp8 blocks: pairable ones (single-piece, row bands) two per workgroup,
+    # the others one each
     nb = p.work_counts()[1]
     assert ft == 256 and fy == (1 if nb else 0) and (nb + 1) // 2 <= fx <= nb
     # the two launches' algorithmic bytes add up to the rank's
     parts = [p.kernel_traffic(k) for k in (0, 1)]
     assert tuple(map(sum, zip(*parts))) == p.traffic()
-    if name == "dsv3_ep64_to_ep8_fp8":  # routed-expert blocks (97 %) are single-piece: two per workgroup
-        assert fx <= 0.52 * nb
+    if name == "dsv3_ep64_to_ep8_fp8":
+        # routed-expert blocks (97 %) are single-piece and the shared expert's
+        # are row bands: all pair up
+        assert fx == (nb + 1) // 2
     _expect(wb.WB_EINVAL, p.launch_grid, 4, 0)
     _expect(wb.WB_EINVAL, p.launch_grid, 0, 1)
 

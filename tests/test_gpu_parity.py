@@ -119,9 +119,10 @@ def test_transposed_trainer_shards(rows, cols, split):
 
 
 def test_fp8_paired_and_general_blocks():
-    """fp8 blocks of one launch on both kernel paths: 19 single-piece blocks
-    (taken two per workgroup, the last one alone; pairs that straddle tensors
-    and block rows; ragged right and bottom edges) and blocks filled from two
+    """fp8 blocks of one unpack on all three paths of the block kernel: 19 single-piece
+    blocks, of which 9 are full 128 x 128 (8 taken as full pairs, the odd one
+    out with the other 10: ragged right and bottom edges, pairs that straddle
+    tensors and block rows, the last one alone), and blocks filled from two
     wire pieces or from an unaligned one (one per workgroup)."""
     cat = [CkptTensor("T", 300, 392), CkptTensor("V", 130, 264), CkptTensor("W", 128, 128), CkptTensor("U", 200, 136)]
     r0 = RankLayout([Local("t0", "bf16", 1, 256, 392), Local("v", "bf16", 1, 130, 264), Local("u0", "bf16", 1, 200, 60)],
@@ -142,8 +143,42 @@ def test_fp8_paired_and_general_blocks():
     p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
     nb = p.work_counts()[1]
     gx = p.launch_grid(1)[0]
-    assert nb == 12 + 6 + 1 + 4 and gx == (19 + 1) // 2 + 4, (nb, gx)
+    assert nb == 12 + 6 + 1 + 4 and gx == 8 // 2 + (19 - 8 + 1) // 2 + 4, (nb, gx)
     roundtrip(tr, ro, _values(cat, "bf16"), label="fp8-paths")
+
+
+@pytest.mark.parametrize("copies", [2, 3, 5, 8, 10])
+def test_fp8_row_band_blocks(copies):
+    """A tensor replicated on ``copies`` trainer ranks is cut into row bands
+    among them, so each fp8 block of a rollout rank's copy is filled by up to
+    four full-width bands (paired with other blocks, each row read from its
+    band) or, with more bands, by the one-block path; ragged bottom and right
+    edges, and a single-piece tensor beside it."""
+    cat = [CkptTensor("S", 300, 264), CkptTensor("P", 128, 384)]
+    ranks = []
+    for r in range(copies):
+        locs = [Local("s", "bf16", 1, 300, 264)] + ([Local("p", "bf16", 1, 128, 384)] if r == 0 else [])
+        pls = [Placement(0, 0, 300, 0, 264, 0, 0, 264)] + ([Placement(1, 0, 128, 0, 384, 1, 0, 384)] if r == 0 else [])
+        ranks.append(RankLayout(locs, pls))
+    tr = Layout(cat, ranks)
+    locs, pls = [], []
+    for t, c in enumerate(cat):
+        u = len(locs)
+        locs += [Local("q" + c.name, "f8e4m3", 1, c.rows, c.cols, 128, scale=u + 1),
+                 Local("s" + c.name, "f32", 1, -(-c.rows // 128), -(-c.cols // 128), scales=u)]
+        pls.append(Placement(t, 0, c.rows, 0, c.cols, u, 0, c.cols))
+    ro = Layout(cat, [RankLayout(locs, pls)])
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
+    gx = p.launch_grid(1)[0]
+    # rows of S split as floor(j * 300 / copies): pieces per block row of S
+    # (3 block columns each, the last 8 wide; the last block row 44 high)
+    cuts = [j * 300 // copies for j in range(copies + 1)]
+    pieces = [sum(1 for a, b in zip(cuts, cuts[1:]) if a < min(300, 128 * (i + 1)) and b > 128 * i) for i in range(3)]
+    full = 3 + sum(2 for i, n in enumerate(pieces) if n == 1 and i < 2)   # P's blocks, then S's whole ones
+    pairable = 3 + sum(3 for n in pieces if n <= 4)
+    assert gx == full // 2 + (pairable - full // 2 * 2 + 1) // 2 + 3 + 9 - pairable, (pieces, gx)
+    assert pairable > full and (copies < 10 or pairable < 12)
+    roundtrip(tr, ro, _values(cat, "bf16"), label=f"fp8-bands-{copies}")
 
 
 def _tiny_catalog_layouts(tdtype, rdtype, block=0):
