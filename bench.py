@@ -232,8 +232,10 @@ def _launch_grids(w):
         x, y, t = plan.launch_grid(launch)
         return x * t, x * max(y, 1) * t
 
-    return {"pack": (threads_x(sp, 0), "wb_tasks_kernel", sp.traffic()),
+    return {"pack": (threads_x(sp, 0), "wb_tasks_kernel", sp.kernel_traffic(0)),
+            "pack_tiles": (threads_x(sp, 4), "wb_tile_kernel", sp.kernel_traffic(4)),
             "unpack": (threads_x(rp, 0), "wb_tasks_kernel", rp.kernel_traffic(0)),
+            "unpack_tiles": (threads_x(rp, 4), "wb_tile_kernel", rp.kernel_traffic(4)),
             "unpack_fp8": (threads_x(rp, 1), "wb_qblock_kernel", rp.kernel_traffic(1))}, rp.buffer_bytes
 
 
@@ -606,7 +608,8 @@ def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
     # the launches of one wb_unpack, all timed together: the copy/cast kernel
     # and the fp8 block kernels that have work
     launches = [(k, lab, kern) for k, lab, kern in
-                ((0, "unpack", "wb::wb_tasks_kernel"), (1, "unpack_fp8", "wb::wb_qblock_kernel"))
+                ((0, "unpack", "wb::wb_tasks_kernel"), (4, "unpack_tiles", "wb::wb_tile_kernel"),
+                 (1, "unpack_fp8", "wb::wb_qblock_kernel"))
                 if rplan.launch_grid(k)[0]]
     dom = " + ".join(kern for _, _, kern in launches) + (
         " (one wb_unpack, timed together)" if len(launches) > 1 else " (unpack)")

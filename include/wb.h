@@ -243,22 +243,24 @@ int wb_plan_local_tensor(const wb_plan_t* plan, int32_t i, int32_t* dtype, int64
 int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
 /* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */
 int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* write_bytes);
-/* The same split by launch: launch 0 is the copy/cast kernel, launch 1 the fp8
- * block kernel (receivers with fp8 tensors only; 0 otherwise); launches 2 and 3
- * are the forward packings of exchange stages 1 and 2 over all rounds
- * (receivers of three-stage plans; 0 otherwise). */
+/* The same split by launch: launch 0 is the copy/cast kernel, launch 4 the
+ * transpose-tile kernel (whole 256 x 256 tiles of 2-byte transposes; 0
+ * otherwise), launch 1 the fp8 block kernel (receivers with fp8 tensors only;
+ * 0 otherwise); launches 2 and 3 are the forward packings of exchange stages
+ * 1 and 2 over all rounds (receivers of three-stage plans; 0 otherwise).
+ * Launches 0, 1 and 4 add up to wb_plan_traffic_bytes. */
 int wb_plan_kernel_traffic(const wb_plan_t* plan, int32_t launch, int64_t* read_bytes, int64_t* write_bytes);
 /* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
 int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
 /* Grid (workgroups in x and y) and workgroup size (threads) of one launch of
  * one round: launch 0 the copy/cast kernel of wb_pack_round / wb_unpack_round,
- * 1 the fp8 block kernel, 2 and 3 the forward packings of exchange stages 1
- * and 2. A copy/cast work item takes several workgroups (one per chunk of its
+ * 4 its transpose-tile kernel (one workgroup per 256 x 256 tile), 1 the fp8
+ * block kernel, 2 and 3 the forward packings of exchange stages 1 and 2. A copy/cast work item takes several workgroups (one per chunk of its
  * vectors), so the copy grid is a multiple of the work-item count; the fp8
  * grid has one workgroup per pair of pairable blocks (single-piece blocks and
  * blocks of full-width row bands) and one per other block. The grid is 0 x 0
  * for a launch that enqueues nothing. WB_EINVAL for a null argument, a launch
- * outside 0..3 or a round out of range. */
+ * outside 0..4 or a round out of range. */
 int wb_plan_launch_grid(const wb_plan_t* plan, int32_t launch, int32_t round, uint32_t* grid_x, uint32_t* grid_y,
                         uint32_t* threads);
 /* Canonical text form of the global plan (one line per segment). */
@@ -273,7 +275,8 @@ int wb_plan_upload(wb_plan_t* plan, void* workspace, size_t bytes, void* stream)
 /* Enqueue the packing kernel of a sender plan: src_ptrs[i] is local tensor i of
  * the rank (wb_plan_num_local_tensors entries), send_buf holds at least
  * wb_plan_buffer_bytes bytes. Writes every payload byte of the rank's regions;
- * bytes between payloads are left as they were. One kernel launch.
+ * bytes between payloads are left as they were. One kernel launch, and one
+ * more when the rank has whole 256 x 256 tiles to transpose.
  * Errors (synchronous): WB_EINVAL (wrong role, not uploaded, null or misaligned
  * pointer), WB_EHIP (launch failure). Device faults surface at stream sync. */
 int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* stream);
@@ -282,7 +285,8 @@ int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* 
  * senders at the offsets the plan gives (wb_plan_peer / wb_plan_region); every
  * element of every local tensor (dst_ptrs, wb_plan_num_local_tensors entries,
  * scale tensors included) is written exactly once. One launch for copy/cast
- * work and one for fp8 blocks when the rank has fp8 tensors.
+ * work (two with whole transpose tiles) and one for fp8 blocks when the rank
+ * has fp8 tensors.
  * Errors as for wb_pack. Calls on one plan must not overlap in time from several
  * host threads (the pointer table is per plan). */
 int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void* stream);

@@ -470,13 +470,19 @@ int wb_plan_traffic_bytes(const wb_plan_t* P, int64_t* read_bytes, int64_t* writ
 }
 
 int wb_plan_kernel_traffic(const wb_plan_t* P, int32_t launch, int64_t* read_bytes, int64_t* write_bytes) {
-  if (!P || !read_bytes || !write_bytes || launch < 0 || launch > 3) return set_error(WB_EINVAL, "bad argument");
-  if (launch >= 2) {
+  if (!P || !read_bytes || !write_bytes || launch < 0 || launch > 4) return set_error(WB_EINVAL, "bad argument");
+  if (launch == 2 || launch == 3) {
     *read_bytes = *write_bytes = P->fwd_bytes[launch - 2];
-    return WB_OK;
+  } else if (launch == 4) {
+    *read_bytes = P->tile_read_bytes;
+    *write_bytes = P->tile_write_bytes;
+  } else if (launch == 1) {
+    *read_bytes = P->q_read_bytes;
+    *write_bytes = P->q_write_bytes;
+  } else {
+    *read_bytes = P->read_bytes - P->q_read_bytes - P->tile_read_bytes;
+    *write_bytes = P->write_bytes - P->q_write_bytes - P->tile_write_bytes;
   }
-  *read_bytes = launch == 0 ? P->read_bytes - P->q_read_bytes : P->q_read_bytes;
-  *write_bytes = launch == 0 ? P->write_bytes - P->q_write_bytes : P->q_write_bytes;
   return WB_OK;
 }
 
@@ -491,10 +497,15 @@ int wb_plan_work_counts(const wb_plan_t* P, int64_t* tasks, int64_t* blocks, int
 int wb_plan_launch_grid(const wb_plan_t* P, int32_t launch, int32_t round, uint32_t* gx, uint32_t* gy,
                         uint32_t* threads) {
   if (!P || !gx || !gy || !threads) return set_error(WB_EINVAL, "null argument");
-  if (launch < 0 || launch > 3) return set_error(WB_EINVAL, "launch must be 0..3");
+  if (launch < 0 || launch > 4) return set_error(WB_EINVAL, "launch must be 0..4");
   if (round < 0 || round >= static_cast<int>(P->rounds.size())) return set_error(WB_EINVAL, "round out of range");
   *gx = *gy = 0;
-  *threads = launch == 1 ? wb::kQBlockThreads : wb::kChunkThreads;
+  *threads = launch == 1 ? wb::kQBlockThreads : launch == 4 ? wb::kTileThreads : wb::kChunkThreads;
+  if (launch == 4) {
+    if (P->round_split.size() == P->rounds.size() && P->round_split[round].tiles)
+      *gx = P->round_split[round].tiles, *gy = 1;
+    return WB_OK;
+  }
   if (launch == 1) {
     const uint32_t n = P->round_qblocks[round + 1] - P->round_qblocks[round];
     if (n) *gx = wb::qblock_workgroups(n, P->round_qfull[round], P->round_qsingle[round]), *gy = 1;

@@ -280,6 +280,17 @@ __device__ void run_transpose(const Task& t, const char* src, char* dst, uint32_
   }
 }
 
+// Column j of an 8 x 8 block of 2-byte elements held as eight 16-byte rows.
+__device__ __forceinline__ u32x4 column8(const u32x4 (&a)[8], int j) {
+  uint32_t o[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t x = a[2 * k][j >> 1], y = a[2 * k + 1][j >> 1];
+    o[k] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
+  }
+  return u32x4{o[0], o[1], o[2], o[3]};
+}
+
 // dst[c][r] = src[r][c] for 2-byte elements, (64..256) rows x 64 columns: each
 // wave takes one 64 x 64 tile (tile `w` of the item, counted down the rows),
 // each lane an 8 x 8 sub-tile that it loads as eight 16-byte rows, transposes
@@ -294,16 +305,7 @@ __device__ void run_transpose16(const Task& t, const char* src, char* dst, uint3
   for (int i = 0; i < 8; ++i)
     a[i] = ld(reinterpret_cast<const u32x4*>(src + (uint64_t(r0 + i) * t.src_ld + c0) * 2));
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    // column j of the sub-tile: element j of each loaded row
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t x = a[2 * k][j >> 1], y = a[2 * k + 1][j >> 1];
-      o[k] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-    }
-    st(u32x4{o[0], o[1], o[2], o[3]}, reinterpret_cast<u32x4*>(dst + (uint64_t(c0 + j) * t.dst_ld + r0) * 2));
-  }
+  for (int j = 0; j < 8; ++j) st(column8(a, j), reinterpret_cast<u32x4*>(dst + (uint64_t(c0 + j) * t.dst_ld + r0) * 2));
 }
 
 }  // namespace
@@ -346,6 +348,35 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
     case TASK_TRANSPOSE: run_transpose(t, src, dst, chunk); break;
     case TASK_TRANSPOSE16: run_transpose16(t, src, dst, chunk * (kThreads / 64) + (threadIdx.x >> 6)); break;
     default: break;
+  }
+}
+
+// dst[c][r] = src[r][c] of one 256 x 256 tile of 2-byte elements per
+// workgroup (TASK_TILE256 items): thread t transposes the 8 x 8 sub-tile at
+// source rows 8 (t / 32) .., columns 8 (t mod 32) .. in registers, LDS
+// regroups the sub-tiles by destination row (padded rows), and each thread
+// then stores eight 16-byte pieces of destination rows, so that on both sides
+// a wave instruction moves two contiguous 512-byte rows.
+__global__ __launch_bounds__(kTileThreads) void wb_tile_kernel(const Task* __restrict__ tasks,
+                                                               const uint64_t* __restrict__ ptrs, const char* buf,
+                                                               const char* aux) {
+  constexpr int G = kTileEdge / 8;
+  __shared__ u32x4 lds[kTileEdge][G + 1];
+  const Task t = tasks[blockIdx.x];
+  const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
+  char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
+  const int cg = threadIdx.x % G, rg = threadIdx.x / G;
+  u32x4 a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    a[i] = ld(reinterpret_cast<const u32x4*>(src + (uint64_t(8 * rg + i) * t.src_ld + 8 * cg) * 2));
+#pragma unroll
+  for (int j = 0; j < 8; ++j) lds[8 * cg + j][rg] = column8(a, j);  // destination row 8 cg + j
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int row = G * k + rg;
+    st(lds[row][cg], reinterpret_cast<u32x4*>(dst + (uint64_t(row) * t.dst_ld + 8 * cg) * 2));
   }
 }
 
@@ -757,7 +788,11 @@ __global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock*
 
 void task_grid(uint32_t n, const TaskSplit& sp, uint32_t* gx, uint32_t* gy) {
   const uint64_t total =
-      (uint64_t(sp.n[0]) << sp.s[0]) + (uint64_t(sp.n[1]) << sp.s[1]) + (n - sp.n[0] - sp.n[1]);
+      (uint64_t(sp.n[0]) << sp.s[0]) + (uint64_t(sp.n[1]) << sp.s[1]) + (n - sp.n[0] - sp.n[1] - sp.tiles);
+  if (total == 0) {
+    *gx = *gy = 0;
+    return;
+  }
   if (total <= kMaxGridX) {
     *gx = static_cast<uint32_t>(total);
     *gy = 1;
@@ -772,10 +807,19 @@ int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint6
   if (n == 0) return hipSuccess;
   uint32_t gx, gy;
   task_grid(n, sp, &gx, &gy);
-  hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS, static_cast<hipStream_t>(stream),
-                     tasks, ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux), n, sp.n[0], sp.n[1],
-                     sp.s[0], sp.s[1]);
-  return hipGetLastError();
+  if (gx) {
+    hipLaunchKernelGGL(wb_tasks_kernel, dim3(gx, gy), dim3(kThreads), WB_TASK_DYN_LDS,
+                       static_cast<hipStream_t>(stream), tasks, ptrs, static_cast<const char*>(buf),
+                       static_cast<const char*>(aux), n - sp.tiles, sp.n[0], sp.n[1], sp.s[0], sp.s[1]);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (sp.tiles) {
+    hipLaunchKernelGGL(wb_tile_kernel, dim3(sp.tiles), dim3(kTileThreads), 0, static_cast<hipStream_t>(stream),
+                       tasks + (n - sp.tiles), ptrs, static_cast<const char*>(buf), static_cast<const char*>(aux));
+    return hipGetLastError();
+  }
+  return hipSuccess;
 }
 
 int launch_qblocks(const QBlock* blocks, uint32_t n, uint32_t nfull, uint32_t npair, const QPiece* pieces,

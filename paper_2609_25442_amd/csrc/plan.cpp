@@ -190,14 +190,38 @@ struct TaskSink {
   }
 
   // dst[c][r] = src[r][c] for an R x C source block. Aligned 2-byte data is
+  // cut into 256 x 256 tiles (taken along the source rows, which measured
+  // fastest for these tiles), transposed by the tile kernel; the edges go to
+  // transpose_small.
+  void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
+                      int64_t R, int64_t C) {
+    const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
+    const bool fast = ss == 2 && ds == 2 && sdt == ddt && soff % 16 == 0 && doff % 16 == 0 && (sld * 2) % 16 == 0 &&
+                      (dld * 2) % 16 == 0;
+    const int64_t RT = fast ? R / kTileEdge * kTileEdge : 0, CT = fast ? C / kTileEdge * kTileEdge : 0;
+    if (RT == 0 || CT == 0) {
+      transpose_small(sidx, soff, sld, sdt, didx, doff, dld, ddt, R, C);
+      return;
+    }
+    for (int64_t r = 0; r < RT; r += kTileEdge)
+      for (int64_t c = 0; c < CT; c += kTileEdge)
+        push(TASK_TILE256, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
+             doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, kTileEdge, kTileEdge);
+    if (CT < C)  // right strip of the tiled rows
+      transpose_small(sidx, soff + CT * 2, sld, sdt, didx, doff + CT * dld * 2, dld, ddt, RT, C - CT);
+    if (RT < R)  // bottom strip, full width
+      transpose_small(sidx, soff + RT * sld * 2, sld, sdt, didx, doff + RT * 2, dld, ddt, R - RT, C);
+  }
+
+  // The same for blocks without whole tiles. Aligned 2-byte data is
   // transposed in registers, in items of up to 256 x 64 taken one 64-column
   // strip at a time, each strip top to bottom: consecutive tiles (and
   // workgroups) read down the source columns and write neighbouring 128-byte
   // spans of the same destination rows, an order that measured 9-13 % faster
   // on gfx950 than row by row. The rest (ragged edges, other dtypes) goes in
   // 64 x 64 LDS tiles.
-  void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
-                      int64_t R, int64_t C) {
+  void transpose_small(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
+                       int64_t R, int64_t C) {
     const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
     const bool fast = ss == 2 && ds == 2 && sdt == ddt && soff % 16 == 0 && doff % 16 == 0 && (sld * 2) % 16 == 0 &&
                       (dld * 2) % 16 == 0;
@@ -530,6 +554,13 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
         inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
         break;
+      case TASK_TILE256:
+        if (t.rows != kTileEdge || t.cols != kTileEdge || ss != 2 || ds != 2 || t.src_off % 16 || t.dst_off % 16 ||
+            (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
+          fail(WB_EINVAL, "internal: bad transpose tile");
+        inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
+        inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
+        break;
       case TASK_TRANSPOSE16:
         if (t.cols != 64 || t.rows % 64 || t.rows > 256 || t.rows == 0 || ss != 2 || ds != 2 ||
             t.src_off % 16 || t.dst_off % 16 || (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
@@ -546,10 +577,10 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   size[0] = P.role == WB_SENDER ? W.st[0].send_bytes[P.rank] : W.recv_total[P.rank];
   aux_size = 0;
   auto check_order = [&](uint32_t a, uint32_t b, const TaskSplit& sp) {
-    if (uint64_t(sp.n[0]) + sp.n[1] > b - a) fail(WB_EINVAL, "internal: work item class sizes");
+    if (uint64_t(sp.n[0]) + sp.n[1] + sp.tiles > b - a) fail(WB_EINVAL, "internal: work item class sizes");
     if (sp.s[0] > 24 || sp.s[1] > 24) fail(WB_EINVAL, "internal: work item class shift");
     for (uint32_t ti = a; ti < b; ++ti) {
-      const int want = ti < a + sp.n[0] ? 0 : ti < a + sp.n[0] + sp.n[1] ? 1 : 2;
+      const int want = ti < a + sp.n[0] ? 0 : ti < a + sp.n[0] + sp.n[1] ? 1 : ti < b - sp.tiles ? 2 : 3;
       if (task_class(P.tasks[ti]) != want) fail(WB_EINVAL, "internal: work item order");
       // every chunk of an item has a workgroup
       if (want < 2 && task_chunks(P.tasks[ti]) > (1u << sp.s[want]))
@@ -1003,9 +1034,11 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
     const auto first = P.tasks.begin() + a, last = P.tasks.begin() + b;
     const auto mid0 = std::stable_partition(first, last, [](const Task& t) { return task_class(t) == 0; });
     const auto mid1 = std::stable_partition(mid0, last, [](const Task& t) { return task_class(t) == 1; });
+    const auto mid2 = std::stable_partition(mid1, last, [](const Task& t) { return task_class(t) == 2; });
     TaskSplit sp;
     sp.n[0] = static_cast<uint32_t>(mid0 - first);
     sp.n[1] = static_cast<uint32_t>(mid1 - mid0);
+    sp.tiles = static_cast<uint32_t>(last - mid2);
     for (int c = 0; c < 2; ++c) {
       uint32_t most = 1;  // workgroups of the copy kernel per item of class c in this launch
       for (auto it = c == 0 ? first : mid0; it != (c == 0 ? mid0 : mid1); ++it) most = std::max(most, task_chunks(*it));
@@ -1019,6 +1052,11 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   for (size_t k = 0; k < nr; ++k) {
     P.round_split[k] = partition(P.round_tasks[k], P.round_tasks[k + 1]);
     for (int st = 0; st < 2; ++st) P.fwd_split[st][k] = partition(P.round_fwd[st][k], P.round_fwd[st][k + 1]);
+    for (uint32_t ti = P.round_tasks[k + 1] - P.round_split[k].tiles; ti < P.round_tasks[k + 1]; ++ti) {
+      const Task& t = P.tasks[ti];
+      P.tile_read_bytes += int64_t(t.rows) * t.cols * dtype_bytes(t.sdt);
+      P.tile_write_bytes += int64_t(t.rows) * t.cols * dtype_bytes(t.ddt);
+    }
   }
   check_work(P, role == WB_SENDER ? trainer.ranks[rank] : rollout.ranks[rank]);
 }

@@ -123,7 +123,14 @@ enum TaskKind : uint8_t {
   TASK_SCALAR = 3,     // any supported pair, element by element
   TASK_TRANSPOSE = 4,  // dst[c][r] = cvt(src[r][c]), one LDS tile of up to 64 x 64
   TASK_TRANSPOSE16 = 5,  // 2-byte dst[c][r] = src[r][c], (64..256) rows x 64 cols, in registers
+  TASK_TILE256 = 6,    // 2-byte dst[c][r] = src[r][c], one 256 x 256 tile through LDS (a launch of its own)
 };
+
+// TASK_TILE256 items run one per workgroup of kTileThreads threads: each
+// thread transposes one 8 x 8 sub-tile, so that a wave instruction moves two
+// 512-byte rows on either side.
+constexpr int kTileEdge = 256;
+constexpr int kTileThreads = (kTileEdge / 8) * (kTileEdge / 8);
 
 struct Task {
   uint64_t src_off, dst_off;
@@ -157,6 +164,7 @@ constexpr uint32_t kMaxGridX = 1u << 22;
 static_assert(kChunkThreads % 64 == 0 && kChunkThreads <= 256, "copy workgroup size");
 
 inline int task_class(const Task& t) {
+  if (t.kind == TASK_TILE256) return 3;
   if (t.kind == TASK_TRANSPOSE || t.kind == TASK_TRANSPOSE16) return 1;
   return t.kind == TASK_SCALAR ? 2 : 0;
 }
@@ -181,11 +189,13 @@ inline uint32_t task_chunks(const Task& t) {
   return static_cast<uint32_t>(vecs == 0 ? 1 : (vecs + kChunkVecs - 1) / kChunkVecs);
 }
 
-// One launch's range: items of classes 0 and 1 at its start (class 2 follows)
-// and log2 of the workgroups per item of each class (fits its longest item).
+// One launch's range: items of classes 0 and 1 at its start, class 2 after
+// them, and log2 of the workgroups per item of classes 0 and 1 (fits its
+// longest item); the last tiles items (class 3) go to the tile kernel.
 struct TaskSplit {
   uint32_t n[2] = {0, 0};
   uint32_t s[2] = {0, 0};
+  uint32_t tiles = 0;
 };
 
 // One fp8 destination block and the wire pieces that fill it. Blocks filled by
@@ -288,6 +298,7 @@ struct wb_plan_t {
   int n_locals = 0;
   int64_t read_bytes = 0, write_bytes = 0;
   int64_t q_read_bytes = 0, q_write_bytes = 0;  // the fp8 launch's share
+  int64_t tile_read_bytes = 0, tile_write_bytes = 0;  // the tile launch's share (pack and unpack ranges)
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
   std::vector<wb::TaskSplit> round_split;  // [k]: class sizes of round k's pack/unpack range
   std::vector<wb::TaskSplit> fwd_split[2]; // the same for the forward range of stage 1 + i, round k
@@ -323,7 +334,8 @@ std::string dump_plan(const wb_plan_t& P);
 // ptrs[1 + u] is local tensor u; work items with index 0 use buf, with index
 // kAuxBuffer aux (the second buffer of a forward launch).
 constexpr uint16_t kAuxBuffer = 0xFFFF;
-// n work items ordered by class, split as in `sp`
+// n work items ordered by class, split as in `sp`: the copy kernel's grid
+// (the last sp.tiles items excluded: one tile-kernel workgroup each)
 void task_grid(uint32_t n, const TaskSplit& sp, uint32_t* gx, uint32_t* gy);
 int launch_tasks(const Task* tasks, uint32_t n, const TaskSplit& sp, const uint64_t* ptrs,
                  const void* buf, const void* aux, void* stream);

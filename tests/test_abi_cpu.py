@@ -111,7 +111,14 @@ def test_copy_launch_grid_is_dense(name):
     ro = wb.Layout.describe(w["model"], w["rollout"])
     for role, rank in ((wb.SENDER, w["pack_rank"]), (wb.RECEIVER, w["unpack_rank"])):
         p = wb.Plan(tr, ro, role, rank)
-        items = p.work_counts()[0]
+        # whole 256 x 256 transpose tiles: one tile-kernel workgroup each
+        tiles, ty, tt = p.launch_grid(4)
+        tr_, tw_ = p.kernel_traffic(4)
+        assert tt == 1024 and ty == (1 if tiles else 0) and tr_ == tw_ == tiles * 256 * 256 * 2
+        if (name, role) == ("llama3_8b_tp4_to_tp2", wb.SENDER):
+            # the row-parallel o and down slabs, [1024, 4096] and [3584, 4096] per layer
+            assert tiles == 32 * (4 + 14) * 16
+        items = p.work_counts()[0] - tiles
         x, y, threads = p.launch_grid(0)
         assert threads in (64, 128, 256) and x <= 1 << 22
         chunk = 16 * threads
@@ -124,14 +131,14 @@ def test_copy_launch_grid_is_dense(name):
     # the others one each
     nb = p.work_counts()[1]
     assert ft == 256 and fy == (1 if nb else 0) and (nb + 1) // 2 <= fx <= nb
-    # the two launches' algorithmic bytes add up to the rank's
-    parts = [p.kernel_traffic(k) for k in (0, 1)]
+    # the launches' algorithmic bytes add up to the rank's
+    parts = [p.kernel_traffic(k) for k in (0, 1, 4)]
     assert tuple(map(sum, zip(*parts))) == p.traffic()
     if name == "dsv3_ep64_to_ep8_fp8":
         # routed-expert blocks (97 %) are single-piece and the shared expert's
         # are row bands: all pair up
         assert fx == (nb + 1) // 2
-    _expect(wb.WB_EINVAL, p.launch_grid, 4, 0)
+    _expect(wb.WB_EINVAL, p.launch_grid, 5, 0)
     _expect(wb.WB_EINVAL, p.launch_grid, 0, 1)
 
 
