@@ -503,9 +503,6 @@ def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
     pack_bytes, unpack_bytes = pr + pw, ur + uw
     fwd_bytes = {st: sum(rplan.kernel_traffic(1 + st)) for st in (1, 2)} if G else {}
     stream = torch.cuda.current_stream()
-    if G and args.pipeline:
-        sys.exit("--pipeline and --node-size are not combined")
-
     if args.pipeline and nr < 2:
         sys.exit("--pipeline needs a round budget that gives more than one round")
     pstream, ustream = torch.cuda.Stream(), torch.cuda.Stream()
@@ -539,6 +536,9 @@ def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
                 splan.pack_round(k, src0, sends[k % 2], pstream)
                 packed[k].record(pstream)
                 ustream.wait_event(packed[k])
+                # the receiver's exchange stages of round k, then its assembly
+                for st in fwds:
+                    rplan.forward_round(k, st, recvs[k], fwds[st], ustream)
                 rplan.unpack_round(k, recvs[k], dst, ustream)
                 done[k].record(ustream)
             stream.wait_stream(ustream)
@@ -725,7 +725,8 @@ def main():
                     help="rollout ranks per node: plan with rollout de-duplication and the two exchange stages; "
                          "each step also runs the unpack rank's forward packings")
     ap.add_argument("--pipeline", action="store_true",
-                    help="with rounds: pack round k+1 on one stream while round k is assembled on another")
+                    help="with rounds: pack round k+1 on one stream while round k is forwarded (with --node-size) "
+                         "and assembled on another")
     ap.add_argument("--plan-stress", action="store_true",
                     help="wb_plan time on a 58-MoE-layer DeepSeek-V3-like catalog (44,776 tensors, EP64 -> EP8 fp8)")
     ap.add_argument("--probe", action="store_true",

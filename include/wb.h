@@ -206,11 +206,15 @@ int wb_plan(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role
  * count follows from the registered-buffer budget). round_budget > 0 bounds the
  * bytes any sender or receiver handles in one round: checkpoint tensors are
  * grouped into units (tensors whose images share an fp8 destination block are
- * one unit, so no block spans rounds), units are visited in catalog order and
- * a unit that would push some rank past the budget opens the next round (a
- * unit larger than the budget is a round of its own). Segments, owners and
- * balance equal those of wb_plan; each round has its own wire offsets under
- * the same rules. round_budget == 0 gives one round (wb_plan).
+ * one unit, so no block spans rounds) and each round is a run of units in
+ * catalog order. Filling with a cap X, a unit that would push some rank past
+ * X opens the next round (so a rank goes past X only through the round's
+ * first unit, one larger than X); the number of rounds n is what filling with the
+ * budget needs, and the rounds are the filling with the smallest cap X <=
+ * budget that still needs only n rounds, so they come out about equal.
+ * Segments, owners and balance equal those of wb_plan; each round has its own
+ * wire offsets under the same rules. round_budget == 0 gives one round
+ * (wb_plan).
  * Errors: as wb_plan; WB_EINVAL for a negative budget. */
 int wb_plan_rounds(const wb_layout_t* trainer, const wb_layout_t* rollout, int32_t role, int32_t rank,
                    int64_t round_budget, wb_plan_t** out);

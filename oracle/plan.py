@@ -394,29 +394,63 @@ def _block_units(rollout: Layout, ntensors: int) -> list[int]:
 
 
 def _assign_rounds(trainer: Layout, rollout: Layout, segments, budget: int) -> int:
+    """Cut the transfer into rounds, each a run of units (tensors that share
+    an fp8 block stay together) visited in catalog order.
+
+    Filling with a cap X means: a unit that would push some sender's send
+    bytes or some receiver's receive bytes past X opens the next round, so a
+    rank goes past X in a round only through the round's first unit (one
+    larger than X on its own). The number of rounds n is what
+    filling with the budget needs (App. D: the round count follows from the
+    registered-buffer budget). The rounds are then the filling with the
+    smallest cap X <= budget that still needs only n rounds (found by
+    bisection over whole bytes): the largest round is as small as n rounds
+    allow, so the model moves in chunks of about equal size (Sec. 3.2)."""
     unit = _block_units(rollout, len(trainer.catalog))
     members: dict[int, list] = {}
     for sg in segments:
         members.setdefault(unit[sg.t], []).append(sg)
     order = sorted(members, key=lambda u: min(sg.t for sg in members[u]))
-    rnd, cur_s, cur_d = 0, {}, {}
+    # bytes of each unit per rank: ("s", sender) and ("d", receiver)
+    size = []
     for u in order:
-        add_s, add_d = {}, {}
+        b = {}
         for sg in members[u]:
             if sg.stage == 0:
-                add_s[sg.s] = add_s.get(sg.s, 0) + sg.nbytes
-            add_d[sg.d] = add_d.get(sg.d, 0) + sg.nbytes
-        over = any(cur_s.get(k, 0) + v > budget for k, v in add_s.items()) or \
-            any(cur_d.get(k, 0) + v > budget for k, v in add_d.items())
-        if over and (cur_s or cur_d):
-            rnd, cur_s, cur_d = rnd + 1, {}, {}
-        for k, v in add_s.items():
-            cur_s[k] = cur_s.get(k, 0) + v
-        for k, v in add_d.items():
-            cur_d[k] = cur_d.get(k, 0) + v
+                b[("s", sg.s)] = b.get(("s", sg.s), 0) + sg.nbytes
+            b[("d", sg.d)] = b.get(("d", sg.d), 0) + sg.nbytes
+        size.append(b)
+
+    def fill(cap):
+        rounds, cur, r = [], {}, 0
+        for b in size:
+            if cur and any(cur.get(k, 0) + v > cap for k, v in b.items()):
+                r, cur = r + 1, {}
+            for k, v in b.items():
+                cur[k] = cur.get(k, 0) + v
+            rounds.append(r)
+        return rounds
+
+    rounds = fill(budget)
+    n = rounds[-1] + 1 if rounds else 1
+    total = {}
+    for b in size:
+        for k, v in b.items():
+            total[k] = total.get(k, 0) + v
+    lo = max([1] + [-(-t // n) for t in total.values()])
+    hi = budget
+    while lo < hi:
+        mid = lo + (hi - lo) // 2
+        cut = fill(mid)
+        if (cut[-1] + 1 if cut else 1) <= n:
+            hi = mid
+        else:
+            lo = mid + 1
+    rounds = fill(lo) if lo < budget else rounds
+    for r, u in zip(rounds, order):
         for sg in members[u]:
-            sg.round = rnd
-    return rnd + 1
+            sg.round = r
+    return (rounds[-1] + 1) if rounds else 1
 
 
 def dump(plan: Plan) -> str:

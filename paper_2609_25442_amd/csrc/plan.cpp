@@ -692,7 +692,15 @@ std::vector<int> block_units(const wb_layout_t& rollout, int ntensors) {
   return unit;
 }
 
-// Greedy rounds over units in order of their first tensor; returns the count.
+// Rounds: each a run of units (tensors sharing an fp8 block stay together)
+// in catalog order. Filling with a cap X: a unit that would push some
+// sender's send bytes or some receiver's receive bytes past X opens the next
+// round, so a rank goes past X in a round only through the round's first
+// unit (one larger than X on its own). The count n is what
+// filling with the budget needs (App. D); the rounds are the filling with the
+// smallest cap X <= budget that still needs only n rounds (bisection over
+// whole bytes), so the largest round is as small as n rounds allow and the
+// chunks come out about equal (Sec. 3.2). Returns n.
 int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::vector<Segment>& segs,
                   int64_t budget) {
   const int nt = static_cast<int>(trainer.catalog.size());
@@ -708,35 +716,56 @@ int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::v
   for (int u = 0; u < nt; ++u)
     if (!members[u].empty()) order.push_back(u);
   std::sort(order.begin(), order.end(), [&](int a, int b) { return first[a] < first[b]; });
+  // bytes of every unit per rank: keys 0..ns-1 senders, ns.. receivers
   const size_t ns = trainer.ranks.size(), nd = rollout.ranks.size();
-  std::vector<int64_t> cur_s(ns, 0), cur_d(nd, 0), add_s(ns, 0), add_d(nd, 0);
-  bool empty = true;
-  int rnd = 0;
-  for (int u : order) {
-    std::vector<int> ts, td;
-    for (size_t i : members[u]) {
+  std::vector<std::vector<std::pair<int, int64_t>>> size(order.size());
+  std::vector<int64_t> add(ns + nd, 0), total(ns + nd, 0);
+  for (size_t k = 0; k < order.size(); ++k) {
+    std::vector<int> keys;
+    for (size_t i : members[order[k]]) {
       const Segment& g = segs[i];
-      if (g.stage == 0) {
-        if (add_s[g.s] == 0) ts.push_back(g.s);
-        add_s[g.s] += g.bytes;
+      const int ks[2] = {g.stage == 0 ? g.s : -1, static_cast<int>(ns) + g.d};
+      for (int key : ks) {
+        if (key < 0) continue;
+        if (add[key] == 0) keys.push_back(key);
+        add[key] += g.bytes;
       }
-      if (add_d[g.d] == 0) td.push_back(g.d);
-      add_d[g.d] += g.bytes;
     }
-    bool over = false;
-    for (int s : ts) over = over || cur_s[s] + add_s[s] > budget;
-    for (int d : td) over = over || cur_d[d] + add_d[d] > budget;
-    if (over && !empty) {
-      ++rnd;
-      std::fill(cur_s.begin(), cur_s.end(), 0);
-      std::fill(cur_d.begin(), cur_d.end(), 0);
-    }
-    for (int s : ts) cur_s[s] += add_s[s], add_s[s] = 0;
-    for (int d : td) cur_d[d] += add_d[d], add_d[d] = 0;
-    empty = false;
-    for (size_t i : members[u]) segs[i].round = rnd;
+    for (int key : keys) size[k].push_back({key, add[key]}), total[key] += add[key], add[key] = 0;
   }
-  return rnd + 1;
+  std::vector<int> rounds(order.size(), 0);
+  std::vector<int64_t> cur(ns + nd, 0);
+  auto fill = [&](int64_t cap) {  // returns the number of rounds
+    std::fill(cur.begin(), cur.end(), 0);
+    int r = 0;
+    bool empty = true;
+    for (size_t k = 0; k < order.size(); ++k) {
+      bool over = false;
+      for (const auto& kv : size[k]) over = over || cur[kv.first] + kv.second > cap;
+      if (over && !empty) {
+        ++r;
+        std::fill(cur.begin(), cur.end(), 0);
+      }
+      for (const auto& kv : size[k]) cur[kv.first] += kv.second;
+      empty = false;
+      rounds[k] = r;
+    }
+    return r + 1;
+  };
+  const int n = fill(budget);
+  int64_t lo = 1, hi = budget;
+  for (int64_t t : total) lo = std::max(lo, (t + n - 1) / n);
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    if (fill(mid) <= n)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  fill(std::min(lo, budget));
+  for (size_t k = 0; k < order.size(); ++k)
+    for (size_t i : members[order[k]]) segs[i].round = rounds[k];
+  return order.empty() ? 1 : rounds.back() + 1;
 }
 
 // Wire offsets of one stage of round k (segments in canonical order, payloads

@@ -122,3 +122,13 @@ def overlapping_rollout_pair():
         ro.append(RankLayout([Local("x", "bf16", 1, 4, 4), Local("y", "bf16", 1, 1, 6)],
                              [Placement(0, r0, r0 + 4, 0, 4, 0, 0, 4), Placement(1, 0, 1, 0, 6, 1, 0, 6)]))
     return Layout(cat, tr), Layout(cat, ro)
+
+
+def hand_rounds_balanced_pair():
+    """The layout pair of tests/golden/hand_plan_rounds_balanced.txt."""
+    sizes = [38, 10, 10, 10, 38]
+    cat = [CkptTensor(f"T{i}", 1, n) for i, n in enumerate(sizes)]
+    tl = [Local(f"t{i}", "f32", 1, 1, n) for i, n in enumerate(sizes)]
+    pl = [Placement(i, 0, 1, 0, n, i, 0, n) for i, n in enumerate(sizes)]
+    rl = [Local(f"x{i}", "bf16", 1, 1, n) for i, n in enumerate(sizes)]
+    return Layout(cat, [RankLayout(tl, pl)]), Layout(cat, [RankLayout(rl, list(pl))])

@@ -64,6 +64,16 @@ def test_generic_builder_hand_plan():
     assert s.buffer_bytes == 4356 and s.peers() == [(0, 0, 272), (1, 4096, 260)]
 
 
+def test_hand_balanced_rounds_golden():
+    from oracle_cases import hand_rounds_balanced_pair
+    tr, ro = hand_rounds_balanced_pair()
+    golden = "".join(l for l in open(os.path.join(ROOT, "tests", "golden", "hand_plan_rounds_balanced.txt"))
+                     if not l.startswith("#"))
+    p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0, round_budget=200)
+    assert p.dump() == golden
+    assert [p.round_buffer_bytes(k) for k in range(3)] == [152, 552, 152]
+
+
 @pytest.mark.parametrize("seed", range(25))
 def test_random_tiny_plans_equal_oracle(seed):
     rng = np.random.default_rng(seed)

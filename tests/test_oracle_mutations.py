@@ -120,6 +120,27 @@ def _wire_align_128(mine, ns, nd):
 _orig_wire = plan._wire
 
 
+def _rounds_filled_to_budget(trainer, rollout, segments, budget):
+    # rounds filled greedily up to the budget, not re-cut into equal chunks
+    unit = plan._block_units(rollout, len(trainer.catalog))
+    order = sorted({unit[g.t] for g in segments}, key=lambda u: min(g.t for g in segments if unit[g.t] == u))
+    r, cur = 0, {}
+    for u in order:
+        mine = [g for g in segments if unit[g.t] == u]
+        add = {}
+        for g in mine:
+            if g.stage == 0:
+                add[("s", g.s)] = add.get(("s", g.s), 0) + g.nbytes
+            add[("d", g.d)] = add.get(("d", g.d), 0) + g.nbytes
+        if cur and any(cur.get(k, 0) + v > budget for k, v in add.items()):
+            r, cur = r + 1, {}
+        for k, v in add.items():
+            cur[k] = cur.get(k, 0) + v
+        for g in mine:
+            g.round = r
+    return r + 1
+
+
 def _quantize_flattened(lc, staged):
     # blocks tiled over the flattened [batch * rows, cols] matrix (scales kept right)
     x = staged.view(np.float32)
@@ -168,6 +189,8 @@ MUTANTS = {
     "payloads 128-byte aligned": (plan, "_wire", _wire_align_128, [T_plan.test_hand_plan_matches_golden]),
     "rounds ignore the budget": (plan, "_assign_rounds", lambda tr, ro, segs, budget: 1,
                                  [T_rounds.test_hand_rounds_match_golden]),
+    "rounds filled up to the budget, not balanced": (plan, "_assign_rounds", _rounds_filled_to_budget,
+                                                     [T_rounds.test_hand_balanced_rounds_match_golden]),
     # exchange stages
     "rollout groups keep only their lowest holder": (plan, "_rollout_groups", _groups_lowest_holder_only,
                                                      [T_exchange.test_hand_exchange_plan_matches_golden]),

@@ -13,7 +13,7 @@ from oracle.plan import build_plan, dump
 from oracle.transfer import expected_rollout, local_index, materialize, network, pack, unpack
 from synthetic_checkpoint.workloads import ORDER, WORKLOADS, scaled
 
-from oracle_cases import hand_rounds_pair, random_model, random_par
+from oracle_cases import hand_rounds_balanced_pair, hand_rounds_pair, random_model, random_par
 from test_oracle_plan import wire_check
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -25,6 +25,87 @@ def test_hand_rounds_match_golden():
     assert dump(build_plan(tr, ro, round_budget=160)) == want
     # a budget of zero means one round and the single-round form
     assert "rounds=" not in dump(build_plan(tr, ro))
+
+
+def test_hand_balanced_rounds_match_golden():
+    tr, ro = hand_rounds_balanced_pair()
+    want = "".join(l for l in open(os.path.join(GOLDEN, "hand_plan_rounds_balanced.txt")) if not l.startswith("#"))
+    assert dump(build_plan(tr, ro, round_budget=200)) == want
+
+
+def _partitions(k, parts):
+    """Every split of k units in order into ``parts`` non-empty runs, as run
+    boundaries [0, b1, ..., k]."""
+    import itertools
+    for cuts in itertools.combinations(range(1, k), parts - 1):
+        yield [0, *cuts, k]
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_rounds_are_min_max_balanced(seed):
+    """Brute force over every way to cut a few units into runs: the plan takes
+    the fewest rounds whose runs fit the budget, and among cuts into that
+    many rounds its largest run is the smallest possible, or at most the even
+    share ceil(total / rounds) of the busiest rank. A run's size is the most
+    bytes it gives a rank that some unit after its first touches (a rank may
+    go past the cap only through the first unit of its round, which can be
+    larger than the cap on its own)."""
+    from oracle.catalog import CkptTensor
+    from oracle.layout import Layout, Local, Placement, RankLayout
+    rng = np.random.default_rng(700 + seed)
+    k = int(rng.integers(3, 9))
+    sizes = [int(x) for x in rng.integers(1, 40, k)]
+    cat = [CkptTensor(f"T{i}", 1, n) for i, n in enumerate(sizes)]
+    # two trainer ranks: a tensor held by one of them or by both (then split)
+    held = [int(rng.integers(0, 3)) for _ in range(k)]
+    trs = []
+    for r in range(2):
+        ts = [i for i in range(k) if held[i] in (r, 2)]
+        trs.append(RankLayout([Local(f"t{i}", "f32", 1, 1, sizes[i]) for i in ts],
+                              [Placement(i, 0, 1, 0, sizes[i], j, 0, sizes[i]) for j, i in enumerate(ts)]))
+    # two rollout ranks: every tensor wanted by one or both
+    want = [int(rng.integers(0, 3)) for _ in range(k)]
+    ros = []
+    for d in range(2):
+        ts = [i for i in range(k) if want[i] in (d, 2)]
+        ros.append(RankLayout([Local(f"x{i}", "bf16", 1, 1, sizes[i]) for i in ts],
+                              [Placement(i, 0, 1, 0, sizes[i], j, 0, sizes[i]) for j, i in enumerate(ts)]))
+    tr, ro = Layout(cat, trs), Layout(cat, ros)
+    one = build_plan(tr, ro)
+    unit_bytes = []
+    for i in range(k):
+        b = {}
+        for g in one.segments:
+            if g.t == i:
+                b[("s", g.s)] = b.get(("s", g.s), 0) + g.nbytes
+                b[("d", g.d)] = b.get(("d", g.d), 0) + g.nbytes
+        unit_bytes.append(b)
+    largest = max(max(b.values()) for b in unit_bytes)
+    total = sum(sum(b.values()) for b in unit_bytes)
+    budget = int(rng.integers(largest // 2 + 1, max(largest // 2 + 2, total // 3)))
+
+    def cost(bounds):  # the largest run: bytes of ranks that a unit after its first touches
+        worst = 0
+        for a, z in zip(bounds, bounds[1:]):
+            per, later = {}, set()
+            for j, b in enumerate(unit_bytes[a:z]):
+                for key, v in b.items():
+                    per[key] = per.get(key, 0) + v
+                    if j:
+                        later.add(key)
+            worst = max([worst] + [per[key] for key in later])
+        return worst
+
+    n = next(p for p in range(1, k + 1) if any(cost(c) <= budget for c in _partitions(k, p)))
+    best = min(cost(c) for p in range(1, n + 1) for c in _partitions(k, p))
+    plan = build_plan(tr, ro, round_budget=budget)
+    assert len(plan.rounds) == n
+    rounds = [min(g.round for g in plan.segments if g.t == i) for i in range(k)]
+    assert rounds == sorted(rounds) and all(g.round == rounds[g.t] for g in plan.segments)
+    bounds = [0] + [i for i in range(1, k) if rounds[i] != rounds[i - 1]] + [k]
+    share = max(-(-sum(b.get(key, 0) for b in unit_bytes) // n) for key in set().union(*unit_bytes))
+    got = cost(bounds)
+    assert got <= budget and (got == best or got <= share), (got, best, share, bounds)
 
 
 def _round_checks(plan, budget):
