@@ -22,8 +22,14 @@ Readings (the paper leaves these open):
 * local tensors are seen as 2-D [batch * rows, cols] fields (a flat buffer is
   one row), and diff2 keeps the tensor's own extent (A = 0 above and to the
   left, nothing is stored past the end);
-* the recombination here is exact on the host; the paper's strided carry
-  records (which keep every pass's list small) are not modelled.
+* the carry (Algorithm 1: ExpandCarry, EmitCarry, with D <- D + carries
+  before NonZeros): pass k's field S_k = diff2(C_k) + Q_(k-1) is split into
+  the entries kept, R_k = S_k mod 2^b (in [0, 2^b)), and the carry into the
+  next pass, Q_k = floor(S_k / 2^b); the last pass keeps S_k whole. Then
+  sum_k 2^(b k) R_k = diff2(A) exactly, and R_k is zero wherever diff2(A) is
+  (the chunk wrap-arounds move into the carries), so every pass keeps only
+  entries next to slice-copy corners. The carries are a sparse field of their
+  own; how they travel between passes is not modelled here.
 
 Everything is computed densely on small tensors with plain integer numpy.
 """
@@ -97,6 +103,28 @@ def recombine(per_chunk: list[dict], b: int) -> dict:
         for pos, v in z.items():
             out[pos] = out.get(pos, 0) + (v << (b * k))
     return {pos: v for pos, v in out.items() if v}
+
+
+def carry_passes(chunk_fields: list[np.ndarray], b: int) -> tuple[list[dict], list[dict]]:
+    """Algorithm 1 with carries, on the chunk fields C_0 .. C_(K-1) of one
+    tensor: for k = 0 .. K-1, D = diff2(C_k) plus the carries of pass k - 1
+    (ExpandCarry; none before pass 0); the entries kept for pass k are
+    NonZeros of D mod 2^b, and D's carry part floor(D / 2^b) goes to pass k + 1
+    (EmitCarry); the last pass keeps D itself. Returns the kept entries and
+    the carries of every pass (the last pass's carries are empty)."""
+    K = len(chunk_fields)
+    kept, carries = [], []
+    Q = np.zeros(chunk_fields[0].shape, dtype=np.int64)
+    for k, C in enumerate(chunk_fields):
+        D = diff2(np.asarray(C, dtype=np.int64)) + Q
+        if k == K - 1:
+            kept.append(nonzeros(D))
+            Q = np.zeros_like(D)
+        else:
+            kept.append(nonzeros(np.mod(D, 1 << b)))
+            Q = np.floor_divide(D, 1 << b)
+        carries.append(nonzeros(Q))
+    return kept, carries
 
 
 def dense(Z: dict, R: int, C: int) -> np.ndarray:

@@ -7,6 +7,13 @@
   differences, supported on at most 16 points (the paper's bound);
 * diff1 is inverted by a two-dimensional prefix sum, so diff2 is lossless;
 * chunked passes recombine exactly to diff2 of the full identifiers;
+* the per-pass carries (Algorithm 1, ExpandCarry and EmitCarry): two worked
+  examples derived by hand (tests/golden/diff2_carries_b4.txt); the carries
+  of pass k equal floor(diff2(A mod M) / M) and the entries kept up to pass k
+  sum to diff2(A mod M) mod M, M = 2^(b (k + 1)) (A mod M is what the first
+  k + 1 chunks hold, and diff2 is linear); the kept entries recombine to
+  diff2(A), lie where diff2(A) is non-zero, and are below 2^b except in the
+  last pass;
 * on every workload (scaled) and on random layouts, the recombined entries of
   every local tensor number at most 16 per placement and give back the exact
   identifier field of the declared placements.
@@ -18,8 +25,8 @@ import numpy as np
 import pytest
 
 from oracle.catalog import CkptTensor
-from oracle.diff2 import (FIRST_ID, chunk_bits, decode, dense, diff1, diff2, field_from_nonzeros, first_ids,
-                          id_chunk, id_fields, nonzeros, num_chunks, probe_fields, recombine, undiff2)
+from oracle.diff2 import (FIRST_ID, carry_passes, chunk_bits, decode, dense, diff1, diff2, field_from_nonzeros,
+                          first_ids, id_chunk, id_fields, nonzeros, num_chunks, probe_fields, recombine, undiff2)
 from oracle.layout import Layout, Local, Placement, RankLayout, describe_layout, layout_from_spec
 from synthetic_checkpoint.workloads import ORDER, scaled
 
@@ -92,6 +99,78 @@ def test_chunked_passes_recombine_exactly(b, seed):
     chunks = [nonzeros(diff2(id_chunk(A, k, b))) for k in range(-(-50 // b))]
     assert recombine(chunks, b) == nonzeros(diff2(A))
     assert np.array_equal(sum(id_chunk(A, k, b) << (b * k) for k in range(-(-50 // b))), A)
+
+
+def _golden_carries():
+    cases, kept, carried = {}, {}, {}
+    for line in open(os.path.join(GOLDEN, "diff2_carries_b4.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        w = line.split()
+        if w[0] == "field":
+            b, K, R, C = map(int, w[2:6])
+            cases[w[1]] = (b, K, np.array(list(map(int, w[6:])), dtype=np.int64).reshape(R, C))
+            kept[w[1]] = [{} for _ in range(K)]
+            carried[w[1]] = [{} for _ in range(K)]
+        else:
+            k, i, j, v = map(int, w[2:])
+            (kept if w[0] == "kept" else carried)[w[1]][k][(i, j)] = v
+    return cases, kept, carried
+
+
+def test_carry_hand_worked_examples():
+    cases, kept, carried = _golden_carries()
+    assert set(cases) == {"row", "slab"}
+    for name, (b, K, A) in cases.items():
+        got_kept, got_carries = carry_passes([id_chunk(A, k, b) for k in range(K)], b)
+        assert got_kept == kept[name], name
+        assert got_carries == carried[name], name
+        assert recombine(got_kept, b) == nonzeros(diff2(A))
+
+
+def _check_carries(A, b, K):
+    kept, carries = carry_passes([id_chunk(A, k, b) for k in range(K)], b)
+    assert recombine(kept, b) == nonzeros(diff2(A))
+    support = nonzeros(diff2(A))
+    for k in range(K):
+        assert set(kept[k]) <= set(support), k
+        if k < K - 1:
+            assert all(0 < v < (1 << b) for v in kept[k].values())
+            M = 1 << (b * (k + 1))
+            P = diff2(np.mod(A, M))
+            assert carries[k] == nonzeros(np.floor_divide(P, M)), k
+            low = sum((dense(kept[j], *A.shape) << (b * j)) for j in range(k + 1))
+            assert np.array_equal(low, np.mod(P, M)), k
+        else:
+            assert carries[k] == {}
+    return kept, carries
+
+
+@pytest.mark.parametrize("b", [4, 16])
+@pytest.mark.parametrize("seed", range(8))
+def test_carries_closed_form_on_random_fields(b, seed):
+    rng = np.random.default_rng(400 + seed)
+    A = rng.integers(0, 2**40, size=(int(rng.integers(1, 24)), int(rng.integers(1, 24))))
+    A[rng.random(A.shape) < 0.3] = 0
+    _check_carries(A, b, -(-40 // b))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_carries_keep_only_corner_entries_of_slice_copies(seed):
+    # identifiers of random layouts, shifted so that 4-bit chunks wrap many
+    # times inside every slice copy and 16-bit chunks wrap across 2^32
+    rng = np.random.default_rng(500 + seed)
+    m = random_model(rng)
+    L = describe_layout(m, random_par(rng, m, "rollout"))
+    r = int(rng.integers(0, L.nranks))
+    for A in id_fields(L, r):
+        for b, shift in ((4, 0), (16, (1 << 32) - int(rng.integers(1, max(2, A.size))))):
+            B = np.where(A > 0, A + shift, 0)
+            K = -(-int(B.max()).bit_length() // b) if B.max() > 0 else 1
+            kept, carries = _check_carries(B, b, K)
+            # the wrap-arounds leave many carries but no kept entries of their own
+            if b == 4 and A.size >= 64 and np.count_nonzero(A) == A.size:
+                assert sum(map(len, carries)) > 0
 
 
 def _check_rank(layout, rank):

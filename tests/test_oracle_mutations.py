@@ -91,6 +91,24 @@ def _recombine_shifted(per_chunk, b):
     return {pos: v for pos, v in out.items() if v}
 
 
+def _carry_passes_variant(drop=False, trunc=False, last_low=False):
+    def run(chunk_fields, b):
+        K = len(chunk_fields)
+        kept, carries = [], []
+        Q = np.zeros(chunk_fields[0].shape, dtype=np.int64)
+        for k, C in enumerate(chunk_fields):
+            D = diff2.diff2(np.asarray(C, dtype=np.int64)) + (0 if drop else Q)
+            if k == K - 1 and not last_low:
+                kept.append(diff2.nonzeros(D))
+                Q = np.zeros_like(D)
+            else:
+                Q = (np.trunc(D / (1 << b)).astype(np.int64) if trunc else np.floor_divide(D, 1 << b))
+                kept.append(diff2.nonzeros(D - (Q << b)))
+            carries.append(diff2.nonzeros(Q))
+        return kept, carries
+    return run
+
+
 _orig_flat_run_rects = layout.flat_run_rects
 
 
@@ -200,6 +218,15 @@ MUTANTS = {
                                              [lambda: T_diff2.test_chunked_passes_recombine_exactly(16, 0),
                                               lambda: T_diff2.test_workloads_probe_recovers_fields(
                                                   "llama3_8b_fsdp8_to_tp1")]),
+    "carries not added to the next pass": (diff2, "carry_passes", _carry_passes_variant(drop=True),
+                                           [T_diff2.test_carry_hand_worked_examples,
+                                            lambda: T_diff2.test_carries_closed_form_on_random_fields(16, 0)]),
+    "carries truncated toward zero": (diff2, "carry_passes", _carry_passes_variant(trunc=True),
+                                      [T_diff2.test_carry_hand_worked_examples,
+                                       lambda: T_diff2.test_carries_closed_form_on_random_fields(16, 0)]),
+    "last pass keeps only its low bits": (diff2, "carry_passes", _carry_passes_variant(last_low=True),
+                                          [T_diff2.test_carry_hand_worked_examples,
+                                           lambda: T_diff2.test_carries_keep_only_corner_entries_of_slice_copies(0)]),
 }
 
 
