@@ -355,20 +355,28 @@ def run_probe(args):
 
         declared = wb.Layout.describe(w["model"], par)
         cat = declared.tensors()
-        stats = {}
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        got = wb.probe_layout(cat, dtype, [load], stats=stats)
-        ms = (time.perf_counter() - t0) * 1e3
         keep = [u for u, lc in enumerate(declared.locals(rank)) if lc["scales"] < 0]
         remap = {u: i for i, u in enumerate(keep)}
         want = sorted((t, r0, r1, c0, c1, remap[u], b, ld, tr)
                       for (t, r0, r1, c0, c1, u, b, ld, tr) in declared.placements(rank))
-        same = sorted(got.placements(0)) == want
-        log(f"[probe] {side} rank {rank}: {ms:.0f} ms, recovered == declared: {same}")
-        # the stencil alone: one batched launch over the loaded tensors of pass 0,
-        # and one over all passes held on the device (what the probe above ran
-        # when it held them); the timed call includes its small table upload
+        modes = {}
+        for hold in (True, False):
+            stats = {}
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            got = wb.probe_layout(cat, dtype, [load], stats=stats, hold_passes=hold)
+            ms = (time.perf_counter() - t0) * 1e3
+            same = sorted(got.placements(0)) == want
+            label = "held_passes" if hold else "carried_passes"
+            log(f"[probe] {side} rank {rank} {label}: {ms:.0f} ms, recovered == declared: {same}")
+            modes[label] = {"probe_ms": round(ms, 1), "recovered_equals_declared": same, "passes": stats[0],
+                            "scan_ms": round(stats["scan_s"][0] * 1e3, 1),
+                            "carry_retries": len(stats.get("carry_retries", []))}
+            del got
+        # the stencils alone: each carry pass over the loaded tensors of that
+        # pass (in order, since a pass reads the carries of the one before),
+        # and one launch over all passes held on the device; a timed call
+        # includes its small table upload
         probe = wb.Probe(cat, dtype)
         ckpt = {n: torch.empty((r, c), dtype=wb.torch_dtype(dtype), device="cuda") for n, r, c in cat}
         held = []
@@ -376,36 +384,58 @@ def run_probe(args):
             for t, (n, r, c) in enumerate(cat):
                 wb.make_ids(ckpt[n], dtype, probe.first_id(t), k)
             held.append([x.clone() for x in load(ckpt)])
+        del ckpt
         shapes = [wb._view_shape(x) for x in held[0]]
-        one = [(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(held[0], shapes)]
+        per_pass = [[(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(h, shapes)] for h in held]
         every = [([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)]
         cap = 1 << 21
         idx = torch.empty(cap, dtype=torch.int64, device="cuda")
         val = torch.empty(cap, dtype=torch.int64, device="cuda")
         count = torch.zeros(1, dtype=torch.int64, device="cuda")
+        carries = torch.zeros(1, dtype=torch.int64, device="cuda")
         nbytes = sum(x.numel() * x.element_size() for x in held[0])
+        numel = sum(x.numel() for x in held[0])
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         stencil = {}
-        for label, fields, npass in (("one_pass", one, 1), ("all_passes", every, probe.num_chunks)):
-            ws = torch.empty(wb.diff2_batch_workspace(fields), dtype=torch.uint8, device="cuda")
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            times = []
-            for rep in range(4):
+        ccap = 16 * (numel >> 16) + 64 * len(shapes) + 4096
+        ws = torch.empty(wb.diff2_carry_workspace(per_pass[0], ccap), dtype=torch.uint8, device="cuda")
+        times = [[] for _ in held]
+        got_counts = [None] * len(held)
+        for rep in range(4):
+            for k, fields in enumerate(per_pass):
                 ev[0].record()
-                wb.diff2_batch(fields, idx, val, count, ws)
+                wb.diff2_carry(fields, k, k + 1 == len(held), ccap, idx, val, count, carries, ws)
                 ev[1].record()
                 torch.cuda.synchronize()
-                times.append(ev[0].elapsed_time(ev[1]))
-            best = min(times[1:])
-            rate = nbytes * npass / (best * 1e-3) / 1e9
-            stencil[label] = {"launches": 1, "bytes": nbytes * npass, "entries": int(count.item()),
-                              "table_bytes": ws.numel(), "ms": round(best, 3), "GB/s": round(rate, 1),
-                              "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
-            log(f"[probe] {side} diff2 {label}: {best:.3f} ms, {rate:.0f} GB/s, {int(count.item())} entries")
-        out["ranks"][side] = {"rank": rank, "probe_ms": round(ms, 1), "recovered_equals_declared": same,
-                              "placements": len(want), "local_tensors": len(keep),
-                              "hold_passes": stats["hold_passes"][0], "passes": stats[0],
-                              "scan_ms": round(stats["scan_s"][0] * 1e3, 1), "diff2": stencil}
-        del held, one, every, ckpt, idx, val, got
+                times[k].append(ev[0].elapsed_time(ev[1]))
+                got_counts[k] = (int(count.item()), int(carries.item()))
+        for k in range(len(held)):
+            best = min(times[k][1:])
+            rate = nbytes / (best * 1e-3) / 1e9
+            stencil[f"carry_pass_{k}"] = {"bytes": nbytes, "entries": got_counts[k][0], "carries": got_counts[k][1],
+                                          "carry_capacity": ccap, "workspace_bytes": ws.numel(),
+                                          "ms": round(best, 3), "GB/s": round(rate, 1),
+                                          "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+            log(f"[probe] {side} diff2 carry pass {k}: {best:.3f} ms, {rate:.0f} GB/s, "
+                f"{got_counts[k][0]} entries, {got_counts[k][1]} carries")
+        del ws
+        ws = torch.empty(wb.diff2_batch_workspace(every), dtype=torch.uint8, device="cuda")
+        times = []
+        for rep in range(4):
+            ev[0].record()
+            wb.diff2_batch(every, idx, val, count, ws)
+            ev[1].record()
+            torch.cuda.synchronize()
+            times.append(ev[0].elapsed_time(ev[1]))
+        best = min(times[1:])
+        rate = nbytes * len(held) / (best * 1e-3) / 1e9
+        stencil["all_passes"] = {"launches": 1, "bytes": nbytes * len(held), "entries": int(count.item()),
+                                 "table_bytes": ws.numel(), "ms": round(best, 3), "GB/s": round(rate, 1),
+                                 "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+        log(f"[probe] {side} diff2 all_passes: {best:.3f} ms, {rate:.0f} GB/s, {int(count.item())} entries")
+        out["ranks"][side] = {"rank": rank, "placements": len(want), "local_tensors": len(keep), **modes,
+                              "diff2": stencil}
+        del held, per_pass, every, idx, val, ws
         torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 

@@ -485,6 +485,45 @@ int wb_diff2_batch_workspace(const wb_field* fields, int32_t n, size_t* bytes);
 int wb_diff2_batch(const wb_field* fields, int32_t n, void* workspace, size_t workspace_bytes, int64_t* index,
                    int64_t* value, int64_t capacity, uint64_t* count, void* stream);
 
+/* Device workspace bytes wb_diff2_carry needs for these n one-pass fields
+ * and room for carry_capacity carries per pass: the tile tables, 2 KiB of
+ * counters, two carry tables of 16-byte slots, each as many slots as the
+ * smallest power of two at least twice carry_capacity (and 64), and 1028
+ * bytes per stencil workgroup for staging its carries. Errors:
+ * WB_EINVAL (bad field, a field of more than one pass, carry_capacity outside
+ * 1..2^36). */
+int wb_diff2_carry_workspace(const wb_field* fields, int32_t n, int64_t carry_capacity, size_t* bytes);
+/* One probing pass with carries (App. B, Algorithm 1: ExpandCarry and
+ * EmitCarry), for loading passes that are not kept: fields are the loaded
+ * local tensors after pass `pass` (one pass each, the same fields in the same
+ * order every pass), `last` is non-zero for the final pass. With D = diff2 of
+ * the pass's chunk field and Q the carries pass - 1 left (none for pass 0),
+ * S = D + Q; a pass other than the last appends (position, S mod 2^16) where
+ * that is non-zero and keeps floor(S / 2^16) as its carries, the last appends
+ * S whole. Then the sum over passes of 2^(16 pass) times the appended values
+ * is diff2 of the identifier field, every value of a pass but the last lies
+ * in 1..65535, and entries appear only where diff2 of the identifier field is
+ * non-zero (next to slice-copy corners): a chunk's wrap-arounds stay in the
+ * carries, on the device. Positions, index, value, capacity and count are as
+ * for wb_diff2_batch (the counter is reset by the call). *carries (device,
+ * 8-byte aligned) gets the number of carries the pass kept (0 for the last
+ * pass); above carry_capacity (or, very rarely, when a carry found no free
+ * slot near its hash, reported as carry_capacity + 1) carries may be lost and
+ * this and later passes are wrong: start again from pass 0 with more room. A pass
+ * whose count exceeded capacity can be run again with more room (same
+ * workspace, same fields). workspace: device memory of at least
+ * wb_diff2_carry_workspace bytes, 8-byte aligned, owned by the caller, the
+ * same buffer with the same carry_capacity for every pass of one probe (it
+ * holds the carries between passes). The call copies the tile table into it
+ * on `stream` and waits for that copy. Passes on one workspace must not
+ * overlap. Six launches at most; the stencil reads each element about once.
+ * Errors: as for wb_diff2_batch, and WB_EINVAL for a field of more than one
+ * pass, a negative pass, a null or misaligned carries, carry_capacity outside
+ * 1..2^36. */
+int wb_diff2_carry(const wb_field* fields, int32_t n, int32_t pass, int32_t last, int64_t carry_capacity,
+                   void* workspace, size_t workspace_bytes, int64_t* index, int64_t* value, int64_t capacity,
+                   uint64_t* count, uint64_t* carries, void* stream);
+
 /* Message of the calling thread's last failed call ("" if none). */
 const char* wb_last_error(void);
 const char* wb_version(void);

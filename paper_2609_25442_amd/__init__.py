@@ -135,6 +135,9 @@ def _load():
         "wb_diff2_batch_workspace": [POINTER(Field), c_int32, POINTER(c_size_t)],
         "wb_diff2_batch": [POINTER(Field), c_int32, c_void_p, c_size_t, c_void_p, c_void_p, c_int64, c_void_p,
                            c_void_p],
+        "wb_diff2_carry_workspace": [POINTER(Field), c_int32, c_int64, POINTER(c_size_t)],
+        "wb_diff2_carry": [POINTER(Field), c_int32, c_int32, c_int32, c_int64, c_void_p, c_size_t, c_void_p,
+                           c_void_p, c_int64, c_void_p, c_void_p, c_void_p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -628,6 +631,29 @@ def diff2_batch(fields, index, value, count, workspace, stream=None):
                               _ptr(value), index.numel(), _ptr(count), _stream_handle(stream)))
 
 
+def diff2_carry_workspace(fields, carry_capacity: int) -> int:
+    """Device workspace bytes of diff2_carry over one-pass ``fields`` with
+    room for ``carry_capacity`` carries per pass."""
+    arr = _field_array(fields)
+    v = c_size_t()
+    _check(lib.wb_diff2_carry_workspace(arr, len(fields), carry_capacity, byref(v)))
+    return v.value
+
+
+def diff2_carry(fields, pass_: int, last: bool, carry_capacity: int, index, value, count, carries, workspace,
+                stream=None):
+    """One probing pass with carries kept on the device (App. B): entries
+    of pass ``pass_`` (values in 1..65535 except in the last pass) into the
+    device tensors index and value (int64); count and carries (uint64 device
+    scalars) get the number of entries and of carries kept for the next
+    pass. ``fields`` as for diff2_batch with one tensor each; ``workspace``
+    (uint8, diff2_carry_workspace bytes) is the same tensor every pass."""
+    arr = _field_array(fields)
+    _check(lib.wb_diff2_carry(arr, len(fields), pass_, int(bool(last)), carry_capacity, _ptr(workspace),
+                              workspace.numel(), _ptr(index), _ptr(value), index.numel(), _ptr(count), _ptr(carries),
+                              _stream_handle(stream)))
+
+
 def _view_shape(t):
     if t.dim() == 1:
         return 1, 1, t.shape[0]
@@ -655,6 +681,31 @@ def _batched_entries(fields, cap, device):
         cap = n
 
 
+class _CarryRoom(Exception):
+    """A carry pass kept more carries than its tables hold."""
+
+    def __init__(self, need):
+        super().__init__(need)
+        self.need = need
+
+
+def _carry_entries(fields, k, last, st, device):
+    """Run carry pass k, growing the entry arrays until they hold every entry
+    (a pass can be run again on the same workspace); returns host (index,
+    value) arrays and the number of carries kept."""
+    import torch
+
+    while True:
+        diff2_carry(fields, k, last, st["cap"], st["idx"], st["val"], st["count"], st["carries"], st["ws"])
+        n, c = int(st["count"].item()), int(st["carries"].item())
+        if c > st["cap"]:
+            raise _CarryRoom(c)
+        if n <= st["idx"].numel():
+            return st["idx"][:n].cpu().numpy(), st["val"][:n].cpu().numpy(), c
+        st["idx"] = torch.empty(n, dtype=torch.int64, device=device)
+        st["val"] = torch.empty(n, dtype=torch.int64, device=device)
+
+
 def _record_split(probe, chunk, offsets, index, value):
     """Hand batched entries to the probe, local tensor by local tensor."""
     import numpy as np
@@ -668,7 +719,7 @@ def _record_split(probe, chunk, offsets, index, value):
 
 
 def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", stats=None,
-                 hold_passes=None) -> "Layout":
+                 hold_passes=None, carry_capacity=None) -> "Layout":
     """Discover a layout from weight loaders: ``loaders[r](ckpt)`` takes the
     checkpoint as {name: tensor} and returns rank r's local tensors (a list of
     1-, 2- or 3-D tensors, always the same shapes, values copied unchanged).
@@ -677,71 +728,108 @@ def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", s
     With ``hold_passes`` a copy of every pass's loaded tensors stays in device
     memory and one diff2 launch over all passes runs at the end (the chunk
     wrap-arounds cancel inside it, so only the identifier field's few entries
-    reach the host); otherwise each pass gets one launch and its entries are
-    recorded before the next load. None picks holding when the passes fit in free
-    device memory with a quarter to spare. ``stats`` (a dict) receives timings
-    and entry counts when given."""
-    import time
-
-    import numpy as np
-    import torch
-
+    reach the host). Otherwise every pass runs diff2_carry as soon as it is
+    loaded: each pass hands the host only the entries next to slice-copy
+    corners and keeps its wrap-arounds as device carries for the next pass
+    (``carry_capacity`` carries per pass, by default about 16 per 2^16
+    elements; a rank whose passes need more is probed again with room for
+    what they needed). None picks holding when the passes fit in free device
+    memory with a quarter to spare. ``stats`` (a dict) receives timings and
+    entry counts when given."""
     tdt = torch_dtype(ckpt_dtype)
     layout = Layout.create(catalog, len(loaders))
-    ckpt = {n: torch.empty((r, c), dtype=tdt, device=device) for n, r, c in catalog}
+    ckpt = {}
     for r, load in enumerate(loaders):
-        probe = Probe(catalog, ckpt_dtype)
-        shapes, held, hold = None, [], hold_passes
-        rec = stats.setdefault(r, []) if stats is not None else None
-        for k in range(probe.num_chunks):
-            t0 = time.perf_counter()
-            for t, (n, rows, cols) in enumerate(catalog):
-                make_ids(ckpt[n], ckpt_dtype, probe.first_id(t), k)
-            t1 = time.perf_counter()
-            locs = load(ckpt)
-            torch.cuda.synchronize()
-            t2 = time.perf_counter()
-            if shapes is None:
-                shapes = [_view_shape(x) for x in locs]
-                for u, (b, rr, cc) in enumerate(shapes):
-                    probe.add_local(names[r][u] if names else f"local{u}", ckpt_dtype, b, rr, cc)
-                offsets = np.cumsum([0] + [b * rr * cc for b, rr, cc in shapes]).astype(np.int64)
-                if hold is None:
-                    need = (probe.num_chunks - 1) * sum(x.numel() * x.element_size() for x in locs)
-                    hold = need * 4 <= torch.cuda.mem_get_info()[0] * 3
-            for u, x in enumerate(locs):
-                if x.dtype != tdt or not x.is_contiguous() or _view_shape(x) != shapes[u]:
-                    raise ValueError(f"loader of rank {r} returned a changed or non-contiguous tensor {u}")
-            entries = 0
-            if hold:
-                # a loader may write into the same buffers every pass, or hand
-                # back checkpoint tensors, which the next pass overwrites
-                held.append([x.clone() for x in locs] if k + 1 < probe.num_chunks else locs)
-            else:
-                fields = [(x, ckpt_dtype, b * rr, cc) for x, (b, rr, cc) in zip(locs, shapes)]
-                idx, val = _batched_entries(fields, max(1 << 16, int(offsets[-1]) // 8192), device)
-                _record_split(probe, k, offsets, idx, val)
-                entries = len(idx)
-            del locs
-            t3 = time.perf_counter()
-            if rec is not None:
-                rec.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries})
-        if hold:
-            t2 = time.perf_counter()
-            fields = [([held[k][u] for k in range(probe.num_chunks)], ckpt_dtype, b * rr, cc)
-                      for u, (b, rr, cc) in enumerate(shapes)]
-            idx, val = _batched_entries(fields, 1 << 16, device)
-            _record_split(probe, 0, offsets, idx, val)
-            del fields, held
-            if rec is not None:
-                rec.append({"pass": "all", "diff2_s": time.perf_counter() - t2, "entries": len(idx)})
-        t4 = time.perf_counter()
+        cap = carry_capacity
+        while True:
+            try:
+                probe, hold = _probe_rank(catalog, ckpt_dtype, tdt, load, r, names, device, stats, hold_passes, cap,
+                                          ckpt)
+                break
+            except _CarryRoom as room:
+                cap = room.need + room.need // 4 + 4096
+                if stats is not None:
+                    stats.setdefault("carry_retries", []).append(cap)
+        t4 = _now()
         probe.scan(layout, r)
         if stats is not None:
-            stats.setdefault("scan_s", []).append(time.perf_counter() - t4)
+            stats.setdefault("scan_s", []).append(_now() - t4)
             stats.setdefault("hold_passes", []).append(bool(hold))
         del probe
     return layout
+
+
+def _now():
+    import time
+
+    return time.perf_counter()
+
+
+def _probe_rank(catalog, ckpt_dtype, tdt, load, r, names, device, stats, hold_passes, carry_capacity, ckpt):
+    """Probe one rank; returns the filled Probe and whether passes were held."""
+    import numpy as np
+    import torch
+
+    if not ckpt:
+        ckpt.update({n: torch.empty((rows, cols), dtype=tdt, device=device) for n, rows, cols in catalog})
+    probe = Probe(catalog, ckpt_dtype)
+    shapes, held, hold, carry = None, [], hold_passes, None
+    rec = stats.setdefault(r, []) if stats is not None else None
+    if rec is not None:
+        rec.clear()
+    for k in range(probe.num_chunks):
+        last = k + 1 == probe.num_chunks
+        t0 = _now()
+        for t, (n, rows, cols) in enumerate(catalog):
+            make_ids(ckpt[n], ckpt_dtype, probe.first_id(t), k)
+        t1 = _now()
+        locs = load(ckpt)
+        torch.cuda.synchronize()
+        t2 = _now()
+        if shapes is None:
+            shapes = [_view_shape(x) for x in locs]
+            for u, (b, rr, cc) in enumerate(shapes):
+                probe.add_local(names[r][u] if names else f"local{u}", ckpt_dtype, b, rr, cc)
+            offsets = np.cumsum([0] + [b * rr * cc for b, rr, cc in shapes]).astype(np.int64)
+            if hold is None:
+                need = (probe.num_chunks - 1) * sum(x.numel() * x.element_size() for x in locs)
+                hold = need * 4 <= torch.cuda.mem_get_info()[0] * 3
+        for u, x in enumerate(locs):
+            if x.dtype != tdt or not x.is_contiguous() or _view_shape(x) != shapes[u]:
+                raise ValueError(f"loader of rank {r} returned a changed or non-contiguous tensor {u}")
+        entries, carries = 0, 0
+        if hold:
+            # a loader may write into the same buffers every pass, or hand
+            # back checkpoint tensors, which the next pass overwrites
+            held.append([x.clone() for x in locs] if not last else locs)
+        else:
+            fields = [(x, ckpt_dtype, b * rr, cc) for x, (b, rr, cc) in zip(locs, shapes)]
+            if carry is None:
+                cap = carry_capacity or 16 * (int(offsets[-1]) >> 16) + 64 * len(fields) + 4096
+                nbytes = diff2_carry_workspace(fields, cap)
+                carry = {"cap": cap, "ws": torch.empty(nbytes, dtype=torch.uint8, device=device),
+                         "idx": torch.empty(1 << 16, dtype=torch.int64, device=device),
+                         "val": torch.empty(1 << 16, dtype=torch.int64, device=device),
+                         "count": torch.zeros(1, dtype=torch.int64, device=device),
+                         "carries": torch.zeros(1, dtype=torch.int64, device=device)}
+            idx, val, carries = _carry_entries(fields, k, last, carry, device)
+            _record_split(probe, k, offsets, idx, val)
+            entries = len(idx)
+        del locs
+        t3 = _now()
+        if rec is not None:
+            rec.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries,
+                        "carries": carries})
+    if hold:
+        t2 = _now()
+        fields = [([held[k][u] for k in range(probe.num_chunks)], ckpt_dtype, b * rr, cc)
+                  for u, (b, rr, cc) in enumerate(shapes)]
+        idx, val = _batched_entries(fields, 1 << 16, device)
+        _record_split(probe, 0, offsets, idx, val)
+        del fields, held
+        if rec is not None:
+            rec.append({"pass": "all", "diff2_s": _now() - t2, "entries": len(idx)})
+    return probe, hold
 
 
 def version() -> str:

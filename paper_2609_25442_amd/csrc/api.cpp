@@ -904,6 +904,113 @@ int wb_diff2_batch(const wb_field* fields, int32_t n, void* workspace, size_t wo
   });
 }
 
+// Workspace of a carry pass: the field and tile tables, the counters of the
+// two carry tables (1 KiB each), the two tables (pass k writes table k % 2
+// and reads the other), each `slots` slots of 16 bytes, slots the smallest
+// power of two at least twice the capacity (64 at least), then the staging
+// area of the stencil's carries (kCarryStage entries of 16 bytes per tile,
+// then a 4-byte count per tile).
+struct CarryLayout {
+  size_t counters = 0, table[2] = {0, 0}, stage = 0, stage_n = 0, bytes = 0;
+  uint64_t slots = 0;
+};
+
+static constexpr int64_t kMaxCarryCapacity = int64_t(1) << 36;
+
+static CarryLayout carry_layout(const Diff2Tables& T, int64_t capacity) {
+  CarryLayout L;
+  L.slots = 64;
+  while (L.slots < uint64_t(2 * capacity)) L.slots <<= 1;
+  const size_t tables = T.tiles_offset() + T.tiles.size() * sizeof(wb::DiffTile);
+  L.counters = (tables + 255) / 256 * 256;
+  const size_t one = L.slots * 16;
+  L.table[0] = L.counters + 2048;
+  L.table[1] = L.table[0] + one;
+  L.stage = L.table[1] + one;
+  L.stage_n = L.stage + T.tiles.size() * wb::kCarryStage * 16;
+  L.bytes = L.stage_n + (T.tiles.size() * 4 + 255) / 256 * 256;
+  return L;
+}
+
+static int carry_fields(const wb_field* fields, int32_t n, bool memory, int64_t carry_capacity, Diff2Tables& T) {
+  if (carry_capacity < 1 || carry_capacity > kMaxCarryCapacity)
+    return set_error(WB_EINVAL, "carry_capacity must be 1..2^36");
+  const int rc = diff2_batch_tables(fields, n, memory, T);
+  if (rc != WB_OK) return rc;
+  for (int32_t fi = 0; fi < n; ++fi)
+    if (fields[fi].passes != 1)
+      return set_error(WB_EINVAL, "field " + std::to_string(fi) + ": a carry pass reads one pass per field");
+  return WB_OK;
+}
+
+int wb_diff2_carry_workspace(const wb_field* fields, int32_t n, int64_t carry_capacity, size_t* bytes) {
+  return guarded([&]() -> int {
+    if (!bytes) return set_error(WB_EINVAL, "bytes is null");
+    Diff2Tables T;
+    const int rc = carry_fields(fields, n, false, carry_capacity, T);
+    if (rc != WB_OK) return rc;
+    *bytes = carry_layout(T, carry_capacity).bytes;
+    return WB_OK;
+  });
+}
+
+int wb_diff2_carry(const wb_field* fields, int32_t n, int32_t pass, int32_t last, int64_t carry_capacity,
+                   void* workspace, size_t workspace_bytes, int64_t* index, int64_t* value, int64_t capacity,
+                   uint64_t* count, uint64_t* carries, void* stream) {
+  return guarded([&]() -> int {
+    if (pass < 0) return set_error(WB_EINVAL, "negative pass");
+    if (capacity < 0) return set_error(WB_EINVAL, "negative capacity");
+    if (!count || reinterpret_cast<uintptr_t>(count) % 8) return set_error(WB_EINVAL, "count must be 8-byte aligned");
+    if (!carries || reinterpret_cast<uintptr_t>(carries) % 8)
+      return set_error(WB_EINVAL, "carries must be 8-byte aligned");
+    if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 8)
+      return set_error(WB_EINVAL, "workspace must be 8-byte aligned");
+    int rc = check_extent(count, 8, "count", 8);
+    if (rc == WB_OK) rc = check_extent(carries, 8, "carries", 8);
+    if (rc == WB_OK && capacity > 0) rc = check_extent(index, capacity * 8, "index", 8);
+    if (rc == WB_OK && capacity > 0) rc = check_extent(value, capacity * 8, "value", 8);
+    if (rc != WB_OK) return rc;
+    Diff2Tables T;
+    rc = carry_fields(fields, n, true, carry_capacity, T);
+    if (rc != WB_OK) return rc;
+    const CarryLayout L = carry_layout(T, carry_capacity);
+    if (L.bytes > workspace_bytes) return set_error(WB_EINVAL, "workspace smaller than wb_diff2_carry_workspace");
+    rc = check_extent(workspace, static_cast<int64_t>(L.bytes), "workspace", 8);
+    if (rc != WB_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    const size_t tables = T.tiles_offset() + T.tiles.size() * sizeof(wb::DiffTile);
+    if (!T.fields.empty()) {
+      std::vector<char> host(tables);
+      std::memcpy(host.data(), T.fields.data(), T.fields.size() * sizeof(wb::DiffField));
+      if (!T.tiles.empty())
+        std::memcpy(host.data() + T.tiles_offset(), T.tiles.data(), T.tiles.size() * sizeof(wb::DiffTile));
+      hipError_t e = hipMemcpyAsync(ws, host.data(), tables, hipMemcpyHostToDevice, st);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (diff2 tables)");
+      e = hipStreamSynchronize(st);  // the host copy is freed on return
+      if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    }
+    wb::CarryTable tab[2];
+    for (int t = 0; t < 2; ++t) {
+      tab[t].slot = reinterpret_cast<int64_t*>(ws + L.table[t]);
+      tab[t].count = reinterpret_cast<unsigned long long*>(ws + L.counters + 1024 * t);
+      tab[t].stage = reinterpret_cast<int64_t*>(ws + L.stage);
+      tab[t].stage_n = reinterpret_cast<int32_t*>(ws + L.stage_n);
+      tab[t].capacity = carry_capacity;
+      tab[t].mask = L.slots - 1;
+    }
+    const wb::CarryTable& next = tab[pass & 1];
+    const wb::CarryTable& in = tab[(pass + 1) & 1];
+    const int e = wb::launch_diff2_carry(reinterpret_cast<const wb::DiffField*>(ws), n,
+                                         reinterpret_cast<const wb::DiffTile*>(ws + T.tiles_offset()),
+                                         int64_t(T.tiles.size()), pass > 0, last != 0, in, next, index, value,
+                                         capacity, reinterpret_cast<unsigned long long*>(count),
+                                         reinterpret_cast<unsigned long long*>(carries), stream);
+    if (e != 0) return set_error(WB_EHIP, std::string("diff2 carry launch: ") + wb::hip_error_string(e));
+    return WB_OK;
+  });
+}
+
 void wb_plan_destroy(wb_plan_t* P) {
   if (!P) return;
   if (P->ptr_event) {

@@ -19,6 +19,22 @@
 // Single-field launches walk one field's tiles with a strided grid; the
 // batched launch takes one tile per workgroup from a table that covers many
 // fields, so all of a rank's tensors take one launch.
+//
+// Entries are gathered per workgroup in LDS (a wavefront ballot and an LDS
+// add place each lane's entry) and appended to the global list with one
+// atomic add per workgroup when the workgroup ends.
+//
+// Carry passes (Algorithm 1, ExpandCarry and EmitCarry): a pass's field is
+// one 16-bit chunk, and the chunk's wrap-arounds make diff2 non-zero every
+// 2^16 identifiers. Pass k's stencil adds to each non-zero D the carry that
+// pass k - 1 left at that position, emits S mod 2^16 when non-zero and
+// inserts floor(S / 2^16) when non-zero into the carry table of pass k + 1;
+// the last pass emits S whole. A second kernel handles the carries at
+// positions where D is zero. The sum over passes of 2^(16 k) times the
+// emitted values is diff2 of the identifier field, and only its positions
+// (next to slice-copy corners) are emitted: the wrap-arounds stay in the
+// device carry tables, which are hash tables (key position + 1, linear
+// probing, at most half full when within capacity).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -55,6 +71,12 @@ struct Sink {
   T* __restrict__ value;
   int64_t capacity;
   unsigned long long* __restrict__ count;
+  __device__ __forceinline__ void operator()(unsigned long long slot, int64_t pos, int64_t v) const {
+    if (slot < static_cast<unsigned long long>(capacity)) {
+      index[slot] = pos;
+      value[slot] = T(v);
+    }
+  }
 };
 
 // The chunk fields a tile reads: element value sum over k < n of p[k] << (16 k).
@@ -66,25 +88,204 @@ struct Passes {
   int n;
 };
 
-// Append the lanes' non-zero entries of one candidate position: one ballot,
-// one atomic add per wavefront.
-template <typename T>
-__device__ __forceinline__ void emit_entries(bool emit, int64_t pos, T d, int lane, const Sink<T>& out) {
-  const unsigned long long m = __ballot(emit);
-  if (m == 0) return;
-  unsigned long long base = 0;
+// One workgroup's entries, in LDS; entries past kWgCap go straight to the
+// global list (one atomic add per wavefront).
+constexpr int kWgCap = 256;
+struct WgBuf {
+  unsigned n;
+  unsigned long long base;
+  int64_t pos[kWgCap];
+  int64_t val[kWgCap];
+};
+
+__device__ __forceinline__ void wg_init(WgBuf& b) {
+  if (threadIdx.x == 0) b.n = 0;
+}
+
+__device__ __forceinline__ unsigned lanes_below(unsigned long long m, int lane) {
+  return lane ? unsigned(__popcll(m & ((1ull << lane) - 1))) : 0u;
+}
+
+// Place (pos, v) of the lanes with `put` in the workgroup's buffer: one
+// ballot and one LDS add per wavefront. Every lane of the wavefront calls it;
+// it returns true for a lane whose entry did not fit (all such lanes of the
+// wavefront then call the spill path together).
+__device__ __forceinline__ bool wg_place(WgBuf& b, bool put, int64_t pos, int64_t v, int lane) {
+  const unsigned long long m = __ballot(put);
+  if (m == 0) return false;
   const int leader = __ffsll(static_cast<long long>(m)) - 1;
-  if (lane == leader) base = atomicAdd(out.count, static_cast<unsigned long long>(__popcll(m)));
-  base = __shfl(base, leader, 64);
-  if (emit) {
-    const unsigned long long below = lane ? (m & ((1ull << lane) - 1)) : 0ull;
-    const int64_t slot = int64_t(base) + __popcll(below);
-    if (slot < out.capacity) {
-      out.index[slot] = pos;
-      out.value[slot] = d;
+  unsigned off = 0;
+  if (lane == leader) off = atomicAdd(&b.n, unsigned(__popcll(m)));
+  off = __shfl(off, leader, 64);
+  const unsigned slot = off + lanes_below(m, lane);
+  if (put && slot < unsigned(kWgCap)) {
+    b.pos[slot] = pos;
+    b.val[slot] = v;
+    return false;
+  }
+  return put;
+}
+
+// Entries that did not fit the buffer: one atomic add per wavefront on the
+// list's counter, then each lane writes its slot.
+template <typename T>
+__device__ __forceinline__ void sink_spill(const Sink<T>& w, bool spill, int64_t pos, int64_t v, int lane) {
+  const unsigned long long ms = __ballot(spill);
+  if (ms == 0) return;
+  const int first = __ffsll(static_cast<long long>(ms)) - 1;
+  unsigned long long g = 0;
+  if (lane == first) g = atomicAdd(w.count, static_cast<unsigned long long>(__popcll(ms)));
+  g = __shfl(g, first, 64);
+  if (spill) w(g + lanes_below(ms, lane), pos, v);
+}
+
+template <typename T>
+__device__ __forceinline__ void sink_append(WgBuf& b, const Sink<T>& w, bool put, int64_t pos, int64_t v, int lane) {
+  sink_spill(w, wg_place(b, put, pos, v, lane), pos, v, lane);
+}
+
+// Hand the workgroup's buffered entries to the global list: one atomic add.
+// Every thread of the workgroup calls it, once, at the end.
+template <typename T>
+__device__ __forceinline__ void sink_flush(WgBuf& b, const Sink<T>& w) {
+  __syncthreads();
+  const unsigned n = b.n < unsigned(kWgCap) ? b.n : unsigned(kWgCap);
+  if (threadIdx.x == 0 && n) b.base = atomicAdd(w.count, static_cast<unsigned long long>(n));
+  __syncthreads();
+  for (unsigned t = threadIdx.x; t < n; t += blockDim.x) w(b.base + t, b.pos[t], b.val[t]);
+}
+
+// The plain entry list of a launch: put() is what a tile calls for every
+// candidate position (all lanes of a wavefront together).
+template <typename T>
+struct ListOut {
+  WgBuf* buf;
+  Sink<T> sink;
+  __device__ __forceinline__ void put(bool nz, int64_t pos, T d, int lane) const {
+    sink_append(*buf, sink, nz, pos, int64_t(d), lane);
+  }
+  __device__ __forceinline__ void flush() const { sink_flush(*buf, sink); }
+};
+
+// Carry tables: slot h holds key position + 1 (0 empty) and field << 32 |
+// carry (as uint32). Inserts probe linearly from the position's hash, at
+// most kCarryProbes slots; one that finds none sets the table's flag.
+__device__ __forceinline__ uint64_t carry_hash(int64_t pos) {
+  uint64_t x = static_cast<uint64_t>(pos);  // MurmurHash3 64-bit finaliser
+  x ^= x >> 33;
+  x *= 0xff51afd7ed558ccdull;
+  x ^= x >> 33;
+  x *= 0xc4ceb9fe1a85ec53ull;
+  x ^= x >> 33;
+  return x;
+}
+
+__device__ __forceinline__ void carry_insert(const CarryTable& t, int64_t pos, int64_t packed) {
+  uint64_t h = carry_hash(pos) & t.mask;
+  const unsigned long long key = static_cast<unsigned long long>(pos + 1);
+  for (int n = 0; n < kCarryProbes; ++n) {
+    if (atomicCAS(reinterpret_cast<unsigned long long*>(t.slot + 2 * h), 0ull, key) == 0ull) {
+      t.slot[2 * h + 1] = packed;
+      return;
+    }
+    h = (h + 1) & t.mask;
+  }
+  t.count[kCarryCounters] = 1;
+}
+
+__device__ __forceinline__ int carry_lookup(const CarryTable& t, int64_t pos) {
+  uint64_t h = carry_hash(pos) & t.mask;
+  for (int n = 0; n < kCarryProbes; ++n) {
+    const int64_t key = t.slot[2 * h];
+    if (key == pos + 1) return static_cast<int32_t>(static_cast<uint32_t>(t.slot[2 * h + 1]));
+    if (key == 0) return 0;
+    h = (h + 1) & t.mask;
+  }
+  return 0;
+}
+
+// Carries are counted per workgroup on one of kCarryCounters counters (an
+// add whose result is not needed), so no single address takes them all.
+__device__ __forceinline__ void carry_spill(const CarryTable& t, bool spill, int64_t pos, int64_t packed, int lane) {
+  const unsigned long long ms = __ballot(spill);
+  if (ms == 0) return;
+  if (lane == __ffsll(static_cast<long long>(ms)) - 1)
+    atomicAdd(t.count + blockIdx.x % kCarryCounters, static_cast<unsigned long long>(__popcll(ms)));
+  if (spill) carry_insert(t, pos, packed);
+}
+
+// The workgroup's buffered carries: counted with one add; with kStage (a
+// stencil tile) the first kCarryStage are staged for the insert launch with
+// plain stores and the rest inserted here, otherwise all are inserted here.
+template <bool kStage>
+__device__ __forceinline__ void carry_flush(WgBuf& b, const CarryTable& t) {
+  __syncthreads();
+  const unsigned n = b.n < unsigned(kWgCap) ? b.n : unsigned(kWgCap);
+  const unsigned m = kStage ? (n < unsigned(kCarryStage) ? n : unsigned(kCarryStage)) : 0u;
+  if (threadIdx.x == 0) {
+    if (kStage) t.stage_n[blockIdx.x] = int32_t(m);
+    if (n) atomicAdd(t.count + blockIdx.x % kCarryCounters, static_cast<unsigned long long>(n));
+  }
+  for (unsigned k = threadIdx.x; k < n; k += blockDim.x) {
+    if (k < m) {
+      int64_t* e = t.stage + 2 * (int64_t(blockIdx.x) * kCarryStage + k);
+      e[0] = b.pos[k];
+      e[1] = b.val[k];
+    } else {
+      carry_insert(t, b.pos[k], b.val[k]);
     }
   }
 }
+
+// A carry pass's output. put() takes a candidate position of the stencil:
+// with carries in (kIn), non-zero D wait in `pending` and are looked up
+// together when the tile ends (one round of table reads per workgroup rather
+// than a stall per wavefront); split() turns S into an emitted value and a
+// carry.
+template <bool kIn, bool kLast, bool kStage>
+struct CarryOut {
+  WgBuf* ebuf;
+  WgBuf* cbuf;
+  WgBuf* pending;
+  Sink<int64_t> sink;
+  CarryTable in, next;
+  int64_t field;
+  __device__ __forceinline__ void split(bool c, int64_t pos, int s, int64_t f, int lane) const {
+    if (kLast) {
+      sink_append(*ebuf, sink, c && s != 0, pos, int64_t(s), lane);
+    } else {
+      const int r = s & 0xFFFF, q = s >> 16;  // arithmetic shift: floor(S / 2^16)
+      sink_append(*ebuf, sink, c && r != 0, pos, int64_t(r), lane);
+      const bool cq = c && q != 0;
+      const int64_t packed = (f << 32) | int64_t(static_cast<uint32_t>(q));
+      carry_spill(next, wg_place(*cbuf, cq, pos, packed, lane), pos, packed, lane);
+    }
+  }
+  __device__ __forceinline__ void put(bool nz, int64_t pos, int d, int lane) const {
+    if (!kIn) {
+      split(nz, pos, d, field, lane);
+      return;
+    }
+    const bool inl = wg_place(*pending, nz, pos, int64_t(d), lane);
+    if (__ballot(inl) == 0) return;
+    split(inl, pos, inl ? d + carry_lookup(in, pos) : 0, field, lane);
+  }
+  __device__ __forceinline__ void flush() const {
+    if (kIn) {
+      __syncthreads();
+      const unsigned n = pending->n < unsigned(kWgCap) ? pending->n : unsigned(kWgCap);
+      for (unsigned b0 = 0; b0 < n; b0 += blockDim.x) {
+        const unsigned k = b0 + threadIdx.x;
+        const bool ok = k < n;
+        const int64_t pos = ok ? pending->pos[k] : 0;
+        const int s = ok ? int(pending->val[k]) + carry_lookup(in, pos) : 0;
+        split(ok, pos, s, field, threadIdx.x & 63);
+      }
+    }
+    sink_flush(*ebuf, sink);
+    if (!kLast) carry_flush<kStage>(*cbuf, next);
+  }
+};
 
 __device__ __forceinline__ int load_chunk(const char* src, int dtype, int64_t k) {
   if (dtype == WB_F32) return int(reinterpret_cast<const float*>(src)[k]);
@@ -104,9 +305,9 @@ __device__ __forceinline__ T load_value(const Passes<P>& s, int dtype, int64_t k
 // two halo rows above. The horizontal difference h(i) = c(i,j) - 2 c(i,j-1) +
 // c(i,j-2) takes its left neighbours from the lanes to the left (the first two
 // lanes of a wavefront load theirs); then D = h(i) - 2 h(i-1) + h(i-2).
-template <typename T, int P>
+template <typename T, int P, class Out>
 __device__ __forceinline__ void elem_tile(const Passes<P>& s, int dtype, int64_t rows, int64_t cols, int64_t base,
-                                          int64_t i0, int64_t jb, const Sink<T>& out) {
+                                          int64_t i0, int64_t jb, const Out& out) {
   const int lane = threadIdx.x & 63;
   const int64_t j = jb + threadIdx.x;
   const bool col = j < cols;
@@ -124,7 +325,7 @@ __device__ __forceinline__ void elem_tile(const Passes<P>& s, int dtype, int64_t
     const T d = h - 2 * h1 + h2;
     h2 = h1;
     h1 = h;
-    emit_entries<T>(col && i >= i0 && d != 0, base + rowbase + j, d, lane, out);
+    out.put(col && i >= i0 && d != 0, base + rowbase + j, d, lane);
   }
 }
 
@@ -178,9 +379,9 @@ __device__ __forceinline__ void load_row_vec(const Passes<P>& s, int64_t rowoff,
 // S), after two halo rows, U rows in flight. The two columns left of a
 // lane's vector are the previous lane's last two (the first lane of each
 // wavefront loads them). Same arithmetic as the ELEM tile.
-template <int V, typename T, int P, int U, int S>
+template <int V, typename T, int P, int U, int S, class Out>
 __device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
-                                         int64_t vb, const Sink<T>& out) {
+                                         int64_t vb, const Out& out) {
   const int lane = threadIdx.x & 63;
   const int64_t nvec = cols / V;
   const int64_t v = vb + threadIdx.x;
@@ -226,16 +427,16 @@ __device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64
       }
       if (__ballot(any != 0) == 0) continue;
 #pragma unroll
-      for (int k = 0; k < V; ++k) emit_entries<T>((any >> k) & 1u, base + i * cols + j0 + k, d[k], lane, out);
+      for (int k = 0; k < V; ++k) out.put((any >> k) & 1u, base + i * cols + j0 + k, d[k], lane);
     }
   }
 }
 
 // FLAT tile of a one-row field: with nothing above, D is the row's second
 // difference. Lane l of sub-tile u takes vector cb + u * kThreads + l.
-template <int V, typename T, int P, int U>
+template <int V, typename T, int P, int U, class Out>
 __device__ __forceinline__ void flat_tile(const Passes<P>& s, int64_t cols, int64_t base, int64_t cb,
-                                          const Sink<T>& out) {
+                                          const Out& out) {
   const int lane = threadIdx.x & 63;
   const int64_t nvec = cols / V;
   T x[U][V];
@@ -267,7 +468,7 @@ __device__ __forceinline__ void flat_tile(const Passes<P>& s, int64_t cols, int6
     for (int k = 0; k < V; ++k) any |= (v < nvec && d[k] != 0) ? (1u << k) : 0u;
     if (__ballot(any != 0) == 0) continue;
 #pragma unroll
-    for (int k = 0; k < V; ++k) emit_entries<T>((any >> k) & 1u, base + v * V + k, d[k], lane, out);
+    for (int k = 0; k < V; ++k) out.put((any >> k) & 1u, base + v * V + k, d[k], lane);
   }
 }
 
@@ -275,67 +476,199 @@ __device__ __forceinline__ void flat_tile(const Passes<P>& s, int64_t cols, int6
 // field's tiles.
 
 __global__ __launch_bounds__(kThreads) void wb_diff2_kernel(const char* __restrict__ src, int dtype, int64_t rows,
-                                                            int64_t cols, Sink<int> out) {
+                                                            int64_t cols, Sink<int> sink) {
+  __shared__ WgBuf buf;
+  wg_init(buf);
+  __syncthreads();
+  const ListOut<int> out{&buf, sink};
   const Passes<1> s{{src}, 1};
   for (int64_t jb = int64_t(blockIdx.x) * kThreads; jb < cols; jb += int64_t(gridDim.x) * kThreads)
     for (int64_t i0 = int64_t(blockIdx.y) * kStrip; i0 < rows; i0 += int64_t(gridDim.y) * kStrip)
       elem_tile<int, 1>(s, dtype, rows, cols, 0, i0, jb, out);
+  out.flush();
 }
 
 template <int V>
 __global__ __launch_bounds__(kThreads) void wb_diff2_vec_kernel(const char* __restrict__ src, int64_t rows,
-                                                                int64_t cols, Sink<int> out) {
+                                                                int64_t cols, Sink<int> sink) {
+  __shared__ WgBuf buf;
+  wg_init(buf);
+  __syncthreads();
+  const ListOut<int> out{&buf, sink};
   const Passes<1> s{{src}, 1};
   const int64_t nvec = cols / V;
   for (int64_t vb = int64_t(blockIdx.x) * kThreads; vb < nvec; vb += int64_t(gridDim.x) * kThreads)
     for (int64_t i0 = int64_t(blockIdx.y) * kVecStrip; i0 < rows; i0 += int64_t(gridDim.y) * kVecStrip)
       vec_tile<V, int, 1, kUnroll, kVecStrip>(s, rows, cols, 0, i0, vb, out);
+  out.flush();
 }
 
 template <int V>
 __global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __restrict__ src, int64_t cols,
-                                                                 Sink<int> out) {
+                                                                 Sink<int> sink) {
+  __shared__ WgBuf buf;
+  wg_init(buf);
+  __syncthreads();
+  const ListOut<int> out{&buf, sink};
   const Passes<1> s{{src}, 1};
   const int64_t nvec = cols / V;
   const int64_t step = int64_t(gridDim.x) * kThreads * kFlatUnroll;
   for (int64_t cb = int64_t(blockIdx.x) * kThreads * kFlatUnroll; cb < nvec; cb += step)
     flat_tile<V, int, 1, kFlatUnroll>(s, cols, 0, cb, out);
+  out.flush();
 }
 
-// Batched launch: workgroup b takes tile b of the table; int64 arithmetic
-// over up to kMaxPasses passes, fewer values in flight per lane, taller VEC
-// tiles and FLAT tiles of several sub-tiles (fewer, larger table rows).
+// Batched launches: workgroup b takes tile b of the table, taller VEC tiles
+// and FLAT tiles of several sub-tiles (fewer, larger table rows). Held passes
+// recombine up to kMaxPasses passes in int64 with fewer values in flight per
+// lane; carry passes read one pass in int.
 constexpr int kBatchUnroll = 2;
+constexpr int kCarryUnroll = 4;
 constexpr int kBatchVecStrip = 128;
 constexpr int kBatchFlatUnroll = 4;
 constexpr int kBatchFlatSub = 4;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
 
-__global__ __launch_bounds__(kThreads) void wb_diff2_batch_kernel(const DiffField* __restrict__ fields,
-                                                                  const DiffTile* __restrict__ tiles,
-                                                                  Sink<int64_t> out) {
-  const DiffTile t = tiles[blockIdx.x];
-  const DiffField& f = fields[t.field];
-  Passes<kMaxPasses> s;
+template <typename T, int P, int U, class Out>
+__device__ __forceinline__ void batch_tile(const DiffField& f, const DiffTile& t, const Out& out) {
+  Passes<P> s;
 #pragma unroll
-  for (int c = 0; c < kMaxPasses; ++c) s.p[c] = static_cast<const char*>(f.src[c]);
-  s.n = f.passes;
+  for (int c = 0; c < P; ++c) s.p[c] = static_cast<const char*>(f.src[c]);
+  s.n = P == 1 ? 1 : f.passes;
   if (f.kind == DIFF_FLAT) {
     for (int q = 0; q < kBatchFlatSub; ++q) {
       const int64_t cb = t.j0 + int64_t(q) * kBatchFlatUnroll * kThreads;
       if (f.dtype == WB_F32)
-        flat_tile<4, int64_t, kMaxPasses, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
+        flat_tile<4, T, P, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
       else
-        flat_tile<8, int64_t, kMaxPasses, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
+        flat_tile<8, T, P, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
     }
   } else if (f.kind == DIFF_VEC) {
     if (f.dtype == WB_F32)
-      vec_tile<4, int64_t, kMaxPasses, kBatchUnroll, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+      vec_tile<4, T, P, U, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
     else
-      vec_tile<8, int64_t, kMaxPasses, kBatchUnroll, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+      vec_tile<8, T, P, U, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
   } else {
-    elem_tile<int64_t, kMaxPasses>(s, f.dtype, f.rows, f.cols, f.base, t.i0, t.j0, out);
+    elem_tile<T, P>(s, f.dtype, f.rows, f.cols, f.base, t.i0, t.j0, out);
   }
 }
+
+__global__ __launch_bounds__(kThreads) void wb_diff2_batch_kernel(const DiffField* __restrict__ fields,
+                                                                  const DiffTile* __restrict__ tiles,
+                                                                  Sink<int64_t> sink) {
+  __shared__ WgBuf buf;
+  wg_init(buf);
+  __syncthreads();
+  const ListOut<int64_t> out{&buf, sink};
+  const DiffTile t = tiles[blockIdx.x];
+  batch_tile<int64_t, kMaxPasses, kBatchUnroll>(fields[t.field], t, out);
+  out.flush();
+}
+
+// Carry pass, stencil part: one tile per workgroup of one pass's fields.
+template <bool kIn, bool kLast>
+__global__ __launch_bounds__(kThreads) void wb_diff2_carry_kernel(const DiffField* __restrict__ fields,
+                                                                  const DiffTile* __restrict__ tiles, CarryTable in,
+                                                                  CarryTable next, Sink<int64_t> sink) {
+  __shared__ WgBuf ebuf, cbuf, pending;
+  wg_init(ebuf);
+  wg_init(cbuf);
+  wg_init(pending);
+  __syncthreads();
+  const DiffTile t = tiles[blockIdx.x];
+  const CarryOut<kIn, kLast, true> out{&ebuf, &cbuf, &pending, sink, in, next, int64_t(t.field)};
+  batch_tile<int, 1, kCarryUnroll>(fields[t.field], t, out);
+  out.flush();
+}
+
+// D at local position p of a one-pass field, straight from the nine
+// neighbours (Eq. diff2 as the outer product of [1, -2, 1] with itself).
+__device__ __forceinline__ int diff2_at(const DiffField& f, int64_t p) {
+  const int64_t i = p / f.cols, j = p - i * f.cols;
+  const char* src = static_cast<const char*>(f.src[0]);
+  int d = 0;
+  for (int a = 0; a < 3 && a <= i; ++a) {
+    const int wa = a == 1 ? -2 : 1;
+    for (int b = 0; b < 3 && b <= j; ++b) {
+      const int w = wa * (b == 1 ? -2 : 1);
+      d += w * load_chunk(src, f.dtype, (i - a) * f.cols + (j - b));
+    }
+  }
+  return d;
+}
+
+// Carry pass, the carries of pass k - 1 at positions where D is zero (the
+// stencil took the others): S is the carry itself. A walk over the slots of
+// the table; slots whose field or position does not fit the fields are
+// skipped.
+template <bool kLast>
+__global__ __launch_bounds__(kThreads) void wb_carry_rest_kernel(const DiffField* __restrict__ fields, int nfields,
+                                                                 CarryTable in, CarryTable next,
+                                                                 Sink<int64_t> sink) {
+  __shared__ WgBuf ebuf, cbuf;
+  wg_init(ebuf);
+  wg_init(cbuf);
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t slots = static_cast<int64_t>(in.mask) + 1;
+  const CarryOut<false, kLast, false> out{&ebuf, &cbuf, nullptr, sink, in, next, 0};
+  for (int64_t b0 = int64_t(blockIdx.x) * kThreads; b0 < slots; b0 += int64_t(gridDim.x) * kThreads) {
+    const int64_t h = b0 + threadIdx.x;
+    int64_t pos = 0, field = 0;
+    int q = 0;
+    bool take = false;
+    if (h < slots) {
+      const int64_t key = in.slot[2 * h];
+      if (key != 0) {
+        pos = key - 1;
+        const int64_t packed = in.slot[2 * h + 1];
+        field = packed >> 32;
+        q = static_cast<int32_t>(static_cast<uint32_t>(packed));
+        if (field >= 0 && field < nfields) {
+          const DiffField& f = fields[field];
+          const int64_t p = pos - f.base;
+          take = q != 0 && f.passes == 1 && p >= 0 && p < f.rows * f.cols && diff2_at(f, p) == 0;
+        }
+      }
+    }
+    out.split(take, pos, q, field, lane);
+  }
+  out.flush();
+}
+
+// Insert the carries the stencil workgroups staged: one thread per staging
+// slot of every tile.
+__global__ __launch_bounds__(kThreads) void wb_carry_insert_kernel(CarryTable next, int64_t ntiles) {
+  const int64_t total = ntiles * kCarryStage;
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  for (int64_t e = int64_t(blockIdx.x) * kThreads + threadIdx.x; e < total; e += stride) {
+    const int64_t t = e / kCarryStage, k = e - t * kCarryStage;
+    if (k < next.stage_n[t]) carry_insert(next, next.stage[2 * e], next.stage[2 * e + 1]);
+  }
+}
+
+// Empty the next carry table, zero its counters and flag and the entry
+// counter (a fill, not a memset: the launches may be captured).
+__global__ __launch_bounds__(kThreads) void wb_carry_clear_kernel(int64_t* slot, int64_t slots,
+                                                                 unsigned long long* carries,
+                                                                 unsigned long long* count) {
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  for (int64_t k = int64_t(blockIdx.x) * kThreads + threadIdx.x; k < slots; k += stride) slot[2 * k] = 0;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x <= kCarryCounters) carries[threadIdx.x] = 0;
+    if (threadIdx.x == 0) *count = 0;
+  }
+}
+
+// The carries a pass kept: the sum of the counters, or past the capacity if
+// an insert found no slot.
+__global__ void wb_carry_report_kernel(const unsigned long long* counters, int64_t capacity, unsigned long long* out) {
+  unsigned long long n = 0;
+  for (int k = 0; k < kCarryCounters; ++k) n += counters[k];
+  if (counters[kCarryCounters] && n <= static_cast<unsigned long long>(capacity))
+    n = static_cast<unsigned long long>(capacity) + 1;
+  *out = n;
+}
+
 
 __global__ void wb_zero_count_kernel(unsigned long long* count) { *count = 0; }
 
@@ -433,6 +766,47 @@ int launch_diff2_batch(const DiffField* fields, const DiffTile* tiles, int64_t n
   const Sink<int64_t> out{index, value, capacity, count};
   hipLaunchKernelGGL(wb_diff2_batch_kernel, dim3(static_cast<unsigned>(ntiles)), dim3(kThreads), 0, st, fields, tiles,
                      out);
+  return hipGetLastError();
+}
+
+int launch_diff2_carry(const DiffField* fields, int32_t nfields, const DiffTile* tiles, int64_t ntiles, bool has_in,
+                       bool last, const CarryTable& in, const CarryTable& next, int64_t* index, int64_t* value,
+                       int64_t capacity, unsigned long long* count, unsigned long long* carries, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t slots = last ? 0 : static_cast<int64_t>(next.mask) + 1;
+  const int64_t clear = (slots + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(wb_carry_clear_kernel, dim3(static_cast<unsigned>(clear < 1 ? 1 : clear < 4096 ? clear : 4096)),
+                     dim3(kThreads), 0, st, next.slot, slots, next.count, count);
+  const Sink<int64_t> sink{index, value, capacity, count};
+  if (ntiles > 0) {
+    const dim3 grid(static_cast<unsigned>(ntiles));
+    if (has_in && last)
+      hipLaunchKernelGGL((wb_diff2_carry_kernel<true, true>), grid, dim3(kThreads), 0, st, fields, tiles, in, next, sink);
+    else if (has_in)
+      hipLaunchKernelGGL((wb_diff2_carry_kernel<true, false>), grid, dim3(kThreads), 0, st, fields, tiles, in, next,
+                         sink);
+    else if (last)
+      hipLaunchKernelGGL((wb_diff2_carry_kernel<false, true>), grid, dim3(kThreads), 0, st, fields, tiles, in, next,
+                         sink);
+    else
+      hipLaunchKernelGGL((wb_diff2_carry_kernel<false, false>), grid, dim3(kThreads), 0, st, fields, tiles, in, next,
+                         sink);
+  }
+  if (ntiles > 0 && !last) {
+    const int64_t want = (ntiles * kCarryStage + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(wb_carry_insert_kernel, dim3(static_cast<unsigned>(want < 8192 ? want : 8192)), dim3(kThreads),
+                       0, st, next, ntiles);
+  }
+  if (has_in) {
+    const int64_t want = (static_cast<int64_t>(in.mask) + kThreads) / kThreads;
+    const dim3 grid(static_cast<unsigned>(want < 4096 ? want : 4096));
+    if (last)
+      hipLaunchKernelGGL(wb_carry_rest_kernel<true>, grid, dim3(kThreads), 0, st, fields, int(nfields), in, next, sink);
+    else
+      hipLaunchKernelGGL(wb_carry_rest_kernel<false>, grid, dim3(kThreads), 0, st, fields, int(nfields), in, next,
+                         sink);
+  }
+  hipLaunchKernelGGL(wb_carry_report_kernel, dim3(1), dim3(1), 0, st, next.count, next.capacity, carries);
   return hipGetLastError();
 }
 

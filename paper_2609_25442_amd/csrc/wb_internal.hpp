@@ -268,6 +268,25 @@ struct DiffTile {
   int64_t i0, j0;
 };
 static_assert(sizeof(DiffTile) == 24, "DiffTile layout");
+// A carry table of the probing passes: `mask + 1` slots (a power of two, at
+// least twice `capacity`) of two int64, key position + 1 (0 empty) and
+// field << 32 | carry as uint32; `count` points to kCarryCounters counters
+// whose sum is the number of carries inserted, then a flag set when an
+// insert found no free slot within kCarryProbes of its hash. The stencil
+// workgroup of tile t stages up to kCarryStage of its carries at
+// stage[2 * (t * kCarryStage + k)] (position, packed carry) and their number
+// at stage_n[t]; a later launch inserts them.
+constexpr int kCarryCounters = 64;
+constexpr int kCarryProbes = 256;
+constexpr int kCarryStage = 64;
+struct CarryTable {
+  int64_t* slot;
+  unsigned long long* count;
+  int64_t* stage;
+  int32_t* stage_n;
+  int64_t capacity;
+  uint64_t mask;
+};
 
 // A local tensor of a probed rank and its recombined diff2 entries.
 struct ProbeLocal {
@@ -357,9 +376,14 @@ void probe_scan(const wb_probe_t& P, wb_layout_t& out, int rank);
 int launch_make_ids(void* dst, int dtype, int64_t numel, int64_t first_id, int shift, uint32_t mask, void* stream);
 int launch_diff2(const void* src, int dtype, int64_t rows, int64_t cols, int64_t* index, int32_t* value,
                  int64_t capacity, unsigned long long* count, void* stream);
-// appends the tiles of one field (element 0 at entry index base) to out
 // fills f.kind and appends the tiles of field f (index fi) to out
 void diff_tiles(int32_t fi, DiffField& f, std::vector<DiffTile>& out);
 int launch_diff2_batch(const DiffField* fields, const DiffTile* tiles, int64_t ntiles, int64_t* index, int64_t* value,
                        int64_t capacity, unsigned long long* count, void* stream);
+// one carry pass: clears `next` (unless last), runs the stencil over the
+// tiles, then (has_in) the carries of `in` at positions the stencil skipped,
+// and copies next's carry count to *carries
+int launch_diff2_carry(const DiffField* fields, int32_t nfields, const DiffTile* tiles, int64_t ntiles, bool has_in,
+                       bool last, const CarryTable& in, const CarryTable& next, int64_t* index, int64_t* value,
+                       int64_t capacity, unsigned long long* count, unsigned long long* carries, void* stream);
 }  // namespace wb

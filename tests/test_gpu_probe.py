@@ -1,14 +1,15 @@
 """Source-map probing on the GPU (Sec. 3.1; App. B, Algorithm 1): the
-identifier-chunk kernel and the diff2 stencil against the oracle, and whole
-ranks probed through torch-slicing weight loaders (the black box) recovering
-exactly the declared slice copies."""
+identifier-chunk kernel and the diff2 stencils (single field, batched, and
+carry passes) against the oracle, and whole ranks probed through
+torch-slicing weight loaders (the black box) recovering exactly the declared
+slice copies, with passes held or carried one at a time."""
 
 import numpy as np
 import pytest
 import torch
 
 import paper_2609_25442_amd as wb
-from oracle.diff2 import diff2, id_chunk, nonzeros
+from oracle.diff2 import carry_passes, diff2, id_chunk, nonzeros
 from oracle.layout import layout_from_spec
 from synthetic_checkpoint.workloads import ORDER, scaled
 
@@ -212,6 +213,143 @@ def test_diff2_batch_capacity_overflow_reports_the_count():
     assert len(got) == 10 and all(want[i] == v for i, v in got.items())
 
 
+def _carry_fields(rng, kind, passes):
+    """Chunk fields of every shape (and a few empty ones): random chunks (a
+    carry at nearly every position), or identifier slices whose bases sit
+    near multiples of 2^32 so that chunk 1 wraps too."""
+    out = []
+    for R, C in SHAPES + [(0, 5), (4, 0), (40, 512)]:
+        if R * C == 0:
+            out.append(([np.zeros((R, C), dtype=np.int64)] * passes, R, C))
+            continue
+        if kind == "random":
+            out.append(([rng.integers(0, 1 << 16, size=(R, C)) for _ in range(passes)], R, C))
+            continue
+        A = np.zeros((R, C), dtype=np.int64)
+        for _ in range(3):
+            a = int(rng.integers(0, R)); b = int(rng.integers(a + 1, R + 1))
+            c = int(rng.integers(0, C)); d = int(rng.integers(c + 1, C + 1))
+            step = int(rng.integers(1, 5000))
+            top = int(rng.integers(1, 1 << (16 * passes - 33))) << 32
+            base = top - int(rng.integers(0, (b - a) * step + (d - c) + 1))
+            i = np.arange(a, b)[:, None]; j = np.arange(c, d)[None, :]
+            A[a:b, c:d] = base + i * step + j
+        out.append(([id_chunk(A, k, 16) for k in range(passes)], R, C))
+    return out
+
+
+def _carry_expected(fields_np, passes):
+    """Oracle entries of every pass (carry_passes) at each field's offset, and
+    the number of carries every pass keeps."""
+    want = [{} for _ in range(passes)]
+    carried = [0] * passes
+    off = 0
+    for chunks, R, C in fields_np:
+        if R * C:
+            kept, carries = carry_passes(chunks, 16)
+            for k in range(passes):
+                for (i, j), v in kept[k].items():
+                    want[k][off + i * C + j] = v
+                carried[k] += len(carries[k])
+        off += R * C
+    return want, carried
+
+
+class _CarryRun:
+    def __init__(self, fields0, carry_cap, cap):
+        self.cap_c = carry_cap
+        self.ws = torch.empty(wb.diff2_carry_workspace(fields0, carry_cap), dtype=torch.uint8, device="cuda")
+        self.idx = torch.full((cap,), -1, dtype=torch.int64, device="cuda")
+        self.val = torch.zeros(cap, dtype=torch.int64, device="cuda")
+        self.count = torch.zeros(1, dtype=torch.int64, device="cuda")
+        self.carries = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+    def run(self, fields, k, last):
+        wb.diff2_carry(fields, k, last, self.cap_c, self.idx, self.val, self.count, self.carries, self.ws)
+        torch.cuda.synchronize()
+        n, c = int(self.count.item()), int(self.carries.item())
+        m = min(n, self.idx.numel())
+        got = dict(zip(self.idx[:m].cpu().numpy().tolist(), self.val[:m].cpu().numpy().tolist()))
+        assert len(got) == m
+        return n, c, got
+
+
+def _carry_gpu_fields(fields_np, k, dtype, keep):
+    """Pass k's fields on the device; the last field starts one element into
+    its allocation (element tiles)."""
+    fields = []
+    for n, (chunks, R, C) in enumerate(fields_np):
+        if n == len(fields_np) - 1:
+            big = _to_gpu(np.concatenate([[7], chunks[k].ravel(), [9]]), dtype)
+            keep.append(big)
+            fields.append((big[1:1 + R * C], dtype, R, C))
+        else:
+            fields.append((_to_gpu(chunks[k], dtype), dtype, R, C))
+    return fields
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", ["random", "slices"])
+def test_diff2_carry_matches_oracle(dtype, kind):
+    """Three passes one at a time, carries kept on the device between them:
+    every pass's entries equal the oracle's kept entries, element by element,
+    and the carries kept equal the oracle's in number. Identifier slices
+    leave entries only where diff2 of the identifiers is non-zero."""
+    passes = 3
+    rng = np.random.default_rng(31 + (kind == "slices"))
+    fields_np = _carry_fields(rng, kind, passes)
+    want, carried = _carry_expected(fields_np, passes)
+    numel = sum(R * C for _, R, C in fields_np)
+    keep = []
+    runner = None
+    for k in range(passes):
+        fields = _carry_gpu_fields(fields_np, k, dtype, keep)
+        if runner is None:
+            runner = _CarryRun(fields, numel + 16, numel + 16)
+        say(f"[diff2 carry] {dtype} {kind} pass {k}: {len(fields)} fields, {numel} elements")
+        n, c, got = runner.run(fields, k, k == passes - 1)
+        assert n == len(want[k]), k
+        assert got == want[k], k
+        assert c == carried[k], k
+    if kind == "slices":
+        full = {}
+        off = 0
+        for chunks, R, C in fields_np:
+            A = sum(ch.astype(np.int64) << (16 * k) for k, ch in enumerate(chunks))
+            for (i, j), v in nonzeros(diff2(A)).items():
+                full[off + i * C + j] = v
+            off += R * C
+        assert all(set(w) <= set(full) for w in want)
+        assert sum(carried) > 0
+
+
+def test_diff2_carry_reruns_and_reports_overflow():
+    """Too few carry slots: the count of carries says so. Too little entry
+    room: the pass is run again on the same workspace with more, and the
+    next pass still gets the right carries."""
+    rng = np.random.default_rng(33)
+    F = [rng.integers(0, 1 << 16, size=(50, 90)) for _ in range(2)]
+    fields_np = [(F, 50, 90)]
+    want, carried = _carry_expected(fields_np, 2)
+    f0 = [(_to_gpu(F[0], "bf16"), "bf16", 50, 90)]
+    f1 = [(_to_gpu(F[1], "bf16"), "bf16", 50, 90)]
+    small = _CarryRun(f0, 10, 4500)
+    say("[diff2 carry] overflow of the carry table")
+    n, c, got = small.run(f0, 0, False)
+    assert c == carried[0] > 10
+    assert n == len(want[0]) and got == want[0]
+    room = _CarryRun(f0, 4500, 10)
+    say("[diff2 carry] overflow of the entries, then the pass again")
+    n, c, got = room.run(f0, 0, False)
+    assert n == len(want[0]) > 10 and len(got) == 10 and all(want[0][i] == v for i, v in got.items())
+    room.idx = torch.full((4500,), -1, dtype=torch.int64, device="cuda")
+    room.val = torch.zeros(4500, dtype=torch.int64, device="cuda")
+    n, c, got = room.run(f0, 0, False)
+    assert got == want[0] and c == carried[0]
+    n, c, got = room.run(f1, 1, True)
+    assert got == want[1] and c == 0
+
+
 def _loaders(w, side, ranks):
     par = w[side]
     fn = ref.STYLES[par["style"]]
@@ -235,6 +373,9 @@ def test_probe_recovers_declared_layouts(name, hold):
         assert stats["hold_passes"] == [hold] * len(ranks)
         for k, r in enumerate(ranks):
             rk = L.ranks[r]
+            if not hold:
+                # every pass hands over only entries next to slice-copy corners
+                assert all(p["entries"] <= 16 * len(rk.placements) for p in stats[k]), stats[k]
             keep = [u for u, lc in enumerate(rk.locals) if lc.scales < 0]
             remap = {u: i for i, u in enumerate(keep)}
             want = sorted((p.t, p.r0, p.r1, p.c0, p.c1, remap[p.u], p.base, p.ld, p.tr) for p in rk.placements)
@@ -249,8 +390,9 @@ def test_probe_recovers_declared_layouts(name, hold):
                                             ("llama3_8b_tp4_to_tp2", "trainer", True)])
 def test_probe_full_size(name, side, hold):
     """The benchmark ranks at full size (16 GB identifier checkpoint), probed
-    through the torch loaders, with the passes held on the device or recorded
-    one by one: the recovered placements equal the declared."""
+    through the torch loaders, with the passes held on the device or carried
+    one at a time (each pass handing over only corner entries): the
+    recovered placements equal the declared."""
     from synthetic_checkpoint.workloads import WORKLOADS
 
     w = WORKLOADS[name]
@@ -258,8 +400,13 @@ def test_probe_full_size(name, side, hold):
     L = layout_from_spec(w["model"], w[side])
     cat = [(c.name, c.rows, c.cols) for c in L.catalog]
     say(f"[probe full] {name} {side} rank {rank} hold_passes={hold}")
-    got = wb.probe_layout(cat, w["trainer"]["dtype"], _loaders(w, side, [rank]), hold_passes=hold)
+    stats = {}
+    got = wb.probe_layout(cat, w["trainer"]["dtype"], _loaders(w, side, [rank]), hold_passes=hold, stats=stats)
     rk = L.ranks[rank]
+    if not hold:
+        say(f"[probe full] passes: {[(p['entries'], p['carries']) for p in stats[0]]}")
+        assert all(p["entries"] <= 16 * len(rk.placements) for p in stats[0])
+        assert stats[0][0]["carries"] > 0 and "carry_retries" not in stats
     keep = [u for u, lc in enumerate(rk.locals) if lc.scales < 0]
     remap = {u: i for i, u in enumerate(keep)}
     want = sorted((p.t, p.r0, p.r1, p.c0, p.c1, remap[p.u], p.base, p.ld, p.tr) for p in rk.placements)

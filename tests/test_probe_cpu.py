@@ -10,7 +10,8 @@ import pytest
 
 import paper_2609_25442_amd as wb
 from oracle.catalog import CkptTensor
-from oracle.diff2 import FIRST_ID, diff2, id_chunk, id_fields, nonzeros, num_chunks, probe_fields, recombine
+from oracle.diff2 import (FIRST_ID, carry_passes, diff2, id_chunk, id_fields, nonzeros, num_chunks, probe_fields,
+                          recombine)
 from oracle.layout import Layout, Local, Placement, RankLayout, describe_layout, layout_from_spec
 from synthetic_checkpoint.workloads import ORDER, scaled
 
@@ -23,15 +24,18 @@ def to_oracle_rank(L: "wb.Layout", rank: int) -> RankLayout:
     return RankLayout(locs, pls)
 
 
-def probe_via_library(layout, rank, dtype="bf16", combined=False):
+def probe_via_library(layout, rank, dtype="bf16", combined=False, carried=False):
     """Feed the oracle's passes of one declared rank into the library scan,
     pass by pass, or (combined) recombined first and recorded as chunk 0, as
-    the batched diff2 over held passes hands them over."""
+    the batched diff2 over held passes hands them over, or (carried) the
+    entries the carry passes keep, pass by pass."""
     cat = [(c.name, c.rows, c.cols) for c in layout.catalog]
     P = wb.Probe(cat, dtype)
     assert P.num_chunks == num_chunks(layout.catalog, 16)
     fields = id_fields(layout, rank)
     per_chunk, _ = probe_fields(fields, 16, P.num_chunks)
+    if carried:
+        per_chunk = [carry_passes([id_chunk(A, k, 16) for k in range(P.num_chunks)], 16)[0] for A in fields]
     rk = layout.ranks[rank]
     for u, lc in enumerate(rk.locals):
         assert P.add_local(lc.name, dtype, lc.batch, lc.rows, lc.cols) == u
@@ -50,8 +54,8 @@ def probe_via_library(layout, rank, dtype="bf16", combined=False):
     return out, fields
 
 
-def check(layout, rank, combined=False):
-    out, fields = probe_via_library(layout, rank, combined=combined)
+def check(layout, rank, combined=False, carried=False):
+    out, fields = probe_via_library(layout, rank, combined=combined, carried=carried)
     got = id_fields(Layout(layout.catalog, [to_oracle_rank(out, 0)]), 0)
     for A, B in zip(fields, got):
         assert np.array_equal(A, B)
@@ -152,3 +156,63 @@ def test_diff2_batch_workspace():
     arr = wb._field_array([(A, "bf16", 4, 4)])
     arr[0].passes = 0
     assert wb.lib.wb_diff2_batch_workspace(arr, 1, wb.byref(wb.c_size_t())) == wb.WB_EINVAL
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_workload_ranks_recovered_from_carried_passes(name):
+    w = scaled(name)
+    for side in ("trainer", "rollout"):
+        L = layout_from_spec(w["model"], w[side])
+        for r in sorted({0, L.nranks - 1}):
+            check(L, r, carried=True)
+
+
+def test_diff2_carry_workspace():
+    """The carry pass's workspace: the field and tile tables of
+    wb_diff2_batch, 256-byte aligned, 2 KiB of counters, two carry tables of
+    16-byte slots, slots the smallest power of two at least twice the
+    capacity and at least 64, then 64 staged carries of 16 bytes and a 4-byte
+    count per tile."""
+    A = 1 << 20
+
+    def tables(cap):
+        slots = 64
+        while slots < 2 * cap:
+            slots *= 2
+        return 2 * slots * 16
+
+    def ws(fields, cap):
+        return wb.diff2_carry_workspace(fields, cap)
+
+    assert ws([], 1) == 2048 + tables(1)
+    assert ws([], 100) == 2048 + tables(100) == 2048 + 2 * 256 * 16
+    f = [(A, "bf16", 300, 4096), (A, "f32", 1, 1 << 20)]
+    head = wb.diff2_batch_workspace(f)
+    ntiles = (head - 2 * 56) // 24
+    stage = ntiles * 64 * 16 + -(-ntiles * 4 // 256) * 256
+    for cap in (1, 33, 1000, 1 << 20):
+        assert ws(f, cap) == -(-head // 256) * 256 + 2048 + tables(cap) + stage
+    for bad_cap in (0, -1, (1 << 36) + 1):
+        with pytest.raises(wb.WbError):
+            ws(f, bad_cap)
+    with pytest.raises(wb.WbError):
+        ws([([A, A + 64], "bf16", 4, 4)], 10)       # a carry pass reads one pass per field
+
+
+def test_diff2_carry_argument_checks():
+    """Refusals decided on the host before any device access."""
+    A = 1 << 20
+    arr = wb._field_array([(A, "bf16", 4, 4)])
+    d = wb.c_void_p(A)
+
+    def call(pass_=0, cap=10, ws=d, nbytes=1 << 20, count=d, carries=d, capacity=4):
+        return wb.lib.wb_diff2_carry(arr, 1, pass_, 0, cap, ws, nbytes, d, d, capacity, count, carries, None)
+
+    assert call(pass_=-1) == wb.WB_EINVAL
+    assert call(capacity=-1) == wb.WB_EINVAL
+    assert call(count=None) == wb.WB_EINVAL
+    assert call(count=wb.c_void_p(A + 4)) == wb.WB_EINVAL
+    assert call(carries=None) == wb.WB_EINVAL
+    assert call(carries=wb.c_void_p(A + 4)) == wb.WB_EINVAL
+    assert call(ws=None) == wb.WB_EINVAL
+    assert call(ws=wb.c_void_p(A + 4)) == wb.WB_EINVAL
