@@ -376,7 +376,8 @@ def run_probe(args):
         # the stencils alone: each carry pass over the loaded tensors of that
         # pass (in order, since a pass reads the carries of the one before),
         # and one launch over all passes held on the device; a timed call
-        # includes its small table upload
+        # includes the library's host work (tile table, its upload and the
+        # wait for it), the field arrays are built beforehand
         probe = wb.Probe(cat, dtype)
         ckpt = {n: torch.empty((r, c), dtype=wb.torch_dtype(dtype), device="cuda") for n, r, c in cat}
         held = []
@@ -386,8 +387,8 @@ def run_probe(args):
             held.append([x.clone() for x in load(ckpt)])
         del ckpt
         shapes = [wb._view_shape(x) for x in held[0]]
-        per_pass = [[(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(h, shapes)] for h in held]
-        every = [([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)]
+        per_pass = [wb._field_array([(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(h, shapes)]) for h in held]
+        every = wb._field_array([([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)])
         cap = 1 << 21
         idx = torch.empty(cap, dtype=torch.int64, device="cuda")
         val = torch.empty(cap, dtype=torch.int64, device="cuda")

@@ -598,6 +598,10 @@ def diff2(src, dtype: str, rows: int, cols: int, index, value, count, stream=Non
 
 
 def _field_array(fields):
+    """ctypes wb_field array of (tensors, dtype, rows, cols) tuples; an array
+    built here before is passed through."""
+    if isinstance(fields, ctypes.Array):
+        return fields
     arr = (Field * len(fields))()
     for f, (ts, dtype, rows, cols) in enumerate(fields):
         ts = list(ts) if isinstance(ts, (list, tuple)) else [ts]

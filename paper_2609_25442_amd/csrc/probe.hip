@@ -164,6 +164,13 @@ struct ListOut {
   __device__ __forceinline__ void put(bool nz, int64_t pos, T d, int lane) const {
     sink_append(*buf, sink, nz, pos, int64_t(d), lane);
   }
+  // the V values of a lane at pos0 .. pos0 + V - 1, bit k of `any` set where
+  // value k is a candidate
+  template <int V>
+  __device__ __forceinline__ void put_row(unsigned any, int64_t pos0, const T* d, int lane) const {
+#pragma unroll
+    for (int k = 0; k < V; ++k) put((any >> k) & 1u, pos0 + k, d[k], lane);
+  }
   __device__ __forceinline__ void flush() const { sink_flush(*buf, sink); }
 };
 
@@ -204,8 +211,9 @@ __device__ __forceinline__ int carry_lookup(const CarryTable& t, int64_t pos) {
   return 0;
 }
 
-// Carries are counted per workgroup on one of kCarryCounters counters (an
-// add whose result is not needed), so no single address takes them all.
+// Carries that do not fit the workgroup's buffer are inserted at once and
+// counted on one of kCarryCounters counters (an add whose result is not
+// needed).
 __device__ __forceinline__ void carry_spill(const CarryTable& t, bool spill, int64_t pos, int64_t packed, int lane) {
   const unsigned long long ms = __ballot(spill);
   if (ms == 0) return;
@@ -214,9 +222,10 @@ __device__ __forceinline__ void carry_spill(const CarryTable& t, bool spill, int
   if (spill) carry_insert(t, pos, packed);
 }
 
-// The workgroup's buffered carries: counted with one add; with kStage (a
-// stencil tile) the first kCarryStage are staged for the insert launch with
-// plain stores and the rest inserted here, otherwise all are inserted here.
+// The workgroup's buffered carries. With kStage (a stencil tile) the first
+// kCarryStage are staged for the insert launch with plain stores and their
+// number stored for the tile (no atomic), the rest inserted and counted
+// here; otherwise all are inserted here and counted with one add.
 template <bool kStage>
 __device__ __forceinline__ void carry_flush(WgBuf& b, const CarryTable& t) {
   __syncthreads();
@@ -224,7 +233,7 @@ __device__ __forceinline__ void carry_flush(WgBuf& b, const CarryTable& t) {
   const unsigned m = kStage ? (n < unsigned(kCarryStage) ? n : unsigned(kCarryStage)) : 0u;
   if (threadIdx.x == 0) {
     if (kStage) t.stage_n[blockIdx.x] = int32_t(m);
-    if (n) atomicAdd(t.count + blockIdx.x % kCarryCounters, static_cast<unsigned long long>(n));
+    if (n > m) atomicAdd(t.count + blockIdx.x % kCarryCounters, static_cast<unsigned long long>(n - m));
   }
   for (unsigned k = threadIdx.x; k < n; k += blockDim.x) {
     if (k < m) {
@@ -237,11 +246,11 @@ __device__ __forceinline__ void carry_flush(WgBuf& b, const CarryTable& t) {
   }
 }
 
-// A carry pass's output. put() takes a candidate position of the stencil:
-// with carries in (kIn), non-zero D wait in `pending` and are looked up
-// together when the tile ends (one round of table reads per workgroup rather
-// than a stall per wavefront); split() turns S into an emitted value and a
-// carry.
+// A carry pass's output. The stencil's candidates (non-zero D) wait in
+// `pending`, placed with one LDS add per wavefront per row, and are split
+// together when the tile ends: the carry of pass k - 1 is looked up (kIn),
+// S = D + carry gives an emitted value and a carry (split). Candidates that
+// do not fit `pending` are split at once.
 template <bool kIn, bool kLast, bool kStage>
 struct CarryOut {
   WgBuf* ebuf;
@@ -261,29 +270,68 @@ struct CarryOut {
       carry_spill(next, wg_place(*cbuf, cq, pos, packed, lane), pos, packed, lane);
     }
   }
+  __device__ __forceinline__ int carry_in(bool c, int64_t pos) const { return kIn && c ? carry_lookup(in, pos) : 0; }
   __device__ __forceinline__ void put(bool nz, int64_t pos, int d, int lane) const {
-    if (!kIn) {
-      split(nz, pos, d, field, lane);
-      return;
-    }
-    const bool inl = wg_place(*pending, nz, pos, int64_t(d), lane);
-    if (__ballot(inl) == 0) return;
-    split(inl, pos, inl ? d + carry_lookup(in, pos) : 0, field, lane);
+    const bool now = wg_place(*pending, nz, pos, int64_t(d), lane);
+    if (__ballot(now) == 0) return;
+    split(now, pos, d + carry_in(now, pos), field, lane);
   }
-  __device__ __forceinline__ void flush() const {
-    if (kIn) {
-      __syncthreads();
-      const unsigned n = pending->n < unsigned(kWgCap) ? pending->n : unsigned(kWgCap);
-      for (unsigned b0 = 0; b0 < n; b0 += blockDim.x) {
-        const unsigned k = b0 + threadIdx.x;
-        const bool ok = k < n;
-        const int64_t pos = ok ? pending->pos[k] : 0;
-        const int s = ok ? int(pending->val[k]) + carry_lookup(in, pos) : 0;
-        split(ok, pos, s, field, threadIdx.x & 63);
+  // All lanes of the wavefront call it, with at least one bit set in some
+  // lane's `any`; the count of a lane (at most 8) is summed over the
+  // wavefront bit by bit with four ballots.
+  template <int V>
+  __device__ __forceinline__ void put_row(unsigned any, int64_t pos0, const int* d, int lane) const {
+    static_assert(V <= 8, "at most 8 values per lane");
+    const unsigned c = __popc(any);
+    const unsigned long long lt = lane ? (1ull << lane) - 1 : 0ull;
+    unsigned below = 0, total = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const unsigned long long m = __ballot((c >> b) & 1u);
+      below += unsigned(__popcll(m & lt)) << b;
+      total += unsigned(__popcll(m)) << b;
+    }
+    unsigned off = 0;
+    if (lane == 0) off = atomicAdd(&pending->n, total);
+    off = __shfl(off, 0, 64);
+    unsigned slot = off + below;
+    unsigned now = 0;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      if ((any >> k) & 1u) {
+        if (slot < unsigned(kWgCap)) {
+          pending->pos[slot] = pos0 + k;
+          pending->val[slot] = d[k];
+        } else {
+          now |= 1u << k;
+        }
+        ++slot;
       }
     }
+    if (__ballot(now != 0) == 0) return;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const bool c1 = (now >> k) & 1u;
+      if (__ballot(c1) == 0) continue;
+      split(c1, pos0 + k, d[k] + carry_in(c1, pos0 + k), field, lane);
+    }
+  }
+  // the emitted values and the carries of the workgroup
+  __device__ __forceinline__ void flush_outputs() const {
     sink_flush(*ebuf, sink);
     if (!kLast) carry_flush<kStage>(*cbuf, next);
+  }
+  __device__ __forceinline__ void flush() const {
+    __syncthreads();
+    const unsigned n = pending->n < unsigned(kWgCap) ? pending->n : unsigned(kWgCap);
+    for (unsigned b0 = 0; b0 < n; b0 += blockDim.x) {
+      const unsigned k = b0 + threadIdx.x;
+      const bool ok = k < n;
+      const int64_t pos = ok ? pending->pos[k] : 0;
+      const int s = ok ? int(pending->val[k]) + carry_in(true, pos) : 0;
+      split(ok, pos, s, field, threadIdx.x & 63);
+    }
+    flush_outputs();
   }
 };
 
@@ -426,8 +474,7 @@ __device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64
         any |= (live && i >= i0 && d[k] != 0) ? (1u << k) : 0u;
       }
       if (__ballot(any != 0) == 0) continue;
-#pragma unroll
-      for (int k = 0; k < V; ++k) out.put((any >> k) & 1u, base + i * cols + j0 + k, d[k], lane);
+      out.template put_row<V>(any, base + i * cols + j0, d, lane);
     }
   }
 }
@@ -467,8 +514,7 @@ __device__ __forceinline__ void flat_tile(const Passes<P>& s, int64_t cols, int6
 #pragma unroll
     for (int k = 0; k < V; ++k) any |= (v < nvec && d[k] != 0) ? (1u << k) : 0u;
     if (__ballot(any != 0) == 0) continue;
-#pragma unroll
-    for (int k = 0; k < V; ++k) out.put((any >> k) & 1u, base + v * V + k, d[k], lane);
+    out.template put_row<V>(any, base + v * V, d, lane);
   }
 }
 
@@ -520,10 +566,11 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __r
 
 // Batched launches: workgroup b takes tile b of the table, taller VEC tiles
 // and FLAT tiles of several sub-tiles (fewer, larger table rows). Held passes
-// recombine up to kMaxPasses passes in int64 with fewer values in flight per
-// lane; carry passes read one pass in int.
+// recombine up to kMaxPasses passes in int64, two rows in flight per lane;
+// carry passes read one pass in int, one row at a time (fewer registers, more
+// wavefronts: measured faster than two or four rows in flight).
 constexpr int kBatchUnroll = 2;
-constexpr int kCarryUnroll = 4;
+constexpr int kCarryUnroll = 1;
 constexpr int kBatchVecStrip = 128;
 constexpr int kBatchFlatUnroll = 4;
 constexpr int kBatchFlatSub = 4;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
@@ -632,7 +679,7 @@ __global__ __launch_bounds__(kThreads) void wb_carry_rest_kernel(const DiffField
     }
     out.split(take, pos, q, field, lane);
   }
-  out.flush();
+  out.flush_outputs();
 }
 
 // Insert the carries the stencil workgroups staged: one thread per staging
@@ -659,14 +706,28 @@ __global__ __launch_bounds__(kThreads) void wb_carry_clear_kernel(int64_t* slot,
   }
 }
 
-// The carries a pass kept: the sum of the counters, or past the capacity if
-// an insert found no slot.
-__global__ void wb_carry_report_kernel(const unsigned long long* counters, int64_t capacity, unsigned long long* out) {
+// The carries a pass kept: the staged counts of the ntiles stencil tiles
+// plus the counters of the carries inserted directly, or past the capacity
+// if an insert found no slot. One workgroup.
+__global__ __launch_bounds__(kThreads) void wb_carry_report_kernel(const int32_t* stage_n, int64_t ntiles,
+                                                                  const unsigned long long* counters,
+                                                                  int64_t capacity, unsigned long long* out) {
+  __shared__ unsigned long long part[kThreads];
   unsigned long long n = 0;
-  for (int k = 0; k < kCarryCounters; ++k) n += counters[k];
-  if (counters[kCarryCounters] && n <= static_cast<unsigned long long>(capacity))
-    n = static_cast<unsigned long long>(capacity) + 1;
-  *out = n;
+  for (int64_t t = threadIdx.x; t < ntiles; t += kThreads) n += static_cast<unsigned long long>(stage_n[t]);
+  if (threadIdx.x < kCarryCounters) n += counters[threadIdx.x];
+  part[threadIdx.x] = n;
+  __syncthreads();
+  for (int w = kThreads / 2; w > 0; w /= 2) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    unsigned long long total = part[0];
+    if (counters[kCarryCounters] && total <= static_cast<unsigned long long>(capacity))
+      total = static_cast<unsigned long long>(capacity) + 1;
+    *out = total;
+  }
 }
 
 
@@ -806,7 +867,8 @@ int launch_diff2_carry(const DiffField* fields, int32_t nfields, const DiffTile*
       hipLaunchKernelGGL(wb_carry_rest_kernel<false>, grid, dim3(kThreads), 0, st, fields, int(nfields), in, next,
                          sink);
   }
-  hipLaunchKernelGGL(wb_carry_report_kernel, dim3(1), dim3(1), 0, st, next.count, next.capacity, carries);
+  hipLaunchKernelGGL(wb_carry_report_kernel, dim3(1), dim3(kThreads), 0, st, next.stage_n, last ? 0 : ntiles,
+                     next.count, next.capacity, carries);
   return hipGetLastError();
 }
 
