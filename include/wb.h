@@ -394,10 +394,10 @@ void wb_plan_destroy(wb_plan_t* plan);
  * gets the identifier 2^24 + its flat position in the checkpoint (catalog
  * order, row-major; 0 marks an element no loader wrote). The checkpoint is
  * loaded once per 16-bit chunk of the identifiers (wb_probe_chunks passes);
- * after pass k the caller runs wb_diff2 on every loaded local tensor and hands
- * the entries to wb_probe_record. The library sums 2^(16 k) times pass k's
- * entries, which is exactly diff2 of the full identifier field because diff2
- * is linear (the paper's carry records are not needed for exactness), and
+ * after pass k the caller runs wb_diff2_carry over the loaded local tensors
+ * (or wb_diff2 on each) and hands the entries to wb_probe_record. The library
+ * sums 2^(16 k) times pass k's entries, which is exactly diff2 of the full
+ * identifier field because diff2 is linear and the carries telescope, and
  * wb_probe_scan turns the result into slice-copy placements without building
  * the identifier field: between rows and columns that hold entries the field
  * is a bilinear polynomial given by prefix sums of four moments of the
@@ -418,9 +418,9 @@ int wb_probe_first_id(const wb_probe_t* probe, int32_t t, int64_t* id);
 int wb_probe_add_local(wb_probe_t* probe, const char* name, int32_t dtype, int64_t batch, int64_t rows, int64_t cols,
                        int32_t* index);
 /* Host arrays of n entries of pass `chunk` for local tensor `local`: flat
- * element index and diff2 value (as wb_diff2 writes them, widened to int64),
- * added times 2^(16 chunk). Entries of wb_diff2_batch over all passes at once
- * are recorded as chunk 0. Errors: WB_EINVAL (index or chunk out of range). */
+ * element index and value (as wb_diff2 or wb_diff2_carry write them, widened
+ * to int64), added times 2^(16 chunk). Entries of wb_diff2_batch over all
+ * passes at once are recorded as chunk 0. Errors: WB_EINVAL (index or chunk out of range). */
 int wb_probe_record(wb_probe_t* probe, int32_t local, int32_t chunk, const int64_t* index, const int64_t* value,
                     int64_t n);
 /* Fill rank `rank` of `layout` (made by wb_layout_create over the same catalog,

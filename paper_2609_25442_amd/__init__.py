@@ -723,23 +723,22 @@ def _record_split(probe, chunk, offsets, index, value):
 
 
 def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", stats=None,
-                 hold_passes=None, carry_capacity=None) -> "Layout":
+                 hold_passes=False, carry_capacity=None) -> "Layout":
     """Discover a layout from weight loaders: ``loaders[r](ckpt)`` takes the
     checkpoint as {name: tensor} and returns rank r's local tensors (a list of
     1-, 2- or 3-D tensors, always the same shapes, values copied unchanged).
     Returns a Layout with one rank per loader.
 
-    With ``hold_passes`` a copy of every pass's loaded tensors stays in device
-    memory and one diff2 launch over all passes runs at the end (the chunk
-    wrap-arounds cancel inside it, so only the identifier field's few entries
-    reach the host). Otherwise every pass runs diff2_carry as soon as it is
-    loaded: each pass hands the host only the entries next to slice-copy
-    corners and keeps its wrap-arounds as device carries for the next pass
-    (``carry_capacity`` carries per pass, by default about 16 per 2^16
-    elements; a rank whose passes need more is probed again with room for
-    what they needed). None picks holding when the passes fit in free device
-    memory with a quarter to spare. ``stats`` (a dict) receives timings and
-    entry counts when given."""
+    Every pass runs diff2_carry as soon as it is loaded: each pass hands the
+    host only the entries next to slice-copy corners and keeps its
+    wrap-arounds as device carries for the next pass (``carry_capacity``
+    carries per pass, by default about 16 per 2^16 elements; a rank whose
+    passes need more is probed again with room for what they needed). With
+    ``hold_passes`` a copy of every pass's loaded tensors stays in device
+    memory instead and one diff2 launch over all passes runs at the end (the
+    chunk wrap-arounds cancel inside it); None holds them when they fit in
+    free device memory with a quarter to spare. ``stats`` (a dict) receives
+    timings and entry counts when given."""
     tdt = torch_dtype(ckpt_dtype)
     layout = Layout.create(catalog, len(loaders))
     ckpt = {}
