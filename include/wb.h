@@ -292,14 +292,20 @@ int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* 
  * work (two with whole transpose tiles) and one for fp8 blocks when the rank
  * has fp8 tensors.
  * Errors as for wb_pack. Calls on one plan must not overlap in time from several
- * host threads (the pointer table is per plan). */
+ * host threads (the pointer tables are per plan; see wb_pack_round). */
 int wb_unpack(wb_plan_t* plan, const void* recv_buf, void* const* dst_ptrs, void* stream);
 
 /* One round of a multi-round plan: the same contracts as wb_pack / wb_unpack for
  * the round's work items and buffer (wb_plan_round_buffer_bytes). The send or
  * receive buffer is a launch argument, so consecutive rounds may alternate
- * between buffers (double buffering) without restaging the pointer table;
- * the local tensors must stay the same, or calls must be stream-ordered.
+ * between buffers (double buffering) at no cost. The local-tensor pointers
+ * are read from a device table: a plan keeps the tables of its last four
+ * pointer sets, so alternating sets costs no copy and no host wait; a new set
+ * refills the least recently staged table, and the host waits only for that
+ * table's staging copy from four sets before. Work on another stream that read
+ * or wrote a table is waited for on the calling stream before the table is
+ * read or rewritten (hipStreamWaitEvent), so calls on several streams may
+ * share a plan when made from one host thread.
  * wb_pack / wb_unpack refuse (WB_EINVAL) plans with more than one round. */
 int wb_pack_round(wb_plan_t* plan, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream);
 int wb_unpack_round(wb_plan_t* plan, int32_t round, const void* recv_buf, void* const* dst_ptrs, void* stream);

@@ -74,19 +74,55 @@ int check_extent(const void* p, int64_t bytes, const char* what, int align = 16)
 }
 
 // Stage a new pointer table into the workspace when the pointers changed.
-int update_pointers(wb_plan_t* P, const std::vector<uint64_t>& ptrs, void* stream) {
-  if (ptrs == P->last_ptrs) return WB_OK;
-  hipEvent_t ev = static_cast<hipEvent_t>(P->ptr_event);
-  hipError_t e = hipEventSynchronize(ev);  // the previous staging copy has left the pinned buffer
-  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-  std::memcpy(P->ptr_stage, ptrs.data(), ptrs.size() * sizeof(uint64_t));
-  e = hipMemcpyAsync(P->ws + P->off_ptrs, P->ptr_stage, ptrs.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
-                     static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (pointer table)");
-  e = hipEventRecord(ev, static_cast<hipStream_t>(stream));
+// The device pointer table of `ptrs` for work enqueued on `stream`. A slot
+// that already holds the set is reused; otherwise the least recently staged
+// slot is restaged. Either way, work on another stream that last touched the
+// slot is waited for on `stream` (no host wait), so a table is never
+// overwritten while read, nor read before its copy; the host waits only for
+// the staging copy of the slot it refills (issued kPtrSlots new sets ago).
+// Returns the slot, or -1 with the error set.
+int table_slot(wb_plan_t* P, const std::vector<uint64_t>& ptrs, void* stream) {
+  hipError_t e;
+  int k = -1;
+  for (int i = 0; i < wb_plan_t::kPtrSlots && k < 0; ++i)
+    if (P->slot_ptrs[i] == ptrs) k = i;
+  const bool restage = k < 0;
+  if (restage) {
+    k = P->next_slot;
+    P->next_slot = (k + 1) % wb_plan_t::kPtrSlots;
+  }
+  if ((restage || P->ptr_stream[k] != stream) &&
+      (e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(P->ptr_done[k]), 0)) !=
+          hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent"), -1;
+  if (restage) {
+    const size_t n = ptrs.size();
+    if ((e = hipEventSynchronize(static_cast<hipEvent_t>(P->ptr_copied[k]))) != hipSuccess)
+      return hip_fail(e, "hipEventSynchronize"), -1;
+    uint64_t* stage = static_cast<uint64_t*>(P->ptr_stage) + k * n;
+    std::memcpy(stage, ptrs.data(), n * sizeof(uint64_t));
+    P->slot_ptrs[k].clear();  // holds nothing until the copy is enqueued
+    if ((e = hipMemcpyAsync(P->ws + P->off_ptrs + k * n * sizeof(uint64_t), stage, n * sizeof(uint64_t),
+                            hipMemcpyHostToDevice, static_cast<hipStream_t>(stream))) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync (pointer table)"), -1;
+    if ((e = hipEventRecord(static_cast<hipEvent_t>(P->ptr_copied[k]), static_cast<hipStream_t>(stream))) !=
+        hipSuccess)
+      return hip_fail(e, "hipEventRecord"), -1;
+    P->slot_ptrs[k] = ptrs;
+  }
+  return k;
+}
+
+// Record that the work just enqueued on stream touched slot k.
+int table_done(wb_plan_t* P, int k, void* stream) {
+  const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(P->ptr_done[k]), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-  P->last_ptrs = ptrs;
+  P->ptr_stream[k] = stream;
   return WB_OK;
+}
+
+const uint64_t* table_at(const wb_plan_t* P, int k) {
+  return reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs) + size_t(k) * (P->n_locals + 1);
 }
 
 int64_t local_bytes(const wb::Local& l) { return l.numel() * wb::dtype_bytes(l.dtype); }
@@ -444,7 +480,7 @@ int wb_plan_local_tensor(const wb_plan_t* P, int32_t i, int32_t* dtype, int64_t*
 static void workspace_layout(const wb_plan_t* P, size_t* ptrs, size_t* tasks, size_t* qb, size_t* qp, size_t* total) {
   size_t off = 0;
   *ptrs = off;
-  off = align256(off + sizeof(uint64_t) * (P->n_locals + 1));
+  off = align256(off + wb_plan_t::kPtrSlots * sizeof(uint64_t) * (P->n_locals + 1));
   *tasks = off;
   off = align256(off + sizeof(wb::Task) * P->tasks.size());
   *qb = off;
@@ -550,21 +586,31 @@ int wb_plan_upload(wb_plan_t* P, void* workspace, size_t bytes, void* stream) {
         (e = hipMemcpyAsync(ws + P->off_qpieces, P->qpieces.data(), sizeof(wb::QPiece) * P->qpieces.size(),
                             hipMemcpyHostToDevice, st)) != hipSuccess)
       return hip_fail(e, "hipMemcpyAsync (fp8 pieces)");
+    for (int k = 0; k < wb_plan_t::kPtrSlots; ++k) {
+      for (void** ev : {&P->ptr_copied[k], &P->ptr_done[k]}) {
+        if (*ev) continue;
+        hipEvent_t h;
+        if ((e = hipEventCreateWithFlags(&h, hipEventDisableTiming)) != hipSuccess)
+          return hip_fail(e, "hipEventCreateWithFlags");
+        *ev = h;
+      }
+    }
     if (!P->ptr_stage) {
-      if ((e = hipHostMalloc(&P->ptr_stage, sizeof(uint64_t) * (P->n_locals + 1), hipHostMallocDefault)) != hipSuccess) {
+      const size_t stage_bytes = wb_plan_t::kPtrSlots * sizeof(uint64_t) * (P->n_locals + 1);
+      if ((e = hipHostMalloc(&P->ptr_stage, stage_bytes, hipHostMallocDefault)) != hipSuccess) {
         P->ptr_stage = nullptr;
         return hip_fail(e, "hipHostMalloc (pointer staging)");
       }
-      hipEvent_t ev;
-      if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess)
-        return hip_fail(e, "hipEventCreateWithFlags");
-      P->ptr_event = ev;
     }
     // the host tables must stay valid until the copies above have run
     if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     P->ws = ws;
     P->ws_bytes = bytes;
-    P->last_ptrs.clear();
+    for (int k = 0; k < wb_plan_t::kPtrSlots; ++k) {
+      P->slot_ptrs[k].clear();
+      P->ptr_stream[k] = stream;  // the new workspace's tables have not been touched yet
+    }
+    P->next_slot = 0;
     return WB_OK;
   });
 }
@@ -582,13 +628,16 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
   if (rc != WB_OK) return rc;
   std::vector<uint64_t> ptrs(P->n_locals + 1, 0);
   for (int i = 0; i < P->n_locals; ++i) ptrs[i + 1] = reinterpret_cast<uint64_t>(locals[i]);
-  if (ptrs != P->last_ptrs) {
+  bool known = false;
+  for (const auto& v : P->slot_ptrs) known = known || v == ptrs;
+  if (!known) {
     for (int i = 0; rc == WB_OK && i < P->n_locals; ++i)
       rc = check_extent(locals[i], local_bytes(R.locals[i]), ("local tensor " + std::to_string(i)).c_str());
     if (rc != WB_OK) return rc;
-    if ((rc = update_pointers(P, ptrs, stream)) != WB_OK) return rc;
   }
-  const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
+  const int slot = table_slot(P, ptrs, stream);
+  if (slot < 0) return WB_EHIP;
+  const uint64_t* table = table_at(P, slot);
   const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
   int e = wb::launch_tasks(tasks + P->round_tasks[round], P->round_tasks[round + 1] - P->round_tasks[round],
                            P->round_split[round], table, buf, nullptr, stream);
@@ -598,7 +647,7 @@ static int run_round(wb_plan_t* P, int round, const void* const* locals, const v
                          P->round_qfull[round], P->round_qsingle[round], reinterpret_cast<const wb::QPiece*>(P->ws + P->off_qpieces), table,
                          buf, stream);
   if (e != 0) return set_error(WB_EHIP, std::string("fp8 launch: ") + wb::hip_error_string(e));
-  return WB_OK;
+  return table_done(P, slot, stream);
 }
 
 int wb_pack_round(wb_plan_t* P, int32_t round, const void* const* src_ptrs, void* send_buf, void* stream) {
@@ -627,6 +676,7 @@ int wb_forward_round(wb_plan_t* P, int32_t round, int32_t stage, const void* rec
     int rc = check_extent(recv_buf, P->rounds[round].recv_total[P->rank], "recv_buf");
     if (rc == WB_OK) rc = check_extent(fwd_buf, P->rounds[round].st[stage].send_bytes[P->rank], "fwd_buf");
     if (rc != WB_OK) return rc;
+    // forwarding reads only the two buffers, never the local-tensor table
     const auto* table = reinterpret_cast<const uint64_t*>(P->ws + P->off_ptrs);
     const auto* tasks = reinterpret_cast<const wb::Task*>(P->ws + P->off_tasks);
     const int e = wb::launch_tasks(tasks + a, b - a, P->fwd_split[stage - 1][round], table,
@@ -1013,9 +1063,12 @@ int wb_diff2_carry(const wb_field* fields, int32_t n, int32_t pass, int32_t last
 
 void wb_plan_destroy(wb_plan_t* P) {
   if (!P) return;
-  if (P->ptr_event) {
-    (void)hipEventSynchronize(static_cast<hipEvent_t>(P->ptr_event));
-    (void)hipEventDestroy(static_cast<hipEvent_t>(P->ptr_event));
+  for (int k = 0; k < wb_plan_t::kPtrSlots; ++k) {
+    for (void* ev : {P->ptr_copied[k], P->ptr_done[k]}) {
+      if (!ev) continue;
+      (void)hipEventSynchronize(static_cast<hipEvent_t>(ev));
+      (void)hipEventDestroy(static_cast<hipEvent_t>(ev));
+    }
   }
   if (P->ptr_stage) (void)hipHostFree(P->ptr_stage);
   delete P;

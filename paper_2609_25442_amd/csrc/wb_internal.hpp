@@ -335,9 +335,16 @@ struct wb_plan_t {
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   size_t off_ptrs = 0, off_tasks = 0, off_qblocks = 0, off_qpieces = 0;
-  void* ptr_stage = nullptr;     // pinned host staging of the pointer table
-  void* ptr_event = nullptr;     // hipEvent_t of the last staging copy
-  std::vector<uint64_t> last_ptrs;
+  // kPtrSlots pointer tables in the workspace (slot k at off_ptrs + k * (n_locals + 1) * 8),
+  // each with its pinned host staging slot, the pointer set it holds, an event
+  // recorded after the last work that wrote or read it and that work's stream
+  static constexpr int kPtrSlots = 4;
+  void* ptr_stage = nullptr;
+  void* ptr_copied[kPtrSlots] = {};  // after the staging copy (the pinned slot is free again)
+  void* ptr_done[kPtrSlots] = {};    // after the last copy or launches touching the table
+  void* ptr_stream[kPtrSlots] = {};  // the stream ptr_done was recorded on
+  std::vector<uint64_t> slot_ptrs[kPtrSlots];
+  int next_slot = 0;
 };
 
 namespace wb {
