@@ -298,11 +298,12 @@ def summarize_trace(workload, trace_csv):
 
 
 def run_ceilings():
-    """This GPU's stream ceilings (paper_2609_25442_amd/wb_ceilings, a separate
-    process: 2 x 8 GiB of device memory while it runs)."""
+    """This GPU's stream ceilings (wb_ceilings, built from ceilings.hip by
+    __graft_entry__.build(); a separate process: 2 x 8 GiB of device memory
+    while it runs)."""
     import subprocess
 
-    exe = os.path.join(ROOT, "paper_2609_25442_amd", "wb_ceilings")
+    exe = os.path.join(ROOT, "wb_ceilings")
     return subprocess.run([exe], capture_output=True, text=True, timeout=300)
 
 
@@ -768,7 +769,7 @@ def main():
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print HBM traffic per launch from two rocprofv3 --pmc runs of this benchmark")
     ap.add_argument("--ceilings", action="store_true",
-                    help="print this GPU's read, write and copy stream ceilings (paper_2609_25442_amd/wb_ceilings)")
+                    help="print this GPU's read, write and copy stream ceilings (wb_ceilings, from ceilings.hip)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
     args = ap.parse_args()

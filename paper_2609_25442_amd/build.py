@@ -18,7 +18,6 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 HOST_SOURCES = ["api.cpp", "layout.cpp", "plan.cpp", "probe.cpp"]
-CEILINGS = os.path.join(HERE, "wb_ceilings")   # stream-bandwidth probe used by bench.py --ceilings
 DEVICE_SOURCES = ["kernels.hip", "probe.hip", "noalloc.hip"]
 # no packed fp32 instructions: hipcc would otherwise form v_pk_*_f32 by itself
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -52,9 +51,6 @@ def build(verbose: bool = False, out: str = OUT, defines=()) -> str:
     tmp = out + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, out)
-    if out == OUT:
-        _run([HIPCC, *DEVICE_FLAGS, os.path.join(CSRC, "ceilings.hip"), "-o", CEILINGS + ".tmp"])
-        os.replace(CEILINGS + ".tmp", CEILINGS)
     if verbose:
         print("built", out)
     return out
