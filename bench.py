@@ -275,6 +275,28 @@ def summarize_counters(workload, fetch_csv, write_csv):
     return out
 
 
+# kernel-trace columns that describe a launch's resources (registers, LDS,
+# workgroup size), reported with its durations
+_RESOURCE_COLUMNS = ("Workgroup_Size", "Arch_VGPR_Count", "Accum_VGPR_Count", "SGPR_Count", "LDS_Block_Size",
+                     "Scratch_Size")
+
+
+def summarize_metric(workload, name, csv_path):
+    """Mean of one rocprofv3 --pmc counter or derived metric (e.g.
+    MeanOccupancyPerCU) per pack and unpack launch of this benchmark."""
+    from synthetic_checkpoint.workloads import WORKLOADS
+
+    grids, _ = _launch_grids(WORKLOADS[workload])
+    rows = [r for r in _read_csv(csv_path) if r["Counter_Name"] == name]
+    out = {"workload": workload, "metric": name, "kernels": {}}
+    for label, ((_, total), kname, _) in grids.items():
+        vals = [float(r["Counter_Value"]) for r in rows
+                if kname in r["Kernel_Name"] and int(r["Grid_Size"]) == total and total > 0]
+        if vals:
+            out["kernels"][label] = {"dispatches": len(vals), "mean": round(statistics.mean(vals), 3)}
+    return out
+
+
 def summarize_trace(workload, trace_csv):
     """Per-launch durations of the pack, unpack and reference-copy kernels from
     a rocprofv3 --kernel-trace run of this benchmark."""
@@ -290,6 +312,10 @@ def summarize_trace(workload, trace_csv):
             res[label] = {"launches": len(ds), "avg_us": round(statistics.mean(ds) / 1e3, 2),
                           "min_us": round(min(ds) / 1e3, 2), "max_us": round(max(ds) / 1e3, 2),
                           "GB/s_at_avg": round((alg[0] + alg[1]) / statistics.mean(ds), 1) if alg else None}
+            first = next(r for r in rows if kname in r["Kernel_Name"] and int(r["Grid_Size_X"]) == gx)
+            used = {k: int(first[k]) for k in _RESOURCE_COLUMNS if first.get(k, "").strip().isdigit()}
+            if used:
+                res[label]["resources"] = used
     copies = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows if "copyBuffer" in r["Kernel_Name"]]
     if copies:
         top = sorted(copies)[-3:]
@@ -604,8 +630,8 @@ def run_workload(args, name, steps, warmup, ceilings=None, with_cpu=False):
             fwd_ms[st] = statistics.mean(e[st].elapsed_time(e[1 + st]) for e in events)
         unpack_ms = statistics.mean(unpack_steps)
         # per-step spread of the two launches (the mean is what the line reports)
-        for name, xs in (("pack", pack_steps), ("unpack", unpack_steps)):
-            spread[name] = {"ms_min": round(min(xs), 4), "ms_median": round(statistics.median(xs), 4),
+        for step, xs in (("pack", pack_steps), ("unpack", unpack_steps)):
+            spread[step] = {"ms_min": round(min(xs), 4), "ms_median": round(statistics.median(xs), 4),
                             "ms_max": round(max(xs), 4)}
         log("unpack ms per step: " + " ".join(f"{x:.3f}" for x in unpack_steps))
     else:
@@ -772,6 +798,8 @@ def main():
                     help="print this GPU's read, write and copy stream ceilings (wb_ceilings, from ceilings.hip)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print per-launch kernel durations from a rocprofv3 --kernel-trace run of this benchmark")
+    ap.add_argument("--summarize-metric", nargs=2, metavar=("NAME", "COUNTER_CSV"),
+                    help="print the mean of one rocprofv3 --pmc counter or derived metric per launch")
     args = ap.parse_args()
     if args.summarize_counters:
         print(json.dumps(summarize_counters(args.workload, *args.summarize_counters), indent=1))
@@ -783,6 +811,9 @@ def main():
         sys.exit(r.returncode)
     if args.summarize_trace:
         print(json.dumps(summarize_trace(args.workload, args.summarize_trace), indent=1))
+        return
+    if args.summarize_metric:
+        print(json.dumps(summarize_metric(args.workload, *args.summarize_metric), indent=1))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the resharding hot path here runs on a single MI355X "

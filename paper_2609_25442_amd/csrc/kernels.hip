@@ -514,17 +514,17 @@ struct PairLane {
 // of rows t / 32 + 8 k, k < 16, as raw bf16. kFull: both blocks present,
 // 128 x 128 and with 8-byte stores, so no load or store needs a predicate.
 // kBands: at least one block of the pair is QB_BANDS; each row's source is
-// base + r * ld2 of the band that holds it (band tables of both blocks are
-// workgroup-uniform, so they stay in scalar registers and each lane selects);
-// otherwise every row follows the single piece's stride.
+// base + r * ld2 of the band that holds it, from the lane's own block's band
+// table (registers: indexed only by unrolled constants); otherwise every row
+// follows the single piece's stride.
 struct PairBands {
-  uint64_t base[2][kMaxBands];  // recv + band offset - first row * pitch (bytes)
-  uint32_t ld2[2][kMaxBands];   // band pitch in bytes
-  uint32_t start[2][kMaxBands]; // first row; bands past the block's last: 256
+  uint64_t base[kMaxBands];   // recv + band offset - first row * pitch (bytes)
+  uint32_t ld2[kMaxBands];    // band pitch in bytes
+  uint32_t start[kMaxBands];  // first row; bands past the block's last: 256
 };
 
 template <bool kFull, bool kBands>
-__device__ __forceinline__ void qblock_pair_run(const PairLane& L, const PairBands* S, int h, bool on,
+__device__ __forceinline__ void qblock_pair_run(const PairLane& L, const PairBands& S, int h, bool on,
                                                 const QBlock& b0, const QBlock& b1, const uint64_t* __restrict__ ptrs) {
   constexpr int R = 16, kStep = 8;
   static_assert(kQBlockThreads == 32 * kStep, "pair mapping");
@@ -538,13 +538,13 @@ __device__ __forceinline__ void qblock_pair_run(const PairLane& L, const PairBan
       const uint32_t r = rb + kStep * k;
       raw[k] = u32x4{0u, 0u, 0u, 0u};
       if (kFull || (int(r) < L.rows && cg < L.cols)) {
-        uint64_t base = h ? S->base[1][0] : S->base[0][0];
-        uint32_t ld2 = h ? S->ld2[1][0] : S->ld2[0][0];
+        uint64_t base = S.base[0];
+        uint32_t ld2 = S.ld2[0];
 #pragma unroll
         for (int j = 1; j < kMaxBands; ++j)
-          if (r >= (h ? S->start[1][j] : S->start[0][j])) {
-            base = h ? S->base[1][j] : S->base[0][j];
-            ld2 = h ? S->ld2[1][j] : S->ld2[0][j];
+          if (r >= S.start[j]) {
+            base = S.base[j];
+            ld2 = S.ld2[j];
           }
         raw[k] = ld(reinterpret_cast<const u32x4*>(base + uint64_t(r) * ld2 + uint64_t(cg) * 2));
       }
@@ -621,7 +621,7 @@ __device__ __forceinline__ void qblock_pair_full(const QBlock* __restrict__ bloc
   const QBlock b0 = blocks[i0];
   const QBlock b1 = blocks[i0 + 1];
   const int h = (threadIdx.x >> 4) & 1;
-  qblock_pair_run<true, false>(pair_lane(b0, b1, h, true, ptrs, recv), nullptr, h, true, b0, b1, ptrs);
+  qblock_pair_run<true, false>(pair_lane(b0, b1, h, true, ptrs, recv), PairBands{}, h, true, b0, b1, ptrs);
 }
 
 // Blocks i0 and i0 + 1 (absent when i0 + 1 == n), both pairable, any extent.
@@ -639,39 +639,39 @@ __device__ __forceinline__ void qblock_pair(const QBlock* __restrict__ blocks, u
                     (b0.flags & b1.flags & QB_VEC_STORE);
   const bool bands = ((b0.flags | b1.flags) & QB_BANDS) != 0;  // uniform over the workgroup
   if (bands) {
+    // the band table of this lane's block (its own stride when it is a
+    // single piece)
+    const uint32_t flags = h ? b1.flags : b0.flags;
+    const uint32_t np = h ? b1.npieces : b0.npieces, p0 = h ? b1.piece0 : b0.piece0;
     PairBands S;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const QBlock& tb = hh ? b1 : b0;
+    for (int j = 0; j < kMaxBands; ++j) {
+      S.base[j] = 0;
+      S.ld2[j] = 0;
+      S.start[j] = 256;
+    }
+    if (flags & QB_BANDS) {
 #pragma unroll
-      for (int j = 0; j < kMaxBands; ++j) {
-        S.base[hh][j] = 0;
-        S.ld2[hh][j] = 0;
-        S.start[hh][j] = 256;
-      }
-      if (tb.flags & QB_BANDS) {
-#pragma unroll
-        for (int j = 0; j < kMaxBands; ++j)
-          if (j < tb.npieces) {
-            const QPiece q = pieces[tb.piece0 + j];
-            S.ld2[hh][j] = q.src_ld * 2;
-            S.base[hh][j] = reinterpret_cast<uint64_t>(recv) + q.src_off - uint64_t(q.r0) * S.ld2[hh][j];
-            S.start[hh][j] = q.r0;
-          }
-      } else {
-        S.ld2[hh][0] = tb.src_ld * 2;
-        S.base[hh][0] = reinterpret_cast<uint64_t>(recv) + tb.src_off;
-        S.start[hh][0] = 0;
-      }
+      for (int j = 0; j < kMaxBands; ++j)
+        if (uint32_t(j) < np) {
+          const QPiece q = pieces[p0 + j];
+          S.ld2[j] = q.src_ld * 2;
+          S.base[j] = reinterpret_cast<uint64_t>(recv) + q.src_off - uint64_t(q.r0) * S.ld2[j];
+          S.start[j] = q.r0;
+        }
+    } else {
+      S.ld2[0] = (h ? b1.src_ld : b0.src_ld) * 2;
+      S.base[0] = reinterpret_cast<uint64_t>(recv) + (h ? b1.src_off : b0.src_off);
+      S.start[0] = 0;
     }
     if (full)
-      qblock_pair_run<true, true>(L, &S, h, on, b0, b1, ptrs);
+      qblock_pair_run<true, true>(L, S, h, on, b0, b1, ptrs);
     else
-      qblock_pair_run<false, true>(L, &S, h, on, b0, b1, ptrs);
+      qblock_pair_run<false, true>(L, S, h, on, b0, b1, ptrs);
   } else if (full) {
-    qblock_pair_run<true, false>(L, nullptr, h, on, b0, b1, ptrs);
+    qblock_pair_run<true, false>(L, PairBands{}, h, on, b0, b1, ptrs);
   } else {
-    qblock_pair_run<false, false>(L, nullptr, h, on, b0, b1, ptrs);
+    qblock_pair_run<false, false>(L, PairBands{}, h, on, b0, b1, ptrs);
   }
 }
 

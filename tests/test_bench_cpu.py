@@ -80,3 +80,42 @@ def test_fingerprint_follows_the_work_tables(monkeypatch):
     assert bench.work_fingerprint(W) == base
     assert bench.work_fingerprint("llama3_8b_fsdp8_to_tp1") != base
 
+
+
+def test_trace_summary_reports_launch_resources(tmp_path):
+    grids, _ = bench._launch_grids(WORKLOADS[W])
+    (unpack_x, _), _, _ = grids["unpack"]
+    name = "wb::wb_tasks_kernel(args)"
+    header = ["Kernel_Name", "Grid_Size_X", "Start_Timestamp", "End_Timestamp", "Workgroup_Size",
+              "Arch_VGPR_Count", "LDS_Block_Size"]
+    _write(tmp_path / "t.csv", header, [(name, unpack_x, 0, 5000, 64, 56, 4224)] * 2)
+    got = bench.summarize_trace(W, str(tmp_path / "t.csv"))
+    assert got["unpack"]["resources"] == {"Workgroup_Size": 64, "Arch_VGPR_Count": 56, "LDS_Block_Size": 4224}
+
+
+def test_metric_summary_averages_per_launch(tmp_path):
+    grids, _ = bench._launch_grids(WORKLOADS[W])
+    (_, unpack_total), _, _ = grids["unpack"]
+    (_, pack_total), _, _ = grids["pack"]
+    name = "wb::wb_tasks_kernel(args)"
+    rows = [(name, unpack_total, "MeanOccupancyPerCU", v) for v in (10.0, 12.0)]
+    rows += [(name, pack_total, "MeanOccupancyPerCU", 20.0), (name, pack_total, "OtherMetric", 99.0)]
+    _write(tmp_path / "m.csv", ["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"], rows)
+    got = bench.summarize_metric(W, "MeanOccupancyPerCU", str(tmp_path / "m.csv"))
+    assert got["kernels"]["unpack"] == {"dispatches": 2, "mean": 11.0}
+    assert got["kernels"]["pack"] == {"dispatches": 1, "mean": 20.0}
+
+
+def test_run_workload_keeps_the_workload_name():
+    """run_workload reports config.workload and looks up stored counters by
+    its `name` argument: nothing in its body may bind that name again (a loop
+    variable of that name once made the line report the workload as
+    "unpack")."""
+    import ast
+
+    tree = ast.parse(open(os.path.join(ROOT, "bench.py")).read())
+    fn = next(n for n in ast.walk(tree) if isinstance(n, ast.FunctionDef) and n.name == "run_workload")
+    assert [a.arg for a in fn.args.args][:2] == ["args", "name"]
+    rebound = [n.lineno for n in ast.walk(fn) if isinstance(n, ast.Name) and n.id == "name"
+               and isinstance(n.ctx, (ast.Store, ast.Del))]
+    assert rebound == []
