@@ -277,8 +277,8 @@ def summarize_counters(workload, fetch_csv, write_csv):
 
 # kernel-trace columns that describe a launch's resources (registers, LDS,
 # workgroup size), reported with its durations
-_RESOURCE_COLUMNS = ("Workgroup_Size", "Arch_VGPR_Count", "Accum_VGPR_Count", "SGPR_Count", "LDS_Block_Size",
-                     "Scratch_Size")
+_RESOURCE_COLUMNS = ("Workgroup_Size", "Workgroup_Size_X", "VGPR_Count", "Arch_VGPR_Count", "Accum_VGPR_Count",
+                     "SGPR_Count", "LDS_Block_Size", "Scratch_Size")
 
 
 def summarize_metric(workload, name, csv_path):
