@@ -314,10 +314,28 @@ __device__ __forceinline__ const char* base_of(uint16_t idx, const uint64_t* ptr
   return idx == 0 ? buf : idx == kAuxBuffer ? aux : reinterpret_cast<const char*>(ptrs[idx]);
 }
 
+// XCD-aware order of a launch's work. The hardware hands workgroup b to XCD
+// b mod 8 (round-robin over the 8 XCDs), and over a long launch the XCDs drift
+// apart, so neighbouring work units (the same DRAM pages; for fp8 blocks, the
+// same 128 rows of a wire payload) end up in flight at different times on
+// different XCDs. Renumbered so that in each run of 8 C workgroups XCD x takes
+// C consecutive units, neighbours are in flight together on one XCD, while the
+// eight XCDs still work within one run (so every HBM channel stays busy). A
+// bijection of [0, total); a tail shorter than 8 C keeps the plain order.
+constexpr uint64_t kXcds = 8;
+constexpr uint64_t kXcdRunCopy = 1024;  // copy/cast chunks (1-2 KiB of source each)
+constexpr uint64_t kXcdRunPairs = 512;  // fp8 block pairs (64 KiB of wire each)
+__device__ __forceinline__ uint64_t xcd_order(uint64_t b, uint64_t total, uint64_t C) {
+  const uint64_t run = kXcds * C, base = b / run * run;
+  if (base + run > total) return b;
+  const uint64_t k = b - base;
+  return base + (k % kXcds) * C + k / kXcds;
+}
+
 // Workgroups are laid out class by class: item i of class 0 takes workgroups
-// [i, i + 1) * 2^s0, chunk = b mod 2^s0; then class 1 the same with s1; then
-// one workgroup per class-2 item. A grid wider than kMaxGridX workgroups is
-// folded into rows of gridDim.x.
+// [i, i + 1) * 2^s0, chunk = b mod 2^s0 (b in XCD-aware order); then class 1
+// the same with s1; then one workgroup per class-2 item. A grid wider than
+// kMaxGridX workgroups is folded into rows of gridDim.x.
 __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restrict__ tasks,
                                                             const uint64_t* __restrict__ ptrs, const char* buf,
                                                             const char* aux, uint32_t ntasks, uint32_t n0,
@@ -327,6 +345,7 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
   uint64_t ti;
   uint32_t chunk = 0;
   if (b < w0) {
+    b = xcd_order(b, w0, kXcdRunCopy);
     ti = b >> s0;
     chunk = uint32_t(b) & ((1u << s0) - 1u);
   } else if ((b -= w0) < w1) {
@@ -767,7 +786,8 @@ __device__ __forceinline__ void qblock_one(const QBlock& b, const QPiece* __rest
 
 // The fp8 blocks of a launch range come in three classes, taken by one launch
 // (the slower classes overlap the bulk instead of trailing it in launches of
-// their own): workgroup w < nfull / 2 takes the full pair 2w, 2w + 1; the next
+// their own): workgroup w < nfull / 2 takes the full pair 2v, 2v + 1, v = w in
+// XCD-aware order; the next
 // ones the other pairable blocks two at a time (the second absent past npair);
 // the rest one block each.
 __global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock* __restrict__ blocks,
@@ -777,7 +797,7 @@ __global__ __launch_bounds__(kQBlockThreads) void wb_qblock_kernel(const QBlock*
                                                                    uint32_t npair) {
   const uint32_t g0 = nfull / 2, g1 = (npair - nfull + 1) / 2;
   if (blockIdx.x < g0) {
-    qblock_pair_full(blocks, 2 * blockIdx.x, ptrs, recv);
+    qblock_pair_full(blocks, 2 * uint32_t(xcd_order(blockIdx.x, g0, kXcdRunPairs)), ptrs, recv);
   } else if (blockIdx.x < g0 + g1) {
     qblock_pair(blocks + nfull, 2 * (blockIdx.x - g0), npair - nfull, pieces, ptrs, recv);
   } else {
