@@ -479,13 +479,15 @@ __device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64
   }
 }
 
-// VEC tile of one pass (carry passes): the same arithmetic as vec_tile, one
-// row at a time, with the next row's vector (and the two values left of it,
-// for the first lane) loaded before the current row is computed: two loads in
-// flight per lane for one row of state (measured 5-7 % faster per pass than
-// one row loaded and then computed; two rows ahead gave nothing more).
-template <int V, typename T, int S, class Out>
-__device__ __forceinline__ void vec_tile_pf(const Passes<1>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
+// VEC tile of the batched launches: the same arithmetic as vec_tile, one row
+// of state per lane, with the next row's vectors of every pass (and, for the
+// first lane, the two values left of them) loaded before the current row is
+// computed, so two rows of loads are in flight per lane. Measured against
+// rows loaded and then computed: carry passes (one pass, int) 5-7 % faster
+// per pass than one row and faster than two or four rows; held passes (three,
+// int64) 9.56 -> 8.03 ms for 48 GB; two rows ahead gave nothing more.
+template <int V, typename T, int P, int S, class Out>
+__device__ __forceinline__ void vec_tile_pf(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
                                             int64_t vb, const Out& out) {
   const int lane = threadIdx.x & 63;
   const int64_t nvec = cols / V;
@@ -495,42 +497,46 @@ __device__ __forceinline__ void vec_tile_pf(const Passes<1>& s, int64_t rows, in
   const int64_t i1 = i0 + S < rows ? i0 + S : rows;
   const int64_t rb = cols * (16 / V);
   const bool left = lane == 0 && j0 >= 2;
-  const char* col = s.p[0] + j0 * (16 / V);
-  const char* lcol = s.p[0] + (j0 - 2) * (16 / V);
   T h1[V], h2[V];
 #pragma unroll
   for (int k = 0; k < V; ++k) h1[k] = h2[k] = 0;
   const int64_t ist = i0 >= 2 ? i0 - 2 : 0;
-  uint4 q = {0u, 0u, 0u, 0u};
-  uint2 lq = {0u, 0u};
-  if (live && ist < i1) {
-    q = *reinterpret_cast<const uint4*>(col + ist * rb);
-    if (left) {
-      if (V == 8) lq.x = *reinterpret_cast<const uint32_t*>(lcol + ist * rb);
-      else lq = *reinterpret_cast<const uint2*>(lcol + ist * rb);
-    }
-  }
-  for (int64_t i = ist; i < i1; ++i) {
-    uint4 qn = {0u, 0u, 0u, 0u};
-    uint2 ln = {0u, 0u};
-    if (live && i + 1 < i1) {
-      qn = *reinterpret_cast<const uint4*>(col + (i + 1) * rb);
-      if (left) {
-        if (V == 8) ln.x = *reinterpret_cast<const uint32_t*>(lcol + (i + 1) * rb);
-        else ln = *reinterpret_cast<const uint2*>(lcol + (i + 1) * rb);
+  auto fetch = [&](int64_t i, uint4* qq, uint2* ll) {
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      qq[c] = uint4{0u, 0u, 0u, 0u};
+      ll[c] = uint2{0u, 0u};
+      if (c < s.n && live && i < i1) {
+        qq[c] = *reinterpret_cast<const uint4*>(s.p[c] + j0 * (16 / V) + i * rb);
+        if (left) {
+          if (V == 8) ll[c].x = *reinterpret_cast<const uint32_t*>(s.p[c] + (j0 - 2) * 2 + i * rb);
+          else ll[c] = *reinterpret_cast<const uint2*>(s.p[c] + (j0 - 2) * 4 + i * rb);
+        }
       }
     }
+  };
+  uint4 q[P];
+  uint2 lq[P];
+  fetch(ist, q, lq);
+  for (int64_t i = ist; i < i1; ++i) {
+    uint4 qn[P];
+    uint2 ln[P];
+    fetch(i + 1, qn, ln);
     T x[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) x[k] = 0;
-    add_vec<V, T>(q, 0, x);
-    T l1, l2;
-    if (V == 8) {
-      l2 = T(lq.x & 0xFFFFu);
-      l1 = T(lq.x >> 16);
-    } else {
-      l2 = T(int(__uint_as_float(lq.x)));
-      l1 = T(int(__uint_as_float(lq.y)));
+    T l1 = 0, l2 = 0;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      if (c >= s.n) break;
+      add_vec<V, T>(q[c], 16 * c, x);
+      if (V == 8) {
+        l2 += T(lq[c].x & 0xFFFFu) << (16 * c);
+        l1 += T(lq[c].x >> 16) << (16 * c);
+      } else {
+        l2 += T(int(__uint_as_float(lq[c].x))) << (16 * c);
+        l1 += T(int(__uint_as_float(lq[c].y))) << (16 * c);
+      }
     }
     T p1 = __shfl_up(x[V - 1], 1, 64), p2 = __shfl_up(x[V - 2], 1, 64);
     if (lane == 0) {
@@ -552,8 +558,11 @@ __device__ __forceinline__ void vec_tile_pf(const Passes<1>& s, int64_t rows, in
       any |= (live && i >= i0 && d[k] != 0) ? (1u << k) : 0u;
     }
     if (__ballot(any != 0) != 0) out.template put_row<V>(any, base + i * cols + j0, d, lane);
-    q = qn;
-    lq = ln;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+      q[c] = qn[c];
+      lq[c] = ln[c];
+    }
   }
 }
 
@@ -643,17 +652,14 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __r
 }
 
 // Batched launches: workgroup b takes tile b of the table, taller VEC tiles
-// and FLAT tiles of several sub-tiles (fewer, larger table rows). Held passes
-// recombine up to kMaxPasses passes in int64, two rows in flight per lane;
-// carry passes read one pass in int, one row at a time with the next row's
-// load in flight (vec_tile_pf: fewer registers and more wavefronts than two
-// or four rows loaded together, which measured slower).
-constexpr int kBatchUnroll = 2;
+// (vec_tile_pf) and FLAT tiles of several sub-tiles (fewer, larger table
+// rows). Held passes recombine up to kMaxPasses passes in int64; carry passes
+// read one pass in int.
 constexpr int kBatchVecStrip = 128;
 constexpr int kBatchFlatUnroll = 4;
 constexpr int kBatchFlatSub = 4;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
 
-template <typename T, int P, int U, class Out>
+template <typename T, int P, class Out>
 __device__ __forceinline__ void batch_tile(const DiffField& f, const DiffTile& t, const Out& out) {
   Passes<P> s;
 #pragma unroll
@@ -668,17 +674,10 @@ __device__ __forceinline__ void batch_tile(const DiffField& f, const DiffTile& t
         flat_tile<8, T, P, kBatchFlatUnroll>(s, f.cols, f.base, cb, out);
     }
   } else if (f.kind == DIFF_VEC) {
-    if constexpr (P == 1) {
-      if (f.dtype == WB_F32)
-        vec_tile_pf<4, T, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
-      else
-        vec_tile_pf<8, T, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
-    } else {
-      if (f.dtype == WB_F32)
-        vec_tile<4, T, P, U, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
-      else
-        vec_tile<8, T, P, U, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
-    }
+    if (f.dtype == WB_F32)
+      vec_tile_pf<4, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+    else
+      vec_tile_pf<8, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
   } else {
     elem_tile<T, P>(s, f.dtype, f.rows, f.cols, f.base, t.i0, t.j0, out);
   }
@@ -692,7 +691,7 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_batch_kernel(const DiffFiel
   __syncthreads();
   const ListOut<int64_t> out{&buf, sink};
   const DiffTile t = tiles[blockIdx.x];
-  batch_tile<int64_t, kMaxPasses, kBatchUnroll>(fields[t.field], t, out);
+  batch_tile<int64_t, kMaxPasses>(fields[t.field], t, out);
   out.flush();
 }
 
@@ -708,7 +707,7 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_carry_kernel(const DiffFiel
   __syncthreads();
   const DiffTile t = tiles[blockIdx.x];
   const CarryOut<kIn, kLast, true> out{&ebuf, &cbuf, &pending, sink, in, next, int64_t(t.field)};
-  batch_tile<int, 1, 1>(fields[t.field], t, out);
+  batch_tile<int, 1>(fields[t.field], t, out);
   out.flush();
 }
 
