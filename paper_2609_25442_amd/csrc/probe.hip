@@ -13,8 +13,8 @@
 //   ELEM  64 rows x 256 columns, one element per lane (any width, any
 //         element-aligned address);
 //   VEC   32 rows (128 batched) x 256 vectors of 16 bytes (8 bf16 or 4 fp32
-//         values), several rows in flight (cols a multiple of the vector,
-//         16-byte aligned field);
+//         values), the next row's loads in flight while a row is computed
+//         (cols a multiple of the vector, 16-byte aligned field);
 //   FLAT  one-row fields, 8 x 256 vectors per tile (16 x 256 batched).
 // Single-field launches walk one field's tiles with a strided grid; the
 // batched launch takes one tile per workgroup from a table that covers many
@@ -48,7 +48,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kStrip = 64;      // rows of an ELEM tile
 constexpr int kVecStrip = 32;   // rows of a VEC tile
-constexpr int kUnroll = 4;      // row vectors in flight per lane (VEC)
 constexpr int kFlatUnroll = 8;  // vectors in flight per lane (FLAT)
 
 __global__ __launch_bounds__(kThreads) void wb_make_ids_kernel(char* dst, int dtype, int64_t numel, int64_t first_id,
@@ -424,71 +423,17 @@ __device__ __forceinline__ void load_row_vec(const Passes<P>& s, int64_t rowoff,
 }
 
 // VEC tile: thread t takes the V columns of vector vb + t over rows [i0, i0 +
-// S), after two halo rows, U rows in flight. The two columns left of a
-// lane's vector are the previous lane's last two (the first lane of each
-// wavefront loads them). Same arithmetic as the ELEM tile.
-template <int V, typename T, int P, int U, int S, class Out>
-__device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
-                                         int64_t vb, const Out& out) {
-  const int lane = threadIdx.x & 63;
-  const int64_t nvec = cols / V;
-  const int64_t v = vb + threadIdx.x;
-  const bool live = v < nvec;
-  const int64_t j0 = v * V;
-  const int64_t i1 = i0 + S < rows ? i0 + S : rows;
-  T h1[V], h2[V];
-#pragma unroll
-  for (int k = 0; k < V; ++k) h1[k] = h2[k] = 0;
-  for (int64_t ib = (i0 >= 2 ? i0 - 2 : 0); ib < i1; ib += U) {
-    T x[U][V];
-    T l1[U], l2[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t i = ib + u;
-      l1[u] = l2[u] = 0;
-#pragma unroll
-      for (int k = 0; k < V; ++k) x[u][k] = 0;
-      if (live && i < i1) load_row_vec<V, T, P>(s, i * cols * (16 / V), j0, lane == 0 && j0 >= 2, x[u], l1[u], l2[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t i = ib + u;
-      if (i >= i1) break;  // uniform: every lane of the workgroup has the same rows
-      T p1 = __shfl_up(x[u][V - 1], 1, 64), p2 = __shfl_up(x[u][V - 2], 1, 64);
-      if (lane == 0) {
-        p1 = l1[u];
-        p2 = l2[u];
-      }
-      T h[V];
-      h[0] = x[u][0] - 2 * p1 + p2;
-      h[1] = x[u][1] - 2 * x[u][0] + p1;
-#pragma unroll
-      for (int k = 2; k < V; ++k) h[k] = x[u][k] - 2 * x[u][k - 1] + x[u][k - 2];
-      T d[V];
-      unsigned any = 0;
-#pragma unroll
-      for (int k = 0; k < V; ++k) {
-        d[k] = h[k] - 2 * h1[k] + h2[k];
-        h2[k] = h1[k];
-        h1[k] = h[k];
-        any |= (live && i >= i0 && d[k] != 0) ? (1u << k) : 0u;
-      }
-      if (__ballot(any != 0) == 0) continue;
-      out.template put_row<V>(any, base + i * cols + j0, d, lane);
-    }
-  }
-}
-
-// VEC tile of the batched launches: the same arithmetic as vec_tile, one row
-// of state per lane, with the next row's vectors of every pass (and, for the
-// first lane, the two values left of them) loaded before the current row is
-// computed, so two rows of loads are in flight per lane. Measured against
+// S), after two halo rows, one row of state per lane. The two columns left of
+// a lane's vector are the previous lane's last two (the first lane of each
+// wavefront loads them). The next row's vectors of every pass (and, for the
+// first lane, the two values left of them) are loaded before the current row
+// is computed, so two rows of loads are in flight per lane. Measured against
 // rows loaded and then computed: carry passes (one pass, int) 5-7 % faster
 // per pass than one row and faster than two or four rows; held passes (three,
-// int64) 9.56 -> 8.03 ms for 48 GB; two rows ahead gave nothing more.
+// int64) 9.56 -> 8.05 ms for 48 GB; two rows ahead gave nothing more.
 template <int V, typename T, int P, int S, class Out>
-__device__ __forceinline__ void vec_tile_pf(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
-                                            int64_t vb, const Out& out) {
+__device__ __forceinline__ void vec_tile(const Passes<P>& s, int64_t rows, int64_t cols, int64_t base, int64_t i0,
+                                         int64_t vb, const Out& out) {
   const int lane = threadIdx.x & 63;
   const int64_t nvec = cols / V;
   const int64_t v = vb + threadIdx.x;
@@ -632,7 +577,7 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_vec_kernel(const char* __re
   const int64_t nvec = cols / V;
   for (int64_t vb = int64_t(blockIdx.x) * kThreads; vb < nvec; vb += int64_t(gridDim.x) * kThreads)
     for (int64_t i0 = int64_t(blockIdx.y) * kVecStrip; i0 < rows; i0 += int64_t(gridDim.y) * kVecStrip)
-      vec_tile<V, int, 1, kUnroll, kVecStrip>(s, rows, cols, 0, i0, vb, out);
+      vec_tile<V, int, 1, kVecStrip>(s, rows, cols, 0, i0, vb, out);
   out.flush();
 }
 
@@ -652,7 +597,7 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __r
 }
 
 // Batched launches: workgroup b takes tile b of the table, taller VEC tiles
-// (vec_tile_pf) and FLAT tiles of several sub-tiles (fewer, larger table
+// (vec_tile) and FLAT tiles of several sub-tiles (fewer, larger table
 // rows). Held passes recombine up to kMaxPasses passes in int64; carry passes
 // read one pass in int.
 constexpr int kBatchVecStrip = 128;
@@ -675,9 +620,9 @@ __device__ __forceinline__ void batch_tile(const DiffField& f, const DiffTile& t
     }
   } else if (f.kind == DIFF_VEC) {
     if (f.dtype == WB_F32)
-      vec_tile_pf<4, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+      vec_tile<4, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
     else
-      vec_tile_pf<8, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
+      vec_tile<8, T, P, kBatchVecStrip>(s, f.rows, f.cols, f.base, t.i0, t.j0, out);
   } else {
     elem_tile<T, P>(s, f.dtype, f.rows, f.cols, f.base, t.i0, t.j0, out);
   }
