@@ -146,7 +146,7 @@ def _check_carries(A, b, K):
     return kept, carries
 
 
-@pytest.mark.parametrize("b", [4, 16])
+@pytest.mark.parametrize("b", [4, 8, 16])
 @pytest.mark.parametrize("seed", range(8))
 def test_carries_closed_form_on_random_fields(b, seed):
     rng = np.random.default_rng(400 + seed)
