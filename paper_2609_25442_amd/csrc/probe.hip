@@ -29,7 +29,9 @@
 // 2^16 identifiers. Pass k's stencil adds to each non-zero D the carry that
 // pass k - 1 left at that position, emits S mod 2^16 when non-zero and
 // inserts floor(S / 2^16) when non-zero into the carry table of pass k + 1;
-// the last pass emits S whole. A second kernel handles the carries at
+// the last pass emits S whole. The stencil's lookups wait in LDS and are made
+// together when its tile ends, and its carries are staged per tile and
+// inserted by a launch of their own; another launch handles the carries at
 // positions where D is zero. The sum over passes of 2^(16 k) times the
 // emitted values is diff2 of the identifier field, and only its positions
 // (next to slice-copy corners) are emitted: the wrap-arounds stay in the
@@ -79,8 +81,9 @@ struct Sink {
 };
 
 // The chunk fields a tile reads: element value sum over k < n of p[k] << (16 k).
-// Single-field launches read one pass as int; batched launches recombine up
-// to kMaxPasses passes as int64 (identifiers below 2^48, |diff2| below 2^52).
+// Single-field and carry launches read one pass as int; the held-pass launch
+// recombines up to kMaxPasses passes as int64 (identifiers below 2^48, |diff2|
+// below 2^52).
 template <int P>
 struct Passes {
   const char* p[P];
