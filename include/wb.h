@@ -194,6 +194,9 @@ typedef enum wb_role { WB_SENDER = 0, WB_RECEIVER = 1 } wb_role;
  *             row-major copy of its rectangle in the sender dtype starting at a
  *             multiple of 256 bytes; buffers hold regions by ascending peer,
  *             each starting at a multiple of 4096 bytes.
+ * A receiver's fp8 block tables are built by up to WB_PLAN_THREADS host
+ * threads (environment, 1..64; default: the CPUs the process may run on, at
+ * most 16); the plan does not depend on the number.
  * Errors: WB_EINVAL (null, rank out of range, catalogs differ, a rollout
  * element held by no trainer, rollout tensors not exactly covered),
  * WB_EUNSUPPORTED (overlapping non-identical trainer rectangles, replicas with
@@ -256,6 +259,11 @@ int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* w
 int wb_plan_kernel_traffic(const wb_plan_t* plan, int32_t launch, int64_t* read_bytes, int64_t* write_bytes);
 /* Kernel work items of this rank: copy/cast tasks, fp8 blocks, fp8 pieces. */
 int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, int64_t* pieces);
+/* 64-bit FNV-1a digest of the kernel work tables wb_plan_upload would copy
+ * (work items, fp8 blocks and pieces, their per-round ranges and class splits)
+ * and of the per-launch byte counts: equal digests mean the same kernel work,
+ * whatever produced the plan (process, build, or number of planning threads). */
+int wb_plan_work_digest(const wb_plan_t* plan, uint64_t* out);
 /* Grid (workgroups in x and y) and workgroup size (threads) of one launch of
  * one round: launch 0 the copy/cast kernel of wb_pack_round / wb_unpack_round,
  * 4 its transpose-tile kernel (one workgroup per 256 x 256 tile), 1 the fp8

@@ -13,7 +13,7 @@ import atexit
 import ctypes
 import os
 import weakref
-from ctypes import POINTER, byref, c_char_p, c_int32, c_int64, c_size_t, c_uint32, c_void_p
+from ctypes import POINTER, byref, c_char_p, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # WB_LIB selects another build of the same library (e.g. a tuning variant)
@@ -110,6 +110,7 @@ def _load():
         "wb_plan_workspace_bytes": [P, POINTER(c_int64)],
         "wb_plan_traffic_bytes": [P, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_work_counts": [P, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)],
+        "wb_plan_work_digest": [P, POINTER(c_uint64)],
         "wb_plan_launch_grid": [P, c_int32, c_int32, POINTER(c_uint32), POINTER(c_uint32), POINTER(c_uint32)],
         "wb_plan_kernel_traffic": [P, c_int32, POINTER(c_int64), POINTER(c_int64)],
         "wb_plan_dump": [P, ctypes.c_char_p, c_size_t, POINTER(c_size_t)],
@@ -493,6 +494,12 @@ class Plan:
         a, b, c = c_int64(), c_int64(), c_int64()
         _check(lib.wb_plan_work_counts(self._h, byref(a), byref(b), byref(c)))
         return a.value, b.value, c.value
+
+    def work_digest(self) -> int:
+        """64-bit digest of the kernel work tables (equal digests, same work)."""
+        v = c_uint64()
+        _check(lib.wb_plan_work_digest(self._h, byref(v)))
+        return v.value
 
     def launch_grid(self, launch=0, round=0):
         """(workgroups in x, in y, threads per workgroup) of one launch of one

@@ -530,6 +530,36 @@ int wb_plan_work_counts(const wb_plan_t* P, int64_t* tasks, int64_t* blocks, int
   return WB_OK;
 }
 
+int wb_plan_work_digest(const wb_plan_t* P, uint64_t* out) {
+  if (!P || !out) return set_error(WB_EINVAL, "null argument");
+  uint64_t h = 1469598103934665603ull;
+  auto add = [&h](const void* p, size_t n) {
+    const unsigned char* c = static_cast<const unsigned char*>(p);
+    for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 1099511628211ull;
+  };
+  auto vec = [&](const auto& v) {
+    const uint64_t n = v.size();
+    add(&n, sizeof n);
+    if (n) add(v.data(), n * sizeof(v[0]));
+  };
+  vec(P->tasks);
+  vec(P->qblocks);
+  vec(P->qpieces);
+  vec(P->round_tasks);
+  vec(P->round_qblocks);
+  vec(P->round_qfull);
+  vec(P->round_qsingle);
+  vec(P->round_qpieces);
+  for (int st = 0; st < 2; ++st) vec(P->round_fwd[st]);
+  vec(P->round_split);
+  for (int st = 0; st < 2; ++st) vec(P->fwd_split[st]);
+  const int64_t v[10] = {P->n_locals,         P->read_bytes,       P->write_bytes,  P->q_read_bytes, P->q_write_bytes,
+                         P->tile_read_bytes,  P->tile_write_bytes, P->fwd_bytes[0], P->fwd_bytes[1], P->role};
+  add(v, sizeof v);
+  *out = h;
+  return WB_OK;
+}
+
 int wb_plan_launch_grid(const wb_plan_t* P, int32_t launch, int32_t round, uint32_t* gx, uint32_t* gy,
                         uint32_t* threads) {
   if (!P || !gx || !gy || !threads) return set_error(WB_EINVAL, "null argument");

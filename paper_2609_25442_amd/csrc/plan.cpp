@@ -8,12 +8,17 @@
 // slices go to the replica furthest below its even share (Sec. 3.2: no
 // redundant transfer, no single-source bottleneck). This file follows the
 // canonical rules stated in wb.h so that every rank derives the same plan.
+#include <sched.h>
+
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <cstdlib>
+#include <exception>
 #include <map>
 #include <numeric>
 #include <sstream>
+#include <thread>
 
 #include "wb_internal.hpp"
 
@@ -257,6 +262,260 @@ int wire_dtype(const wb_layout_t& trainer, const std::vector<Segment>& segs, con
   return S.locals[S.pls[o.src_pl].u].dtype;
 }
 
+// One wire segment's image in a quantised local: matrix e of the stack, its
+// first row and column there.
+struct QSpan {
+  const Segment* g;
+  int64_t e, row0, col0;
+};
+
+// Host threads for planning: WB_PLAN_THREADS if set (1..64), else the CPUs
+// this process may run on, at most 16. The plan does not depend on it.
+int plan_threads() {
+  if (const char* e = std::getenv("WB_PLAN_THREADS")) {
+    const long v = std::strtol(e, nullptr, 10);
+    if (v >= 1 && v <= 64) return static_cast<int>(v);
+  }
+  cpu_set_t set;
+  const int n = sched_getaffinity(0, sizeof set, &set) == 0 ? CPU_COUNT(&set) : 1;
+  return std::max(1, std::min(n, 16));
+}
+
+// fn(i, w) for every i in [0, n) on up to `threads` workers (w is the
+// worker's number, below `threads`), which take indices in increasing order
+// from a shared counter. After an exception no further index is started;
+// every lower index was taken before it and runs to its end, so rethrowing
+// the exception of the lowest index reports what one thread would have.
+template <class F>
+void parallel_for(size_t n, int threads, F&& fn) {
+  const int nw = static_cast<int>(std::min<size_t>(n, std::max(threads, 1)));
+  if (nw <= 1) {
+    for (size_t i = 0; i < n; ++i) fn(i, 0);
+    return;
+  }
+  std::atomic<size_t> next{0};
+  std::atomic<bool> stop{false};
+  std::vector<std::exception_ptr> err(n);
+  auto work = [&](int w) {
+    for (size_t i; !stop.load() && (i = next.fetch_add(1)) < n;) {
+      try {
+        fn(i, w);
+      } catch (...) {
+        err[i] = std::current_exception();
+        stop = true;
+      }
+    }
+  };
+  std::vector<std::thread> pool;
+  for (int w = 1; w < nw; ++w) pool.emplace_back(work, w);
+  work(0);
+  for (auto& th : pool) th.join();
+  for (auto& e : err)
+    if (e) std::rethrow_exception(e);
+}
+
+// What the fp8 tables need of one quantised local, built by qlocal_blocks.
+struct QLocalScratch {
+  std::vector<QBlock> blocks;    // the local's blocks in id order (piece0 relative to the local)
+  std::vector<int> round;        // each block's round
+  std::vector<QPiece> pieces;    // the local's pieces, grouped by block in id order
+  std::vector<uint32_t> count;   // pieces of block i: count[i] .. count[i + 1]
+  std::vector<int64_t> area;
+};
+
+// Block class within a round's launch range: full pairs, other pairable
+// blocks, the rest.
+int qblock_class(const QBlock& b) { return qblock_full_single(b) ? 0 : qblock_pairable(b) ? 1 : 2; }
+
+// The blocks and pieces of quantised local u of rank R from the wire spans
+// that land in it (spans in plan order), numbered within the local: block
+// (e, bi, bj) is block (e nbr + bi) nbc + bj, also its scale's index, and
+// piece0 counts only this local's pieces.
+void qlocal_blocks(const wb_layout_t& trainer, const Rank& R, const wb_plan_t& P, int u, const QSpan* spans,
+                   size_t nspans, QLocalScratch& S) {
+  const Local& l = R.locals[u];
+  const int64_t B = l.block, nbr = (l.rows + B - 1) / B, nbc = (l.cols + B - 1) / B, nb = l.batch * nbr * nbc;
+  S.blocks.assign(nb, QBlock{});
+  S.round.assign(nb, -1);
+  S.count.assign(nb + 1, 0);
+  S.area.assign(nb, 0);
+  auto for_pieces = [&](const QSpan& sp, auto&& fn) {
+    const Segment& g = *sp.g;
+    const int sdt = wire_dtype(trainer, P.segs, g), ss = dtype_bytes(sdt);
+    const int64_t Rr = g.x.rows(), C = g.x.cols();
+    for (int64_t bi = sp.row0 / B; bi <= (sp.row0 + Rr - 1) / B; ++bi)
+      for (int64_t bj = sp.col0 / B; bj <= (sp.col0 + C - 1) / B; ++bj) {
+        const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
+        const int64_t b0 = std::max(sp.col0, bj * B), b1 = std::min(sp.col0 + C, (bj + 1) * B);
+        const int64_t rows = std::min(B, l.rows - bi * B), cols = std::min(B, l.cols - bj * B);
+        QPiece pc{};
+        pc.src_off = g.recv_off + uint64_t(((a0 - sp.row0) * C + (b0 - sp.col0)) * ss);
+        pc.src_ld = static_cast<uint32_t>(C);
+        pc.r0 = static_cast<uint8_t>(a0 - bi * B);
+        pc.r1m1 = static_cast<uint8_t>(a1 - bi * B - 1);
+        pc.c0 = static_cast<uint8_t>(b0 - bj * B);
+        pc.c1m1 = static_cast<uint8_t>(b1 - bj * B - 1);
+        pc.sdt = static_cast<uint8_t>(sdt);
+        const bool single = sdt == WB_BF16 && a0 == bi * B && b0 == bj * B && a1 - a0 == rows && b1 - b0 == cols &&
+                            cols % 8 == 0 && pc.src_off % 16 == 0 && (uint64_t(C) * 2) % 16 == 0;
+        fn((sp.e * nbr + bi) * nbc + bj, pc, single, (a1 - a0) * (b1 - b0));
+      }
+  };
+  for (size_t i = 0; i < nspans; ++i)
+    for_pieces(spans[i], [&](int64_t id, const QPiece& pc, bool single, int64_t a) {
+      S.area[id] += a;
+      if (S.round[id] >= 0 && S.round[id] != spans[i].g->round) fail(WB_EINVAL, "internal: fp8 block spans rounds");
+      S.round[id] = spans[i].g->round;
+      if (single) {
+        QBlock& b = S.blocks[id];
+        b.flags |= QB_SINGLE;
+        b.src_off = pc.src_off;
+        b.src_ld = pc.src_ld;
+      } else {
+        ++S.count[id + 1];
+      }
+    });
+  for (int64_t i = 0; i < nb; ++i) S.count[i + 1] += S.count[i];
+  S.pieces.resize(S.count[nb]);
+  {
+    std::vector<uint32_t> fill(S.count.begin(), S.count.end() - 1);
+    for (size_t i = 0; i < nspans; ++i)
+      for_pieces(spans[i], [&](int64_t id, const QPiece& pc, bool single, int64_t) {
+        if (!single) S.pieces[fill[id]++] = pc;
+      });
+  }
+  for (int64_t e = 0; e < l.batch; ++e)
+    for (int64_t bi = 0; bi < nbr; ++bi)
+      for (int64_t bj = 0; bj < nbc; ++bj) {
+        const int64_t id = (e * nbr + bi) * nbc + bj;
+        const int64_t rows = std::min(B, l.rows - bi * B), cols = std::min(B, l.cols - bj * B);
+        if (S.area[id] != rows * cols) fail(WB_EINVAL, "fp8 block of " + l.name + " is not exactly covered");
+        const uint32_t p0 = S.count[id], np = S.count[id + 1] - p0;
+        if (np > 65535) fail(WB_EUNSUPPORTED, "too many pieces in one fp8 block");
+        QBlock& b = S.blocks[id];
+        b.dst_off = uint64_t((e * l.rows + bi * B) * l.cols + bj * B);
+        b.piece0 = p0;
+        b.npieces = static_cast<uint16_t>(np);
+        b.dst_ld = static_cast<uint32_t>(l.cols);
+        b.scale_off = static_cast<uint32_t>(id);
+        b.dst_idx = static_cast<uint16_t>(1 + u);
+        b.scale_idx = static_cast<uint16_t>(1 + l.scale);
+        b.rows_m1 = static_cast<uint8_t>(rows - 1);
+        b.cols_m1 = static_cast<uint8_t>(cols - 1);
+        if (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) b.flags |= QB_VEC_STORE;
+        bool bf16 = true;
+        for (uint32_t i = p0; i < p0 + np; ++i) bf16 = bf16 && S.pieces[i].sdt == WB_BF16;
+        if (bf16) b.flags |= QB_BF16_SOURCE;
+        // row bands: every piece spans the block's width, 16-byte aligned
+        // rows; sorted by first row they tile the block from row 0
+        if (bf16 && np >= 2 && np <= uint32_t(kMaxBands) && cols % 8 == 0) {
+          QPiece* pc = S.pieces.data() + p0;
+          std::sort(pc, pc + np, [](const QPiece& a, const QPiece& c) { return a.r0 < c.r0; });
+          bool bands = true;
+          for (uint32_t i = 0; i < np; ++i)
+            bands = bands && pc[i].c0 == 0 && pc[i].c1m1 == cols - 1 && pc[i].src_off % 16 == 0 &&
+                    (uint64_t(pc[i].src_ld) * 2) % 16 == 0 && pc[i].r0 == (i ? pc[i - 1].r1m1 + 1 : 0);
+          if (bands && pc[np - 1].r1m1 == rows - 1) b.flags |= QB_BANDS;
+        }
+      }
+}
+
+// The fp8 block and piece tables of a rollout rank. Block ids run over the
+// quantised locals, then batch, block row, block column; pieces are grouped
+// by block in id order (canonical segment order within a block, row bands
+// sorted by first row). A block filled whole by one aligned bf16 wire piece
+// (QB_SINGLE) keeps that piece's address in its own descriptor, which is all
+// the pair path reads, and takes no piece. Every piece adds to its block's
+// covered area, so a block with a whole piece and any other one fails the
+// exact-cover check. The blocks are then grouped by round and, within a
+// round, ordered full pairs, other pairable blocks, the rest, each class in
+// id order (consecutive pairable blocks are mostly horizontal neighbours).
+// Locals are independent: each is built twice on the planning threads, once
+// to count its pieces and its blocks per (round, class), once to write them
+// where those counts place them.
+void build_qblocks(const wb_layout_t& trainer, const Rank& R, wb_plan_t& P, const std::vector<QSpan>& qspans,
+                   int64_t nblocks) {
+  const int nrounds = static_cast<int>(P.rounds.size());
+  const size_t nl = R.locals.size();
+  // the spans of each local, in plan order
+  std::vector<size_t> span0(nl + 1, 0);
+  for (const QSpan& sp : qspans) ++span0[R.pls[sp.g->dst_pl].u + 1];
+  for (size_t u = 0; u < nl; ++u) span0[u + 1] += span0[u];
+  std::vector<QSpan> spans(qspans.size());
+  {
+    std::vector<size_t> at(span0.begin(), span0.end() - 1);
+    for (const QSpan& sp : qspans) spans[at[R.pls[sp.g->dst_pl].u]++] = sp;
+  }
+  std::vector<int> ql;
+  for (size_t u = 0; u < nl; ++u)
+    if (R.locals[u].block > 0) ql.push_back(static_cast<int>(u));
+  const size_t nq = ql.size();
+  const int threads = nblocks >= (int64_t(1) << 15) ? plan_threads() : 1;
+  // pass 1: per local, its pieces, its blocks per (round, class) and the
+  // local piece range each round reads
+  std::vector<uint32_t> npieces(nq);
+  std::vector<uint32_t> cls(nq * nrounds * 3);
+  std::vector<uint32_t> plo(nq * nrounds, UINT32_MAX), phi(nq * nrounds, 0);
+  std::vector<QLocalScratch> scratch(threads);
+  parallel_for(nq, threads, [&](size_t i, int w) {
+    QLocalScratch& S = scratch[w];
+    const int u = ql[i];
+    qlocal_blocks(trainer, R, P, u, spans.data() + span0[u], span0[u + 1] - span0[u], S);
+    npieces[i] = static_cast<uint32_t>(S.pieces.size());
+    for (size_t b = 0; b < S.blocks.size(); ++b) {
+      const int k = S.round[b];
+      ++cls[(i * nrounds + k) * 3 + qblock_class(S.blocks[b])];
+      if (S.blocks[b].npieces) {
+        plo[i * nrounds + k] = std::min(plo[i * nrounds + k], S.blocks[b].piece0);
+        phi[i * nrounds + k] = std::max(phi[i * nrounds + k], S.blocks[b].piece0 + S.blocks[b].npieces);
+      }
+    }
+  });
+  // global piece base of every local, block positions of every (local, round, class)
+  std::vector<uint64_t> pbase(nq + 1, 0);
+  for (size_t i = 0; i < nq; ++i) pbase[i + 1] = pbase[i] + npieces[i];
+  if (pbase[nq] > UINT32_MAX) fail(WB_EUNSUPPORTED, "too many fp8 pieces");
+  std::vector<uint32_t> pos(nq * nrounds * 3);
+  uint32_t at = 0;
+  for (int k = 0; k < nrounds; ++k) {
+    P.round_qblocks[k] = at;
+    uint32_t n[3] = {0, 0, 0};
+    for (int c = 0; c < 3; ++c)
+      for (size_t i = 0; i < nq; ++i) {
+        pos[(i * nrounds + k) * 3 + c] = at;
+        at += cls[(i * nrounds + k) * 3 + c];
+        n[c] += cls[(i * nrounds + k) * 3 + c];
+      }
+    P.round_qsingle[k] = n[0] + n[1];
+    P.round_qfull[k] = n[0] & ~1u;  // an odd one out stays with the other pairable blocks
+    uint32_t lo = UINT32_MAX, hi = 0;
+    for (size_t i = 0; i < nq; ++i)
+      if (phi[i * nrounds + k]) {
+        lo = std::min<uint32_t>(lo, static_cast<uint32_t>(pbase[i] + plo[i * nrounds + k]));
+        hi = std::max<uint32_t>(hi, static_cast<uint32_t>(pbase[i] + phi[i * nrounds + k]));
+      }
+    P.round_qpieces[2 * k] = hi ? lo : 0;
+    P.round_qpieces[2 * k + 1] = hi;
+  }
+  P.round_qblocks[nrounds] = at;
+  if (at != uint64_t(nblocks)) fail(WB_EINVAL, "internal: fp8 block count");
+  // pass 2: the same blocks again, written in place
+  P.qblocks.resize(nblocks);
+  P.qpieces.resize(pbase[nq]);
+  parallel_for(nq, threads, [&](size_t i, int w) {
+    QLocalScratch& S = scratch[w];
+    const int u = ql[i];
+    qlocal_blocks(trainer, R, P, u, spans.data() + span0[u], span0[u + 1] - span0[u], S);
+    std::copy(S.pieces.begin(), S.pieces.end(), P.qpieces.begin() + pbase[i]);
+    uint32_t* p = pos.data() + i * nrounds * 3;
+    for (size_t b = 0; b < S.blocks.size(); ++b) {
+      QBlock q = S.blocks[b];
+      q.piece0 += static_cast<uint32_t>(pbase[i]);
+      P.qblocks[p[S.round[b] * 3 + qblock_class(q)]++] = q;
+    }
+  });
+}
+
 void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_plan_t& P) {
   TaskSink sink{P.tasks, env_task_bytes()};
   const int nrounds = static_cast<int>(P.rounds.size());
@@ -295,22 +554,16 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
   }
   const Rank& R = rollout.ranks[P.rank];
   P.n_locals = static_cast<int>(R.locals.size());
-  // fp8 block bookkeeping: first block id of every quantised local
-  std::vector<int64_t> block_base(R.locals.size(), -1);
+  // fp8 blocks of all quantised locals
   int64_t nblocks = 0;
   for (size_t u = 0; u < R.locals.size(); ++u) {
     const Local& l = R.locals[u];
     if (l.block <= 0) continue;
-    block_base[u] = nblocks;
     nblocks += l.batch * ((l.rows + l.block - 1) / l.block) * ((l.cols + l.block - 1) / l.block);
     P.write_bytes += R.locals[l.scale].numel() * 4;
     P.q_write_bytes += R.locals[l.scale].numel() * 4;
   }
-  struct Span {
-    const Segment* g;
-    int64_t e, row0, col0;
-  };
-  std::vector<Span> qspans;
+  std::vector<QSpan> qspans;
   for (int k = 0; k < nrounds; ++k) {
   for (const Segment* gp : by_round[k]) {
     const Segment& g = *gp;
@@ -363,142 +616,7 @@ void build_rank_view(const wb_layout_t& trainer, const wb_layout_t& rollout, wb_
       P.round_fwd[st][k + 1] = static_cast<uint32_t>(P.tasks.size());
     }
   }
-  if (nblocks == 0) return;
-  // Blocks are built in id order (locals, then batch, block row, block column).
-  // A block filled whole by one aligned bf16 wire piece (QB_SINGLE) keeps that
-  // piece's address in its own descriptor, which is all the pair path reads,
-  // and takes no piece-table entry; the other blocks list their pieces (count
-  // per block, prefix, fill; canonical segment order within a block). Every
-  // piece adds to its block's covered area, so a block with a whole piece and
-  // any other one fails the exact-cover check.
-  P.qblocks.assign(nblocks, QBlock{});
-  std::vector<uint32_t> count(nblocks + 1, 0);
-  std::vector<int64_t> area(nblocks, 0);
-  std::vector<int> block_round(nblocks, -1);
-  auto for_pieces = [&](const Span& sp, auto&& fn) {
-    const Segment& g = *sp.g;
-    const Placement& q = R.pls[g.dst_pl];
-    const Local& dl = R.locals[q.u];
-    const int sdt = wire_dtype(trainer, P.segs, g), ss = dtype_bytes(sdt);
-    const int64_t B = dl.block, nbr = (dl.rows + B - 1) / B, nbc = (dl.cols + B - 1) / B;
-    const int64_t Rr = g.x.rows(), C = g.x.cols();
-    for (int64_t bi = sp.row0 / B; bi <= (sp.row0 + Rr - 1) / B; ++bi)
-      for (int64_t bj = sp.col0 / B; bj <= (sp.col0 + C - 1) / B; ++bj) {
-        const int64_t a0 = std::max(sp.row0, bi * B), a1 = std::min(sp.row0 + Rr, (bi + 1) * B);
-        const int64_t b0 = std::max(sp.col0, bj * B), b1 = std::min(sp.col0 + C, (bj + 1) * B);
-        const int64_t rows = std::min(B, dl.rows - bi * B), cols = std::min(B, dl.cols - bj * B);
-        QPiece pc{};
-        pc.src_off = g.recv_off + uint64_t(((a0 - sp.row0) * C + (b0 - sp.col0)) * ss);
-        pc.src_ld = static_cast<uint32_t>(C);
-        pc.r0 = static_cast<uint8_t>(a0 - bi * B);
-        pc.r1m1 = static_cast<uint8_t>(a1 - bi * B - 1);
-        pc.c0 = static_cast<uint8_t>(b0 - bj * B);
-        pc.c1m1 = static_cast<uint8_t>(b1 - bj * B - 1);
-        pc.sdt = static_cast<uint8_t>(sdt);
-        const bool single = sdt == WB_BF16 && a0 == bi * B && b0 == bj * B && a1 - a0 == rows && b1 - b0 == cols &&
-                            cols % 8 == 0 && pc.src_off % 16 == 0 && (uint64_t(C) * 2) % 16 == 0;
-        fn(block_base[q.u] + (sp.e * nbr + bi) * nbc + bj, pc, single, (a1 - a0) * (b1 - b0));
-      }
-  };
-  for (const Span& sp : qspans)
-    for_pieces(sp, [&](int64_t id, const QPiece& pc, bool single, int64_t a) {
-      area[id] += a;
-      if (block_round[id] >= 0 && block_round[id] != sp.g->round) fail(WB_EINVAL, "internal: fp8 block spans rounds");
-      block_round[id] = sp.g->round;
-      if (single) {
-        QBlock& b = P.qblocks[id];
-        b.flags |= QB_SINGLE;
-        b.src_off = pc.src_off;
-        b.src_ld = pc.src_ld;
-      } else {
-        ++count[id + 1];
-      }
-    });
-  for (int64_t i = 0; i < nblocks; ++i) count[i + 1] += count[i];
-  P.qpieces.resize(count[nblocks]);
-  {
-    std::vector<uint32_t> fill(count.begin(), count.end() - 1);
-    for (const Span& sp : qspans)
-      for_pieces(sp, [&](int64_t id, const QPiece& pc, bool single, int64_t) {
-        if (!single) P.qpieces[fill[id]++] = pc;
-      });
-  }
-  for (size_t u = 0; u < R.locals.size(); ++u) {
-    const Local& l = R.locals[u];
-    if (l.block <= 0) continue;
-    const int64_t B = l.block, nbr = (l.rows + B - 1) / B, nbc = (l.cols + B - 1) / B;
-    for (int64_t e = 0; e < l.batch; ++e)
-      for (int64_t bi = 0; bi < nbr; ++bi)
-        for (int64_t bj = 0; bj < nbc; ++bj) {
-          const int64_t id = block_base[u] + (e * nbr + bi) * nbc + bj;
-          const int64_t rows = std::min(B, l.rows - bi * B), cols = std::min(B, l.cols - bj * B);
-          if (area[id] != rows * cols) fail(WB_EINVAL, "fp8 block of " + l.name + " is not exactly covered");
-          if (count[id + 1] - count[id] > 65535) fail(WB_EUNSUPPORTED, "too many pieces in one fp8 block");
-          QBlock& b = P.qblocks[id];
-          b.dst_off = uint64_t((e * l.rows + bi * B) * l.cols + bj * B);
-          b.piece0 = count[id];
-          b.npieces = static_cast<uint16_t>(count[id + 1] - count[id]);
-          b.dst_ld = static_cast<uint32_t>(l.cols);
-          b.scale_off = static_cast<uint32_t>((e * nbr + bi) * nbc + bj);
-          b.dst_idx = static_cast<uint16_t>(1 + u);
-          b.scale_idx = static_cast<uint16_t>(1 + l.scale);
-          b.rows_m1 = static_cast<uint8_t>(rows - 1);
-          b.cols_m1 = static_cast<uint8_t>(cols - 1);
-          if (b.dst_off % 8 == 0 && l.cols % 8 == 0 && cols % 8 == 0) b.flags |= QB_VEC_STORE;
-          bool bf16 = true;
-          for (uint32_t i = count[id]; i < count[id + 1]; ++i) bf16 = bf16 && P.qpieces[i].sdt == WB_BF16;
-          if (bf16) b.flags |= QB_BF16_SOURCE;
-          // row bands: every piece spans the block's width, 16-byte aligned
-          // rows; sorted by first row they tile the block from row 0
-          const uint32_t np = count[id + 1] - count[id];
-          if (bf16 && np >= 2 && np <= uint32_t(kMaxBands) && cols % 8 == 0) {
-            QPiece* pc = P.qpieces.data() + count[id];
-            std::sort(pc, pc + np, [](const QPiece& a, const QPiece& c) { return a.r0 < c.r0; });
-            bool bands = true;
-            for (uint32_t i = 0; i < np; ++i)
-              bands = bands && pc[i].c0 == 0 && pc[i].c1m1 == cols - 1 && pc[i].src_off % 16 == 0 &&
-                      (uint64_t(pc[i].src_ld) * 2) % 16 == 0 && pc[i].r0 == (i ? pc[i - 1].r1m1 + 1 : 0);
-            if (bands && pc[np - 1].r1m1 == rows - 1) b.flags |= QB_BANDS;
-          }
-        }
-  }
-  // group the blocks by round, canonical block order within a round (a
-  // counting placement; one round needs none)
-  std::vector<uint32_t> start(nrounds + 1, 0);
-  for (int64_t i = 0; i < nblocks; ++i) ++start[block_round[i] + 1];
-  for (int k = 0; k < nrounds; ++k) start[k + 1] += start[k];
-  P.round_qblocks.assign(start.begin(), start.end());
-  if (nrounds > 1) {
-    std::vector<uint32_t> at(nblocks);
-    for (int64_t i = 0; i < nblocks; ++i) at[start[block_round[i]]++] = static_cast<uint32_t>(i);
-    std::vector<QBlock> sorted;
-    sorted.reserve(nblocks);
-    for (int64_t i = 0; i < nblocks; ++i) sorted.push_back(P.qblocks[at[i]]);
-    P.qblocks.swap(sorted);
-  }
-  // within a round, the single-piece blocks first (block order within each
-  // class, so consecutive single-piece blocks are mostly horizontal neighbours)
-  for (int k = 0; k < nrounds; ++k) {
-    const auto first = P.qblocks.begin() + P.round_qblocks[k], last = P.qblocks.begin() + P.round_qblocks[k + 1];
-    const auto mid = std::stable_partition(first, last, qblock_pairable);
-    P.round_qsingle[k] = static_cast<uint32_t>(mid - first);
-    // full pairs first among the pairable blocks (an odd one out stays with
-    // the other pairable blocks)
-    const auto fmid = std::stable_partition(first, mid, qblock_full_single);
-    P.round_qfull[k] = static_cast<uint32_t>(fmid - first) & ~1u;
-  }
-  // the range of the piece table each round's blocks read
-  for (int k = 0; k < nrounds; ++k) {
-    uint32_t lo = UINT32_MAX, hi = 0;
-    for (uint32_t i = P.round_qblocks[k]; i < P.round_qblocks[k + 1]; ++i) {
-      const QBlock& b = P.qblocks[i];
-      if (b.npieces == 0) continue;
-      lo = std::min(lo, b.piece0);
-      hi = std::max(hi, b.piece0 + b.npieces);
-    }
-    P.round_qpieces[2 * k] = hi ? lo : 0;
-    P.round_qpieces[2 * k + 1] = hi;
-  }
+  if (nblocks > 0) build_qblocks(trainer, R, P, qspans, nblocks);
 }
 
 // Every byte a work item touches lies inside its buffer, and vector work items
@@ -610,7 +728,7 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   if (P.round_qpieces.size() != 2 * nr || P.round_qpieces[2 * k] > P.round_qpieces[2 * k + 1] ||
       P.round_qpieces[2 * k + 1] > P.qpieces.size())
     fail(WB_EINVAL, "internal: fp8 piece range of a round");
-  for (uint32_t bi = P.round_qblocks[k]; bi < P.round_qblocks[k + 1]; ++bi) {
+  auto check_block = [&](uint32_t bi) {
     const QBlock& b = P.qblocks[bi];
     if (qblock_pairable(b) != (bi < P.round_qblocks[k] + P.round_qsingle[k]) ||
         (bi < P.round_qblocks[k] + P.round_qfull[k] && !qblock_full_single(b)))
@@ -647,7 +765,13 @@ void check_work(const wb_plan_t& P, const Rank& R) {
       const uint64_t es = dtype_bytes(q.sdt);
       inside(0, q.src_off, (uint64_t(q.r1m1 - q.r0) * q.src_ld + (q.c1m1 - q.c0) + 1) * es, "fp8 piece");
     }
-  }
+  };
+  // blocks in runs of 2^14 on the planning threads (the checks only read)
+  const uint32_t b0 = P.round_qblocks[k], nb = P.round_qblocks[k + 1] - b0, run = 1u << 14;
+  parallel_for((nb + run - 1) / run, nb >= 2 * run ? plan_threads() : 1, [&](size_t i, int) {
+    const uint32_t lo = b0 + static_cast<uint32_t>(i) * run, hi = lo + std::min(run, b0 + nb - lo);
+    for (uint32_t bi = lo; bi < hi; ++bi) check_block(bi);
+  });
   }
 }
 
@@ -768,14 +892,31 @@ int assign_rounds(const wb_layout_t& trainer, const wb_layout_t& rollout, std::v
   return order.empty() ? 1 : rounds.back() + 1;
 }
 
+// The segments of every (round, stage), each list in canonical order.
+struct SegRange {
+  const uint32_t *first, *last;
+};
+struct SegIndex {
+  std::vector<uint32_t> idx, start;
+  SegIndex(const std::vector<Segment>& segs, int nrounds) : idx(segs.size()), start(size_t(nrounds) * 3 + 1, 0) {
+    for (const Segment& g : segs) ++start[size_t(g.round) * 3 + g.stage + 1];
+    for (size_t i = 1; i < start.size(); ++i) start[i] += start[i - 1];
+    std::vector<uint32_t> fill(start.begin(), start.end() - 1);
+    for (size_t i = 0; i < segs.size(); ++i) idx[fill[size_t(segs[i].round) * 3 + segs[i].stage]++] = uint32_t(i);
+  }
+  SegRange of(int k, int stage) const {
+    return {idx.data() + start[size_t(k) * 3 + stage], idx.data() + start[size_t(k) * 3 + stage + 1]};
+  }
+};
+
 // Wire offsets of one stage of round k (segments in canonical order, payloads
 // at multiples of 256 bytes within their region, regions at multiples of 4096
 // bytes; senders' buffers by ascending receiver, receivers' by ascending
 // sender). Offsets are relative to the stage's receive section.
-void wire_stage(std::vector<Segment>& segs, int k, int stage, int ns, int nd, StageWire& W) {
+void wire_stage(std::vector<Segment>& segs, const SegRange& in, int ns, int nd, StageWire& W) {
   std::vector<int64_t> end(size_t(ns) * nd, -1);
-  for (Segment& g : segs) {
-    if (g.round != k || g.stage != stage) continue;
+  for (const uint32_t* i = in.first; i != in.last; ++i) {
+    Segment& g = segs[*i];
     int64_t& e = end[size_t(g.s) * nd + g.d];
     const int64_t off = e < 0 ? 0 : align_up(e, kPayloadAlign);
     g.send_off = g.recv_off = off;
@@ -809,8 +950,8 @@ void wire_stage(std::vector<Segment>& segs, int k, int stage, int ns, int nd, St
     }
     W.recv_bytes[d] = pos;
   }
-  for (Segment& g : segs) {
-    if (g.round != k || g.stage != stage) continue;
+  for (const uint32_t* i = in.first; i != in.last; ++i) {
+    Segment& g = segs[*i];
     g.send_off += W.send_region[size_t(g.s) * nd + g.d];
     g.recv_off += W.recv_region[size_t(g.s) * nd + g.d];
   }
@@ -819,14 +960,15 @@ void wire_stage(std::vector<Segment>& segs, int k, int stage, int ns, int nd, St
 // All stages of round k: the exchange sections follow the receive section in
 // every rollout rank's buffer (a non-empty section starts on a 4096-byte
 // boundary); forwarded segments read where their source segment landed.
-void wire_round(wb_plan_t& P, int k) {
+void wire_round(wb_plan_t& P, int k, const SegIndex& at) {
   const int ns = P.n_send, nd = P.n_recv;
   RoundWire& W = P.rounds[k];
-  wire_stage(P.segs, k, 0, ns, nd, W.st[0]);
+  wire_stage(P.segs, at.of(k, 0), ns, nd, W.st[0]);
   W.recv_total = W.st[0].recv_bytes;
   for (int stage = 1; stage <= 2; ++stage) {
     StageWire& S = W.st[stage];
-    wire_stage(P.segs, k, stage, nd, nd, S);
+    const SegRange in = at.of(k, stage);
+    wire_stage(P.segs, in, nd, nd, S);
     std::vector<int64_t> base(nd);
     for (int d = 0; d < nd; ++d) {
       if (S.recv_bytes[d]) W.recv_total[d] = align_up(W.recv_total[d], kRegionAlign);
@@ -835,8 +977,8 @@ void wire_round(wb_plan_t& P, int k) {
     }
     for (size_t i = 0; i < S.recv_region.size(); ++i)
       if (S.recv_region[i] >= 0) S.recv_region[i] += base[i % nd];
-    for (Segment& g : P.segs) {
-      if (g.round != k || g.stage != stage) continue;
+    for (const uint32_t* i = in.first; i != in.last; ++i) {
+      Segment& g = P.segs[*i];
       g.recv_off += base[g.d];
       g.src_off = P.segs[g.src_seg].recv_off;
     }
@@ -1007,6 +1149,9 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
   // segment to the other holders in the receiver's node
   if (G > 0) {
     const size_t n0 = P.segs.size();
+    size_t more = 0;  // every holder of a replicated group receives each of its segments once
+    for (size_t gi = 0; gi < n0; ++gi) more += rgroups[rg_of[P.segs[gi].d][P.segs[gi].dst_pl]].holders.size() - 1;
+    P.segs.reserve(n0 + more);
     for (size_t gi = 0; gi < n0; ++gi) {
       const Segment g = P.segs[gi];
       const RGroup& h = rgroups[rg_of[g.d][g.dst_pl]];
@@ -1047,13 +1192,16 @@ void build_plan(const wb_layout_t& trainer, const wb_layout_t& rollout, int role
     }
   }
 
+  if (P.segs.size() > 0x7FFFFFFF) fail(WB_EUNSUPPORTED, "too many segments");
+
   // 5. rounds, then 4. wire offsets per round
   P.n_send = ns;
   P.n_recv = nd;
   P.node_size = G;
   const int nrounds = round_budget > 0 ? assign_rounds(trainer, rollout, P.segs, round_budget) : 1;
   P.rounds.assign(nrounds, RoundWire{});
-  for (int k = 0; k < nrounds; ++k) wire_round(P, k);
+  const SegIndex at(P.segs, nrounds);
+  for (int k = 0; k < nrounds; ++k) wire_round(P, k, at);
 
   P.role = role;
   P.rank = rank;
@@ -1118,11 +1266,17 @@ std::string dump_plan(const wb_plan_t& P) {
     return o.str();
   }
   o << " rounds=" << P.rounds.size() << "\n";
+  std::vector<size_t> start(P.rounds.size() + 1, 0), idx(P.segs.size());  // segments by round, in order
+  for (const Segment& g : P.segs) ++start[g.round + 1];
+  for (size_t k = 0; k < P.rounds.size(); ++k) start[k + 1] += start[k];
+  {
+    std::vector<size_t> fill(start.begin(), start.end() - 1);
+    for (size_t i = 0; i < P.segs.size(); ++i) idx[fill[P.segs[i].round]++] = i;
+  }
   for (size_t k = 0; k < P.rounds.size(); ++k) {
     o << "round " << k << "\n";
     sizes(P.rounds[k]);
-    for (const Segment& g : P.segs)
-      if (g.round == static_cast<int>(k)) seg(g);
+    for (size_t i = start[k]; i < start[k + 1]; ++i) seg(P.segs[idx[i]]);
   }
   return o.str();
 }

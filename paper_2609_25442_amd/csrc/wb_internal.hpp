@@ -2,9 +2,11 @@
 #pragma once
 
 #include <cstdint>
+#include <memory>
 #include <stdexcept>
 #include <string>
 #include <unordered_map>
+#include <utility>
 #include <vector>
 
 #include "../../include/wb.h"
@@ -17,6 +19,28 @@ struct Error : std::runtime_error {
   Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
 };
 [[noreturn]] inline void fail(int code, const std::string& msg) { throw Error(code, msg); }
+
+// Allocator that leaves new elements of trivial types uninitialised on
+// resize, so a large table is first touched by the threads that fill it
+// (every element must then be written before it is read).
+template <class T>
+struct NoInitAlloc : std::allocator<T> {
+  template <class U>
+  struct rebind {
+    using other = NoInitAlloc<U>;
+  };
+  NoInitAlloc() = default;
+  template <class U>
+  NoInitAlloc(const NoInitAlloc<U>&) noexcept {}
+  template <class U>
+  void construct(U* p) noexcept {
+    ::new (static_cast<void*>(p)) U;
+  }
+  template <class U, class... A>
+  void construct(U* p, A&&... a) {
+    ::new (static_cast<void*>(p)) U(std::forward<A>(a)...);
+  }
+};
 
 inline int dtype_bytes(int dt) {
   switch (dt) {
@@ -213,6 +237,7 @@ struct QBlock {
   uint8_t rows_m1, cols_m1;  // block extent minus one (blocks are at most 128 x 128)
   uint8_t flags, pad0;
   uint16_t pad1;
+  uint32_t pad2;        // every byte a named member: copies carry zeros, not indeterminate padding
 };
 static_assert(sizeof(QBlock) == 48, "QBlock layout");
 
@@ -321,8 +346,8 @@ struct wb_plan_t {
   std::vector<wb::Task> tasks;          // pack or unpack work by round, then forward work by stage and round
   std::vector<wb::TaskSplit> round_split;  // [k]: class sizes of round k's pack/unpack range
   std::vector<wb::TaskSplit> fwd_split[2]; // the same for the forward range of stage 1 + i, round k
-  std::vector<wb::QBlock> qblocks;      // grouped by round
-  std::vector<wb::QPiece> qpieces;
+  std::vector<wb::QBlock, wb::NoInitAlloc<wb::QBlock>> qblocks;  // grouped by round
+  std::vector<wb::QPiece, wb::NoInitAlloc<wb::QPiece>> qpieces;
   std::vector<uint32_t> round_tasks, round_qblocks;  // [k] .. [k + 1] is round k's range
   std::vector<uint32_t> round_qfull;    // [k]: blocks of full pairs at the start of round k's block range (even)
   std::vector<uint32_t> round_qsingle;  // [k]: pairable blocks (full pairs, QB_SINGLE, QB_BANDS) at its start

@@ -478,3 +478,25 @@ def test_noalloc_entry_reads_only_planned_tables(name):
         assert wb.lib.wb_unpack_round_noalloc(p._h, p.num_rounds, None, ptrs, None) == wb.WB_EINVAL
     s = wb.Plan(tr, ro, wb.SENDER, w["pack_rank"])
     assert wb.lib.wb_unpack_round_noalloc(s._h, 0, None, ptrs, None) == wb.WB_EINVAL
+
+
+@pytest.mark.parametrize("budget,G", [(0, 0), (1 << 30, 0), (0, 2)])
+def test_plan_threads_change_nothing(budget, G, monkeypatch):
+    """The full DeepSeek-V3 rollout rank's fp8 tables (1.4 M blocks, built local
+    by local on the planning threads and checked in runs of 2^14 blocks) and
+    every other work table are the same for 1, 3 and 16 planning threads, with
+    rounds and with exchange stages; the digest does see the tables (1 KiB work
+    items change it)."""
+    w = WORKLOADS["dsv3_ep64_to_ep8_fp8"]
+    tr = wb.Layout.describe(w["model"], w["trainer"])
+    ro = wb.Layout.describe(w["model"], w["rollout"])
+    seen = set()
+    for n in ("1", "3", "16"):
+        monkeypatch.setenv("WB_PLAN_THREADS", n)
+        p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=budget, node_size=G)
+        assert p.work_counts()[1] > 1 << 20
+        seen.add((p.work_digest(), p.dump()))
+    assert len(seen) == 1
+    monkeypatch.setenv("WB_TASK_BYTES", "1024")
+    p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=budget, node_size=G)
+    assert p.work_digest() != next(iter(seen))[0]
