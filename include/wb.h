@@ -251,8 +251,8 @@ int wb_plan_workspace_bytes(const wb_plan_t* plan, int64_t* out);
 /* Algorithmic bytes one wb_pack or wb_unpack of this rank reads and writes. */
 int wb_plan_traffic_bytes(const wb_plan_t* plan, int64_t* read_bytes, int64_t* write_bytes);
 /* The same split by launch: launch 0 is the copy/cast kernel, launch 4 the
- * transpose-tile kernel (whole 256 x 256 tiles of 2-byte transposes; 0
- * otherwise), launch 1 the fp8 block kernel (receivers with fp8 tensors only;
+ * transpose-tile kernel (whole tiles of 128 source rows x 512 source columns
+ * of 2-byte transposes; 0 otherwise), launch 1 the fp8 block kernel (receivers with fp8 tensors only;
  * 0 otherwise); launches 2 and 3 are the forward packings of exchange stages
  * 1 and 2 over all rounds (receivers of three-stage plans; 0 otherwise).
  * Launches 0, 1 and 4 add up to wb_plan_traffic_bytes. */
@@ -266,7 +266,7 @@ int wb_plan_work_counts(const wb_plan_t* plan, int64_t* tasks, int64_t* blocks, 
 int wb_plan_work_digest(const wb_plan_t* plan, uint64_t* out);
 /* Grid (workgroups in x and y) and workgroup size (threads) of one launch of
  * one round: launch 0 the copy/cast kernel of wb_pack_round / wb_unpack_round,
- * 4 its transpose-tile kernel (one workgroup per 256 x 256 tile), 1 the fp8
+ * 4 its transpose-tile kernel (one workgroup per 128 x 512 tile), 1 the fp8
  * block kernel, 2 and 3 the forward packings of exchange stages 1 and 2. A copy/cast work item takes several workgroups (one per chunk of its
  * vectors), so the copy grid is a multiple of the work-item count; the fp8
  * grid has one workgroup per pair of pairable blocks (single-piece blocks and
@@ -288,7 +288,7 @@ int wb_plan_upload(wb_plan_t* plan, void* workspace, size_t bytes, void* stream)
  * the rank (wb_plan_num_local_tensors entries), send_buf holds at least
  * wb_plan_buffer_bytes bytes. Writes every payload byte of the rank's regions;
  * bytes between payloads are left as they were. One kernel launch, and one
- * more when the rank has whole 256 x 256 tiles to transpose.
+ * more when the rank has whole 128 x 512 tiles to transpose.
  * Errors (synchronous): WB_EINVAL (wrong role, not uploaded, null or misaligned
  * pointer), WB_EHIP (launch failure). Device faults surface at stream sync. */
 int wb_pack(wb_plan_t* plan, const void* const* src_ptrs, void* send_buf, void* stream);

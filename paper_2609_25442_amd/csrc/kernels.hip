@@ -370,32 +370,39 @@ __global__ __launch_bounds__(kThreads) void wb_tasks_kernel(const Task* __restri
   }
 }
 
-// dst[c][r] = src[r][c] of one 256 x 256 tile of 2-byte elements per
-// workgroup (TASK_TILE256 items): thread t transposes the 8 x 8 sub-tile at
-// source rows 8 (t / 32) .., columns 8 (t mod 32) .. in registers, LDS
-// regroups the sub-tiles by destination row (padded rows), and each thread
-// then stores eight 16-byte pieces of destination rows, so that on both sides
-// a wave instruction moves two contiguous 512-byte rows.
+// dst[c][r] = src[r][c] of one kTileRows x kTileCols tile of 2-byte elements
+// per workgroup (TASK_TILE items): thread t transposes the 8 x 8 sub-tile at
+// source rows 8 (t / 64) .., columns 8 (t mod 64) .. in registers (a wave
+// instruction reads 1 KiB of one source row), LDS regroups the sub-tiles by
+// destination row, and each thread then stores eight 16-byte pieces of
+// destination rows (a wave instruction writes four whole 256-byte rows). The
+// 16-byte words of destination row r sit in LDS at word w ^ ((r / 8) mod 16):
+// the sub-tiles of one wave land in 16 different bank groups, and a row read
+// back is a permutation of its own words.
 __global__ __launch_bounds__(kTileThreads) void wb_tile_kernel(const Task* __restrict__ tasks,
                                                                const uint64_t* __restrict__ ptrs, const char* buf,
                                                                const char* aux) {
-  constexpr int G = kTileEdge / 8;
-  __shared__ u32x4 lds[kTileEdge][G + 1];
+  constexpr int GR = kTileRows / 8, GC = kTileCols / 8;  // 16-byte words per destination / source row
+  __shared__ u32x4 lds[kTileCols][GR];
   const Task t = tasks[blockIdx.x];
   const char* src = base_of(t.src_idx, ptrs, buf, aux) + t.src_off;
   char* dst = const_cast<char*>(base_of(t.dst_idx, ptrs, buf, aux)) + t.dst_off;
-  const int cg = threadIdx.x % G, rg = threadIdx.x / G;
+  const int cg = threadIdx.x % GC, rg = threadIdx.x / GC;
   u32x4 a[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
     a[i] = ld(reinterpret_cast<const u32x4*>(src + (uint64_t(8 * rg + i) * t.src_ld + 8 * cg) * 2));
 #pragma unroll
-  for (int j = 0; j < 8; ++j) lds[8 * cg + j][rg] = column8(a, j);  // destination row 8 cg + j
+  for (int j = 0; j < 8; ++j) {
+    const int row = 8 * cg + j;  // destination row
+    lds[row][rg ^ ((row >> 3) & (GR - 1))] = column8(a, j);
+  }
   __syncthreads();
+  const int w = threadIdx.x % GR, r0 = threadIdx.x / GR;
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const int row = G * k + rg;
-    st(lds[row][cg], reinterpret_cast<u32x4*>(dst + (uint64_t(row) * t.dst_ld + 8 * cg) * 2));
+    const int row = r0 + (kTileThreads / GR) * k;
+    st(lds[row][w ^ ((row >> 3) & (GR - 1))], reinterpret_cast<u32x4*>(dst + (uint64_t(row) * t.dst_ld + 8 * w) * 2));
   }
 }
 

@@ -195,23 +195,23 @@ struct TaskSink {
   }
 
   // dst[c][r] = src[r][c] for an R x C source block. Aligned 2-byte data is
-  // cut into 256 x 256 tiles (taken along the source rows, which measured
-  // fastest for these tiles), transposed by the tile kernel; the edges go to
-  // transpose_small.
+  // cut into tiles of 128 source rows by 512 source columns (taken along the
+  // source rows, which measured fastest for these tiles), transposed by the
+  // tile kernel; the edges go to transpose_small.
   void transpose_rect(int sidx, uint64_t soff, int64_t sld, int sdt, int didx, uint64_t doff, int64_t dld, int ddt,
                       int64_t R, int64_t C) {
     const int ss = dtype_bytes(sdt), ds = dtype_bytes(ddt);
     const bool fast = ss == 2 && ds == 2 && sdt == ddt && soff % 16 == 0 && doff % 16 == 0 && (sld * 2) % 16 == 0 &&
                       (dld * 2) % 16 == 0;
-    const int64_t RT = fast ? R / kTileEdge * kTileEdge : 0, CT = fast ? C / kTileEdge * kTileEdge : 0;
+    const int64_t RT = fast ? R / kTileRows * kTileRows : 0, CT = fast ? C / kTileCols * kTileCols : 0;
     if (RT == 0 || CT == 0) {
       transpose_small(sidx, soff, sld, sdt, didx, doff, dld, ddt, R, C);
       return;
     }
-    for (int64_t r = 0; r < RT; r += kTileEdge)
-      for (int64_t c = 0; c < CT; c += kTileEdge)
-        push(TASK_TILE256, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
-             doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, kTileEdge, kTileEdge);
+    for (int64_t r = 0; r < RT; r += kTileRows)
+      for (int64_t c = 0; c < CT; c += kTileCols)
+        push(TASK_TILE, sidx, soff + (r * sld + c) * 2, static_cast<uint32_t>(sld), sdt, didx,
+             doff + (c * dld + r) * 2, static_cast<uint32_t>(dld), ddt, kTileRows, kTileCols);
     if (CT < C)  // right strip of the tiled rows
       transpose_small(sidx, soff + CT * 2, sld, sdt, didx, doff + CT * dld * 2, dld, ddt, RT, C - CT);
     if (RT < R)  // bottom strip, full width
@@ -672,8 +672,8 @@ void check_work(const wb_plan_t& P, const Rank& R) {
         inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");
         inside(t.dst_idx, t.dst_off, (uint64_t(t.cols - 1) * t.dst_ld + t.rows) * ds, "transpose destination");
         break;
-      case TASK_TILE256:
-        if (t.rows != kTileEdge || t.cols != kTileEdge || ss != 2 || ds != 2 || t.src_off % 16 || t.dst_off % 16 ||
+      case TASK_TILE:
+        if (t.rows != kTileRows || t.cols != kTileCols || ss != 2 || ds != 2 || t.src_off % 16 || t.dst_off % 16 ||
             (t.src_ld * 2) % 16 || (t.dst_ld * 2) % 16)
           fail(WB_EINVAL, "internal: bad transpose tile");
         inside(t.src_idx, t.src_off, (uint64_t(t.rows - 1) * t.src_ld + t.cols) * ss, "transpose source");

@@ -147,14 +147,14 @@ enum TaskKind : uint8_t {
   TASK_SCALAR = 3,     // any supported pair, element by element
   TASK_TRANSPOSE = 4,  // dst[c][r] = cvt(src[r][c]), one LDS tile of up to 64 x 64
   TASK_TRANSPOSE16 = 5,  // 2-byte dst[c][r] = src[r][c], (64..256) rows x 64 cols, in registers
-  TASK_TILE256 = 6,    // 2-byte dst[c][r] = src[r][c], one 256 x 256 tile through LDS (a launch of its own)
+  TASK_TILE = 6,       // 2-byte dst[c][r] = src[r][c], one kTileRows x kTileCols tile through LDS (a launch of its own)
 };
 
-// TASK_TILE256 items run one per workgroup of kTileThreads threads: each
-// thread transposes one 8 x 8 sub-tile, so that a wave instruction moves two
-// 512-byte rows on either side.
-constexpr int kTileEdge = 256;
-constexpr int kTileThreads = (kTileEdge / 8) * (kTileEdge / 8);
+// TASK_TILE items run one per workgroup of kTileThreads threads: each thread
+// transposes one 8 x 8 sub-tile, so that a wave instruction reads 1 KiB of one
+// source row and writes 256 bytes of each of four destination rows.
+constexpr int kTileRows = 128, kTileCols = 512;  // of the source block
+constexpr int kTileThreads = (kTileRows / 8) * (kTileCols / 8);
 
 struct Task {
   uint64_t src_off, dst_off;
@@ -188,7 +188,7 @@ constexpr uint32_t kMaxGridX = 1u << 22;
 static_assert(kChunkThreads % 64 == 0 && kChunkThreads <= 256, "copy workgroup size");
 
 inline int task_class(const Task& t) {
-  if (t.kind == TASK_TILE256) return 3;
+  if (t.kind == TASK_TILE) return 3;
   if (t.kind == TASK_TRANSPOSE || t.kind == TASK_TRANSPOSE16) return 1;
   return t.kind == TASK_SCALAR ? 2 : 0;
 }

@@ -121,13 +121,13 @@ def test_copy_launch_grid_is_dense(name):
     ro = wb.Layout.describe(w["model"], w["rollout"])
     for role, rank in ((wb.SENDER, w["pack_rank"]), (wb.RECEIVER, w["unpack_rank"])):
         p = wb.Plan(tr, ro, role, rank)
-        # whole 256 x 256 transpose tiles: one tile-kernel workgroup each
+        # whole transpose tiles of 128 source rows x 512 columns: one tile-kernel workgroup each
         tiles, ty, tt = p.launch_grid(4)
         tr_, tw_ = p.kernel_traffic(4)
-        assert tt == 1024 and ty == (1 if tiles else 0) and tr_ == tw_ == tiles * 256 * 256 * 2
+        assert tt == 1024 and ty == (1 if tiles else 0) and tr_ == tw_ == tiles * 128 * 512 * 2
         if (name, role) == ("llama3_8b_tp4_to_tp2", wb.SENDER):
             # the row-parallel o and down slabs, [1024, 4096] and [3584, 4096] per layer
-            assert tiles == 32 * (4 + 14) * 16
+            assert tiles == 32 * (8 + 28) * 8
         items = p.work_counts()[0] - tiles
         x, y, threads = p.launch_grid(0)
         assert threads in (64, 128, 256) and x <= 1 << 22

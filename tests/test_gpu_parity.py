@@ -102,14 +102,15 @@ def test_generator_matches_on_gpu():
 
 
 @pytest.mark.parametrize("rows,cols,split", [(520, 200, 1), (640, 264, 2), (130, 77, 1), (1024, 512, 3), (384, 1100, 2),
-                                            (768, 1536, 2), (1000, 1296, 2), (1024, 4096, 4)])
+                                            (768, 1536, 2), (1000, 1296, 2), (1024, 4096, 4), (1536, 1024, 4)])
 def test_transposed_trainer_shards(rows, cols, split):
     """Trainer ranks hold column slabs of T stored transposed (row-parallel
-    shards); the rollout wants T row-major in one tensor. Whole 256 x 256 tiles
-    of aligned slabs (16-byte rows on both sides) go to the tile kernel: 768 x
-    1536 in two slabs gives 9 tiles each and nothing else; 1000 x 1296 gives
-    648 x 1000 slabs, 6 tiles each, a right strip for the register transposes
-    (64-column strips of up to 256 rows) and the LDS tiles, and a bottom strip;
+    shards); the rollout wants T row-major in one tensor. Whole tiles of 128
+    slab rows x 512 slab columns of aligned slabs (16-byte rows on both sides)
+    go to the tile kernel: 1536 x 1024 in four slabs gives 2 x 3 tiles each and
+    nothing else; 520 x 200 one tile and strips for the register transposes
+    (64-column strips of up to 256 rows) and the LDS tiles; 1000 x 1296 gives
+    648 x 1000 slabs, 5 tiles each, a right and a bottom strip;
     1024 x 4096 in four slabs is the shape of a Llama-3-8B o slab. Slabs whose
     rows are not 16-byte multiples (384 x 1100: 1100-byte rows) and odd widths
     go to the LDS tiles."""
@@ -123,15 +124,16 @@ def test_transposed_trainer_shards(rows, cols, split):
     p = wb.Plan(to_wb(tr), to_wb(ro), wb.SENDER, 0)
     slab = cuts[1] - cuts[0]
     aligned = (slab * 2) % 16 == 0 and (rows * 2) % 16 == 0
-    assert p.launch_grid(4)[0] == ((slab // 256) * (rows // 256) if aligned else 0)
+    assert p.launch_grid(4)[0] == ((slab // 128) * (rows // 512) if aligned else 0)
     roundtrip(tr, ro, _values(cat, "bf16"), label=f"transposed-{rows}x{cols}/{split}")
 
 
-@pytest.mark.parametrize("rows,cols", [(600, 520), (512, 768), (256, 300)])
+@pytest.mark.parametrize("rows,cols", [(600, 520), (512, 768), (256, 300), (600, 1096), (256, 1024)])
 def test_transposed_rollout_tiles(rows, cols):
     """The unpack direction: the rollout stores T transposed, so its
-    assembly transposes whole 256 x 256 tiles (and the ragged strips) out of
-    the row-major wire payloads of two trainer ranks (row halves of T)."""
+    assembly transposes whole tiles of 128 payload rows x 512 columns (and the
+    ragged strips) out of the row-major wire payloads of two trainer ranks
+    (row halves of T)."""
     cat = [CkptTensor("T", rows, cols)]
     h = rows // 2
     tr = Layout(cat, [RankLayout([Local("a", "bf16", 1, h, cols)], [Placement(0, 0, h, 0, cols, 0, 0, cols)]),
@@ -140,7 +142,7 @@ def test_transposed_rollout_tiles(rows, cols):
     p = wb.Plan(to_wb(tr), to_wb(ro), wb.RECEIVER, 0)
     # whole tiles where the payload's rows and its place in x are 16-byte aligned
     aligned = (cols * 2) % 16 == 0 and (rows * 2) % 16 == 0
-    tiles = [(n // 256) * (cols // 256) if aligned and (r0 * 2) % 16 == 0 else 0 for r0, n in ((0, h), (h, rows - h))]
+    tiles = [(n // 128) * (cols // 512) if aligned and (r0 * 2) % 16 == 0 else 0 for r0, n in ((0, h), (h, rows - h))]
     assert p.launch_grid(4)[0] == sum(tiles)
     roundtrip(tr, ro, _values(cat, "bf16"), label=f"transposed-rollout-{rows}x{cols}")
 
