@@ -3,18 +3,20 @@ allocate) against wb_unpack_round through an uploaded workspace: the rollout
 tensors agree byte for byte on consecutive calls (a larger plan, then a
 smaller one, so the second call finds the first call's tables in the
 library's array), over every round of multi-round plans on plans that were
-never uploaded, and a round whose tables exceed the array is refused before
-any pointer is looked at."""
+never uploaded, with whole transpose tiles, and a round whose tables exceed
+the array is refused before any pointer is looked at."""
 
 import pytest
 import torch
 
 import paper_2609_25442_amd as wb
-from oracle.layout import layout_from_spec
+from oracle.catalog import CkptTensor
+from oracle.layout import Layout, Local, Placement, RankLayout, layout_from_spec
 from oracle.plan import build_plan
 from synthetic_checkpoint.workloads import ORDER, WORKLOADS, scaled
 
 from gpu_util import say, workspace_for
+from wb_cases import to_wb
 
 pytestmark = pytest.mark.gpu
 
@@ -43,12 +45,15 @@ def _raw(t):
 
 def _compare(name, w, budget, seed):
     tr, ro = _layouts(w)
-    d = w["unpack_rank"]
+    return _compare_layouts(name, tr, ro, w["unpack_rank"], w["trainer"]["dtype"], budget, seed)
+
+
+def _compare_layouts(name, tr, ro, d, dtype, budget, seed):
     up = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=budget)
     free = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=budget)     # never uploaded
     ws = workspace_for(up)
     up.upload(ws)
-    recvs = _receive_buffers(up, w["trainer"]["dtype"], seed)
+    recvs = _receive_buffers(up, dtype, seed)
     want = wb.allocate_locals(ro, d)
     got = wb.allocate_locals(ro, d)
     for a, b in zip(want, got):
@@ -79,6 +84,20 @@ def test_noalloc_every_round(name):
     total = sum(g.nbytes for g in build_plan(otr, oro).segments)
     budget = max(4096, total // (4 * oro.nranks))
     assert _compare(name, w, budget, 3) > 2
+
+
+@pytest.mark.parametrize("rows,cols", [(256, 1024), (600, 1096)])
+def test_noalloc_transposed_rollout_tiles(rows, cols):
+    # a rollout that stores T transposed: whole transpose tiles (a launch of
+    # their own) and, for 600 x 1096, ragged strips and unaligned payloads
+    cat = [CkptTensor("T", rows, cols)]
+    h = rows // 2
+    tr = Layout(cat, [RankLayout([Local("a", "bf16", 1, h, cols)], [Placement(0, 0, h, 0, cols, 0, 0, cols)]),
+                      RankLayout([Local("b", "bf16", 1, rows - h, cols)], [Placement(0, h, rows, 0, cols, 0, 0, cols)])])
+    ro = Layout(cat, [RankLayout([Local("x", "bf16", 1, cols, rows)], [Placement(0, 0, rows, 0, cols, 0, 0, rows, 1)])])
+    tr, ro = to_wb(tr), to_wb(ro)
+    assert wb.Plan(tr, ro, wb.RECEIVER, 0).launch_grid(4)[0] > 0
+    _compare_layouts(f"transposed {rows}x{cols}", tr, ro, 0, "bf16", 0, 4)
 
 
 def test_noalloc_refuses_tables_beyond_the_array():
