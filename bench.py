@@ -388,7 +388,16 @@ def run_probe(args):
                       for (t, r0, r1, c0, c1, u, b, ld, tr) in declared.placements(rank))
         modes = {}
         wb.probe_layout(cat, dtype, [load])  # untimed: loads the code objects of every launch
+        # holding the passes needs the rank's loaded tensors once per pass
+        # (and the identifier tensors it reads, about as large)
+        es = {"f32": 4, "bf16": 2, "f8e4m3": 1}
+        local_bytes = sum(lc["numel"] * es[dtype] for u, lc in enumerate(declared.locals(rank)) if u in keep)
+        hold_fits = local_bytes * (wb.Probe(cat, dtype).num_chunks + 1) * 4 <= torch.cuda.mem_get_info()[0] * 3
         for hold in (True, False):
+            if hold and not hold_fits:
+                modes["held_passes"] = None
+                log(f"[probe] {side} rank {rank} held_passes: skipped ({local_bytes / 1e9:.1f} GB per pass)")
+                continue
             stats = {}
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -402,69 +411,76 @@ def run_probe(args):
                             "carry_retries": len(stats.get("carry_retries", []))}
             del got
         # the stencils alone: each carry pass over the loaded tensors of that
-        # pass (in order, since a pass reads the carries of the one before),
-        # and one launch over all passes held on the device; a timed call
-        # includes the library's host work (tile table, its upload and the
-        # wait for it), the field arrays are built beforehand
+        # pass (pass by pass, since a pass reads the carries of the one before;
+        # repeating a pass rewrites the same table from the same input), and,
+        # when all passes fit on the device, one launch over all of them held;
+        # a timed call includes the library's host work (tile table, its
+        # upload and the wait for it), the field arrays are built beforehand
         probe = wb.Probe(cat, dtype)
-        ckpt = {n: torch.empty((r, c), dtype=wb.torch_dtype(dtype), device="cuda") for n, r, c in cat}
-        held = []
-        for k in range(probe.num_chunks):
-            for t, (n, r, c) in enumerate(cat):
-                wb.make_ids(ckpt[n], dtype, probe.first_id(t), k)
-            held.append([x.clone() for x in load(ckpt)])
-        del ckpt
-        shapes = [wb._view_shape(x) for x in held[0]]
-        per_pass = [wb._field_array([(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(h, shapes)]) for h in held]
-        every = wb._field_array([([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)])
+        ids = wb._IdCheckpoint(cat, dtype, wb.torch_dtype(dtype), "cuda")
         cap = 1 << 21
         idx = torch.empty(cap, dtype=torch.int64, device="cuda")
         val = torch.empty(cap, dtype=torch.int64, device="cuda")
         count = torch.zeros(1, dtype=torch.int64, device="cuda")
         carries = torch.zeros(1, dtype=torch.int64, device="cuda")
-        nbytes = sum(x.numel() * x.element_size() for x in held[0])
-        numel = sum(x.numel() for x in held[0])
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        stencil = {}
-        ccap = 16 * (numel >> 16) + 64 * len(shapes) + 4096
-        ws = torch.empty(wb.diff2_carry_workspace(per_pass[0], ccap), dtype=torch.uint8, device="cuda")
-        times = [[] for _ in held]
-        got_counts = [None] * len(held)
-        for rep in range(4):
-            for k, fields in enumerate(per_pass):
+        stencil, held, ws = {}, [], None
+        for k in range(probe.num_chunks):
+            ids.start_pass(probe, k)
+            locs = load(ids)  # may hold views of the identifier tensors: cloned only to be held
+            if k == 0:
+                shapes = [wb._view_shape(x) for x in locs]
+                nbytes = sum(x.numel() * x.element_size() for x in locs)
+                numel = sum(x.numel() for x in locs)
+                ccap = 16 * (numel >> 16) + 64 * len(shapes) + 4096
+                hold_all = nbytes * probe.num_chunks * 4 <= torch.cuda.mem_get_info()[0] * 3
+            fields = wb._field_array([(x, dtype, b * rr, cc) for x, (b, rr, cc) in zip(locs, shapes)])
+            if ws is None:
+                ws = torch.empty(wb.diff2_carry_workspace(fields, ccap), dtype=torch.uint8, device="cuda")
+            times = []
+            for rep in range(4):
                 ev[0].record()
-                wb.diff2_carry(fields, k, k + 1 == len(held), ccap, idx, val, count, carries, ws)
+                wb.diff2_carry(fields, k, k + 1 == probe.num_chunks, ccap, idx, val, count, carries, ws)
                 ev[1].record()
                 torch.cuda.synchronize()
-                times[k].append(ev[0].elapsed_time(ev[1]))
-                got_counts[k] = (int(count.item()), int(carries.item()))
-        for k in range(len(held)):
-            best = min(times[k][1:])
+                times.append(ev[0].elapsed_time(ev[1]))
+            best = min(times[1:])
             rate = nbytes / (best * 1e-3) / 1e9
-            stencil[f"carry_pass_{k}"] = {"bytes": nbytes, "entries": got_counts[k][0], "carries": got_counts[k][1],
+            got = (int(count.item()), int(carries.item()))
+            stencil[f"carry_pass_{k}"] = {"bytes": nbytes, "entries": got[0], "carries": got[1],
                                           "carry_capacity": ccap, "workspace_bytes": ws.numel(),
                                           "ms": round(best, 3), "GB/s": round(rate, 1),
                                           "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
             log(f"[probe] {side} diff2 carry pass {k}: {best:.3f} ms, {rate:.0f} GB/s, "
-                f"{got_counts[k][0]} entries, {got_counts[k][1]} carries")
-        del ws
-        ws = torch.empty(wb.diff2_batch_workspace(every), dtype=torch.uint8, device="cuda")
-        times = []
-        for rep in range(4):
-            ev[0].record()
-            wb.diff2_batch(every, idx, val, count, ws)
-            ev[1].record()
-            torch.cuda.synchronize()
-            times.append(ev[0].elapsed_time(ev[1]))
-        best = min(times[1:])
-        rate = nbytes * len(held) / (best * 1e-3) / 1e9
-        stencil["all_passes"] = {"launches": 1, "bytes": nbytes * len(held), "entries": int(count.item()),
-                                 "table_bytes": ws.numel(), "ms": round(best, 3), "GB/s": round(rate, 1),
-                                 "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
-        log(f"[probe] {side} diff2 all_passes: {best:.3f} ms, {rate:.0f} GB/s, {int(count.item())} entries")
+                f"{got[0]} entries, {got[1]} carries")
+            if hold_all:
+                held.append([x.clone() for x in locs])
+            del fields, locs
+        del ws, ids
+        if hold_all:
+            every = wb._field_array([([h[u] for h in held], dtype, b * rr, cc) for u, (b, rr, cc) in enumerate(shapes)])
+            ws = torch.empty(wb.diff2_batch_workspace(every), dtype=torch.uint8, device="cuda")
+            times = []
+            for rep in range(4):
+                ev[0].record()
+                wb.diff2_batch(every, idx, val, count, ws)
+                ev[1].record()
+                torch.cuda.synchronize()
+                times.append(ev[0].elapsed_time(ev[1]))
+            best = min(times[1:])
+            rate = nbytes * len(held) / (best * 1e-3) / 1e9
+            stencil["all_passes"] = {"launches": 1, "bytes": nbytes * len(held), "entries": int(count.item()),
+                                     "table_bytes": ws.numel(), "ms": round(best, 3), "GB/s": round(rate, 1),
+                                     "frac_of_hbm_peak": round(rate / HBM_PEAK_GBS, 4)}
+            log(f"[probe] {side} diff2 all_passes: {best:.3f} ms, {rate:.0f} GB/s, {int(count.item())} entries")
+            del every, ws
+        else:
+            stencil["all_passes"] = None
+            log(f"[probe] {side} diff2 all_passes: skipped ({probe.num_chunks} passes of {nbytes / 1e9:.1f} GB "
+                f"do not fit on the device together)")
         out["ranks"][side] = {"rank": rank, "placements": len(want), "local_tensors": len(keep), **modes,
                               "diff2": stencil}
-        del held, per_pass, every, idx, val, ws
+        del held, idx, val
         torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 

@@ -10,6 +10,7 @@ kernels in HIP). Importing this package fails if the library is not built
 from __future__ import annotations
 
 import atexit
+import collections.abc
 import ctypes
 import os
 import weakref
@@ -748,7 +749,7 @@ def probe_layout(catalog, ckpt_dtype: str, loaders, names=None, device="cuda", s
     timings and entry counts when given."""
     tdt = torch_dtype(ckpt_dtype)
     layout = Layout.create(catalog, len(loaders))
-    ckpt = {}
+    ckpt = _IdCheckpoint(catalog, ckpt_dtype, tdt, device)
     for r, load in enumerate(loaders):
         cap = carry_capacity
         while True:
@@ -775,13 +776,52 @@ def _now():
     return time.perf_counter()
 
 
+class _IdCheckpoint(collections.abc.Mapping):
+    """The identifier checkpoint a loader reads, {name: tensor}, made on
+    demand: a tensor is allocated the first time any pass reads it and filled
+    with the current pass's chunk of its identifiers the first time that pass
+    reads it. Tensors no loader reads are never made, so a rank of a checkpoint
+    larger than the GPU (a DeepSeek-V3 expert-parallel rank) is probed with
+    device memory for its own tensors only."""
+
+    def __init__(self, catalog, ckpt_dtype, tdt, device):
+        self._cat = {n: (t, rows, cols) for t, (n, rows, cols) in enumerate(catalog)}
+        self._dtype, self._tdt, self._device = ckpt_dtype, tdt, device
+        self._tensors, self._filled = {}, set()
+        self._probe, self._k = None, 0
+        self.ids_s = 0.0
+
+    def start_pass(self, probe, k):
+        self._probe, self._k = probe, k
+        self._filled.clear()
+        self.ids_s = 0.0
+
+    def __getitem__(self, name):
+        import torch
+
+        t, rows, cols = self._cat[name]
+        x = self._tensors.get(name)
+        if x is None:
+            x = self._tensors[name] = torch.empty((rows, cols), dtype=self._tdt, device=self._device)
+        if name not in self._filled:
+            t0 = _now()
+            make_ids(x, self._dtype, self._probe.first_id(t), self._k)
+            self.ids_s += _now() - t0
+            self._filled.add(name)
+        return x
+
+    def __iter__(self):
+        return iter(self._cat)
+
+    def __len__(self):
+        return len(self._cat)
+
+
 def _probe_rank(catalog, ckpt_dtype, tdt, load, r, names, device, stats, hold_passes, carry_capacity, ckpt):
     """Probe one rank; returns the filled Probe and whether passes were held."""
     import numpy as np
     import torch
 
-    if not ckpt:
-        ckpt.update({n: torch.empty((rows, cols), dtype=tdt, device=device) for n, rows, cols in catalog})
     probe = Probe(catalog, ckpt_dtype)
     shapes, held, hold, carry = None, [], hold_passes, None
     rec = stats.setdefault(r, []) if stats is not None else None
@@ -789,9 +829,7 @@ def _probe_rank(catalog, ckpt_dtype, tdt, load, r, names, device, stats, hold_pa
         rec.clear()
     for k in range(probe.num_chunks):
         last = k + 1 == probe.num_chunks
-        t0 = _now()
-        for t, (n, rows, cols) in enumerate(catalog):
-            make_ids(ckpt[n], ckpt_dtype, probe.first_id(t), k)
+        ckpt.start_pass(probe, k)
         t1 = _now()
         locs = load(ckpt)
         torch.cuda.synchronize()
@@ -828,8 +866,8 @@ def _probe_rank(catalog, ckpt_dtype, tdt, load, r, names, device, stats, hold_pa
         del locs
         t3 = _now()
         if rec is not None:
-            rec.append({"pass": k, "ids_s": t1 - t0, "load_s": t2 - t1, "diff2_s": t3 - t2, "entries": entries,
-                        "carries": carries})
+            rec.append({"pass": k, "ids_s": ckpt.ids_s, "load_s": t2 - t1 - ckpt.ids_s, "diff2_s": t3 - t2,
+                        "entries": entries, "carries": carries})
     if hold:
         t2 = _now()
         fields = [([held[k][u] for k in range(probe.num_chunks)], ckpt_dtype, b * rr, cc)

@@ -387,12 +387,19 @@ def test_probe_recovers_declared_layouts(name, hold):
 @pytest.mark.parametrize("name,side,hold", [("llama3_8b_fsdp8_to_tp1", "trainer", True),
                                             ("llama3_8b_fsdp8_to_tp1", "rollout", True),
                                             ("llama3_8b_fsdp8_to_tp1", "rollout", False),
-                                            ("llama3_8b_tp4_to_tp2", "trainer", True)])
+                                            ("llama3_8b_tp4_to_tp2", "trainer", True),
+                                            ("mixtral_ep8fsdp2_to_ep2", "trainer", False),
+                                            ("dsv3_ep64_to_ep8_fp8", "trainer", True),
+                                            ("dsv3_ep64_to_ep8_fp8", "rollout", False)])
 def test_probe_full_size(name, side, hold):
-    """The benchmark ranks at full size (16 GB identifier checkpoint), probed
-    through the torch loaders, with the passes held on the device or carried
-    one at a time (each pass handing over only corner entries): the
-    recovered placements equal the declared."""
+    """The benchmark ranks at full size, probed through the torch loaders, with
+    the passes held on the device or carried one at a time (each pass handing
+    over only corner entries): the recovered placements equal the declared.
+    The identifier checkpoint is made on demand, tensor by tensor as the loader
+    reads it: the DeepSeek-V3 checkpoint (1.8 x 10^11 elements, 362 GB in bf16)
+    is larger than the GPU, and its expert-parallel rollout rank reads 47 GB of
+    it per pass (the fp8 tensors are probed in the checkpoint's bf16, before
+    quantisation)."""
     from synthetic_checkpoint.workloads import WORKLOADS
 
     w = WORKLOADS[name]
