@@ -810,6 +810,9 @@ class _IdCheckpoint(collections.abc.Mapping):
             self._filled.add(name)
         return x
 
+    def __contains__(self, name):  # a membership test makes nothing
+        return name in self._cat
+
     def __iter__(self):
         return iter(self._cat)
 

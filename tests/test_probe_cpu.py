@@ -216,3 +216,27 @@ def test_diff2_carry_argument_checks():
     assert call(carries=wb.c_void_p(A + 4)) == wb.WB_EINVAL
     assert call(ws=None) == wb.WB_EINVAL
     assert call(ws=wb.c_void_p(A + 4)) == wb.WB_EINVAL
+
+
+def test_identifier_checkpoint_is_made_on_demand(monkeypatch):
+    """The checkpoint a probed loader reads makes a tensor the first time it is
+    read and fills it once per pass; membership tests, iteration and len make
+    nothing (make_ids replaced by a recorder: no GPU needed)."""
+    import torch
+
+    made = []
+    monkeypatch.setattr(wb, "make_ids", lambda x, dt, first, k: made.append((x.shape, first, k)))
+    cat = [("a", 2, 3), ("b", 1, 4), ("c", 5, 1)]
+    probe = wb.Probe(cat, "bf16")
+    ck = wb._IdCheckpoint(cat, "bf16", torch.bfloat16, "cpu")
+    ck.start_pass(probe, 0)
+    assert "b" in ck and "z" not in ck and list(ck) == ["a", "b", "c"] and len(ck) == 3 and made == []
+    x = ck["b"]
+    assert x.shape == (1, 4) and x.dtype == torch.bfloat16 and made == [((1, 4), probe.first_id(1), 0)]
+    assert ck["b"] is x and len(made) == 1           # read again in the same pass: not refilled
+    ck.start_pass(probe, 1)
+    assert ck["b"] is x and made[-1] == ((1, 4), probe.first_id(1), 1)
+    ck["a"]
+    assert [m[0] for m in made] == [(1, 4), (1, 4), (2, 3)]
+    with pytest.raises(KeyError):
+        ck["z"]
