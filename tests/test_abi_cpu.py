@@ -500,3 +500,31 @@ def test_plan_threads_change_nothing(budget, G, monkeypatch):
     monkeypatch.setenv("WB_TASK_BYTES", "1024")
     p = wb.Plan(tr, ro, wb.RECEIVER, w["unpack_rank"], round_budget=budget, node_size=G)
     assert p.work_digest() != next(iter(seen))[0]
+
+
+def test_c_client_compiles_and_plans(tmp_path):
+    """include/wb.h is a C header: a C99 program using it (tests/c_abi_plan.c)
+    compiles without warnings under -pedantic, links against libwb.so and, on
+    a machine without a GPU, plans the tiny workload's rollout rank 1 exactly
+    as the Python binding does (buffer bytes, work counts, canonical dump)."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    libdir = os.path.dirname(os.path.abspath(wb.LIB_PATH))
+    exe = str(tmp_path / "c_abi_plan")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c_abi_plan.c"), "-o", exe, "-L", libdir, "-l:" + os.path.basename(wb.LIB_PATH),
+                    "-Wl,-rpath," + libdir, "-Wl,-rpath-link," + os.path.join(rocm, "lib")],
+                   check=True, capture_output=True, text=True)
+    out = subprocess.run([exe], check=True, capture_output=True, text=True, timeout=60).stdout
+    version, counts, dump = out.split("\n", 2)
+    w = WORKLOADS["tiny_fsdp2_to_tp2"]
+    p = wb.Plan(wb.Layout.describe(w["model"], w["trainer"]), wb.Layout.describe(w["model"], w["rollout"]),
+                wb.RECEIVER, 1)
+    assert version == wb.version()
+    assert [int(x) for x in counts.split()] == [p.buffer_bytes, *p.work_counts()]
+    assert dump == p.dump()
