@@ -15,7 +15,7 @@
 //   VEC   32 rows (128 batched) x 256 vectors of 16 bytes (8 bf16 or 4 fp32
 //         values), the next row's loads in flight while a row is computed
 //         (cols a multiple of the vector, 16-byte aligned field);
-//   FLAT  one-row fields, 8 x 256 vectors per tile (16 x 256 batched).
+//   FLAT  one-row fields, 8 x 256 vectors per tile (32 x 256 batched).
 // Single-field launches walk one field's tiles with a strided grid; the
 // batched launch takes one tile per workgroup from a table that covers many
 // fields, so all of a rank's tensors take one launch.
@@ -605,7 +605,7 @@ __global__ __launch_bounds__(kThreads) void wb_diff2_flat_kernel(const char* __r
 // read one pass in int.
 constexpr int kBatchVecStrip = 128;
 constexpr int kBatchFlatUnroll = 4;
-constexpr int kBatchFlatSub = 4;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
+constexpr int kBatchFlatSub = 8;  // sub-tiles of kBatchFlatUnroll x kThreads vectors per FLAT tile
 
 template <typename T, int P, class Out>
 __device__ __forceinline__ void batch_tile(const DiffField& f, const DiffTile& t, const Out& out) {
