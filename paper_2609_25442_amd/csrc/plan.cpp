@@ -18,6 +18,7 @@
 #include <map>
 #include <numeric>
 #include <sstream>
+#include <system_error>
 #include <thread>
 
 #include "wb_internal.hpp"
@@ -307,7 +308,11 @@ void parallel_for(size_t n, int threads, F&& fn) {
     }
   };
   std::vector<std::thread> pool;
-  for (int w = 1; w < nw; ++w) pool.emplace_back(work, w);
+  try {
+    for (int w = 1; w < nw; ++w) pool.emplace_back(work, w);
+  } catch (const std::system_error&) {
+    // no more threads to be had: the ones started and this one take every index
+  }
   work(0);
   for (auto& th : pool) th.join();
   for (auto& e : err)
