@@ -195,8 +195,9 @@ typedef enum wb_role { WB_SENDER = 0, WB_RECEIVER = 1 } wb_role;
  *             multiple of 256 bytes; buffers hold regions by ascending peer,
  *             each starting at a multiple of 4096 bytes.
  * A receiver's fp8 block tables are built by up to WB_PLAN_THREADS host
- * threads (environment, 1..64; default: the CPUs the process may run on, at
- * most 16); the plan does not depend on the number.
+ * threads (environment, 1..64, for any plan with fp8 blocks; default: one for
+ * fewer than 32768 blocks, else the CPUs the process may run on, at most 16);
+ * the plan does not depend on the number.
  * Errors: WB_EINVAL (null, rank out of range, catalogs differ, a rollout
  * element held by no trainer, rollout tensors not exactly covered),
  * WB_EUNSUPPORTED (overlapping non-identical trainer rectangles, replicas with

@@ -270,13 +270,15 @@ struct QSpan {
   int64_t e, row0, col0;
 };
 
-// Host threads for planning: WB_PLAN_THREADS if set (1..64), else the CPUs
-// this process may run on, at most 16. The plan does not depend on it.
-int plan_threads() {
+// Host threads for a planning step over `work` items: WB_PLAN_THREADS if set
+// (1..64), else one below `small` items and otherwise the CPUs this process
+// may run on, at most 16. The plan does not depend on it.
+int plan_threads(int64_t work, int64_t small) {
   if (const char* e = std::getenv("WB_PLAN_THREADS")) {
     const long v = std::strtol(e, nullptr, 10);
     if (v >= 1 && v <= 64) return static_cast<int>(v);
   }
+  if (work < small) return 1;
   cpu_set_t set;
   const int n = sched_getaffinity(0, sizeof set, &set) == 0 ? CPU_COUNT(&set) : 1;
   return std::max(1, std::min(n, 16));
@@ -455,7 +457,7 @@ void build_qblocks(const wb_layout_t& trainer, const Rank& R, wb_plan_t& P, cons
   for (size_t u = 0; u < nl; ++u)
     if (R.locals[u].block > 0) ql.push_back(static_cast<int>(u));
   const size_t nq = ql.size();
-  const int threads = nblocks >= (int64_t(1) << 15) ? plan_threads() : 1;
+  const int threads = plan_threads(nblocks, int64_t(1) << 15);
   // pass 1: per local, its pieces, its blocks per (round, class) and the
   // local piece range each round reads
   std::vector<uint32_t> npieces(nq);
@@ -773,7 +775,7 @@ void check_work(const wb_plan_t& P, const Rank& R) {
   };
   // blocks in runs of 2^14 on the planning threads (the checks only read)
   const uint32_t b0 = P.round_qblocks[k], nb = P.round_qblocks[k + 1] - b0, run = 1u << 14;
-  parallel_for((nb + run - 1) / run, nb >= 2 * run ? plan_threads() : 1, [&](size_t i, int) {
+  parallel_for((nb + run - 1) / run, plan_threads(nb, 2 * run), [&](size_t i, int) {
     const uint32_t lo = b0 + static_cast<uint32_t>(i) * run, hi = lo + std::min(run, b0 + nb - lo);
     for (uint32_t bi = lo; bi < hi; ++bi) check_block(bi);
   });

@@ -528,3 +528,25 @@ def test_c_client_compiles_and_plans(tmp_path):
     assert version == wb.version()
     assert [int(x) for x in counts.split()] == [p.buffer_bytes, *p.work_counts()]
     assert dump == p.dump()
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_plan_threads_change_nothing_on_random_fp8_layouts(seed, monkeypatch):
+    """Random layouts with fp8 rollouts of 4 x 4 blocks (ragged, multi-piece
+    and row-band blocks), rounds and exchange stages: with WB_PLAN_THREADS set
+    every plan builds its fp8 tables on that many threads, and 1 and 7 threads
+    give the same work tables and dump on every rollout rank."""
+    rng = np.random.default_rng(5000 + seed)
+    m = random_model(rng)
+    otr = describe_layout(m, random_par(rng, m, "trainer"))
+    oro = describe_layout(m, random_par(rng, m, "rollout", blocks=(4,)))
+    tr, ro = to_wb(otr), to_wb(oro)
+    budget = int(rng.choice([0, 0, 300, 3000]))
+    G = int(rng.integers(0, oro.nranks + 1))
+    for d in range(oro.nranks):
+        seen = set()
+        for n in ("1", "7"):
+            monkeypatch.setenv("WB_PLAN_THREADS", n)
+            p = wb.Plan(tr, ro, wb.RECEIVER, d, round_budget=budget, node_size=G)
+            seen.add((p.work_digest(), p.dump()))
+        assert len(seen) == 1, (seed, d)
