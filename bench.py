@@ -344,7 +344,9 @@ def run_plan_stress():
     m = dict(w["model"], num_layers=58)
     tr = wb.Layout.describe(m, w["trainer"])
     ro = wb.Layout.describe(m, w["rollout"])
-    out = {"metric": "wb_plan ms (58-layer DeepSeek-V3-like catalog)", "tensors": len(tr.tensors()), "plan_ms": {}}
+    out = {"metric": "wb_plan ms (58-layer DeepSeek-V3-like catalog)", "tensors": len(tr.tensors()), "plan_ms": {},
+           "host_cpu_count": os.cpu_count(), "host_affinity_cpus": len(os.sched_getaffinity(0)),
+           "plan_threads": os.environ.get("WB_PLAN_THREADS", "default (allowed CPUs, at most 16)")}
     for label, role, G in (("receiver", wb.RECEIVER, 0), ("sender", wb.SENDER, 0), ("receiver_exchange_G4", wb.RECEIVER, 4)):
         ts = []
         for _ in range(5):

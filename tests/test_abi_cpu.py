@@ -204,6 +204,9 @@ def test_error_paths():
     p = wb.Plan(tr, ro, wb.RECEIVER, 0)
     _expect(wb.WB_EINVAL, p.unpack, 0, [0] * p.num_local_tensors, 0)
     _expect(wb.WB_EINVAL, p.pack, [0] * p.num_local_tensors, 0, 0)
+    # queries with null arguments
+    assert wb.lib.wb_plan_work_digest(p._h, None) == wb.WB_EINVAL
+    assert wb.lib.wb_plan_work_digest(None, wb.byref(wb.c_uint64())) == wb.WB_EINVAL
 
 
 def test_hand_rounds_golden():
